@@ -1,0 +1,419 @@
+"""Seeded synthetic inputs for the eventually consistent collective data path.
+
+This package produces inputs only: random numbers, block partitions,
+arrival schedules, stencil and R-MAT matrices.  It holds none of the
+method's arithmetic (no staleness rule, no assembly, no reduction, no
+iteration), so it can feed both the oracle and the GPU path without either
+of them depending on the other.
+
+Every workload is a pure function of (config id, sizes); the seed of config c
+is ``2203170630 + c`` and each kind of draw uses its own named stream.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import subprocess
+from dataclasses import dataclass, field
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "gen.c")
+_LIB = os.path.join(_HERE, "libgen.so")
+
+# Named random streams (one per kind of draw).
+STREAM_PARTITION = 0
+STREAM_B = 1
+STREAM_Q = 2
+STREAM_ARRIVAL = 3
+STREAM_EDGES = 4
+STREAM_COUNTS = 5
+STREAM_PAYLOAD = 6
+STREAM_PAYLOAD_REDUCE = 7
+
+SEED_BASE = 2203170630
+
+# R-MAT quadrant probabilities (Graph500 values) and their cumulative sums.
+RMAT_A, RMAT_B, RMAT_C, RMAT_D = 0.57, 0.19, 0.19, 0.05
+RMAT_T1, RMAT_T2, RMAT_T3 = 0.57, 0.76, 0.95
+
+UNBOUNDED = 0x7FFFFFFF
+
+
+def seed_of(config: int) -> int:
+    return SEED_BASE + int(config)
+
+
+def build(force: bool = False) -> str:
+    """Compile gen.c into libgen.so with gcc (no floating-point contraction)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fopenmp", "-fPIC",
+                               "-shared", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        L = ctypes.CDLL(_LIB)
+        u64, i64, i32, dbl, vp = (ctypes.c_uint64, ctypes.c_int64, ctypes.c_int32,
+                                  ctypes.c_double, ctypes.c_void_p)
+        L.gen_stream_key.restype = u64
+        L.gen_stream_key.argtypes = [u64, u64]
+        L.gen_u64.restype = u64
+        L.gen_u64.argtypes = [u64, u64, u64]
+        L.gen_splitmix64_sequence.argtypes = [u64, i64, vp]
+        L.gen_uniform.argtypes = [u64, u64, u64, i64, vp]
+        L.gen_uniform_range.argtypes = [u64, u64, u64, i64, dbl, dbl, vp]
+        L.gen_uniform_at.argtypes = [u64, u64, i64, vp, dbl, dbl, vp]
+        L.gen_normal.argtypes = [u64, u64, i64, vp]
+        L.gen_arrival_mask.argtypes = [u64, u64, i64, i32, vp, vp]
+        L.gen_stencil_size.argtypes = [ctypes.c_int, i64, vp, vp]
+        L.gen_stencil_csr.restype = i64
+        L.gen_stencil_csr.argtypes = [ctypes.c_int, i64, dbl, vp, vp, vp]
+        L.gen_rmat_edges.argtypes = [u64, u64, ctypes.c_int, i64, dbl, dbl, dbl, vp, vp]
+        L.gen_out_degree.argtypes = [i64, i64, vp, vp]
+        L.gen_pull_csr.restype = ctypes.c_int
+        L.gen_pull_csr.argtypes = [i64, i64, vp, vp, vp, vp, vp]
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+# ----------------------------------------------------------------------------
+# random numbers
+# ----------------------------------------------------------------------------
+
+def splitmix64_sequence(state: int, n: int) -> np.ndarray:
+    out = np.empty(n, dtype=np.uint64)
+    lib().gen_splitmix64_sequence(state, n, _p(out))
+    return out
+
+
+def u64(seed: int, stream: int, ctr: int) -> int:
+    return int(lib().gen_u64(seed, stream, ctr))
+
+
+def uniform(seed: int, stream: int, n: int, ctr0: int = 0, lo: float = 0.0,
+            hi: float = 1.0) -> np.ndarray:
+    out = np.empty(n, dtype=np.float64)
+    if n:
+        if lo == 0.0 and hi == 1.0:
+            lib().gen_uniform(seed, stream, ctr0, n, _p(out))
+        else:
+            lib().gen_uniform_range(seed, stream, ctr0, n, lo, hi, _p(out))
+    return out
+
+
+def uniform_at(seed: int, stream: int, ctrs: np.ndarray, lo: float = 0.0,
+               hi: float = 1.0) -> np.ndarray:
+    ctrs = np.ascontiguousarray(ctrs, dtype=np.uint64)
+    out = np.empty(ctrs.shape[0], dtype=np.float64)
+    if ctrs.shape[0]:
+        lib().gen_uniform_at(seed, stream, ctrs.shape[0], _p(ctrs), lo, hi, _p(out))
+    return out
+
+
+def normal(seed: int, stream: int, n: int) -> np.ndarray:
+    out = np.empty(n, dtype=np.float64)
+    if n:
+        lib().gen_normal(seed, stream, n, _p(out))
+    return out
+
+
+def arrival_mask(seed: int, T: int, q: np.ndarray) -> np.ndarray:
+    """[T][P] uint8 table; row 0 is all ones (initial exchange)."""
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    P = q.shape[0]
+    out = np.empty((T, P), dtype=np.uint8)
+    lib().gen_arrival_mask(seed, STREAM_ARRIVAL, T, P, _p(q), _p(out))
+    return out
+
+
+# ----------------------------------------------------------------------------
+# partitions
+# ----------------------------------------------------------------------------
+
+def dirichlet_partition(n: int, P: int, seed: int) -> np.ndarray:
+    """Block sizes from a flat Dirichlet(1) draw.
+
+    w_p = -ln(1 - U_p) (Exp(1)); the normalised weights give ideal sizes
+    w_p / sum(w) * n; sizes are their floors plus one for the largest
+    remainders (ties to the lower rank); a size of 0 then takes one element
+    from the largest block (lowest rank among ties)."""
+    u = uniform(seed, STREAM_PARTITION, P)
+    w = np.array([-math.log(1.0 - float(x)) for x in u])
+    W = math.fsum(w)
+    ideal = [float(wp) / W * n for wp in w]
+    sizes = [int(math.floor(x)) for x in ideal]
+    rem = n - sum(sizes)
+    order = sorted(range(P), key=lambda p: (-(ideal[p] - sizes[p]), p))
+    for p in order[:rem]:
+        sizes[p] += 1
+    for p in range(P):
+        if sizes[p] == 0:
+            big = max(range(P), key=lambda r: (sizes[r], -r))
+            sizes[big] -= 1
+            sizes[p] = 1
+    assert sum(sizes) == n and min(sizes) >= 1
+    return np.array(sizes, dtype=np.int64)
+
+
+def lognormal_counts(P: int, seed: int, mean: float = 65536.0, sigma: float = 1.0) -> np.ndarray:
+    """counts_p = max(1, round-half-even(exp(mu + sigma z_p))) with
+    mu = ln(mean) - sigma^2/2 so that E[X] = mean; z_p standard normal by
+    Box-Muller from the counts stream."""
+    z = normal(seed, STREAM_COUNTS, P)
+    mu = math.log(mean) - 0.5 * sigma * sigma
+    return np.array([max(1, int(round(math.exp(mu + sigma * float(zp))))) for zp in z],
+                    dtype=np.int64)
+
+
+def exclusive_scan(counts: np.ndarray) -> np.ndarray:
+    d = np.zeros(len(counts), dtype=np.int64)
+    if len(counts) > 1:
+        d[1:] = np.cumsum(counts[:-1])
+    return d
+
+
+def edge_balanced_partition(row_ptr: np.ndarray, P: int) -> np.ndarray:
+    """Contiguous row ranges balanced by nonzeros: r_p = min{i : row_ptr[i]*P >= p*nnz},
+    r_P = n.  Returns the block sizes."""
+    n = row_ptr.shape[0] - 1
+    nnz = int(row_ptr[-1])
+    rp = row_ptr.astype(np.int64)
+    starts = [int(np.searchsorted(rp * P, p * nnz, side="left")) for p in range(P)]
+    starts[0] = 0
+    bounds = starts + [n]
+    return np.diff(np.array(bounds, dtype=np.int64))
+
+
+# ----------------------------------------------------------------------------
+# matrices
+# ----------------------------------------------------------------------------
+
+@dataclass
+class CSR:
+    n_rows: int
+    n_cols: int
+    row_ptr: np.ndarray  # int32 [n+1]
+    col: np.ndarray      # int32 [nnz]
+    val: np.ndarray      # float64 [nnz]
+
+    @property
+    def nnz(self) -> int:
+        return int(self.row_ptr[-1])
+
+    def to_dense(self) -> np.ndarray:
+        A = np.zeros((self.n_rows, self.n_cols))
+        for i in range(self.n_rows):
+            for k in range(self.row_ptr[i], self.row_ptr[i + 1]):
+                A[i, self.col[k]] += self.val[k]
+        return A
+
+
+def stencil_size(dim: int, N: int):
+    n = ctypes.c_int64()
+    nnz = ctypes.c_int64()
+    lib().gen_stencil_size(dim, N, ctypes.byref(n), ctypes.byref(nnz))
+    return n.value, nnz.value
+
+
+def stencil_csr(dim: int, N: int, diag: float) -> CSR:
+    n, nnz = stencil_size(dim, N)
+    row_ptr = np.empty(n + 1, dtype=np.int32)
+    col = np.empty(nnz, dtype=np.int32)
+    val = np.empty(nnz, dtype=np.float64)
+    got = lib().gen_stencil_csr(dim, N, diag, _p(row_ptr), _p(col), _p(val))
+    if got != nnz:
+        raise ValueError("stencil too large for int32 indices (dim=%d N=%d)" % (dim, N))
+    return CSR(n, n, row_ptr, col, val)
+
+
+def rmat_edges(seed: int, scale: int, n_edges: int):
+    src = np.empty(n_edges, dtype=np.int32)
+    dst = np.empty(n_edges, dtype=np.int32)
+    lib().gen_rmat_edges(seed, STREAM_EDGES, scale, n_edges, RMAT_T1, RMAT_T2, RMAT_T3,
+                         _p(src), _p(dst))
+    return src, dst
+
+
+def out_degree(n: int, src: np.ndarray) -> np.ndarray:
+    out = np.empty(n, dtype=np.int32)
+    lib().gen_out_degree(n, src.shape[0], _p(src), _p(out))
+    return out
+
+
+def pull_csr(n: int, src: np.ndarray, dst: np.ndarray) -> CSR:
+    E = src.shape[0]
+    row_ptr = np.empty(n + 1, dtype=np.int32)
+    col = np.empty(E, dtype=np.int32)
+    val = np.empty(E, dtype=np.float64)
+    rc = lib().gen_pull_csr(n, E, _p(src), _p(dst), _p(row_ptr), _p(col), _p(val))
+    if rc != 0:
+        raise RuntimeError("gen_pull_csr failed (%d)" % rc)
+    return CSR(n, n, row_ptr, col, val)
+
+
+# ----------------------------------------------------------------------------
+# workloads
+# ----------------------------------------------------------------------------
+
+@dataclass
+class Iterative:
+    """One of the iterative configurations: T iterations of select/assemble,
+    a block-row sweep and a residual norm."""
+    name: str
+    kind: str                 # "jacobi" or "power"
+    A: CSR
+    counts: np.ndarray        # int64 [P] block sizes, tiling [0, n) in rank order
+    displs: np.ndarray        # int64 [P]
+    S: int                    # maximum staleness
+    mask: np.ndarray          # uint8 [T][P]
+    T: int
+    x0: np.ndarray
+    b: Optional[np.ndarray] = None
+    alpha: float = 0.0
+    beta: float = 0.0
+    tol: float = 0.0          # stop after the first t with rho_t < tol (0: never)
+    norm: int = 2             # 2: L2 of the Jacobi residual, 1: L1 of the update
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def P(self) -> int:
+        return int(self.counts.shape[0])
+
+    @property
+    def n(self) -> int:
+        return self.A.n_rows
+
+
+def config1() -> Iterative:
+    """1-D tridiag(-1, 4, -1), n = 4096, b ~ U[0,1), P = 4 Dirichlet(1) blocks,
+    every block arrives every iteration, S = 0, 50 iterations."""
+    seed = seed_of(1)
+    n = 4096
+    A = stencil_csr(1, n, 4.0)
+    counts = dirichlet_partition(n, 4, seed)
+    T = 50
+    return Iterative("cfg1-jacobi-1d", "jacobi", A, counts, exclusive_scan(counts), 0,
+                     np.ones((T, 4), dtype=np.uint8), T, np.zeros(n),
+                     b=uniform(seed, STREAM_B, n), norm=2,
+                     meta={"dim": 1, "N": n, "diag": 4.0, "q": 1.0})
+
+
+def config2(N: int = 1024, T: int = 200) -> Iterative:
+    """2-D 5-point Laplacian N x N with the diagonal shifted by +4 (diag 8),
+    b ~ N(0,1), P = 16 uneven blocks, Bernoulli(0.9) arrivals, S = 3."""
+    seed = seed_of(2)
+    A = stencil_csr(2, N, 8.0)
+    n = A.n_rows
+    P = 16
+    counts = dirichlet_partition(n, P, seed)
+    q = np.full(P, 0.9)
+    return Iterative("cfg2-jacobi-2d", "jacobi", A, counts, exclusive_scan(counts), 3,
+                     arrival_mask(seed, T, q), T, np.zeros(n), b=normal(seed, STREAM_B, n),
+                     norm=2, meta={"dim": 2, "N": N, "diag": 8.0, "q": 0.9})
+
+
+def config3(scale: int = 22, edge_factor: int = 16, T: int = 100, P: int = 64) -> Iterative:
+    """PageRank power iteration x <- 0.85 W x + 0.15/n on an R-MAT graph
+    (2^scale vertices, edge_factor * 2^scale edges), W = A^T D^-1 in pull CSR,
+    P edge-balanced blocks, Bernoulli(0.8) arrivals, S = 4, stop at
+    ||dx||_1 < 1e-10 or after T iterations."""
+    seed = seed_of(3)
+    n = 1 << scale
+    E = edge_factor * n
+    src, dst = rmat_edges(seed, scale, E)
+    W = pull_csr(n, src, dst)
+    del src, dst
+    counts = edge_balanced_partition(W.row_ptr, P)
+    q = np.full(P, 0.8)
+    return Iterative("cfg3-pagerank-rmat", "power", W, counts, exclusive_scan(counts), 4,
+                     arrival_mask(seed, T, q), T, np.full(n, 1.0 / n), alpha=0.85,
+                     beta=0.15 / n, tol=1e-10, norm=1,
+                     meta={"scale": scale, "edges": E, "q": 0.8})
+
+
+def config5(N: int = 400, T: int = 100, P: int = 512) -> Iterative:
+    """3-D 7-point Laplacian N^3 with the diagonal shifted by +6 (diag 12),
+    b ~ U[0,1), P uneven blocks, per-rank arrival probability q_p ~ U[0.6, 0.95],
+    S = 5."""
+    seed = seed_of(5)
+    A = stencil_csr(3, N, 12.0)
+    n = A.n_rows
+    counts = dirichlet_partition(n, P, seed)
+    q = 0.6 + 0.35 * uniform(seed, STREAM_Q, P)
+    return Iterative("cfg5-jacobi-3d", "jacobi", A, counts, exclusive_scan(counts), 5,
+                     arrival_mask(seed, T, q), T, np.zeros(n), b=uniform(seed, STREAM_B, n),
+                     norm=2, meta={"dim": 3, "N": N, "diag": 12.0, "q": "U[0.6,0.95]"})
+
+
+@dataclass
+class Allgatherv:
+    """Collective data path alone: P ranks, lognormal counts, prefix-sum
+    displacements, a packed send arena at the same offsets, every rank
+    arriving every repetition."""
+    counts: np.ndarray
+    displs: np.ndarray
+    send: np.ndarray
+    reps: int
+    mask: np.ndarray
+    S: int = UNBOUNDED
+
+    @property
+    def P(self) -> int:
+        return int(self.counts.shape[0])
+
+
+def config4a(P: int = 256, reps: int = 1000, mean: float = 65536.0) -> Allgatherv:
+    seed = seed_of(4)
+    counts = lognormal_counts(P, seed, mean=mean)
+    displs = exclusive_scan(counts)
+    E = int(counts.sum())
+    send = uniform(seed, STREAM_PAYLOAD, E, lo=-1.0, hi=1.0)
+    return Allgatherv(counts, displs, send, reps, np.ones((reps, P), dtype=np.uint8))
+
+
+@dataclass
+class Allreduce:
+    """Partial allreduce-sum of P vectors of m elements; rank p's contribution
+    at repetition r is U[-1,1) from its own payload stream at counters
+    (r*P + p)*m + i; Bernoulli(q) arrivals; stale contributions substituted."""
+    P: int
+    m: int
+    reps: int
+    mask: np.ndarray
+    S: int
+    seed: int
+    q: float
+
+    def fresh_ctr0(self, p: int, r: int) -> int:
+        return (r * self.P + p) * self.m
+
+    def fresh(self, p: int, r: int) -> np.ndarray:
+        return uniform(self.seed, STREAM_PAYLOAD_REDUCE, self.m, ctr0=self.fresh_ctr0(p, r),
+                       lo=-1.0, hi=1.0)
+
+    def fresh_at(self, p: int, r: int, idx: np.ndarray) -> np.ndarray:
+        ctr = np.uint64(self.fresh_ctr0(p, r)) + np.asarray(idx, dtype=np.uint64)
+        return uniform_at(self.seed, STREAM_PAYLOAD_REDUCE, ctr, lo=-1.0, hi=1.0)
+
+
+def config4b(P: int = 256, m: int = 1 << 22, reps: int = 1000, q: float = 0.7,
+             S: int = UNBOUNDED) -> Allreduce:
+    seed = seed_of(4)
+    return Allreduce(P, m, reps, arrival_mask(seed, reps, np.full(P, q)), S, seed, q)
