@@ -1,0 +1,249 @@
+/*
+ * libecc -- eventually consistent collectives and the iterations they feed,
+ * on one AMD Instinct MI355X (gfx950).
+ *
+ * Method: Iakymchuk et al., "Efficient and Eventually Consistent Collective
+ * Operations" (arXiv 2203.17063).  Section III-A and Algorithm 1 define the
+ * stale-synchronous (SSP) collective: each call advances a logical clock,
+ * a contribution is used if its clock is at least clock - slack, and only
+ * data that is too stale makes the caller wait for an update; the last data
+ * received for each source is kept in dedicated receive memory and re-read
+ * when nothing newer has arrived; a reduced result carries the minimum
+ * clock of its inputs.  Section III also names the two extra collective
+ * parameters this library exposes as outputs ("status": which blocks were
+ * used, their age, the clock of the result).  Table I and Section II give
+ * the resource model: resources are allocated and metadata exchanged once
+ * at set-up and released at shut-down.
+ *
+ * Here P "virtual ranks" live on one GPU: rank p's contribution is a block
+ * of a vector in HBM, a delivery is a copy plus a version update, and the
+ * arrival of each block at each clock comes from a caller-supplied mask.
+ *
+ * Conventions for every call:
+ *   - Pointers prefixed d_ are device (HBM) pointers, h_ are host pointers.
+ *     The caller owns every vector, mask, slot and matrix array; the library
+ *     never frees caller memory.  A plan owns only its small metadata.
+ *   - Calls are asynchronous on the plan's HIP stream unless stated.  Buffers
+ *     passed to a call must stay valid until the stream reaches that work.
+ *   - Every call returns an ecc_status_t.  Argument errors are detected on the
+ *     host before anything is enqueued and leave the plan unchanged; the text
+ *     of the last error of the calling thread is ecc_last_error().
+ *   - A plan is not thread-safe.  Calls that share a plan, or that write the
+ *     same buffers, must not overlap.
+ *   - Indices of CSR matrices are int32 (nnz < 2^31); values are fp64.
+ */
+#ifndef LIBECC_H
+#define LIBECC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ecc_plan_s *ecc_plan_t;
+typedef struct ecc_matrix_s *ecc_matrix_t;
+
+typedef enum {
+    ECC_OK = 0,
+    ECC_ERR_ARG = 1,      /* a bad argument (null pointer, negative size, ...) */
+    ECC_ERR_OVERLAP = 2,  /* two ranks' blocks overlap in the receive vector   */
+    ECC_ERR_RANGE = 3,    /* a size exceeds what the layout supports           */
+    ECC_ERR_ALLOC = 4,    /* a device or host allocation failed                */
+    ECC_ERR_DEVICE = 5,   /* a HIP call or kernel launch failed                */
+    ECC_ERR_STATE = 6     /* the call does not fit the plan or matrix          */
+} ecc_status_t;
+
+/* max_staleness value meaning "no bound": after the initial exchange a block
+ * is taken only when it arrives, never forced. */
+#define ECC_UNBOUNDED 0x7fffffff
+
+#define ECC_NORM_L1 1
+#define ECC_NORM_L2 2
+
+#define ECC_KIND_JACOBI 0  /* x_next_i = (b_i - sum_{j!=i} a_ij y_j) / a_ii       */
+#define ECC_KIND_POWER 1   /* x_next_j = alpha * sum_i w_ji y_i + beta           */
+
+typedef struct {
+    int64_t n_rows, n_cols, nnz;
+    const int32_t *d_row_ptr; /* [n_rows + 1], row_ptr[0] = 0, non-decreasing */
+    const int32_t *d_col;     /* [nnz], each in [0, n_cols)                   */
+    const double *d_val;      /* [nnz]                                        */
+} ecc_csr_t;
+
+/* ---------------------------------------------------------------------------
+ * Host-only helpers (no GPU needed).
+ * ------------------------------------------------------------------------- */
+
+/* Version of this interface (incremented on incompatible changes). */
+int32_t ecc_abi_version(void);
+
+/* Text of the last error on the calling thread ("" if none). */
+const char *ecc_last_error(void);
+
+/* Name of a status code. */
+const char *ecc_status_string(ecc_status_t s);
+
+/* Check a block layout without creating anything.  Same rules as
+ * ecc_plan_create: P >= 1; max_staleness >= 0; if h_counts is non-NULL then
+ * h_displs must be too, every count and displacement is >= 0, and no two
+ * non-empty blocks [displs[p], displs[p] + counts[p]) overlap
+ * (ECC_ERR_OVERLAP); the extent max(displs + counts) must be < 2^40
+ * (ECC_ERR_RANGE).  Unsorted displacements and gaps are allowed. */
+ecc_status_t ecc_plan_validate(int32_t P, const int64_t *h_counts, const int64_t *h_displs,
+                               int32_t max_staleness);
+
+/* ---------------------------------------------------------------------------
+ * Plan: the set-up phase of Table I.  A plan holds the rank layout, the
+ * slack S (max_staleness), the logical clock and, per rank, the version
+ * (clock at which its data last arrived; -1 before the first call) and age.
+ * ------------------------------------------------------------------------- */
+
+/* Create a plan for P ranks.  h_counts/h_displs (host, P entries each,
+ * copied) describe where rank p's block lives in the assembled vector; both
+ * may be NULL for a plan used only with ecc_allreduce_partial.  hip_stream is
+ * a hipStream_t (NULL: the default stream).  Allocates a few KB of device
+ * memory on the current device.  Validation as ecc_plan_validate. */
+ecc_status_t ecc_plan_create(int32_t P, const int64_t *h_counts, const int64_t *h_displs,
+                             int32_t max_staleness, void *hip_stream, ecc_plan_t *out);
+
+/* Release the plan's device metadata (waits for its stream first). */
+ecc_status_t ecc_plan_destroy(ecc_plan_t plan);
+
+/* Clock := 0, every version := -1, forced counter := 0 (asynchronous). */
+ecc_status_t ecc_plan_reset(ecc_plan_t plan);
+
+/* Change the stream later calls are enqueued on. */
+ecc_status_t ecc_plan_set_stream(ecc_plan_t plan, void *hip_stream);
+
+/* Synchronising read of the plan state: clock (= number of collective calls
+ * since create/reset), total forced arrivals, and optionally the per-rank
+ * version and age after the last call (host arrays of P int32, nullable). */
+ecc_status_t ecc_plan_stats(ecc_plan_t plan, int64_t *clock, int64_t *forced_total,
+                            int32_t *h_version, int32_t *h_age);
+
+/* ---------------------------------------------------------------------------
+ * Collectives.  Each call is one clock step t = current clock (Algorithm 1
+ * increments the clock on entry; t is that value minus one) and advances the
+ * clock by one.  The staleness decision for every rank p is
+ *     eff[p] = version[p] < 0  ||  arrived[p]  ||  t - version[p] > S
+ * ("wait only if the data received is too stale": a block older than S
+ * clocks is delivered now, a *forced* arrival); then version[p] := t where
+ * eff[p] and age[p] := t - version[p], so 0 <= age <= S.
+ * ------------------------------------------------------------------------- */
+
+/* allgatherv-style assembly with last-received semantics (the per-source
+ * receive memory of Section III-A, rcv_data_vec).  For every rank with
+ * eff[p]:  d_recv[displs[p] + j] = d_send[p][j] for 0 <= j < counts[p].
+ * Blocks without eff, and gaps between blocks, keep their previous contents.
+ *   d_send     device array of P device pointers (rank p's block); entries of
+ *              ranks with count 0 are not read.  The blocks must not overlap
+ *              d_recv's written ranges.
+ *   d_recv     device vector of at least max(displs + counts) doubles.
+ *   d_arrived  device array of P bytes (non-zero: arrived at this clock).
+ *   d_eff_out  optional device array of P bytes: eff of this call.
+ *   d_age_out  optional device array of P int32: age after this call.
+ * Requires a plan created with counts/displs (else ECC_ERR_STATE). */
+ecc_status_t ecc_allgatherv_assemble(ecc_plan_t plan, const double *const *d_send,
+                                     double *d_recv, const uint8_t *d_arrived,
+                                     uint8_t *d_eff_out, int32_t *d_age_out);
+
+/* Same, with every rank's block at the same offset in one packed send
+ * vector: rank p's block starts at d_send_base + displs[p]. */
+ecc_status_t ecc_allgatherv_assemble_packed(ecc_plan_t plan, const double *d_send_base,
+                                            double *d_recv, const uint8_t *d_arrived,
+                                            uint8_t *d_eff_out, int32_t *d_age_out);
+
+/* Partial allreduce (sum) with stale substitution: the reduction of
+ * Algorithm 1 over the newest contribution held for each rank.
+ *   for every p with eff[p]:  d_slots[p][i] = d_fresh[p][i]
+ *   d_result[i] = ((slot_0[i] + slot_1[i]) + slot_2[i]) + ...   (rank order,
+ *                 so the result is bitwise reproducible)
+ *   *d_result_clock = min_p version[p]  (the minimum-clock rule; nullable)
+ *   m          elements per rank (>= 0).
+ *   d_fresh    device array of P device pointers to this clock's
+ *              contributions (read only where eff[p]).
+ *   d_slots    device array of P device pointers to the caller-owned receive
+ *              memory of each rank (m doubles each); read every call, written
+ *              where eff[p].  At the plan's first call every rank is eff, so
+ *              the slots need no initialisation.
+ *   d_result   device vector of m doubles; must not alias any slot or fresh.
+ *   d_arrived, d_eff_out as for the assembly. */
+ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *const *d_fresh,
+                                   double *const *d_slots, double *d_result,
+                                   const uint8_t *d_arrived, uint8_t *d_eff_out,
+                                   int32_t *d_result_clock);
+
+/* ---------------------------------------------------------------------------
+ * Block-row iterations consuming the assembled vector.  Rank p owns rows
+ * [displs[p], displs[p] + counts[p]); the plan's blocks must tile
+ * [0, n_rows) in rank order (displs = exclusive prefix sum of counts) and
+ * the matrix must be square, else ECC_ERR_STATE.  Row i of block
+ * p = [lo, hi) reads the view
+ *     y_j = x_own[j] if lo <= j < hi  (a rank's own block is always current)
+ *     y_j = x_hat[j] otherwise        (the assembled, possibly stale, vector)
+ * ------------------------------------------------------------------------- */
+
+/* Analyse a CSR matrix once for a plan (set-up, synchronising): builds the
+ * row-block work list (blocks never straddle a rank boundary; rows longer
+ * than one work item are split and recombined in a fixed order), and for
+ * ECC_KIND_JACOBI checks that every row has exactly one diagonal entry and
+ * that it is non-zero (else ECC_ERR_ARG).  The matrix arrays are referenced,
+ * not copied: they must outlive the handle and stay unchanged. */
+ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
+                               ecc_matrix_t *out);
+ecc_status_t ecc_matrix_destroy(ecc_matrix_t A);
+
+/* Number of doubles a d_partials buffer for this matrix must hold. */
+int64_t ecc_partials_size(ecc_matrix_t A);
+
+/* One Jacobi sweep (textbook Jacobi on the block-row view above):
+ *   s_i = sum over the row's off-diagonal entries of a_ij * y_j (CSR order)
+ *   d_x_next[i] = (b_i - s_i) / a_ii
+ *   r_i = (b_i - s_i) - a_ii * x_own[i]
+ * and writes ecc_partials_size(A) partial sums of r_i^2 to d_partials, whose
+ * total ecc_residual(..., ECC_NORM_L2, ...) turns into ||r||_2.  d_x_next
+ * must not alias d_x_own, d_x_hat or d_b.  Does not advance the clock. */
+ecc_status_t ecc_iterate_jacobi(ecc_plan_t plan, ecc_matrix_t A, const double *d_b,
+                                const double *d_x_own, const double *d_x_hat,
+                                double *d_x_next, double *d_partials);
+
+/* One power-iteration step (PageRank with W = A^T D^-1 stored by rows):
+ *   d_x_next[j] = alpha * (sum_i w_ji * y_i) + beta
+ * with partial sums of |x_next_j - x_own_j| in d_partials (ECC_NORM_L1). */
+ecc_status_t ecc_iterate_spmv(ecc_plan_t plan, ecc_matrix_t W, double alpha, double beta,
+                              const double *d_x_own, const double *d_x_hat, double *d_x_next,
+                              double *d_partials);
+
+/* Second pass of the norm: reduces n_partials values in a fixed order
+ * (deterministic) to sqrt(sum) (ECC_NORM_L2) or sum (ECC_NORM_L1).  Writes
+ * *d_out (device, asynchronous) and/or *h_out (host: synchronises); at least
+ * one must be non-NULL. */
+ecc_status_t ecc_residual(ecc_plan_t plan, const double *d_partials, int64_t n_partials,
+                          int32_t norm, double *h_out, double *d_out);
+
+/* ---------------------------------------------------------------------------
+ * Loop control: T iterations of  assemble -> sweep -> norm -> swap, each on
+ * the plan's next clock.  ECC_KIND_JACOBI uses d_b and the L2 residual;
+ * ECC_KIND_POWER uses alpha, beta and the L1 norm of the update.  If tol > 0
+ * the loop stops after the first iteration whose norm is below tol (checked
+ * on the device: no host round trip per iteration).
+ *   d_x       in: x^0; out: the last iterate.  n_rows doubles.
+ *   d_x_tmp   workspace, n_rows doubles.
+ *   d_x_hat   the assembled vector, n_rows doubles (contents on entry unused:
+ *             at the plan's first clock every block arrives).
+ *   d_mask    device [T][P] bytes; row t is the arrival mask of iteration t.
+ *   d_rho     device [T] doubles: the norm of every iteration run.
+ *   d_eff_hist, d_age_hist  optional device [T][P] histories.
+ *   h_iters   out: iterations run.
+ * Synchronises at the end. */
+ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double *d_b, double alpha,
+                       double beta, double *d_x, double *d_x_tmp, double *d_x_hat,
+                       const uint8_t *d_mask, int32_t T, double tol, double *d_rho,
+                       uint8_t *d_eff_hist, int32_t *d_age_hist, int32_t *h_iters);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIBECC_H */

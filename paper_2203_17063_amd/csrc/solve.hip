@@ -1,0 +1,77 @@
+// Loop control of the data path: T iterations of
+//   staleness decision + assembly  ->  block-row sweep  ->  norm  ->  swap,
+// each on the plan's next clock, enqueued without host round trips.  A
+// tolerance is checked on the device: the norm pass raises a flag that makes
+// every later kernel of the loop return at entry, so the state (versions,
+// ages, iterate) is exactly that after the first iteration below tolerance.
+#include <algorithm>
+
+#include "ecc_common.h"
+
+namespace ecc {
+
+__global__ void k_ctrl_reset(int32_t *ctrl) {
+    if (threadIdx.x == 0) {
+        ctrl[0] = 0;
+        ctrl[1] = 0;
+    }
+}
+
+}  // namespace ecc
+
+using namespace ecc;
+
+extern "C" ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double *d_b,
+                                  double alpha, double beta, double *d_x, double *d_x_tmp,
+                                  double *d_x_hat, const uint8_t *d_mask, int32_t T, double tol,
+                                  double *d_rho, uint8_t *d_eff_hist, int32_t *d_age_hist,
+                                  int32_t *h_iters) {
+    clear_error();
+    ecc_status_t st = check_plan(plan);
+    if (st != ECC_OK) return st;
+    ECC_ARG(A != nullptr, "matrix is NULL");
+    if (A->plan != plan) {
+        set_error("matrix was created for another plan");
+        return ECC_ERR_STATE;
+    }
+    ECC_ARG(T >= 0, "T must be >= 0");
+    ECC_ARG(h_iters != nullptr, "h_iters is NULL");
+    const int64_t n = A->A.n_rows;
+    ECC_ARG(n == 0 || (d_x && d_x_tmp && d_x_hat), "NULL vector argument");
+    ECC_ARG(d_x != d_x_tmp && d_x != d_x_hat && d_x_tmp != d_x_hat, "vectors must be distinct");
+    ECC_ARG(T == 0 || (d_mask && d_rho), "d_mask and d_rho are required");
+    ECC_ARG(A->kind != ECC_KIND_JACOBI || n == 0 || d_b, "d_b is NULL");
+    const int32_t norm = (A->kind == ECC_KIND_JACOBI) ? ECC_NORM_L2 : ECC_NORM_L1;
+    const int64_t clock0 = plan->clock;
+    const int32_t P = plan->P;
+
+    hipLaunchKernelGGL(k_ctrl_reset, dim3(1), dim3(64), 0, plan->stream, plan->d_ctrl);
+    ECC_LAUNCH_CHECK();
+    const int32_t *done = plan->d_ctrl;
+    double *cur = d_x, *nxt = d_x_tmp;
+    for (int32_t t = 0; t < T; ++t) {
+        st = launch_assemble(plan, nullptr, cur, d_x_hat, d_mask + (int64_t)t * P,
+                             d_eff_hist ? d_eff_hist + (int64_t)t * P : nullptr,
+                             d_age_hist ? d_age_hist + (int64_t)t * P : nullptr, done);
+        if (st != ECC_OK) return st;
+        st = launch_sweep(A, d_b, alpha, beta, cur, d_x_hat, nxt, A->d_partials, 0, done);
+        if (st != ECC_OK) return st;
+        st = solve_pass2(A, norm, d_b, alpha, beta, cur, nxt, d_rho + t, tol, plan->d_ctrl, t,
+                         done);
+        if (st != ECC_OK) return st;
+        std::swap(cur, nxt);
+    }
+    int32_t ctrl[2] = {0, 0};
+    ECC_HIP(hipMemcpyAsync(ctrl, plan->d_ctrl, sizeof(ctrl), hipMemcpyDeviceToHost, plan->stream));
+    ECC_HIP(hipStreamSynchronize(plan->stream));
+    const int32_t iters = ctrl[1];
+    plan->clock = clock0 + iters;
+    *h_iters = iters;
+    // iterate x^iters sits in d_x for an even count, in d_x_tmp for an odd one
+    if ((iters & 1) && n > 0) {
+        ECC_HIP(hipMemcpyAsync(d_x, d_x_tmp, sizeof(double) * n, hipMemcpyDeviceToDevice,
+                               plan->stream));
+        ECC_HIP(hipStreamSynchronize(plan->stream));
+    }
+    return ECC_OK;
+}
