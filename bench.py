@@ -1,0 +1,462 @@
+#!/usr/bin/env python3
+"""Benchmark of the eventually consistent collective data path on one MI355X.
+
+Default workload: 2-D 5-point Laplacian 1024x1024 (diagonal 8), 16 uneven
+block-row ranks, Bernoulli(0.9) arrivals, maximum staleness 3, 200 Jacobi
+iterations.  One step = one complete solve (plan reset, then 200 x
+[staleness decision + allgatherv assembly -> block-row sweep -> residual
+norm]) on inputs already resident in HBM.
+
+Metric: assembled+iterated GB/s (algorithmic bytes of assembly + sweep + norm,
+each distinct element counted once) and iterations/s, with the dominant
+kernel's achieved bandwidth against the HBM roofline.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--config 1|2|3|4a|4b|5]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD specification
+METRIC = "assembled+iterated GB/s and iterations/s at 1 GPU; % of HBM peak"
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def sweep_bytes(n, nnz):
+    """Algorithmic bytes of one sweep: col + val per nonzero, row_ptr, the x view,
+    b (or x_own for the update norm), the written iterate."""
+    return 12 * nnz + 28 * n + 4
+
+
+def kernel_source_digest(names):
+    h = hashlib.sha256()
+    for nm in names:
+        with open(os.path.join(ROOT, "paper_2203_17063_amd", "csrc", nm), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(kernel_tag, digest):
+    """HBM traffic per launch from the committed rocprofv3 counter summary, or
+    None when absent or taken on other kernel sources."""
+    path = os.path.join(PROFILES, "%s.counters.txt" % kernel_tag)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_digest") != digest:
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+# ----------------------------------------------------------------------------
+# workloads
+# ----------------------------------------------------------------------------
+
+def build_workload(cfg):
+    import workloads as W
+    if cfg == "1":
+        return W.config1()
+    if cfg == "2":
+        return W.config2()
+    if cfg == "3":
+        return W.config3()
+    if cfg == "5":
+        return W.config5()
+    if cfg == "4a":
+        return W.config4a()
+    if cfg == "4b":
+        return W.config4b()
+    raise ValueError(cfg)
+
+
+def describe(cfg, prob):
+    if cfg in ("1", "2", "5"):
+        dims = {"1": "1-D tridiagonal", "2": "2-D 5-point", "5": "3-D 7-point"}[cfg]
+        return {"workload": "jacobi %s Laplacian n=%d, P=%d block-row ranks, S=%d, %s arrivals, "
+                            "%d iterations" % (dims, prob.n, prob.P, prob.S,
+                                               "all" if cfg == "1" else "Bernoulli",
+                                               prob.T),
+                "n": prob.n, "nnz": prob.A.nnz, "P": prob.P, "max_staleness": prob.S,
+                "iterations": prob.T, "config_id": cfg}
+    if cfg == "3":
+        return {"workload": "pagerank power iteration on R-MAT scale %d (%d edges), P=%d, S=%d, "
+                            "Bernoulli(0.8), <=%d iterations or L1 < 1e-10"
+                            % (prob.meta["scale"], prob.A.nnz, prob.P, prob.S, prob.T),
+                "n": prob.n, "nnz": prob.A.nnz, "P": prob.P, "max_staleness": prob.S,
+                "iterations": prob.T, "config_id": cfg}
+    if cfg == "4a":
+        return {"workload": "allgatherv assembly, P=%d lognormal counts, %d elements, %d reps"
+                            % (prob.P, int(prob.counts.sum()), prob.reps),
+                "P": prob.P, "elements": int(prob.counts.sum()), "reps": prob.reps,
+                "config_id": cfg}
+    return {"workload": "partial allreduce-sum, P=%d x %d elements, Bernoulli(%.1f), stale "
+                        "substitution, %d reps" % (prob.P, prob.m, prob.q, prob.reps),
+            "P": prob.P, "m": prob.m, "reps": prob.reps, "config_id": cfg}
+
+
+# ----------------------------------------------------------------------------
+# GPU legs
+# ----------------------------------------------------------------------------
+
+def run_iterative_gpu(cfg, prob, steps, warmup):
+    import torch
+    from paper_2203_17063_amd import capi as E
+    from paper_2203_17063_amd import runner as R
+
+    mem0 = torch.cuda.mem_get_info()[0]
+    run = R.Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts, prob.S,
+                      prob.mask, prob.kind, b=prob.b, alpha=prob.alpha, beta=prob.beta,
+                      x0=prob.x0)
+    torch.cuda.synchronize()
+    footprint = mem0 - torch.cuda.mem_get_info()[0]
+    # one untimed solve records the eff history (bytes of the assembly)
+    iters = run.solve(tol=prob.tol, histories=True)
+    eff_hist = run.eff_hist.cpu().numpy()[:iters]
+    for _ in range(warmup):
+        run.solve(tol=prob.tol)
+    E.ecc_plan_set_timing(run.plan.handle, True)
+    for k in (E.ECC_TIMING_ASSEMBLE, E.ECC_TIMING_SWEEP, E.ECC_TIMING_NORM):
+        E.ecc_plan_timing(run.plan.handle, k, reset=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        it = run.solve(tol=prob.tol)
+        assert it == iters
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    times = {k: E.ecc_plan_timing(run.plan.handle, getattr(E, "ECC_TIMING_" + k))
+             for k in ("ASSEMBLE", "SWEEP", "NORM")}
+    E.ecc_plan_set_timing(run.plan.handle, False)
+    # untimed reference: same solves without the timing events
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(steps):
+        run.solve(tol=prob.tol)
+    torch.cuda.synchronize()
+    wall_plain = time.perf_counter() - t1
+    rho = run.d_rho.cpu().numpy()[:iters]
+    n_part = int(run.d_partials.numel())
+    run.close()
+
+    counts = prob.counts
+    eff_elems = np.array([int(counts[eff_hist[t] == 1].sum()) for t in range(iters)])
+    # algorithmic bytes of the data path: assembly (read + write of every
+    # arrived element), sweep, norm partials
+    b_assemble = float(np.sum(16 * eff_elems + 14 * prob.P))
+    b_sweep = float(sweep_bytes(prob.n, prob.A.nnz))
+    b_norm = 8.0 * n_part
+    bytes_per_step = b_assemble + iters * (b_sweep + b_norm)
+    # one fused launch per iteration: the sweep plus the write of the arrived
+    # blocks into the assembled vector (their read is the sweep's own x read)
+    fused = times["SWEEP"][1] > 0 and times["ASSEMBLE"][1] == 0
+    dom = b_sweep + b_norm + (8.0 * float(eff_elems.mean()) + 14 * prob.P if fused else 0.0)
+    return {
+        "iters": iters, "wall": wall, "wall_plain": wall_plain, "times": times,
+        "bytes_per_step": bytes_per_step, "dominant": "sweep",
+        "dominant_bytes": dom, "footprint": footprint, "rho_last": float(rho[-1]),
+        "unit_per_step": iters, "fused": fused,
+    }
+
+
+def run_allgatherv_gpu(prob, steps, warmup):
+    import torch
+    from paper_2203_17063_amd import capi as E
+    from paper_2203_17063_amd import runner as R
+
+    mem0 = torch.cuda.mem_get_info()[0]
+    send = torch.from_numpy(prob.send).cuda()
+    recv = torch.empty_like(send)
+    d_mask = torch.from_numpy(prob.mask).cuda()
+    plan = R.Plan(prob.P, prob.counts, prob.displs, prob.S)
+    torch.cuda.synchronize()
+    footprint = mem0 - torch.cuda.mem_get_info()[0]
+
+    def step():
+        plan.reset()
+        for r in range(prob.reps):
+            E.ecc_allgatherv_assemble_packed(plan.handle, send, recv, d_mask[r].data_ptr())
+
+    for _ in range(warmup):
+        step()
+    E.ecc_plan_set_timing(plan.handle, True)
+    E.ecc_plan_timing(plan.handle, E.ECC_TIMING_ASSEMBLE, reset=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    times = {"ASSEMBLE": E.ecc_plan_timing(plan.handle, E.ECC_TIMING_ASSEMBLE)}
+    E.ecc_plan_set_timing(plan.handle, False)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    wall_plain = time.perf_counter() - t1
+    assert torch.equal(recv, send)
+    plan.close()
+    per_rep = 16.0 * float(prob.counts.sum()) + 14 * prob.P
+    return {"iters": prob.reps, "wall": wall, "wall_plain": wall_plain, "times": times,
+            "bytes_per_step": per_rep * prob.reps, "dominant": "assemble",
+            "dominant_bytes": per_rep, "footprint": footprint, "unit_per_step": prob.reps}
+
+
+def run_allreduce_gpu(prob, steps, warmup):
+    import torch
+    from paper_2203_17063_amd import capi as E
+    from paper_2203_17063_amd import runner as R
+
+    mem0 = torch.cuda.mem_get_info()[0]
+    P, m = prob.P, prob.m
+    # every repetition reuses rank p's repetition-0 contribution (same bytes moved)
+    fresh = [torch.from_numpy(prob.fresh(p, 0)).cuda() for p in range(P)]
+    slots = [torch.empty(m, dtype=torch.float64, device="cuda") for _ in range(P)]
+    result = torch.empty(m, dtype=torch.float64, device="cuda")
+    d_fresh, d_slots = R.ptr_array(fresh), R.ptr_array(slots)
+    d_mask = torch.from_numpy(prob.mask).cuda()
+    plan = R.Plan(P, None, None, prob.S)
+    eff = torch.empty((prob.reps, P), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    footprint = mem0 - torch.cuda.mem_get_info()[0]
+
+    def step(record=False):
+        plan.reset()
+        for r in range(prob.reps):
+            E.ecc_allreduce_partial(plan.handle, m, d_fresh, d_slots, result,
+                                    d_mask[r].data_ptr(), eff[r] if record else None)
+
+    step(record=True)
+    n_eff = eff.sum(dim=1).cpu().numpy().astype(np.int64)
+    for _ in range(warmup):
+        step()
+    E.ecc_plan_set_timing(plan.handle, True)
+    E.ecc_plan_timing(plan.handle, E.ECC_TIMING_ALLREDUCE, reset=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    times = {"ALLREDUCE": E.ecc_plan_timing(plan.handle, E.ECC_TIMING_ALLREDUCE)}
+    E.ecc_plan_set_timing(plan.handle, False)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    wall_plain = time.perf_counter() - t1
+    plan.close()
+    per_rep = [8.0 * m * (P + int(a) + 1) + 14 * P for a in n_eff]
+    return {"iters": prob.reps, "wall": wall, "wall_plain": wall_plain, "times": times,
+            "bytes_per_step": float(sum(per_rep)), "dominant": "allreduce",
+            "dominant_bytes": float(np.mean(per_rep)), "footprint": footprint,
+            "unit_per_step": prob.reps}
+
+
+# ----------------------------------------------------------------------------
+# CPU baseline: the oracle as it stands, on a bounded sample
+# ----------------------------------------------------------------------------
+
+def cpu_baseline(cfg, prob, res, budget_s=12.0):
+    import oracle
+    cores = 1
+    if cfg in ("1", "2", "3", "5"):
+        # whole iterations of the oracle; sample = first k iterations
+        per_iter_bytes = res["bytes_per_step"] / res["iters"]
+        t0 = time.perf_counter()
+        k = 0
+        sample_iters = res["iters"] if cfg in ("1", "2") else min(res["iters"], 8)
+        done_iters = 0
+        while True:
+            oracle.run_iterative(prob, T=sample_iters, threads=cores)
+            done_iters += sample_iters
+            k += 1
+            if time.perf_counter() - t0 >= budget_s or cfg in ("3", "5") or k >= 50:
+                break
+        dt = time.perf_counter() - t0
+        gbs = per_iter_bytes * done_iters / dt / 1e9
+        return {"value": round(gbs, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
+                "sample": "%d oracle iterations (%d run(s) of %d) of this workload, 1 thread, "
+                          "%.1f s; %.3g iterations/s" % (done_iters, k, sample_iters, dt,
+                                                         done_iters / dt)}
+    if cfg == "4a":
+        version = np.full(prob.P, -1, dtype=np.int32)
+        recv = np.empty_like(prob.send)
+        sends = [prob.send[d:d + c] for d, c in zip(prob.displs, prob.counts)]
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < budget_s and reps < prob.reps:
+            eff, _, _ = oracle.select(prob.S, reps, prob.mask[reps], version)
+            oracle.allgatherv(prob.counts, prob.displs, eff, sends, recv)
+            reps += 1
+        dt = time.perf_counter() - t0
+        per_rep = res["bytes_per_step"] / res["iters"]
+        return {"value": round(per_rep * reps / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
+                "kind": "oracle", "sample": "%d of %d repetitions, 1 thread, %.1f s"
+                                            % (reps, prob.reps, dt)}
+    # 4b: a few repetitions over stored vectors
+    P, m = prob.P, prob.m
+    fresh = [prob.fresh(p, 0) for p in range(P)]
+    slots = [np.zeros(m) for _ in range(P)]
+    version = np.full(P, -1, dtype=np.int32)
+    t0 = time.perf_counter()
+    reps = 0
+    nbytes = 0.0
+    while time.perf_counter() - t0 < budget_s and reps < prob.reps:
+        eff, _, _ = oracle.select(prob.S, reps, prob.mask[reps], version)
+        oracle.allreduce(eff, fresh, slots)
+        nbytes += 8.0 * m * (P + int(eff.sum()) + 1)
+        reps += 1
+    dt = time.perf_counter() - t0
+    return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
+            "kind": "oracle", "sample": "%d of %d repetitions over stored vectors, 1 thread, "
+                                        "%.1f s" % (reps, prob.reps, dt)}
+
+
+def copy_probe(n_doubles=1 << 29, reps=10):
+    """Measured copy ceiling: a plain 16-byte streaming copy of 4 GiB (far
+    beyond the 256 MB Infinity Cache) with libecc's ecc_stream_copy, and the
+    runtime's own device-to-device copy for comparison; read + write bytes per
+    second."""
+    import torch
+    from paper_2203_17063_amd import capi as E
+    x = torch.empty(n_doubles, dtype=torch.float64, device="cuda").fill_(1.0)
+    y = torch.empty_like(x)
+    stream = torch.cuda.current_stream().cuda_stream
+    out = {}
+    for name, fn in (("ecc_stream_copy", lambda: E.ecc_stream_copy(y, x, n_doubles, stream)),
+                     ("runtime_copy", lambda: y.copy_(x))):
+        fn()
+        torch.cuda.synchronize()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for _ in range(reps):
+            fn()
+        ev1.record()
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / reps
+        nbytes = 2 * 8 * n_doubles
+        out[name] = {"bytes_per_copy": nbytes, "avg_ms": round(ms, 4),
+                     "gbs": round(nbytes / ms / 1e6, 2),
+                     "frac_of_peak": round(nbytes / ms / 1e6 / HBM_PEAK_GBS, 4)}
+    assert torch.equal(x, y)
+    return {"copy_probe": out}
+
+
+# ----------------------------------------------------------------------------
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="2", choices=["1", "2", "3", "4a", "4b", "5"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only measure a plain 4 GiB device copy (copy ceiling)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the data path runs P virtual ranks inside one "
+              "GPU's HBM and this build has no multi-GPU leg (requested --gpus %d)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    from paper_2203_17063_amd import capi
+    capi.lib()
+    if args.copy_probe:
+        print(json.dumps(copy_probe()), flush=True)
+        return
+
+    cfg = args.config
+    print("[bench] generating workload config %s" % cfg, file=sys.stderr, flush=True)
+    prob = build_workload(cfg)
+    print("[bench] running on GPU", file=sys.stderr, flush=True)
+    if cfg in ("1", "2", "3", "5"):
+        res = run_iterative_gpu(cfg, prob, args.steps, args.warmup)
+        digest = kernel_source_digest(["sweep.hip", "ecc_common.h"])
+        tag = "sweep_%s_cfg%s" % ("jacobi" if prob.kind == "jacobi" else "pagerank", cfg)
+        dom_ms, dom_n = res["times"]["SWEEP"]
+    elif cfg == "4a":
+        res = run_allgatherv_gpu(prob, args.steps, args.warmup)
+        digest = kernel_source_digest(["collectives.hip", "ecc_common.h"])
+        tag = "assemble_cfg4a"
+        dom_ms, dom_n = res["times"]["ASSEMBLE"]
+    else:
+        res = run_allreduce_gpu(prob, args.steps, args.warmup)
+        digest = kernel_source_digest(["collectives.hip", "ecc_common.h"])
+        tag = "allreduce_cfg4b"
+        dom_ms, dom_n = res["times"]["ALLREDUCE"]
+
+    steps = args.steps
+    wall = res["wall"]
+    ms_per_step = wall / steps * 1e3
+    gbs = res["bytes_per_step"] * steps / wall / 1e9
+    iters_per_s = res["unit_per_step"] * steps / wall
+    avg_dom_s = dom_ms / max(dom_n, 1) / 1e3
+    achieved = res["dominant_bytes"] / avg_dom_s / 1e9 if avg_dom_s > 0 else None
+    traffic = read_traffic(tag, digest)
+    line = {
+        "metric": METRIC,
+        "value": round(gbs, 3),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic (seeded generators; no dataset)",
+        "config": describe(cfg, prob),
+        "iterations_per_s": round(iters_per_s, 2),
+        "hbm_peak_frac": round(gbs / HBM_PEAK_GBS, 4),
+        "ms_per_step_without_timing_events": round(res["wall_plain"] / steps * 1e3, 4),
+        "peak_hbm_footprint_gb": round(res["footprint"] / 1e9, 3),
+        "kernel_avg_us": {k.lower(): round(v[0] / max(v[1], 1) * 1e3, 3)
+                          for k, v in res["times"].items()},
+        "roofline": {
+            "kernel": tag,
+            "bound": "hbm",
+            "achieved": round(achieved, 2) if achieved else None,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": res["dominant_bytes"],
+            "avg_launch_us": round(avg_dom_s * 1e6, 3),
+            "launches_timed": dom_n,
+        },
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] oracle CPU baseline", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(cfg, prob, res)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -122,6 +122,20 @@ ecc_status_t ecc_plan_set_stream(ecc_plan_t plan, void *hip_stream);
 ecc_status_t ecc_plan_stats(ecc_plan_t plan, int64_t *clock, int64_t *forced_total,
                             int32_t *h_version, int32_t *h_age);
 
+/* Optional per-kernel timing on the plan's stream (diagnostics).  While
+ * enabled, each launch of the libecc kernels below is bracketed by two HIP
+ * events recorded on the plan's stream; ecc_plan_timing synchronises, adds
+ * up the elapsed times of the launches recorded so far for one kernel, and
+ * optionally clears them.  Disabled by default; enabling it adds two event
+ * records per launch. */
+#define ECC_TIMING_ASSEMBLE 0   /* staleness decision + assembly */
+#define ECC_TIMING_ALLREDUCE 1  /* partial allreduce             */
+#define ECC_TIMING_SWEEP 2      /* Jacobi / power-iteration sweep */
+#define ECC_TIMING_NORM 3       /* split-row fix-up + norm pass  */
+ecc_status_t ecc_plan_set_timing(ecc_plan_t plan, int32_t enable);
+ecc_status_t ecc_plan_timing(ecc_plan_t plan, int32_t kernel, double *total_ms,
+                             int64_t *launches, int32_t reset);
+
 /* ---------------------------------------------------------------------------
  * Collectives.  Each call is one clock step t = current clock (Algorithm 1
  * increments the clock on entry; t is that value minus one) and advances the
@@ -241,6 +255,14 @@ ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double *d_b, doubl
                        double beta, double *d_x, double *d_x_tmp, double *d_x_hat,
                        const uint8_t *d_mask, int32_t T, double tol, double *d_rho,
                        uint8_t *d_eff_hist, int32_t *d_age_hist, int32_t *h_iters);
+
+/* ---------------------------------------------------------------------------
+ * Measurement utility: a plain streaming copy d_dst[i] = d_src[i], 0 <= i < n,
+ * with 16-byte accesses (both buffers 16-byte aligned, n even, no overlap),
+ * enqueued on hip_stream.  Benchmarks use it as the copy ceiling of the
+ * device memory and to calibrate hardware byte counters.
+ * ------------------------------------------------------------------------- */
+ecc_status_t ecc_stream_copy(double *d_dst, const double *d_src, int64_t n, void *hip_stream);
 
 #ifdef __cplusplus
 }

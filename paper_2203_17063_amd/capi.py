@@ -20,6 +20,7 @@ ECC_ERR_ALLOC, ECC_ERR_DEVICE, ECC_ERR_STATE = 4, 5, 6
 ECC_UNBOUNDED = 0x7FFFFFFF
 ECC_NORM_L1, ECC_NORM_L2 = 1, 2
 ECC_KIND_JACOBI, ECC_KIND_POWER = 0, 1
+ECC_TIMING_ASSEMBLE, ECC_TIMING_ALLREDUCE, ECC_TIMING_SWEEP, ECC_TIMING_NORM = 0, 1, 2, 3
 
 STATUS_NAMES = {0: "ECC_OK", 1: "ECC_ERR_ARG", 2: "ECC_ERR_OVERLAP", 3: "ECC_ERR_RANGE",
                 4: "ECC_ERR_ALLOC", 5: "ECC_ERR_DEVICE", 6: "ECC_ERR_STATE"}
@@ -51,6 +52,8 @@ _SIGS = [
     ("ecc_plan_reset", ctypes.c_int, [_VP]),
     ("ecc_plan_set_stream", ctypes.c_int, [_VP, _VP]),
     ("ecc_plan_stats", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP]),
+    ("ecc_plan_set_timing", ctypes.c_int, [_VP, _I32]),
+    ("ecc_plan_timing", ctypes.c_int, [_VP, _I32, _VP, _VP, _I32]),
     ("ecc_allgatherv_assemble", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP]),
     ("ecc_allgatherv_assemble_packed", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP]),
     ("ecc_allreduce_partial", ctypes.c_int, [_VP, _I64, _VP, _VP, _VP, _VP, _VP, _VP]),
@@ -60,6 +63,7 @@ _SIGS = [
     ("ecc_iterate_jacobi", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     ("ecc_iterate_spmv", ctypes.c_int, [_VP, _VP, _D, _D, _VP, _VP, _VP, _VP]),
     ("ecc_residual", ctypes.c_int, [_VP, _VP, _I64, _I32, _VP, _VP]),
+    ("ecc_stream_copy", ctypes.c_int, [_VP, _VP, _I64, _VP]),
     ("ecc_solve", ctypes.c_int, [_VP, _VP, _VP, _D, _D, _VP, _VP, _VP, _VP, _I32, _D, _VP, _VP,
                                  _VP, _VP]),
 ]
@@ -153,6 +157,19 @@ def ecc_plan_stats(plan, P: int):
     return clock.value, forced.value, ver, age
 
 
+def ecc_plan_set_timing(plan, enable: bool):
+    _check(lib().ecc_plan_set_timing(plan, 1 if enable else 0))
+
+
+def ecc_plan_timing(plan, kernel: int, reset: bool = False):
+    """Returns (total_ms, launches) of the launches of `kernel` timed so far."""
+    ms = ctypes.c_double()
+    n = ctypes.c_int64()
+    _check(lib().ecc_plan_timing(plan, kernel, ctypes.addressof(ms), ctypes.addressof(n),
+                                 1 if reset else 0))
+    return ms.value, n.value
+
+
 def ecc_allgatherv_assemble(plan, d_send, d_recv, d_arrived, d_eff_out=None, d_age_out=None):
     _check(lib().ecc_allgatherv_assemble(plan, _ptr(d_send), _ptr(d_recv), _ptr(d_arrived),
                                          _ptr(d_eff_out), _ptr(d_age_out)))
@@ -214,3 +231,7 @@ def ecc_solve(plan, mat, d_b, alpha, beta, d_x, d_x_tmp, d_x_hat, d_mask, T, tol
                            _ptr(d_x_hat), _ptr(d_mask), T, tol, _ptr(d_rho), _ptr(d_eff_hist),
                            _ptr(d_age_hist), ctypes.addressof(iters)))
     return iters.value
+
+
+def ecc_stream_copy(d_dst, d_src, n, stream=None):
+    _check(lib().ecc_stream_copy(_ptr(d_dst), _ptr(d_src), n, stream))

@@ -13,47 +13,6 @@
 
 namespace ecc {
 
-// Bookkeeping of one step (run by workgroup 0): new versions and ages, the
-// eff flags, the forced-arrival count and, for reductions, the clock of the
-// result (the minimum version).
-__device__ void record_step(int32_t P, int32_t S, int64_t t, const uint8_t *__restrict__ arrived,
-                            const int32_t *__restrict__ ver_in, int32_t *__restrict__ ver_out,
-                            int32_t *__restrict__ age_state, uint8_t *__restrict__ eff_state,
-                            unsigned long long *__restrict__ forced,
-                            uint8_t *__restrict__ eff_user, int32_t *__restrict__ age_user,
-                            int32_t *__restrict__ result_clock) {
-    __shared__ int s_cnt[1024];
-    __shared__ int s_min[1024];
-    int cnt = 0, mn = 0x7fffffff;
-    for (int32_t p = threadIdx.x; p < P; p += blockDim.x) {
-        const int32_t v = ver_in[p];
-        const uint8_t a = arrived[p];
-        const bool e = stale_select(v, a, t, S);
-        if (e && a == 0 && v >= 0) ++cnt;
-        const int32_t nv = e ? (int32_t)t : v;
-        const int32_t age = (int32_t)(t - nv);
-        ver_out[p] = nv;
-        age_state[p] = age;
-        eff_state[p] = e ? 1 : 0;
-        if (eff_user) eff_user[p] = e ? 1 : 0;
-        if (age_user) age_user[p] = age;
-        mn = min(mn, nv);
-    }
-    s_cnt[threadIdx.x] = cnt;
-    s_min[threadIdx.x] = mn;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        unsigned long long total = 0;
-        int m = 0x7fffffff;
-        for (int i = 0; i < (int)blockDim.x; ++i) {
-            total += (unsigned long long)s_cnt[i];
-            m = min(m, s_min[i]);
-        }
-        *forced = *forced + total;
-        if (result_clock) *result_clock = m;
-    }
-}
-
 // Assembly: workgroup 0 records the step; workgroup 1 + k copies tile k if
 // its rank's block is taken at this step.  Copies use 16-byte accesses when
 // source and destination have the same alignment modulo 16 bytes.
@@ -226,6 +185,7 @@ ecc_status_t launch_assemble(ecc_plan_t plan, const double *const *d_send,
         set_error("too many assembly tiles");
         return ECC_ERR_RANGE;
     }
+    TimedLaunch timed(plan, ECC_TIMING_ASSEMBLE);
     hipLaunchKernelGGL(k_assemble, dim3((unsigned)grid), dim3(kAssembleThreads), 0, plan->stream,
                        plan->P, plan->S, t, d_arrived, ver_in, ver_out, plan->d_age, plan->d_eff,
                        plan->d_forced, d_eff_out, d_age_out, plan->d_tiles, plan->d_displs,
@@ -296,6 +256,7 @@ ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *con
     const int64_t t = plan->clock;
     const int32_t *ver_in = plan->d_version + (t & 1) * plan->P;
     int32_t *ver_out = plan->d_version + ((t + 1) & 1) * plan->P;
+    TimedLaunch timed(plan, ECC_TIMING_ALLREDUCE);
     hipLaunchKernelGGL(k_allreduce, dim3((unsigned)grid), dim3(kReduceThreads), 0, plan->stream,
                        plan->P, plan->S, t, d_arrived, ver_in, ver_out, plan->d_age, plan->d_eff,
                        plan->d_forced, d_eff_out, d_result_clock, m, d_fresh, d_slots, d_result);

@@ -56,7 +56,9 @@ constexpr int kSweepThreads = 256;
 constexpr int kStreamCap = 2048;         // nonzeros staged in LDS by a stream item
 constexpr int kStreamRows = 256;         // rows of one stream item at most
 constexpr int kVectorCap = 16384;        // nonzeros of one vector item / piece
-constexpr int kPass2Threads = 1024;
+constexpr int kMaxSweepBlocks = 8192;    // workgroups of one sweep launch at most
+constexpr int kFusedMaxP = 1024;         // ranks whose state a fused sweep stages in LDS
+constexpr int kNormThreads = 256;        // threads of every norm reduction
 
 // One assembly tile: `len` elements of rank `rank` starting `off` elements
 // into its block.
@@ -66,18 +68,24 @@ struct Tile {
     int32_t len;
 };
 
-// One sweep work item.  kind: 0 stream (rows [row0, row0 + a)), 1 vector (row
-// row0 by the whole workgroup), 2 piece a of row row0 (nonzeros
-// [row_ptr[row0] + a*kVectorCap, ...), result to piece slot b).
+// One sweep work item: rows [row0, row0 + nrows) of rank `rank`, whose block
+// is [lo, hi), touching nonzeros [k0, k1).  kind: stream (many short rows
+// staged in LDS), vector (one long row, whole workgroup) or piece (slice
+// [k0, k1) of a very long row; its partial sum goes to piece slot `slot`).
 enum { kItemStream = 0, kItemVector = 1, kItemPiece = 2 };
 struct WorkItem {
     int32_t row0;
-    int32_t a;
-    int32_t b;
-    int32_t kind_rank;  // kind << 24 | rank
+    int32_t nrows;
+    int32_t k0, k1;
+    int32_t lo, hi;
+    int32_t kind;
+    int32_t rank;
+    int32_t slot;
+    int32_t pad[3];
 };
+static_assert(sizeof(WorkItem) == 48, "work item layout");
 
-// A row split into pieces, recombined by the second pass in piece order.
+// A row split into pieces, recombined by the last workgroup in piece order.
 struct Fixup {
     int32_t row;
     int32_t slot0;
@@ -153,6 +161,71 @@ __device__ __forceinline__ double block_sum(double v, double *scratch) {
     return total;
 }
 
+// Bookkeeping of one clock step (run by one whole workgroup): new versions
+// and ages, the eff flags, the forced-arrival count and the minimum version
+// (the clock of a reduced result).  Returns nothing; thread 0 writes.
+__device__ __forceinline__ void record_step(int32_t P, int32_t S, int64_t t,
+                                            const uint8_t *__restrict__ arrived,
+                                            const int32_t *__restrict__ ver_in,
+                                            int32_t *__restrict__ ver_out,
+                                            int32_t *__restrict__ age_state,
+                                            uint8_t *__restrict__ eff_state,
+                                            unsigned long long *__restrict__ forced,
+                                            uint8_t *__restrict__ eff_user,
+                                            int32_t *__restrict__ age_user,
+                                            int32_t *__restrict__ result_clock) {
+    __shared__ int s_cnt[16];
+    __shared__ int s_min[16];
+    int cnt = 0, mn = 0x7fffffff;
+    for (int32_t p = threadIdx.x; p < P; p += blockDim.x) {
+        const int32_t v = ver_in[p];
+        const uint8_t a = arrived[p];
+        const bool e = stale_select(v, a, t, S);
+        if (e && a == 0 && v >= 0) ++cnt;
+        const int32_t nv = e ? (int32_t)t : v;
+        const int32_t age = (int32_t)(t - nv);
+        ver_out[p] = nv;
+        age_state[p] = age;
+        eff_state[p] = e ? 1 : 0;
+        if (eff_user) eff_user[p] = e ? 1 : 0;
+        if (age_user) age_user[p] = age;
+        mn = min(mn, nv);
+    }
+    for (int off = 32; off >= 1; off >>= 1) {
+        cnt += __shfl_xor(cnt, off, 64);
+        mn = min(mn, __shfl_xor(mn, off, 64));
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        s_cnt[wave] = cnt;
+        s_min[wave] = mn;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long total = 0;
+        int m = 0x7fffffff;
+        for (int w = 0; w < (int)(blockDim.x >> 6); ++w) {
+            total += (unsigned long long)s_cnt[w];
+            m = min(m, s_min[w]);
+        }
+        *forced = *forced + total;
+        if (result_clock) *result_clock = m;
+    }
+    __syncthreads();
+}
+
+// Deterministic reduction of n values to their sum by kNormThreads threads:
+// thread j adds values j, j + kNormThreads, ... in order, then a fixed tree.
+// The value at index `n - 1` may be supplied in a register (`last`, used when
+// `use_last`) instead of being read, with the same order of operations.
+__device__ __forceinline__ double reduce_values(const double *__restrict__ v, int64_t n,
+                                                bool use_last, double last, double *scratch) {
+    double acc = 0.0;
+    for (int64_t k = threadIdx.x; k < n; k += kNormThreads)
+        acc += (use_last && k == n - 1) ? last : v[k];
+    return block_sum<kNormThreads>(acc, scratch);
+}
+
 }  // namespace ecc
 
 // ---------------------------------------------------------------------------
@@ -181,6 +254,13 @@ struct ecc_plan_s {
     int64_t n_tiles = 0;
     int32_t *d_ctrl = nullptr;      // [0] done flag, [1] iterations run (loop control)
     double *d_scalar = nullptr;     // scratch result of ecc_residual
+
+    // optional event timing per kernel kind
+    bool timing = false;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> pending[4];
+    std::vector<hipEvent_t> event_pool;
+    double timed_ms[4] = {0, 0, 0, 0};
+    int64_t timed_launches[4] = {0, 0, 0, 0};
 };
 
 struct ecc_matrix_s {
@@ -193,7 +273,8 @@ struct ecc_matrix_s {
     int64_t n_fixups = 0;
     double2 *d_pieces = nullptr;    // (partial sum, diagonal) per piece
     int64_t n_pieces = 0;
-    double *d_partials = nullptr;   // internal partials used by ecc_solve
+    int32_t grid = 1;               // workgroups of a sweep launch
+    double *d_partials = nullptr;   // internal partials of ecc_solve: 2 x (grid + 1)
 };
 
 namespace ecc {
@@ -202,12 +283,52 @@ ecc_status_t launch_assemble(ecc_plan_t plan, const double *const *d_send,
                              const double *d_send_base, double *d_recv,
                              const uint8_t *d_arrived, uint8_t *d_eff_out, int32_t *d_age_out,
                              const int32_t *d_done);
-ecc_status_t launch_sweep(ecc_matrix_t M, const double *d_b, double alpha, double beta,
-                          const double *d_x_own, const double *d_x_hat, double *d_x_next,
-                          double *d_partials, int32_t zero_extra, const int32_t *d_done);
-// Split-row fix-up plus norm of one loop iteration (internal partials).
-ecc_status_t solve_pass2(ecc_matrix_t M, int32_t norm, const double *d_b, double alpha,
-                         double beta, const double *d_x_own, double *d_x_next, double *d_out,
-                         double tol, int32_t *d_ctrl, int32_t t, const int32_t *d_done);
+// One sweep launch.  With `arrived` non-NULL it is a whole loop iteration:
+// staleness decision, assembly of the arrived blocks into x_hat and the sweep
+// on the assembled view, on the plan's next clock.  Workgroup 0 also reduces
+// `prev_partials` (if given) into *prev_rho with `norm`.
+struct SweepLaunch {
+    const double *b = nullptr;
+    double alpha = 0.0, beta = 0.0;
+    const double *x_own = nullptr;
+    double *x_hat = nullptr;
+    double *x_next = nullptr;
+    double *partials = nullptr;
+    const uint8_t *arrived = nullptr;
+    uint8_t *eff_user = nullptr;
+    int32_t *age_user = nullptr;
+    const double *prev_partials = nullptr;
+    double *prev_rho = nullptr;
+    int32_t norm = 0;
+    const int32_t *done = nullptr;
+};
+ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L);
+// Second pass: split rows (their contribution -> partial G) and, with
+// norm != 0, the norm into *rho_out and the loop control block.
+struct Pass2Launch {
+    double *partials = nullptr;
+    const double *b = nullptr;
+    double alpha = 0.0, beta = 0.0;
+    const double *x_own = nullptr;
+    double *x_next = nullptr;
+    double *x_hat = nullptr;
+    bool step = false;  // loop iteration: also assemble arrived split rows
+    int32_t norm = 0;
+    double *rho_out = nullptr;
+    double tol = 0.0;
+    int32_t *ctrl = nullptr;
+    int64_t t = 0;
+    const int32_t *done = nullptr;
+};
+ecc_status_t launch_pass2(ecc_matrix_t M, const Pass2Launch &L);
 ecc_status_t check_plan(ecc_plan_t plan);
+
+// Event timing around one launch (no-ops unless the plan's timing is on).
+struct TimedLaunch {
+    ecc_plan_t plan;
+    int kind;
+    hipEvent_t start = nullptr, stop = nullptr;
+    TimedLaunch(ecc_plan_t p, int k);
+    ~TimedLaunch();
+};
 }  // namespace ecc

@@ -70,6 +70,32 @@ static std::vector<Tile> make_tiles(const std::vector<int64_t> &counts,
     return tiles;
 }
 
+static hipEvent_t take_event(ecc_plan_t plan) {
+    if (!plan->event_pool.empty()) {
+        hipEvent_t e = plan->event_pool.back();
+        plan->event_pool.pop_back();
+        return e;
+    }
+    // no system-scope fence: the events only order work on this device
+    hipEvent_t e = nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
+    return e;
+}
+
+TimedLaunch::TimedLaunch(ecc_plan_t p, int k) : plan(p), kind(k) {
+    if (!plan || !plan->timing) return;
+    start = take_event(plan);
+    stop = take_event(plan);
+    if (start && stop && hipEventRecord(start, plan->stream) == hipSuccess) return;
+    start = stop = nullptr;
+}
+
+TimedLaunch::~TimedLaunch() {
+    if (!start || !stop) return;
+    if (hipEventRecord(stop, plan->stream) == hipSuccess)
+        plan->pending[kind].push_back({start, stop});
+}
+
 }  // namespace ecc
 
 using namespace ecc;
@@ -227,7 +253,48 @@ ecc_status_t ecc_plan_destroy(ecc_plan_t plan) {
     (void)hipFree(plan->d_displs);
     (void)hipFree(plan->d_tiles);
     (void)hipFree(plan->d_block_start);
+    for (auto &v : plan->pending)
+        for (auto &pr : v) {
+            (void)hipEventDestroy(pr.first);
+            (void)hipEventDestroy(pr.second);
+        }
+    for (hipEvent_t e : plan->event_pool) (void)hipEventDestroy(e);
     delete plan;
+    return ECC_OK;
+}
+
+ecc_status_t ecc_plan_set_timing(ecc_plan_t plan, int32_t enable) {
+    clear_error();
+    ecc_status_t st = check_plan(plan);
+    if (st != ECC_OK) return st;
+    plan->timing = enable != 0;
+    return ECC_OK;
+}
+
+ecc_status_t ecc_plan_timing(ecc_plan_t plan, int32_t kernel, double *total_ms,
+                             int64_t *launches, int32_t reset) {
+    clear_error();
+    ecc_status_t st = check_plan(plan);
+    if (st != ECC_OK) return st;
+    ECC_ARG(kernel >= 0 && kernel < 4, "unknown kernel %d", kernel);
+    ECC_HIP(hipStreamSynchronize(plan->stream));
+    for (int k = 0; k < 4; ++k) {
+        for (auto &pr : plan->pending[k]) {
+            float ms = 0.f;
+            ECC_HIP(hipEventElapsedTime(&ms, pr.first, pr.second));
+            plan->timed_ms[k] += ms;
+            plan->timed_launches[k] += 1;
+            plan->event_pool.push_back(pr.first);
+            plan->event_pool.push_back(pr.second);
+        }
+        plan->pending[k].clear();
+    }
+    if (total_ms) *total_ms = plan->timed_ms[kernel];
+    if (launches) *launches = plan->timed_launches[kernel];
+    if (reset) {
+        plan->timed_ms[kernel] = 0.0;
+        plan->timed_launches[kernel] = 0;
+    }
     return ECC_OK;
 }
 

@@ -1,7 +1,9 @@
 // Loop control of the data path: T iterations of
 //   staleness decision + assembly  ->  block-row sweep  ->  norm  ->  swap,
-// each on the plan's next clock, enqueued without host round trips.  A
-// tolerance is checked on the device: the norm pass raises a flag that makes
+// each on the plan's next clock, enqueued without host round trips.  Each
+// iteration is one fused kernel launch (see sweep.hip) unless the plan has
+// more ranks than a workgroup stages in LDS; then the assembly is its own
+// launch.  A tolerance is checked on the device: the norm pass raises a flag that makes
 // every later kernel of the loop return at entry, so the state (versions,
 // ages, iterate) is exactly that after the first iteration below tolerance.
 #include <algorithm>
@@ -42,23 +44,73 @@ extern "C" ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double 
     ECC_ARG(T == 0 || (d_mask && d_rho), "d_mask and d_rho are required");
     ECC_ARG(A->kind != ECC_KIND_JACOBI || n == 0 || d_b, "d_b is NULL");
     const int32_t norm = (A->kind == ECC_KIND_JACOBI) ? ECC_NORM_L2 : ECC_NORM_L1;
+    ECC_ARG(n == 0 || plan->d_block_start, "plan blocks do not tile the rows");
     const int64_t clock0 = plan->clock;
     const int32_t P = plan->P;
 
     hipLaunchKernelGGL(k_ctrl_reset, dim3(1), dim3(64), 0, plan->stream, plan->d_ctrl);
     ECC_LAUNCH_CHECK();
     const int32_t *done = plan->d_ctrl;
+    const int64_t G1 = (int64_t)A->grid + 1;
+    // Without a tolerance and without split rows, every iteration is a single
+    // launch: workgroup 0 of launch t reduces launch t-1's partials (double
+    // buffer), and one last pass reduces those of the final iteration.
+    // Otherwise a one-workgroup pass follows each sweep (split rows, norm and
+    // the convergence flag).  The assembly is fused into the sweep while the
+    // rank state fits in LDS.
+    const bool fused = P <= kFusedMaxP;
+    const bool deferred = fused && tol <= 0.0 && A->n_fixups == 0;
     double *cur = d_x, *nxt = d_x_tmp;
     for (int32_t t = 0; t < T; ++t) {
-        st = launch_assemble(plan, nullptr, cur, d_x_hat, d_mask + (int64_t)t * P,
-                             d_eff_hist ? d_eff_hist + (int64_t)t * P : nullptr,
-                             d_age_hist ? d_age_hist + (int64_t)t * P : nullptr, done);
+        const int64_t tt = plan->clock;
+        const uint8_t *mask_t = d_mask + (int64_t)t * P;
+        uint8_t *eff_t = d_eff_hist ? d_eff_hist + (int64_t)t * P : nullptr;
+        int32_t *age_t = d_age_hist ? d_age_hist + (int64_t)t * P : nullptr;
+        double *part = A->d_partials + (deferred ? (t & 1) * G1 : 0);
+        if (!fused) {
+            st = launch_assemble(plan, nullptr, cur, d_x_hat, mask_t, eff_t, age_t, done);
+            if (st != ECC_OK) return st;
+        }
+        SweepLaunch L;
+        L.b = d_b;
+        L.alpha = alpha;
+        L.beta = beta;
+        L.x_own = cur;
+        L.x_hat = d_x_hat;
+        L.x_next = nxt;
+        L.partials = part;
+        L.norm = norm;
+        L.done = done;
+        if (fused) {
+            L.arrived = mask_t;
+            L.eff_user = eff_t;
+            L.age_user = age_t;
+        }
+        if (deferred && t > 0) {
+            L.prev_partials = A->d_partials + ((t - 1) & 1) * G1;
+            L.prev_rho = d_rho + (t - 1);
+        }
+        st = launch_sweep(A, L);
         if (st != ECC_OK) return st;
-        st = launch_sweep(A, d_b, alpha, beta, cur, d_x_hat, nxt, A->d_partials, 0, done);
-        if (st != ECC_OK) return st;
-        st = solve_pass2(A, norm, d_b, alpha, beta, cur, nxt, d_rho + t, tol, plan->d_ctrl, t,
-                         done);
-        if (st != ECC_OK) return st;
+        if (!deferred || t == T - 1) {
+            Pass2Launch F;
+            F.partials = part;
+            F.b = d_b;
+            F.alpha = alpha;
+            F.beta = beta;
+            F.x_own = cur;
+            F.x_next = nxt;
+            F.x_hat = d_x_hat;
+            F.step = fused;
+            F.norm = norm;
+            F.rho_out = d_rho + t;
+            F.tol = tol;
+            F.ctrl = plan->d_ctrl;
+            F.t = tt - clock0;
+            F.done = done;
+            st = launch_pass2(A, F);
+            if (st != ECC_OK) return st;
+        }
         std::swap(cur, nxt);
     }
     int32_t ctrl[2] = {0, 0};

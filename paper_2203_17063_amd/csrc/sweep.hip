@@ -9,10 +9,28 @@
 // one rank whose nonzeros fit in LDS -- they are loaded with coalesced
 // accesses and each row is then summed by 1..64 lanes; a "vector" item is one
 // long row summed by the whole workgroup; a "piece" is a fixed-size slice of
-// a very long row whose partial sum is recombined, in piece order, by the
-// second pass.  Items never straddle a rank boundary, so [lo, hi) is uniform
-// per item.  Rows summed by a single lane accumulate in CSR order with no
-// fused multiply-add, exactly like the sequential definition.
+// a very long row whose partial sum is recombined, in piece order, at the
+// end.  Items never straddle a rank boundary, so [lo, hi) is uniform per
+// item.  Rows summed by a single lane accumulate in CSR order with no fused
+// multiply-add, exactly like the sequential definition.
+//
+// Each workgroup writes one partial norm.  Split rows and the reduction of
+// the partials (in a fixed order, so results are deterministic run to run)
+// belong to a second pass that starts after the sweep has finished: a
+// separate one-workgroup launch, or -- in a loop without a tolerance and
+// without split rows -- workgroup 0 of the next iteration's launch.  No
+// device-wide fence or atomic is used inside a launch: on a multi-XCD part
+// an agent-scope release writes back the XCD's L2, which would cost more
+// than the launch boundary.
+//
+// Loop iterations use the same kernel with the staleness decision and the
+// assembly fused in: every workgroup evaluates the decision for all ranks
+// from the previous versions (read-only in this launch), reads a column of
+// another rank from x_own when that rank's block arrives at this step and
+// from x_hat otherwise -- exactly the values the assembled vector holds
+// after the step's assembly -- and writes its own rows into x_hat when its
+// rank arrives.  No entry of x_hat that is written is read in the same
+// launch, so the fused step equals assemble-then-sweep bit for bit.
 #include <algorithm>
 #include <vector>
 
@@ -20,205 +38,367 @@
 
 namespace ecc {
 
-constexpr int kMaxSweepBlocks = 8192;
+struct SweepArgs {
+    const WorkItem *items;
+    int32_t n_items;
+    const int32_t *row_ptr;
+    const int32_t *col;
+    const double *val;
+    const double *b;
+    double alpha, beta;
+    const double *x_own;
+    double *x_hat;
+    double *x_next;
+    double *partials;
+    double2 *pieces;
+    // fused loop iteration (step != 0)
+    int32_t step;
+    int32_t P, S;
+    int64_t t;
+    const uint8_t *arrived;
+    const int32_t *ver_in;
+    int32_t *ver_out;
+    int32_t *age_state;
+    uint8_t *eff_state;
+    unsigned long long *forced;
+    uint8_t *eff_user;
+    int32_t *age_user;
+    const int32_t *block_start;
+    // workgroup 0: zero partial G; reduce the previous iteration's partials
+    int32_t zero_extra;
+    const double *prev_partials;
+    double *prev_rho;
+    int32_t norm;
+    const int32_t *done;
+};
+
+// Rank state staged in LDS by a fused step.
+struct StepView {
+    const uint8_t *eff;   // [P] this step's decision
+    const int32_t *bs;    // [P + 1] block starts
+    int32_t P;
+};
+
+// Does the assembled vector hold x_own at column c (rank of c arrives at this
+// step)?  Binary search of the block starts, with a one-entry per-lane cache.
+__device__ __forceinline__ bool col_arrives(const StepView &v, int32_t c, int32_t &clo,
+                                            int32_t &chi, bool &ceff) {
+    if (c >= clo && c < chi) return ceff;
+    int32_t a = 0, z = v.P;  // bs[a] <= c < bs[z]
+    while (z - a > 1) {
+        const int32_t mid = (a + z) >> 1;
+        if (v.bs[mid] <= c) a = mid;
+        else z = mid;
+    }
+    clo = v.bs[a];
+    chi = v.bs[a + 1];
+    ceff = v.eff[a] != 0;
+    return ceff;
+}
+
+template <bool STEP>
+__device__ __forceinline__ double view_load(int32_t c, int32_t lo, int32_t hi,
+                                            const double *__restrict__ x_own,
+                                            const double *__restrict__ x_hat,
+                                            const StepView &sv, int32_t &clo, int32_t &chi,
+                                            bool &ceff) {
+    bool own = (c >= lo && c < hi);
+    if constexpr (STEP) {
+        if (!own) own = col_arrives(sv, c, clo, chi, ceff);
+    }
+    return (own ? x_own : x_hat)[c];
+}
 
 // Row epilogue; returns the row's contribution to the norm (r_i^2 for Jacobi,
 // |x_next_j - x_own_j| for the power step).
 template <int KIND>
-__device__ __forceinline__ double row_finish(int32_t i, double s, double dg,
-                                             const double *__restrict__ b, double alpha,
-                                             double beta, const double *__restrict__ x_own,
+__device__ __forceinline__ double row_finish(int32_t i, double s, double dg, double bi,
+                                             double xo, double alpha, double beta,
                                              double *__restrict__ x_next) {
     if constexpr (KIND == ECC_KIND_JACOBI) {
-        const double bs = b[i] - s;
+        const double bs = bi - s;
         const double xn = bs / dg;
         x_next[i] = xn;
-        const double r = bs - dg * x_own[i];
+        const double r = bs - dg * xo;
         return r * r;
     } else {
         const double xn = alpha * s + beta;
         x_next[i] = xn;
-        return fabs(xn - x_own[i]);
+        return fabs(xn - xo);
     }
 }
 
-// Accumulate entries [k_begin, k_end) of row i with stride `step` starting at
-// `first`, reading (col, val) through the given accessors.
-template <int KIND>
-__device__ __forceinline__ void row_accumulate_global(
-    int32_t i, int32_t first, int32_t k_end, int32_t step, const int32_t *__restrict__ col,
-    const double *__restrict__ val, int32_t lo, int32_t hi, const double *__restrict__ x_own,
-    const double *__restrict__ x_hat, double &s, double &dg) {
-    int32_t k = first;
-    // four independent loads in flight per lane
-    for (; k + 3 * step < k_end; k += 4 * step) {
-        int32_t c[4];
-        double v[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            c[u] = col[k + u * step];
-            v[u] = val[k + u * step];
-        }
-        double y[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const double *src = (c[u] >= lo && c[u] < hi) ? x_own : x_hat;
-            y[u] = src[c[u]];
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            if (KIND == ECC_KIND_JACOBI && c[u] == i) {
-                dg = v[u];
-            } else {
-                s = s + v[u] * y[u];
-            }
-        }
-    }
-    for (; k < k_end; k += step) {
-        const int32_t c = col[k];
-        const double v = val[k];
-        if (KIND == ECC_KIND_JACOBI && c == i) {
-            dg = v;
-            continue;
-        }
-        const double *src = (c >= lo && c < hi) ? x_own : x_hat;
-        s = s + v * src[c];
-    }
+// Lanes per row of a stream item: rows of at most 16 nonzeros on average are
+// summed by one lane in CSR order; longer ones by up to 64 lanes, keeping at
+// least 8 nonzeros per lane.
+__device__ __forceinline__ int lanes_per_row(int32_t nnz, int32_t nr) {
+    int tpr = 1;
+    if (nnz > 16 * nr)
+        while (tpr < 64 && tpr * 2 * nr <= kSweepThreads && nnz >= 16 * tpr * nr) tpr *= 2;
+    return tpr;
 }
 
-template <int KIND>
-__global__ __launch_bounds__(kSweepThreads) void k_sweep(
-    const WorkItem *__restrict__ items, int32_t n_items, const int32_t *__restrict__ row_ptr,
-    const int32_t *__restrict__ col, const double *__restrict__ val,
-    const int32_t *__restrict__ block_start, const double *__restrict__ b, double alpha,
-    double beta, const double *__restrict__ x_own, const double *__restrict__ x_hat,
-    double *__restrict__ x_next, double *__restrict__ partials, double2 *__restrict__ pieces,
-    int32_t zero_extra, const int32_t *__restrict__ done) {
+template <int KIND, bool STEP>
+__global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
     __shared__ int32_t s_col[kStreamCap];
     __shared__ double s_val[kStreamCap];
     __shared__ double s_red[kSweepThreads / 64];
-    if (done && *done) return;
+    __shared__ uint8_t s_eff[STEP ? kFusedMaxP : 1];
+    __shared__ int32_t s_bs[STEP ? kFusedMaxP + 1 : 1];
+    if (a.done && *a.done) return;
     const int tid = threadIdx.x;
+    StepView sv{s_eff, s_bs, a.P};
+    if constexpr (STEP) {
+        for (int32_t p = tid; p < a.P; p += kSweepThreads)
+            s_eff[p] = stale_select(a.ver_in[p], a.arrived[p], a.t, a.S) ? 1 : 0;
+        for (int32_t p = tid; p <= a.P; p += kSweepThreads) s_bs[p] = a.block_start[p];
+        if (blockIdx.x == 0)
+            record_step(a.P, a.S, a.t, a.arrived, a.ver_in, a.ver_out, a.age_state, a.eff_state,
+                        a.forced, a.eff_user, a.age_user, nullptr);
+        __syncthreads();
+    }
+    const int32_t G = gridDim.x;
+    if (blockIdx.x == 0) {
+        // no split rows: their norm contribution (partial G) is zero
+        if (a.zero_extra && tid == 0) a.partials[G] = 0.0;
+        // deferred norm of the previous loop iteration, whose partials the
+        // kernel boundary has made visible (same order as a separate pass)
+        if (a.prev_partials) {
+            const double sum = reduce_values(a.prev_partials, (int64_t)G + 1, false, 0.0, s_red);
+            if (tid == 0) *a.prev_rho = (a.norm == ECC_NORM_L2) ? sqrt(sum) : sum;
+        }
+    }
+    // XCD-aware order: workgroups dispatched to the same XCD (blockIdx mod 8)
+    // take consecutive items, so neighbouring rows share that XCD's L2.
+    const int32_t L = (G % 8 == 0) ? (int32_t)((blockIdx.x % 8) * (G / 8) + blockIdx.x / 8)
+                                   : (int32_t)blockIdx.x;
     double contrib = 0.0;
 
-    for (int32_t w = blockIdx.x; w < n_items; w += gridDim.x) {
-        const WorkItem it = items[w];
-        const int kind = it.kind_rank >> 24;
-        const int32_t p = it.kind_rank & 0xffffff;
-        const int32_t lo = block_start[p], hi = block_start[p + 1];
+    for (int32_t w = L; w < a.n_items; w += G) {
+        const WorkItem it = a.items[w];
+        const int32_t lo = it.lo, hi = it.hi;
+        const bool own_arrives = STEP && s_eff[it.rank] != 0;
+        int32_t clo = 0, chi = 0;  // lookup cache (empty)
+        bool ceff = false;
 
-        if (kind == kItemStream) {
-            const int32_t r0 = it.row0, nr = it.a;
-            const int32_t k0 = row_ptr[r0], k1 = row_ptr[r0 + nr];
-            for (int32_t k = k0 + tid; k < k1; k += kSweepThreads) {
-                s_col[k - k0] = col[k];
-                s_val[k - k0] = val[k];
-            }
-            __syncthreads();
-            // lanes per row: short rows (<= 16 nonzeros on average) are summed by
-            // one lane in CSR order; longer ones by up to 64 lanes, keeping at
-            // least 4 nonzeros per lane
-            const int32_t nnz_item = k1 - k0;
-            int tpr = 1;
-            if (nnz_item > 16 * nr)
-                while (tpr < 64 && tpr * 2 * nr <= kSweepThreads && nnz_item >= 8 * tpr * nr)
-                    tpr *= 2;
+        if (it.kind == kItemStream) {
+            const int32_t r0 = it.row0, nr = it.nrows, k0 = it.k0, k1 = it.k1;
+            const int32_t nnz = k1 - k0;
+            const int tpr = lanes_per_row(nnz, nr);
             const int lane = tid & (tpr - 1);
             const int32_t rr = tid / tpr;
-            if (rr < nr) {
-                const int32_t i = r0 + rr;
-                const int32_t rs = row_ptr[i] - k0, re = row_ptr[i + 1] - k0;
-                double s = 0.0, dg = 0.0;
-                for (int32_t k = rs + lane; k < re; k += tpr) {
-                    const int32_t c = s_col[k];
-                    const double v = s_val[k];
-                    if (KIND == ECC_KIND_JACOBI && c == i) {
-                        dg = v;
-                        continue;
-                    }
-                    const double *src = (c >= lo && c < hi) ? x_own : x_hat;
-                    s = s + v * src[c];
+            const bool active = rr < nr;
+            const int32_t i = r0 + (active ? rr : 0);
+            // per-row loads, independent of the staged nonzeros
+            int32_t rp0 = 0, rp1 = 0;
+            double bi = 0.0, xo = 0.0;
+            if (active) {
+                rp0 = a.row_ptr[i];
+                rp1 = a.row_ptr[i + 1];
+                xo = a.x_own[i];
+                if (KIND == ECC_KIND_JACOBI) bi = a.b[i];
+            }
+            // stage the item's nonzeros: all loads first, then the LDS stores
+            static_assert(kStreamCap == 8 * kSweepThreads, "eight nonzeros per thread");
+            if (nnz > 0) {  // reads are clamped into [k0, k1) so all are in flight together
+                int32_t cv[8];
+                double vv[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int32_t kc = min(k0 + tid + u * kSweepThreads, k1 - 1);
+                    cv[u] = a.col[kc];
+                    vv[u] = a.val[kc];
                 }
-                if (tpr > 1) {
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int32_t k = tid + u * kSweepThreads;
+                    if (k < nnz) {
+                        s_col[k] = cv[u];
+                        s_val[k] = vv[u];
+                    }
+                }
+            }
+            __syncthreads();
+            if (active) {
+                const int32_t rs = rp0 - k0, re = rp1 - k0;
+                double s = 0.0, dg = 0.0;
+                if (tpr == 1) {
+                    // up to 8 entries with all gathers in flight, then in order
+                    const int32_t len = re - rs;
+                    int32_t c8[8];
+                    double v8[8], y8[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        // entries past the row's end repeat its last one (unused)
+                        const int32_t k = (len > 0) ? rs + min(j, len - 1) : 0;
+                        c8[j] = (len > 0) ? s_col[k] : 0;
+                        v8[j] = (len > 0) ? s_val[k] : 0.0;
+                    }
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        y8[j] = (j < len) ? view_load<STEP>(c8[j], lo, hi, a.x_own, a.x_hat, sv,
+                                                            clo, chi, ceff)
+                                          : 0.0;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        if (j < len) {
+                            if (KIND == ECC_KIND_JACOBI && c8[j] == i) dg = v8[j];
+                            else s = s + v8[j] * y8[j];
+                        }
+                    }
+                    for (int32_t k = rs + 8; k < re; ++k) {
+                        const int32_t c = s_col[k];
+                        const double v = s_val[k];
+                        if (KIND == ECC_KIND_JACOBI && c == i) {
+                            dg = v;
+                            continue;
+                        }
+                        s = s + v * view_load<STEP>(c, lo, hi, a.x_own, a.x_hat, sv, clo, chi,
+                                                    ceff);
+                    }
+                } else {
+                    for (int32_t k = rs + lane; k < re; k += tpr) {
+                        const int32_t c = s_col[k];
+                        const double v = s_val[k];
+                        if (KIND == ECC_KIND_JACOBI && c == i) {
+                            dg = v;
+                            continue;
+                        }
+                        s = s + v * view_load<STEP>(c, lo, hi, a.x_own, a.x_hat, sv, clo, chi,
+                                                    ceff);
+                    }
                     s = group_sum_dyn(s, tpr);
                     if (KIND == ECC_KIND_JACOBI) dg = group_sum_dyn(dg, tpr);
                 }
-                if (lane == 0) contrib += row_finish<KIND>(i, s, dg, b, alpha, beta, x_own, x_next);
+                if (lane == 0) {
+                    contrib += row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+                    if (own_arrives) a.x_hat[i] = xo;
+                }
             }
             __syncthreads();  // LDS is reused by the next item
         } else {
+            // one long row (or a slice of it) by the whole workgroup
             const int32_t i = it.row0;
-            int32_t ks = row_ptr[i], ke = row_ptr[i + 1];
-            if (kind == kItemPiece) {
-                ks = ks + it.a * kVectorCap;
-                ke = min(ke, ks + kVectorCap);
-            }
             double s = 0.0, dg = 0.0;
-            row_accumulate_global<KIND>(i, ks + tid, ke, kSweepThreads, col, val, lo, hi, x_own,
-                                        x_hat, s, dg);
+            int32_t k = it.k0 + tid;
+            for (; k + 3 * kSweepThreads < it.k1; k += 4 * kSweepThreads) {
+                int32_t c[4];
+                double v[4], y[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    c[u] = a.col[k + u * kSweepThreads];
+                    v[u] = a.val[k + u * kSweepThreads];
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    y[u] = view_load<STEP>(c[u], lo, hi, a.x_own, a.x_hat, sv, clo, chi, ceff);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    if (KIND == ECC_KIND_JACOBI && c[u] == i) dg = v[u];
+                    else s = s + v[u] * y[u];
+                }
+            }
+            for (; k < it.k1; k += kSweepThreads) {
+                const int32_t c = a.col[k];
+                const double v = a.val[k];
+                if (KIND == ECC_KIND_JACOBI && c == i) {
+                    dg = v;
+                    continue;
+                }
+                s = s + v * view_load<STEP>(c, lo, hi, a.x_own, a.x_hat, sv, clo, chi, ceff);
+            }
             s = block_sum<kSweepThreads>(s, s_red);
             if (KIND == ECC_KIND_JACOBI) dg = block_sum<kSweepThreads>(dg, s_red);
             if (tid == 0) {
-                if (kind == kItemPiece)
-                    pieces[it.b] = make_double2(s, dg);
-                else
-                    contrib += row_finish<KIND>(i, s, dg, b, alpha, beta, x_own, x_next);
+                if (it.kind == kItemPiece) {
+                    a.pieces[it.slot] = make_double2(s, dg);
+                } else {
+                    const double xo = a.x_own[i];
+                    const double bi = (KIND == ECC_KIND_JACOBI) ? a.b[i] : 0.0;
+                    contrib += row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+                    if (own_arrives) a.x_hat[i] = xo;
+                }
             }
         }
     }
+
     const double total = block_sum<kSweepThreads>(contrib, s_red);
-    if (tid == 0) partials[blockIdx.x] = total;
-    // no split rows: the extra partial (split-row contributions) is zero
-    if (zero_extra && blockIdx.x == 0 && tid == 0) partials[gridDim.x] = 0.0;
+    if (tid == 0) a.partials[blockIdx.x] = total;
 }
 
-// Second pass, one workgroup.  (1) Rows split into pieces are finished: their
-// piece sums are added in piece order, the row epilogue runs, and the
-// contributions go to partials[n_main].  (2) If `norm` is non-zero, the
-// n_main + 1 partials are reduced in a fixed order to sqrt(sum) (L2) or sum
-// (L1), written to *out; with a control block, ctrl[1] := t + 1 and
-// ctrl[0] := 1 once the norm is below tol.
+// Second pass of a sweep, one workgroup of kNormThreads.  (1) Rows split into
+// pieces are finished: the piece sums are added in piece order, the row
+// epilogue runs (and, in a loop iteration, an arrived rank's split row is
+// written into x_hat), and their norm contribution becomes partial `G`.
+// (2) With norm != 0 the G + 1 partials are reduced in a fixed order to
+// sqrt(sum) (L2) or sum (L1) in *rho_out; with a control block, ctrl[1] :=
+// t + 1 and ctrl[0] := 1 once the norm is below tol.
+struct Pass2Args {
+    double *partials;
+    int32_t G;
+    const Fixup *fixups;
+    int32_t n_fixups;
+    const double2 *pieces;
+    const double *b;
+    double alpha, beta;
+    const double *x_own;
+    double *x_next;
+    double *x_hat;
+    const uint8_t *eff_state;  // loop iteration: rank arrivals of this step
+    int32_t norm;
+    double *rho_out;
+    double tol;
+    int32_t *ctrl;
+    int64_t t;
+    const int32_t *done;
+};
+
 template <int KIND>
-__global__ __launch_bounds__(kPass2Threads) void k_pass2(
-    double *__restrict__ partials, int64_t n_main, int32_t do_fixups,
-    const Fixup *__restrict__ fixups, int32_t n_fixups, const double2 *__restrict__ pieces,
-    const double *__restrict__ b,
-    double alpha, double beta, const double *__restrict__ x_own, double *__restrict__ x_next,
-    int32_t norm, double *__restrict__ out, double tol, int32_t *__restrict__ ctrl, int32_t t,
-    const int32_t *__restrict__ done) {
-    __shared__ double s_red[kPass2Threads / 64];
-    if (done && *done) return;
+__global__ __launch_bounds__(kNormThreads) void k_pass2(Pass2Args a) {
+    __shared__ double s_red[kNormThreads / 64];
+    __shared__ double s_fx;
+    if (a.done && *a.done) return;
     const int tid = threadIdx.x;
-    if (do_fixups) {
-        double acc = 0.0;
-        for (int32_t f = tid; f < n_fixups; f += kPass2Threads) {
-            const Fixup fx = fixups[f];
-            double s = 0.0, dg = 0.0;
-            for (int32_t j = 0; j < fx.npieces; ++j) {
-                const double2 pc = pieces[fx.slot0 + j];
-                s = s + pc.x;
-                dg = dg + pc.y;
-            }
-            acc += row_finish<KIND>(fx.row, s, dg, b, alpha, beta, x_own, x_next);
+    double fx = 0.0;
+    for (int32_t f = tid; f < a.n_fixups; f += kNormThreads) {
+        const Fixup fu = a.fixups[f];
+        double s = 0.0, dg = 0.0;
+        for (int32_t j = 0; j < fu.npieces; ++j) {
+            const double2 pc = a.pieces[fu.slot0 + j];
+            s = s + pc.x;
+            dg = dg + pc.y;
         }
-        const double tot = block_sum<kPass2Threads>(acc, s_red);
-        if (tid == 0) partials[n_main] = tot;
-        __syncthreads();
-        __threadfence_block();
+        const double xo = a.x_own[fu.row];
+        const double bi = (KIND == ECC_KIND_JACOBI) ? a.b[fu.row] : 0.0;
+        fx += row_finish<KIND>(fu.row, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+        if (a.eff_state && a.eff_state[fu.rank]) a.x_hat[fu.row] = xo;
     }
-    if (norm == 0) return;
-    const int64_t n = n_main + 1;
-    double acc = 0.0;
-    for (int64_t k = tid; k < n; k += kPass2Threads) acc += partials[k];
-    const double tot = block_sum<kPass2Threads>(acc, s_red);
+    const double fx_total = block_sum<kNormThreads>(fx, s_red);
     if (tid == 0) {
-        const double v = (norm == ECC_NORM_L2) ? sqrt(tot) : tot;
-        if (out) *out = v;
-        if (ctrl) {
-            ctrl[1] = t + 1;
-            if (tol > 0.0 && v < tol) ctrl[0] = 1;
+        a.partials[a.G] = fx_total;
+        s_fx = fx_total;
+    }
+    __syncthreads();
+    if (a.norm == 0) return;
+    const double sum = reduce_values(a.partials, (int64_t)a.G + 1, true, s_fx, s_red);
+    if (tid == 0) {
+        const double v = (a.norm == ECC_NORM_L2) ? sqrt(sum) : sum;
+        if (a.rho_out) *a.rho_out = v;
+        if (a.ctrl) {
+            a.ctrl[1] = (int32_t)a.t + 1;
+            if (a.tol > 0.0 && v < a.tol) a.ctrl[0] = 1;
         }
     }
+}
+
+// Standalone second pass: norm of n partial values (same order of operations
+// as the last workgroup of a sweep).
+__global__ __launch_bounds__(kNormThreads) void k_residual(const double *__restrict__ partials,
+                                                          int64_t n, int32_t norm,
+                                                          double *__restrict__ out) {
+    __shared__ double s_red[kNormThreads / 64];
+    const double sum = reduce_values(partials, n, false, 0.0, s_red);
+    if (threadIdx.x == 0) *out = (norm == ECC_NORM_L2) ? sqrt(sum) : sum;
 }
 
 // Structural check of a matrix for a plan: counts rows whose diagonal entry is
@@ -250,26 +430,44 @@ __global__ void k_check(int32_t n_rows, int32_t n_cols, const int32_t *__restric
 // host side
 // ---------------------------------------------------------------------------
 
+// Work items of a matrix for a plan's row blocks: very long rows first (as
+// pieces, then whole), then runs of short rows in row order.
 static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_t> &counts,
                         std::vector<WorkItem> &items, std::vector<Fixup> &fixups,
                         int64_t &n_pieces) {
     std::vector<WorkItem> big, vec, stream;
     n_pieces = 0;
     int64_t row = 0;
+    auto make = [](int64_t r0, int64_t nr, int64_t k0, int64_t k1, int64_t lo, int64_t hi,
+                   int kind, int64_t p, int64_t slot) {
+        WorkItem w{};
+        w.row0 = (int32_t)r0;
+        w.nrows = (int32_t)nr;
+        w.k0 = (int32_t)k0;
+        w.k1 = (int32_t)k1;
+        w.lo = (int32_t)lo;
+        w.hi = (int32_t)hi;
+        w.kind = kind;
+        w.rank = (int32_t)p;
+        w.slot = (int32_t)slot;
+        return w;
+    };
     for (size_t p = 0; p < counts.size(); ++p) {
-        const int64_t hi = row + counts[p];
-        int64_t i = row;
+        const int64_t lo = row, hi = row + counts[p];
+        int64_t i = lo;
         while (i < hi) {
             const int64_t len = (int64_t)rp[i + 1] - rp[i];
             if (len > kStreamCap) {
                 if (len <= kVectorCap) {
-                    vec.push_back({(int32_t)i, 1, 0, (int32_t)((kItemVector << 24) | (int32_t)p)});
+                    vec.push_back(make(i, 1, rp[i], rp[i + 1], lo, hi, kItemVector, p, 0));
                 } else {
                     const int32_t np = (int32_t)((len + kVectorCap - 1) / kVectorCap);
                     fixups.push_back({(int32_t)i, (int32_t)n_pieces, np, (int32_t)p});
-                    for (int32_t j = 0; j < np; ++j)
-                        big.push_back({(int32_t)i, j, (int32_t)(n_pieces + j),
-                                       (int32_t)((kItemPiece << 24) | (int32_t)p)});
+                    for (int32_t j = 0; j < np; ++j) {
+                        const int64_t ka = rp[i] + (int64_t)j * kVectorCap;
+                        const int64_t kb = std::min<int64_t>(rp[i + 1], ka + kVectorCap);
+                        big.push_back(make(i, 1, ka, kb, lo, hi, kItemPiece, p, n_pieces + j));
+                    }
                     n_pieces += np;
                 }
                 ++i;
@@ -283,8 +481,7 @@ static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_
                 nnz += l;
                 ++i;
             }
-            stream.push_back({(int32_t)start, (int32_t)(i - start), 0,
-                              (int32_t)((kItemStream << 24) | (int32_t)p)});
+            stream.push_back(make(start, i - start, rp[start], rp[i], lo, hi, kItemStream, p, 0));
         }
         row = hi;
     }
@@ -294,48 +491,94 @@ static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_
     items.insert(items.end(), stream.begin(), stream.end());
 }
 
-ecc_status_t launch_sweep(ecc_matrix_t M, const double *d_b, double alpha, double beta,
-                          const double *d_x_own, const double *d_x_hat, double *d_x_next,
-                          double *d_partials, int32_t zero_extra, const int32_t *d_done) {
+static int32_t sweep_grid(int64_t n_items) {
+    int64_t g = std::max<int64_t>(1, std::min<int64_t>(n_items, kMaxSweepBlocks));
+    if (g >= 8) g -= g % 8;
+    return (int32_t)g;
+}
+
+ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     ecc_plan_t pl = M->plan;
-    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(M->n_items, kMaxSweepBlocks));
-    if (M->kind == ECC_KIND_JACOBI)
-        hipLaunchKernelGGL(k_sweep<ECC_KIND_JACOBI>, dim3(grid), dim3(kSweepThreads), 0,
-                           pl->stream, M->d_items, (int32_t)M->n_items, M->A.d_row_ptr, M->A.d_col,
-                           M->A.d_val, pl->d_block_start, d_b, alpha, beta, d_x_own, d_x_hat,
-                           d_x_next, d_partials, M->d_pieces, zero_extra, d_done);
-    else
-        hipLaunchKernelGGL(k_sweep<ECC_KIND_POWER>, dim3(grid), dim3(kSweepThreads), 0,
-                           pl->stream, M->d_items, (int32_t)M->n_items, M->A.d_row_ptr, M->A.d_col,
-                           M->A.d_val, pl->d_block_start, d_b, alpha, beta, d_x_own, d_x_hat,
-                           d_x_next, d_partials, M->d_pieces, zero_extra, d_done);
+    SweepArgs a{};
+    a.items = M->d_items;
+    a.n_items = (int32_t)M->n_items;
+    a.row_ptr = M->A.d_row_ptr;
+    a.col = M->A.d_col;
+    a.val = M->A.d_val;
+    a.b = L.b;
+    a.alpha = L.alpha;
+    a.beta = L.beta;
+    a.x_own = L.x_own;
+    a.x_hat = L.x_hat;
+    a.x_next = L.x_next;
+    a.partials = L.partials;
+    a.pieces = M->d_pieces;
+    a.zero_extra = M->n_fixups == 0 ? 1 : 0;
+    a.prev_partials = L.prev_partials;
+    a.prev_rho = L.prev_rho;
+    a.norm = L.norm;
+    a.done = L.done;
+    const bool step = L.arrived != nullptr;
+    if (step) {
+        const int64_t t = pl->clock;
+        if (pl->P > kFusedMaxP || !pl->d_block_start) {
+            set_error("internal: fused step does not fit the plan");
+            return ECC_ERR_STATE;
+        }
+        a.step = 1;
+        a.P = pl->P;
+        a.S = pl->S;
+        a.t = t;
+        a.arrived = L.arrived;
+        a.ver_in = pl->d_version + (t & 1) * pl->P;
+        a.ver_out = pl->d_version + ((t + 1) & 1) * pl->P;
+        a.age_state = pl->d_age;
+        a.eff_state = pl->d_eff;
+        a.forced = pl->d_forced;
+        a.eff_user = L.eff_user;
+        a.age_user = L.age_user;
+        a.block_start = pl->d_block_start;
+    }
+    TimedLaunch timed(pl, ECC_TIMING_SWEEP);
+    const dim3 grid(M->grid), block(kSweepThreads);
+    if (M->kind == ECC_KIND_JACOBI) {
+        if (step) hipLaunchKernelGGL((k_sweep<ECC_KIND_JACOBI, true>), grid, block, 0, pl->stream, a);
+        else hipLaunchKernelGGL((k_sweep<ECC_KIND_JACOBI, false>), grid, block, 0, pl->stream, a);
+    } else {
+        if (step) hipLaunchKernelGGL((k_sweep<ECC_KIND_POWER, true>), grid, block, 0, pl->stream, a);
+        else hipLaunchKernelGGL((k_sweep<ECC_KIND_POWER, false>), grid, block, 0, pl->stream, a);
+    }
     ECC_LAUNCH_CHECK();
+    if (step) pl->clock += 1;
     return ECC_OK;
 }
 
-static int64_t n_main_partials(ecc_matrix_t M) {
-    return std::max<int64_t>(1, std::min<int64_t>(M->n_items, kMaxSweepBlocks));
-}
-
-static ecc_status_t launch_pass2_impl(ecc_plan_t pl, ecc_matrix_t M, double *d_partials,
-                                      int64_t n_main, bool do_fixups, int32_t norm,
-                                      const double *d_b, double alpha, double beta,
-                                      const double *d_x_own, double *d_x_next, double *d_out,
-                                      double tol, int32_t *d_ctrl, int32_t t,
-                                      const int32_t *d_done) {
-    const Fixup *fx = (M && M->n_fixups > 0) ? M->d_fixups : nullptr;
-    const int32_t nf = fx ? (int32_t)M->n_fixups : 0;
-    const double2 *pc = M ? M->d_pieces : nullptr;
-    const int kind = M ? M->kind : ECC_KIND_POWER;
-    const int32_t fix = do_fixups ? 1 : 0;
-    if (kind == ECC_KIND_JACOBI)
-        hipLaunchKernelGGL(k_pass2<ECC_KIND_JACOBI>, dim3(1), dim3(kPass2Threads), 0, pl->stream,
-                           d_partials, n_main, fix, fx, nf, pc, d_b, alpha, beta, d_x_own,
-                           d_x_next, norm, d_out, tol, d_ctrl, t, d_done);
+ecc_status_t launch_pass2(ecc_matrix_t M, const Pass2Launch &L) {
+    ecc_plan_t pl = M->plan;
+    Pass2Args a{};
+    a.partials = L.partials;
+    a.G = M->grid;
+    a.fixups = M->d_fixups;
+    a.n_fixups = (int32_t)M->n_fixups;
+    a.pieces = M->d_pieces;
+    a.b = L.b;
+    a.alpha = L.alpha;
+    a.beta = L.beta;
+    a.x_own = L.x_own;
+    a.x_next = L.x_next;
+    a.x_hat = L.x_hat;
+    a.eff_state = L.step ? pl->d_eff : nullptr;
+    a.norm = L.norm;
+    a.rho_out = L.rho_out;
+    a.tol = L.tol;
+    a.ctrl = L.ctrl;
+    a.t = L.t;
+    a.done = L.done;
+    TimedLaunch timed(pl, ECC_TIMING_NORM);
+    if (M->kind == ECC_KIND_JACOBI)
+        hipLaunchKernelGGL(k_pass2<ECC_KIND_JACOBI>, dim3(1), dim3(kNormThreads), 0, pl->stream, a);
     else
-        hipLaunchKernelGGL(k_pass2<ECC_KIND_POWER>, dim3(1), dim3(kPass2Threads), 0, pl->stream,
-                           d_partials, n_main, fix, fx, nf, pc, d_b, alpha, beta, d_x_own,
-                           d_x_next, norm, d_out, tol, d_ctrl, t, d_done);
+        hipLaunchKernelGGL(k_pass2<ECC_KIND_POWER>, dim3(1), dim3(kNormThreads), 0, pl->stream, a);
     ECC_LAUNCH_CHECK();
     return ECC_OK;
 }
@@ -410,6 +653,10 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     std::vector<Fixup> fixups;
     int64_t n_pieces = 0;
     build_items(rp, plan->counts, items, fixups, n_pieces);
+    if ((int64_t)items.size() >= (int64_t(1) << 31)) {
+        set_error("too many work items");
+        return ECC_ERR_RANGE;
+    }
 
     ecc_matrix_s *M = new (std::nothrow) ecc_matrix_s();
     if (!M) {
@@ -422,6 +669,7 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     M->n_items = (int64_t)items.size();
     M->n_fixups = (int64_t)fixups.size();
     M->n_pieces = n_pieces;
+    M->grid = sweep_grid(M->n_items);
     auto fail = [&](const char *what) {
         set_error("%s", what);
         ecc_matrix_destroy(M);
@@ -443,7 +691,9 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     }
     if (n_pieces > 0 && hipMalloc((void **)&M->d_pieces, sizeof(double2) * n_pieces) != hipSuccess)
         return fail("hipMalloc of piece sums failed");
-    if (hipMalloc((void **)&M->d_partials, sizeof(double) * (n_main_partials(M) + 1)) != hipSuccess)
+    // two buffers of G + 1 partials: a loop iteration writes one while the
+    // next launch reduces the other
+    if (hipMalloc((void **)&M->d_partials, sizeof(double) * 2 * (M->grid + 1)) != hipSuccess)
         return fail("hipMalloc of partials failed");
     *out = M;
     return ECC_OK;
@@ -462,7 +712,7 @@ ecc_status_t ecc_matrix_destroy(ecc_matrix_t M) {
 
 int64_t ecc_partials_size(ecc_matrix_t M) {
     if (!M) return 0;
-    return n_main_partials(M) + 1;
+    return (int64_t)M->grid + 1;
 }
 
 static ecc_status_t iterate(ecc_plan_t plan, ecc_matrix_t M, int32_t kind, const double *d_b,
@@ -477,17 +727,31 @@ static ecc_status_t iterate(ecc_plan_t plan, ecc_matrix_t M, int32_t kind, const
         return ECC_ERR_STATE;
     }
     const int64_t n = M->A.n_rows;
-    ECC_ARG(n == 0 || (d_x_own && d_x_hat && d_x_next && d_partials), "NULL vector argument");
+    ECC_ARG(d_partials != nullptr, "d_partials is NULL");
+    ECC_ARG(n == 0 || (d_x_own && d_x_hat && d_x_next), "NULL vector argument");
     ECC_ARG(kind != ECC_KIND_JACOBI || n == 0 || d_b, "d_b is NULL");
     ECC_ARG(n == 0 || (d_x_next != d_x_own && d_x_next != d_x_hat && d_x_next != d_b),
             "d_x_next must not alias an input");
-    const bool split = M->n_fixups > 0;
-    st = launch_sweep(M, d_b, alpha, beta, d_x_own, d_x_hat, d_x_next, d_partials,
-                      split ? 0 : 1, nullptr);
-    if (st != ECC_OK || !split) return st;
-    // finish the rows that were split into pieces
-    return launch_pass2_impl(plan, M, d_partials, n_main_partials(M), true, 0, d_b, alpha, beta,
-                             d_x_own, d_x_next, nullptr, 0.0, nullptr, 0, nullptr);
+    // x_hat is only read by a plain sweep
+    SweepLaunch L;
+    L.b = d_b;
+    L.alpha = alpha;
+    L.beta = beta;
+    L.x_own = d_x_own;
+    L.x_hat = const_cast<double *>(d_x_hat);
+    L.x_next = d_x_next;
+    L.partials = d_partials;
+    st = launch_sweep(M, L);
+    if (st != ECC_OK || M->n_fixups == 0) return st;
+    // finish the rows split into pieces (their norm contribution -> partial G)
+    Pass2Launch F;
+    F.partials = d_partials;
+    F.b = d_b;
+    F.alpha = alpha;
+    F.beta = beta;
+    F.x_own = d_x_own;
+    F.x_next = d_x_next;
+    return launch_pass2(M, F);
 }
 
 ecc_status_t ecc_iterate_jacobi(ecc_plan_t plan, ecc_matrix_t A, const double *d_b,
@@ -513,10 +777,12 @@ ecc_status_t ecc_residual(ecc_plan_t plan, const double *d_partials, int64_t n_p
     ECC_ARG(n_partials >= 1 && d_partials, "need at least one partial");
     ECC_ARG(h_out || d_out, "h_out and d_out are both NULL");
     double *dst = d_out ? d_out : plan->d_scalar;
-    st = launch_pass2_impl(plan, nullptr, const_cast<double *>(d_partials), n_partials - 1, false,
-                           norm, nullptr, 0.0, 0.0, nullptr, nullptr, dst, 0.0, nullptr, 0,
-                           nullptr);
-    if (st != ECC_OK) return st;
+    {
+        TimedLaunch timed(plan, ECC_TIMING_NORM);
+        hipLaunchKernelGGL(k_residual, dim3(1), dim3(kNormThreads), 0, plan->stream, d_partials,
+                           n_partials, norm, dst);
+        ECC_LAUNCH_CHECK();
+    }
     if (h_out) {
         ECC_HIP(hipMemcpyAsync(h_out, dst, sizeof(double), hipMemcpyDeviceToHost, plan->stream));
         ECC_HIP(hipStreamSynchronize(plan->stream));
@@ -525,12 +791,3 @@ ecc_status_t ecc_residual(ecc_plan_t plan, const double *d_partials, int64_t n_p
 }
 
 }  // extern "C"
-
-namespace ecc {
-ecc_status_t solve_pass2(ecc_matrix_t M, int32_t norm, const double *d_b, double alpha,
-                         double beta, const double *d_x_own, double *d_x_next, double *d_out,
-                         double tol, int32_t *d_ctrl, int32_t t, const int32_t *d_done) {
-    return launch_pass2_impl(M->plan, M, M->d_partials, n_main_partials(M), true, norm, d_b,
-                             alpha, beta, d_x_own, d_x_next, d_out, tol, d_ctrl, t, d_done);
-}
-}  // namespace ecc

@@ -306,9 +306,46 @@ def test_solve_config5_small(N, P):
     _solve_and_compare(W.config5(N=N, T=60, P=P), bitwise=True)
 
 
-@pytest.mark.parametrize("scale", [8, 12, 15])
+@pytest.mark.parametrize("scale", [8, 12, 15, 17])
 def test_solve_config3_small(scale):
+    """Scale 15 has rows summed by a whole workgroup; scale 17 also has rows
+    longer than one work item, split into pieces and recombined."""
     _solve_and_compare(W.config3(scale=scale, T=60), bitwise=False)
+
+
+def test_solve_many_ranks_unfused():
+    """More ranks than a workgroup stages in LDS: separate assembly launches."""
+    _solve_and_compare(W.config5(N=24, T=30, P=2048), bitwise=True)
+
+
+def _arrow_problem(n=40000, T=40, P=7, S=2):
+    """Jacobi on an arrow matrix: row 0 and column 0 are dense, so row 0 is
+    split into pieces; a few other rows are long enough for one workgroup."""
+    rng = np.random.default_rng(77)
+    rows = []
+    for i in range(n):
+        if i == 0:
+            cols = np.arange(n)
+        elif i % 9973 == 0:
+            cols = np.unique(np.concatenate([[0, i], rng.choice(n, 5000, replace=False)]))
+        else:
+            cols = np.unique(np.array([0, i, max(i - 1, 0), min(i + 1, n - 1)]))
+        vals = np.where(cols == i, 0.0, -rng.uniform(0.1, 1.0, cols.size))
+        vals[cols == i] = 2.0 * np.abs(vals).sum() + 1.0
+        rows.append((cols, vals))
+    rp = np.zeros(n + 1, dtype=np.int32)
+    rp[1:] = np.cumsum([c.size for c, _ in rows])
+    A = W.CSR(n, n, rp, np.concatenate([c for c, _ in rows]).astype(np.int32),
+              np.concatenate([v for _, v in rows]))
+    counts = W.dirichlet_partition(n, P, 5)
+    mask = (rng.random((T, P)) < 0.6).astype(np.uint8)
+    mask[0] = 1
+    return W.Iterative("arrow-jacobi", "jacobi", A, counts, W.exclusive_scan(counts), S, mask,
+                       T, np.zeros(n), b=rng.standard_normal(n), norm=2)
+
+
+def test_solve_arrow_split_rows():
+    _solve_and_compare(_arrow_problem(), bitwise=False)
 
 
 def test_solve_config3_tolerance_stop():
@@ -319,9 +356,10 @@ def test_solve_config3_tolerance_stop():
 
 def test_step_api_matches_solve():
     """assemble -> iterate -> residual through the separate calls reproduce the
-    loop-control call bit for bit."""
+    loop-control call bit for bit (fused single-launch loop, the loop with a
+    second pass per iteration, and split rows)."""
     R = _runner()
-    for prob in (W.config2(N=40, T=25), W.config3(scale=11, T=25)):
+    for prob in (W.config2(N=40, T=25), W.config3(scale=11, T=25), _arrow_problem(T=12)):
         announce("step api", prob.name)
         run = R.Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts, prob.S,
                           prob.mask, prob.kind, b=prob.b, alpha=prob.alpha, beta=prob.beta,
