@@ -70,9 +70,11 @@ struct Tile {
 
 // One sweep work item: rows [row0, row0 + nrows) of rank `rank`, whose block
 // is [lo, hi), touching nonzeros [k0, k1).  kind: stream (many short rows
-// staged in LDS), vector (one long row, whole workgroup) or piece (slice
-// [k0, k1) of a very long row; its partial sum goes to piece slot `slot`).
-enum { kItemStream = 0, kItemVector = 1, kItemPiece = 2 };
+// staged in LDS), vector (one long row, whole workgroup), piece (slice
+// [k0, k1) of a very long row; its partial sum goes to piece slot `slot`) or
+// rows (entries [k0, k1) of the row list: rows of similar length, `slot`
+// lanes each).
+enum { kItemStream = 0, kItemVector = 1, kItemPiece = 2, kItemRows = 3 };
 struct WorkItem {
     int32_t row0;
     int32_t nrows;
@@ -274,6 +276,9 @@ struct ecc_matrix_s {
     double2 *d_pieces = nullptr;    // (partial sum, diagonal) per piece
     int64_t n_pieces = 0;
     int32_t grid = 1;               // workgroups of a sweep launch
+    bool irregular = false;         // row lengths vary widely: row-list items
+    int64_t bandwidth = 0;          // max |col - row|
+    int32_t *d_rowlist = nullptr;   // rows of the row-list items, by rank and length class
     double *d_partials = nullptr;   // internal partials of ecc_solve: 2 x (grid + 1)
 };
 

@@ -36,6 +36,13 @@
 
 #include "ecc_common.h"
 
+#ifndef ECC_STREAM_NT
+#define ECC_STREAM_NT 0
+#endif
+#ifndef ECC_GRID_PER_ITEM
+#define ECC_GRID_PER_ITEM 0
+#endif
+
 namespace ecc {
 
 struct SweepArgs {
@@ -51,6 +58,8 @@ struct SweepArgs {
     double *x_next;
     double *partials;
     double2 *pieces;
+    const int32_t *rowlist;
+    int32_t interleave;  // items dealt round-robin instead of in XCD ranges
     // fused loop iteration (step != 0)
     int32_t step;
     int32_t P, S;
@@ -79,32 +88,48 @@ struct StepView {
     int32_t P;
 };
 
-// Does the assembled vector hold x_own at column c (rank of c arrives at this
-// step)?  Binary search of the block starts, with a one-entry per-lane cache.
-__device__ __forceinline__ bool col_arrives(const StepView &v, int32_t c, int32_t &clo,
-                                            int32_t &chi, bool &ceff) {
-    if (c >= clo && c < chi) return ceff;
+// Two most recently used rank windows of one lane: [lo, hi) with the rank's
+// arrival flag.  Kept across the items of a workgroup (arrivals are fixed
+// within a launch); a stencil row's off-block neighbours sit in one or two
+// ranks that change only every few items.
+struct RankCache {
+    int32_t lo0 = 0, hi0 = 0, lo1 = 0, hi1 = 0;
+    bool e0 = false, e1 = false, next = false;
+};
+
+// Does the assembled vector hold x_own at column c (the rank of c arrives at
+// this step)?  Cache hit, else binary search of the LDS-staged block starts.
+__device__ __forceinline__ bool col_arrives(const StepView &v, int32_t c, RankCache &rc) {
+    if (c >= rc.lo0 && c < rc.hi0) return rc.e0;
+    if (c >= rc.lo1 && c < rc.hi1) return rc.e1;
     int32_t a = 0, z = v.P;  // bs[a] <= c < bs[z]
     while (z - a > 1) {
         const int32_t mid = (a + z) >> 1;
         if (v.bs[mid] <= c) a = mid;
         else z = mid;
     }
-    clo = v.bs[a];
-    chi = v.bs[a + 1];
-    ceff = v.eff[a] != 0;
-    return ceff;
+    const bool e = v.eff[a] != 0;
+    if (rc.next) {
+        rc.lo1 = v.bs[a];
+        rc.hi1 = v.bs[a + 1];
+        rc.e1 = e;
+    } else {
+        rc.lo0 = v.bs[a];
+        rc.hi0 = v.bs[a + 1];
+        rc.e0 = e;
+    }
+    rc.next = !rc.next;
+    return e;
 }
 
 template <bool STEP>
 __device__ __forceinline__ double view_load(int32_t c, int32_t lo, int32_t hi,
                                             const double *__restrict__ x_own,
                                             const double *__restrict__ x_hat,
-                                            const StepView &sv, int32_t &clo, int32_t &chi,
-                                            bool &ceff) {
+                                            const StepView &sv, RankCache &rc) {
     bool own = (c >= lo && c < hi);
     if constexpr (STEP) {
-        if (!own) own = col_arrives(sv, c, clo, chi, ceff);
+        if (!own) own = col_arrives(sv, c, rc);
     }
     return (own ? x_own : x_hat)[c];
 }
@@ -138,15 +163,301 @@ __device__ __forceinline__ int lanes_per_row(int32_t nnz, int32_t nr) {
     return tpr;
 }
 
+// Loads of arrays that are streamed once per sweep (CSR arrays, b): marked
+// non-temporal so that they do not evict the reused iterate from L2.
+template <typename T>
+__device__ __forceinline__ T ld_stream(const T *p) {
+#if ECC_STREAM_NT
+    return __builtin_nontemporal_load(p);
+#else
+    return *p;
+#endif
+}
+
+// Accumulates a lane's entries k0, k0 + stride, ... (< k1) of row i, in that
+// order, W at a time: the next W (col, val) loads are in flight while the
+// current W gathers of y complete.  With stride 1 this is the row's CSR
+// order.  Jacobi skips (and records) the diagonal entry.
+template <int KIND, bool STEP, int W>
+__device__ __forceinline__ void seg_accumulate(int32_t i, int32_t k0, int32_t k1, int32_t stride,
+                                               const SweepArgs &a, int32_t lo, int32_t hi,
+                                               const StepView &sv, RankCache &rc, double &s,
+                                               double &dg) {
+    if (k0 >= k1) return;
+    int32_t c[W];
+    double v[W];
+#pragma unroll
+    for (int u = 0; u < W; ++u) {
+        const int32_t k = k0 + u * stride;
+        c[u] = (k < k1) ? ld_stream(a.col + k) : 0;
+        v[u] = (k < k1) ? ld_stream(a.val + k) : 0.0;
+    }
+    for (int32_t k = k0; k < k1; k += W * stride) {
+        double y[W];
+#pragma unroll
+        for (int u = 0; u < W; ++u)
+            y[u] = (k + u * stride < k1) ? view_load<STEP>(c[u], lo, hi, a.x_own, a.x_hat, sv, rc)
+                                          : 0.0;
+        const int32_t kn = k + W * stride;
+        int32_t cn[W];
+        double vn[W];
+#pragma unroll
+        for (int u = 0; u < W; ++u) {
+            const int32_t kk = kn + u * stride;
+            cn[u] = (kk < k1) ? ld_stream(a.col + kk) : 0;
+            vn[u] = (kk < k1) ? ld_stream(a.val + kk) : 0.0;
+        }
+#pragma unroll
+        for (int u = 0; u < W; ++u) {
+            if (k + u * stride < k1) {
+                if (KIND == ECC_KIND_JACOBI && c[u] == i) dg = v[u];
+                else s = s + v[u] * y[u];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < W; ++u) {
+            c[u] = cn[u];
+            v[u] = vn[u];
+        }
+    }
+}
+
+// A short row (at most 8 entries) on one lane, in CSR order, all gathers in
+// flight together.
 template <int KIND, bool STEP>
+__device__ __forceinline__ void short_row(int32_t i, int32_t ks, int32_t ke, const SweepArgs &a,
+                                          int32_t lo, int32_t hi, const StepView &sv,
+                                          RankCache &rc, double &s, double &dg) {
+    const int32_t len = ke - ks;
+    int32_t c8[8];
+    double v8[8], y8[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        c8[j] = (j < len) ? ld_stream(a.col + ks + j) : 0;
+        v8[j] = (j < len) ? ld_stream(a.val + ks + j) : 0.0;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        y8[j] = (j < len) ? view_load<STEP>(c8[j], lo, hi, a.x_own, a.x_hat, sv, rc) : 0.0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        if (j < len) {
+            if (KIND == ECC_KIND_JACOBI && c8[j] == i) dg = v8[j];
+            else s = s + v8[j] * y8[j];
+        }
+    }
+}
+
+// Registers that carry the next stream item's data while the current one is
+// computed: its nonzeros (eight per thread, coalesced) and the per-row values
+// of the row this thread will finish.
+struct StreamPrefetch {
+    int32_t cv[8];
+    double vv[8];
+    int32_t rp0, rp1;
+    double bi, xo;
+};
+
+template <int KIND>
+__device__ __forceinline__ void stream_load(const WorkItem &it, const SweepArgs &a,
+                                            StreamPrefetch &pf) {
+    const int tid = threadIdx.x;
+    const int32_t nnz = it.k1 - it.k0;
+    static_assert(kStreamCap == 8 * kSweepThreads, "eight nonzeros per thread");
+    if (nnz > 0) {  // reads clamped into [k0, k1) so that all are in flight together
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int32_t kc = min(it.k0 + tid + u * kSweepThreads, it.k1 - 1);
+            pf.cv[u] = ld_stream(a.col + kc);
+            pf.vv[u] = ld_stream(a.val + kc);
+        }
+    }
+    const int tpr = lanes_per_row(nnz, it.nrows);
+    const int32_t rr = tid / tpr;
+    pf.rp0 = pf.rp1 = 0;
+    pf.bi = pf.xo = 0.0;
+    if (rr < it.nrows) {
+        const int32_t i = it.row0 + rr;
+        pf.rp0 = ld_stream(a.row_ptr + i);
+        pf.rp1 = ld_stream(a.row_ptr + i + 1);
+        pf.xo = a.x_own[i];
+        if (KIND == ECC_KIND_JACOBI) pf.bi = ld_stream(a.b + i);
+    }
+}
+
+__device__ __forceinline__ void stream_stage(const WorkItem &it, const StreamPrefetch &pf,
+                                             int32_t *s_col, double *s_val) {
+    const int32_t nnz = it.k1 - it.k0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int32_t k = threadIdx.x + u * kSweepThreads;
+        if (k < nnz) {
+            s_col[k] = pf.cv[u];
+            s_val[k] = pf.vv[u];
+        }
+    }
+}
+
+// The rows of a stream item from the staged nonzeros; returns this thread's
+// norm contribution.
+template <int KIND, bool STEP>
+__device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0, int32_t rp1,
+                                                 double bi, double xo, const SweepArgs &a,
+                                                 const int32_t *s_col, const double *s_val,
+                                                 const StepView &sv, RankCache &rc,
+                                                 bool own_arrives) {
+    const int tid = threadIdx.x;
+    const int32_t nnz = it.k1 - it.k0;
+    const int tpr = lanes_per_row(nnz, it.nrows);
+    const int lane = tid & (tpr - 1);
+    const int32_t rr = tid / tpr;
+    if (rr >= it.nrows) return 0.0;
+    const int32_t i = it.row0 + rr;
+    const int32_t lo = it.lo, hi = it.hi;
+    const int32_t rs = rp0 - it.k0, re = rp1 - it.k0;
+    double s = 0.0, dg = 0.0;
+    if (tpr == 1) {
+        // up to eight entries with all gathers in flight, summed in CSR order
+        const int32_t len = re - rs;
+        int32_t c8[8];
+        double v8[8], y8[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            // entries past the row's end are read but unused (LDS is padded)
+            c8[j] = s_col[rs + j];
+            v8[j] = s_val[rs + j];
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            y8[j] = (j < len) ? view_load<STEP>(c8[j], lo, hi, a.x_own, a.x_hat, sv, rc)
+                              : 0.0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (j < len) {
+                if (KIND == ECC_KIND_JACOBI && c8[j] == i) dg = v8[j];
+                else s = s + v8[j] * y8[j];
+            }
+        }
+        for (int32_t k = rs + 8; k < re; ++k) {
+            const int32_t c = s_col[k];
+            const double v = s_val[k];
+            if (KIND == ECC_KIND_JACOBI && c == i) {
+                dg = v;
+                continue;
+            }
+            s = s + v * view_load<STEP>(c, lo, hi, a.x_own, a.x_hat, sv, rc);
+        }
+    } else {
+        for (int32_t k = rs + lane; k < re; k += tpr) {
+            const int32_t c = s_col[k];
+            const double v = s_val[k];
+            if (KIND == ECC_KIND_JACOBI && c == i) {
+                dg = v;
+                continue;
+            }
+            s = s + v * view_load<STEP>(c, lo, hi, a.x_own, a.x_hat, sv, rc);
+        }
+        s = group_sum_dyn(s, tpr);
+        if (KIND == ECC_KIND_JACOBI) dg = group_sum_dyn(dg, tpr);
+    }
+    if (lane != 0) return 0.0;
+    if (STEP && own_arrives) a.x_hat[i] = xo;
+    return row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+}
+
+// One long row (or a slice of it) by the whole workgroup; returns the norm
+// contribution (in thread 0).
+template <int KIND, bool STEP>
+__device__ __forceinline__ double long_compute(const WorkItem &it, const SweepArgs &a,
+                                               const StepView &sv, RankCache &rc,
+                                               bool own_arrives, double *s_red) {
+    const int tid = threadIdx.x;
+    const int32_t i = it.row0, lo = it.lo, hi = it.hi;
+    double s = 0.0, dg = 0.0;
+    seg_accumulate<KIND, STEP, 4>(i, it.k0 + tid, it.k1, kSweepThreads, a, lo, hi, sv, rc, s, dg);
+    s = block_sum<kSweepThreads>(s, s_red);
+    if (KIND == ECC_KIND_JACOBI) dg = block_sum<kSweepThreads>(dg, s_red);
+    if (tid != 0) return 0.0;
+    if (it.kind == kItemPiece) {
+        a.pieces[it.slot] = make_double2(s, dg);
+        return 0.0;
+    }
+    const double xo = a.x_own[i];
+    const double bi = (KIND == ECC_KIND_JACOBI) ? a.b[i] : 0.0;
+    if (STEP && own_arrives) a.x_hat[i] = xo;
+    return row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+}
+
+// A row-list item: rows of similar length, `tpr` lanes per row reading the
+// row's nonzeros directly (contiguous per row); rows of one lane are summed
+// in CSR order.  Returns this thread's norm contribution.
+template <int KIND, bool STEP>
+__device__ __forceinline__ double rows_compute(const WorkItem &it, const SweepArgs &a,
+                                               const StepView &sv, RankCache &rc,
+                                               bool own_arrives) {
+    const int tid = threadIdx.x;
+    const int tpr = it.slot;
+    const int lane = tid & (tpr - 1);
+    const int32_t li = it.k0 + tid / tpr;
+    if (li >= it.k1) return 0.0;
+    const int32_t i = a.rowlist[li];
+    const int32_t lo = it.lo, hi = it.hi;
+    const int32_t ks = a.row_ptr[i], ke = a.row_ptr[i + 1];
+    double s = 0.0, dg = 0.0;
+    if (tpr == 1) {
+        short_row<KIND, STEP>(i, ks, ke, a, lo, hi, sv, rc, s, dg);  // class of rows <= 8
+    } else {
+        seg_accumulate<KIND, STEP, 4>(i, ks + lane, ke, tpr, a, lo, hi, sv, rc, s, dg);
+        s = group_sum_dyn(s, tpr);
+        if (KIND == ECC_KIND_JACOBI) dg = group_sum_dyn(dg, tpr);
+    }
+    if (lane != 0) return 0.0;
+    const double xo = a.x_own[i];
+    const double bi = (KIND == ECC_KIND_JACOBI) ? a.b[i] : 0.0;
+    if (STEP && own_arrives) a.x_hat[i] = xo;
+    return row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+}
+
+// ROWS selects the layout: row-list items (matrices with very uneven rows) or
+// stream items; both may contain vector items and pieces.
+template <int KIND, bool STEP, bool ROWS>
 __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
-    __shared__ int32_t s_col[kStreamCap];
-    __shared__ double s_val[kStreamCap];
+    // padded by 8 so that a row's first eight entries can be read unclamped
+    __shared__ int32_t s_col[kStreamCap + 8];
+    __shared__ double s_val[kStreamCap + 8];
     __shared__ double s_red[kSweepThreads / 64];
     __shared__ uint8_t s_eff[STEP ? kFusedMaxP : 1];
     __shared__ int32_t s_bs[STEP ? kFusedMaxP + 1 : 1];
     if (a.done && *a.done) return;
     const int tid = threadIdx.x;
+    const int32_t G = gridDim.x;
+    // XCD-aware order: workgroups are dispatched round-robin over the 8 XCDs
+    // (blockIdx mod 8).  The items are split into 8 contiguous ranges, one
+    // per XCD, and the XCD's workgroups walk its range together, so each
+    // XCD's L2 sees consecutive rows and their neighbours.  Matrices with
+    // very uneven rows deal items round-robin instead, so that the heavy
+    // items (listed first) spread over every XCD.
+    int64_t i_begin = 0, i_end = a.n_items;
+    int32_t w_first = blockIdx.x, w_step = G;
+    if (!a.interleave && G % 8 == 0 && G >= 8) {
+        const int32_t xcd = blockIdx.x % 8;
+        i_begin = (int64_t)a.n_items * xcd / 8;
+        i_end = (int64_t)a.n_items * (xcd + 1) / 8;
+        w_first = (int32_t)(i_begin + blockIdx.x / 8);
+        w_step = G / 8;
+    }
+    // the first item's loads go out before the prologue below
+    int32_t w = w_first;
+    WorkItem cur{}, nxt{};
+    StreamPrefetch pf;
+    const bool have0 = w < i_end;
+    if (have0) {
+        cur = a.items[w];
+        if (!ROWS && cur.kind == kItemStream) stream_load<KIND>(cur, a, pf);
+    }
+    bool have_next = (int64_t)w + w_step < i_end;
+    if (have_next) nxt = a.items[w + w_step];
+
     StepView sv{s_eff, s_bs, a.P};
     if constexpr (STEP) {
         for (int32_t p = tid; p < a.P; p += kSweepThreads)
@@ -155,9 +466,7 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
         if (blockIdx.x == 0)
             record_step(a.P, a.S, a.t, a.arrived, a.ver_in, a.ver_out, a.age_state, a.eff_state,
                         a.forced, a.eff_user, a.age_user, nullptr);
-        __syncthreads();
     }
-    const int32_t G = gridDim.x;
     if (blockIdx.x == 0) {
         // no split rows: their norm contribution (partial G) is zero
         if (a.zero_extra && tid == 0) a.partials[G] = 0.0;
@@ -168,158 +477,43 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
             if (tid == 0) *a.prev_rho = (a.norm == ECC_NORM_L2) ? sqrt(sum) : sum;
         }
     }
-    // XCD-aware order: workgroups dispatched to the same XCD (blockIdx mod 8)
-    // take consecutive items, so neighbouring rows share that XCD's L2.
-    const int32_t L = (G % 8 == 0) ? (int32_t)((blockIdx.x % 8) * (G / 8) + blockIdx.x / 8)
-                                   : (int32_t)blockIdx.x;
+    if constexpr (STEP) __syncthreads();
+
+    // Software pipeline over this workgroup's items: while an item is computed
+    // from LDS, the loads of the next one (and the descriptor of the one
+    // after) are in flight.
     double contrib = 0.0;
-
-    for (int32_t w = L; w < a.n_items; w += G) {
-        const WorkItem it = a.items[w];
-        const int32_t lo = it.lo, hi = it.hi;
-        const bool own_arrives = STEP && s_eff[it.rank] != 0;
-        int32_t clo = 0, chi = 0;  // lookup cache (empty)
-        bool ceff = false;
-
-        if (it.kind == kItemStream) {
-            const int32_t r0 = it.row0, nr = it.nrows, k0 = it.k0, k1 = it.k1;
-            const int32_t nnz = k1 - k0;
-            const int tpr = lanes_per_row(nnz, nr);
-            const int lane = tid & (tpr - 1);
-            const int32_t rr = tid / tpr;
-            const bool active = rr < nr;
-            const int32_t i = r0 + (active ? rr : 0);
-            // per-row loads, independent of the staged nonzeros
-            int32_t rp0 = 0, rp1 = 0;
-            double bi = 0.0, xo = 0.0;
-            if (active) {
-                rp0 = a.row_ptr[i];
-                rp1 = a.row_ptr[i + 1];
-                xo = a.x_own[i];
-                if (KIND == ECC_KIND_JACOBI) bi = a.b[i];
-            }
-            // stage the item's nonzeros: all loads first, then the LDS stores
-            static_assert(kStreamCap == 8 * kSweepThreads, "eight nonzeros per thread");
-            if (nnz > 0) {  // reads are clamped into [k0, k1) so all are in flight together
-                int32_t cv[8];
-                double vv[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int32_t kc = min(k0 + tid + u * kSweepThreads, k1 - 1);
-                    cv[u] = a.col[kc];
-                    vv[u] = a.val[kc];
-                }
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int32_t k = tid + u * kSweepThreads;
-                    if (k < nnz) {
-                        s_col[k] = cv[u];
-                        s_val[k] = vv[u];
-                    }
-                }
-            }
+    RankCache rc;
+    bool have = have0;
+    while (have) {
+        const bool own_arrives = STEP && s_eff[cur.rank] != 0;
+        const bool next_stream = !ROWS && have_next && nxt.kind == kItemStream;
+        WorkItem nn{};
+        const bool have_nn = (int64_t)w + 2 * (int64_t)w_step < i_end;
+        if (!ROWS && cur.kind == kItemStream) {
+            stream_stage(cur, pf, s_col, s_val);
+            const int32_t rp0 = pf.rp0, rp1 = pf.rp1;
+            const double bi = pf.bi, xo = pf.xo;
             __syncthreads();
-            if (active) {
-                const int32_t rs = rp0 - k0, re = rp1 - k0;
-                double s = 0.0, dg = 0.0;
-                if (tpr == 1) {
-                    // up to 8 entries with all gathers in flight, then in order
-                    const int32_t len = re - rs;
-                    int32_t c8[8];
-                    double v8[8], y8[8];
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        // entries past the row's end repeat its last one (unused)
-                        const int32_t k = (len > 0) ? rs + min(j, len - 1) : 0;
-                        c8[j] = (len > 0) ? s_col[k] : 0;
-                        v8[j] = (len > 0) ? s_val[k] : 0.0;
-                    }
-#pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        y8[j] = (j < len) ? view_load<STEP>(c8[j], lo, hi, a.x_own, a.x_hat, sv,
-                                                            clo, chi, ceff)
-                                          : 0.0;
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        if (j < len) {
-                            if (KIND == ECC_KIND_JACOBI && c8[j] == i) dg = v8[j];
-                            else s = s + v8[j] * y8[j];
-                        }
-                    }
-                    for (int32_t k = rs + 8; k < re; ++k) {
-                        const int32_t c = s_col[k];
-                        const double v = s_val[k];
-                        if (KIND == ECC_KIND_JACOBI && c == i) {
-                            dg = v;
-                            continue;
-                        }
-                        s = s + v * view_load<STEP>(c, lo, hi, a.x_own, a.x_hat, sv, clo, chi,
-                                                    ceff);
-                    }
-                } else {
-                    for (int32_t k = rs + lane; k < re; k += tpr) {
-                        const int32_t c = s_col[k];
-                        const double v = s_val[k];
-                        if (KIND == ECC_KIND_JACOBI && c == i) {
-                            dg = v;
-                            continue;
-                        }
-                        s = s + v * view_load<STEP>(c, lo, hi, a.x_own, a.x_hat, sv, clo, chi,
-                                                    ceff);
-                    }
-                    s = group_sum_dyn(s, tpr);
-                    if (KIND == ECC_KIND_JACOBI) dg = group_sum_dyn(dg, tpr);
-                }
-                if (lane == 0) {
-                    contrib += row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
-                    if (own_arrives) a.x_hat[i] = xo;
-                }
-            }
+            if (next_stream) stream_load<KIND>(nxt, a, pf);
+            if (have_nn) nn = a.items[w + 2 * w_step];
+            contrib += stream_compute<KIND, STEP>(cur, rp0, rp1, bi, xo, a, s_col, s_val, sv, rc,
+                                                  own_arrives);
             __syncthreads();  // LDS is reused by the next item
+        } else if (ROWS && cur.kind == kItemRows) {
+            if (have_nn) nn = a.items[w + 2 * w_step];
+            contrib += rows_compute<KIND, STEP>(cur, a, sv, rc, own_arrives);
+            if (next_stream) stream_load<KIND>(nxt, a, pf);
         } else {
-            // one long row (or a slice of it) by the whole workgroup
-            const int32_t i = it.row0;
-            double s = 0.0, dg = 0.0;
-            int32_t k = it.k0 + tid;
-            for (; k + 3 * kSweepThreads < it.k1; k += 4 * kSweepThreads) {
-                int32_t c[4];
-                double v[4], y[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    c[u] = a.col[k + u * kSweepThreads];
-                    v[u] = a.val[k + u * kSweepThreads];
-                }
-#pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    y[u] = view_load<STEP>(c[u], lo, hi, a.x_own, a.x_hat, sv, clo, chi, ceff);
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    if (KIND == ECC_KIND_JACOBI && c[u] == i) dg = v[u];
-                    else s = s + v[u] * y[u];
-                }
-            }
-            for (; k < it.k1; k += kSweepThreads) {
-                const int32_t c = a.col[k];
-                const double v = a.val[k];
-                if (KIND == ECC_KIND_JACOBI && c == i) {
-                    dg = v;
-                    continue;
-                }
-                s = s + v * view_load<STEP>(c, lo, hi, a.x_own, a.x_hat, sv, clo, chi, ceff);
-            }
-            s = block_sum<kSweepThreads>(s, s_red);
-            if (KIND == ECC_KIND_JACOBI) dg = block_sum<kSweepThreads>(dg, s_red);
-            if (tid == 0) {
-                if (it.kind == kItemPiece) {
-                    a.pieces[it.slot] = make_double2(s, dg);
-                } else {
-                    const double xo = a.x_own[i];
-                    const double bi = (KIND == ECC_KIND_JACOBI) ? a.b[i] : 0.0;
-                    contrib += row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
-                    if (own_arrives) a.x_hat[i] = xo;
-                }
-            }
+            if (have_nn) nn = a.items[w + 2 * w_step];
+            contrib += long_compute<KIND, STEP>(cur, a, sv, rc, own_arrives, s_red);
+            if (next_stream) stream_load<KIND>(nxt, a, pf);
         }
+        w += w_step;
+        have = have_next;
+        cur = nxt;
+        have_next = have_nn;
+        nxt = nn;
     }
 
     const double total = block_sum<kSweepThreads>(contrib, s_red);
@@ -403,11 +597,12 @@ __global__ __launch_bounds__(kNormThreads) void k_residual(const double *__restr
 
 // Structural check of a matrix for a plan: counts rows whose diagonal entry is
 // missing, duplicated or zero (Jacobi only) and entries whose column is out of
-// range.  bad[0] = bad rows, bad[1] = bad columns.
+// range, and finds the bandwidth max |col - row|.  bad[0] = bad rows,
+// bad[1] = bad columns, bad[2] = bandwidth.
 __global__ void k_check(int32_t n_rows, int32_t n_cols, const int32_t *__restrict__ row_ptr,
                         const int32_t *__restrict__ col, const double *__restrict__ val,
                         int32_t check_diag, unsigned long long *__restrict__ bad) {
-    unsigned long long bad_rows = 0, bad_cols = 0;
+    unsigned long long bad_rows = 0, bad_cols = 0, band = 0;
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n_rows;
          i += gridDim.x * blockDim.x) {
         int ndiag = 0;
@@ -415,6 +610,8 @@ __global__ void k_check(int32_t n_rows, int32_t n_cols, const int32_t *__restric
         for (int32_t k = row_ptr[i]; k < row_ptr[i + 1]; ++k) {
             const int32_t c = col[k];
             if (c < 0 || c >= n_cols) ++bad_cols;
+            const int64_t d = (int64_t)c - i;
+            band = max(band, (unsigned long long)(d < 0 ? -d : d));
             if (c == i) {
                 ++ndiag;
                 zero = zero || (val[k] == 0.0);
@@ -424,19 +621,39 @@ __global__ void k_check(int32_t n_rows, int32_t n_cols, const int32_t *__restric
     }
     if (bad_rows) atomicAdd(&bad[0], bad_rows);
     if (bad_cols) atomicAdd(&bad[1], bad_cols);
+    if (band) atomicMax(&bad[2], band);
 }
 
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
 
-// Work items of a matrix for a plan's row blocks: very long rows first (as
-// pieces, then whole), then runs of short rows in row order.
+// Work items of a matrix for a plan's row blocks.  Rows longer than one LDS
+// stage become vector items (one workgroup) or pieces of kVectorCap nonzeros
+// (recombined in order); they come first.  The other rows form, for a
+// regular matrix, runs of consecutive short rows (stream items); for a
+// matrix whose row lengths vary widely (longest row > 64 and > 8 x (mean +
+// 1)), row-list items of one length class per rank: <= 8 nonzeros with one
+// lane per row, <= 32 with 4, <= 128 with 16, longer with 64.
+static bool rows_irregular(const std::vector<int32_t> &rp) {
+    const int64_t n = (int64_t)rp.size() - 1;
+    if (n <= 0) return false;
+    int64_t mx = 0;
+    for (int64_t i = 0; i < n; ++i) mx = std::max<int64_t>(mx, (int64_t)rp[i + 1] - rp[i]);
+    const double mean = (double)rp[n] / (double)n;
+    return mx > 64 && (double)mx > 8.0 * (mean + 1.0);
+}
+
 static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_t> &counts,
-                        std::vector<WorkItem> &items, std::vector<Fixup> &fixups,
+                        bool irregular, std::vector<WorkItem> &items,
+                        std::vector<Fixup> &fixups, std::vector<int32_t> &rowlist,
                         int64_t &n_pieces) {
     std::vector<WorkItem> big, vec, stream;
+    std::vector<WorkItem> cls[4];
+    static const int kClassMax[4] = {8, 32, 128, kStreamCap};
+    static const int kClassLanes[4] = {1, 4, 16, 64};
     n_pieces = 0;
+    rowlist.clear();
     int64_t row = 0;
     auto make = [](int64_t r0, int64_t nr, int64_t k0, int64_t k1, int64_t lo, int64_t hi,
                    int kind, int64_t p, int64_t slot) {
@@ -454,6 +671,7 @@ static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_
     };
     for (size_t p = 0; p < counts.size(); ++p) {
         const int64_t lo = row, hi = row + counts[p];
+        std::vector<int32_t> by_class[4];
         int64_t i = lo;
         while (i < hi) {
             const int64_t len = (int64_t)rp[i + 1] - rp[i];
@@ -473,6 +691,13 @@ static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_
                 ++i;
                 continue;
             }
+            if (irregular) {
+                int c = 0;
+                while (len > kClassMax[c]) ++c;
+                by_class[c].push_back((int32_t)i);
+                ++i;
+                continue;
+            }
             const int64_t start = i;
             int64_t nnz = 0;
             while (i < hi && i - start < kStreamRows) {
@@ -483,16 +708,53 @@ static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_
             }
             stream.push_back(make(start, i - start, rp[start], rp[i], lo, hi, kItemStream, p, 0));
         }
+        for (int c = 0; c < 4; ++c) {
+            const int64_t per_item = kSweepThreads / kClassLanes[c];
+            const std::vector<int32_t> &rows = by_class[c];
+            for (size_t s0 = 0; s0 < rows.size(); s0 += per_item) {
+                const int64_t l0 = (int64_t)rowlist.size() + 0;
+                const size_t s1 = std::min(rows.size(), s0 + (size_t)per_item);
+                rowlist.insert(rowlist.end(), rows.begin() + s0, rows.begin() + s1);
+                cls[c].push_back(make(rows[s0], (int64_t)(s1 - s0), l0, l0 + (int64_t)(s1 - s0),
+                                      lo, hi, kItemRows, p, kClassLanes[c]));
+            }
+        }
         row = hi;
     }
     items.clear();
     items.insert(items.end(), big.begin(), big.end());
     items.insert(items.end(), vec.begin(), vec.end());
+    for (int c = 3; c >= 0; --c) items.insert(items.end(), cls[c].begin(), cls[c].end());
     items.insert(items.end(), stream.begin(), stream.end());
 }
 
-static int32_t sweep_grid(int64_t n_items) {
-    int64_t g = std::max<int64_t>(1, std::min<int64_t>(n_items, kMaxSweepBlocks));
+// Workgroups of a sweep: as many as the device holds at once (each then
+// walks several items through the load/compute pipeline), at most one per
+// item, rounded down to a multiple of the 8 XCDs.
+static int32_t sweep_grid(int64_t n_items, int kind, bool rows) {
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        cus = 256;
+    hipError_t e;
+    if (kind == ECC_KIND_JACOBI)
+        e = rows ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                       &per_cu, k_sweep<ECC_KIND_JACOBI, true, true>, kSweepThreads, 0)
+                 : hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                       &per_cu, k_sweep<ECC_KIND_JACOBI, true, false>, kSweepThreads, 0);
+    else
+        e = rows ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                       &per_cu, k_sweep<ECC_KIND_POWER, true, true>, kSweepThreads, 0)
+                 : hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                       &per_cu, k_sweep<ECC_KIND_POWER, true, false>, kSweepThreads, 0);
+    if (e != hipSuccess || per_cu < 1) per_cu = 4;
+    const int64_t resident = (int64_t)std::max(cus, 1) * per_cu;
+#if ECC_GRID_PER_ITEM
+    (void)resident;
+    int64_t g = std::max<int64_t>(1, std::min<int64_t>(n_items, (int64_t)1 << 20));
+#else
+    int64_t g = std::max<int64_t>(1, std::min<int64_t>({n_items, resident, (int64_t)kMaxSweepBlocks}));
+#endif
     if (g >= 8) g -= g % 8;
     return (int32_t)g;
 }
@@ -513,6 +775,8 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     a.x_next = L.x_next;
     a.partials = L.partials;
     a.pieces = M->d_pieces;
+    a.rowlist = M->d_rowlist;
+    a.interleave = M->irregular ? 1 : 0;
     a.zero_extra = M->n_fixups == 0 ? 1 : 0;
     a.prev_partials = L.prev_partials;
     a.prev_rho = L.prev_rho;
@@ -541,13 +805,28 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     }
     TimedLaunch timed(pl, ECC_TIMING_SWEEP);
     const dim3 grid(M->grid), block(kSweepThreads);
+    hipStream_t st = pl->stream;
+    const bool rows = M->irregular;
+#define ECC_SWEEP_LAUNCH(K, S, R) \
+    hipLaunchKernelGGL((k_sweep<K, S, R>), grid, block, 0, st, a)
     if (M->kind == ECC_KIND_JACOBI) {
-        if (step) hipLaunchKernelGGL((k_sweep<ECC_KIND_JACOBI, true>), grid, block, 0, pl->stream, a);
-        else hipLaunchKernelGGL((k_sweep<ECC_KIND_JACOBI, false>), grid, block, 0, pl->stream, a);
+        if (step) {
+            if (rows) ECC_SWEEP_LAUNCH(ECC_KIND_JACOBI, true, true);
+            else ECC_SWEEP_LAUNCH(ECC_KIND_JACOBI, true, false);
+        } else {
+            if (rows) ECC_SWEEP_LAUNCH(ECC_KIND_JACOBI, false, true);
+            else ECC_SWEEP_LAUNCH(ECC_KIND_JACOBI, false, false);
+        }
     } else {
-        if (step) hipLaunchKernelGGL((k_sweep<ECC_KIND_POWER, true>), grid, block, 0, pl->stream, a);
-        else hipLaunchKernelGGL((k_sweep<ECC_KIND_POWER, false>), grid, block, 0, pl->stream, a);
+        if (step) {
+            if (rows) ECC_SWEEP_LAUNCH(ECC_KIND_POWER, true, true);
+            else ECC_SWEEP_LAUNCH(ECC_KIND_POWER, true, false);
+        } else {
+            if (rows) ECC_SWEEP_LAUNCH(ECC_KIND_POWER, false, true);
+            else ECC_SWEEP_LAUNCH(ECC_KIND_POWER, false, false);
+        }
     }
+#undef ECC_SWEEP_LAUNCH
     ECC_LAUNCH_CHECK();
     if (step) pl->clock += 1;
     return ECC_OK;
@@ -626,10 +905,11 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     ECC_ARG(rp[n] == A->nnz, "row_ptr[n] = %d differs from nnz = %lld", rp[n], (long long)A->nnz);
 
     // structural check on the device
+    int64_t bandwidth = 0;
     if (n > 0) {
         unsigned long long *d_bad = nullptr;
-        ECC_HIP(hipMalloc((void **)&d_bad, 2 * sizeof(unsigned long long)));
-        unsigned long long h_bad[2] = {0, 0};
+        ECC_HIP(hipMalloc((void **)&d_bad, 3 * sizeof(unsigned long long)));
+        unsigned long long h_bad[3] = {0, 0, 0};
         hipError_t e = hipMemcpy(d_bad, h_bad, sizeof(h_bad), hipMemcpyHostToDevice);
         if (e == hipSuccess) {
             const int blocks = (int)std::min<int64_t>(4096, (n + 255) / 256);
@@ -647,12 +927,15 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
         }
         ECC_ARG(h_bad[1] == 0, "%llu column indices are out of range", h_bad[1]);
         ECC_ARG(h_bad[0] == 0, "%llu rows lack a single non-zero diagonal entry", h_bad[0]);
+        bandwidth = (int64_t)h_bad[2];
     }
 
     std::vector<WorkItem> items;
     std::vector<Fixup> fixups;
+    std::vector<int32_t> rowlist;
     int64_t n_pieces = 0;
-    build_items(rp, plan->counts, items, fixups, n_pieces);
+    const bool irregular = rows_irregular(rp);
+    build_items(rp, plan->counts, irregular, items, fixups, rowlist, n_pieces);
     if ((int64_t)items.size() >= (int64_t(1) << 31)) {
         set_error("too many work items");
         return ECC_ERR_RANGE;
@@ -669,7 +952,9 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     M->n_items = (int64_t)items.size();
     M->n_fixups = (int64_t)fixups.size();
     M->n_pieces = n_pieces;
-    M->grid = sweep_grid(M->n_items);
+    M->irregular = irregular;
+    M->bandwidth = bandwidth;
+    M->grid = sweep_grid(M->n_items, kind, irregular);
     auto fail = [&](const char *what) {
         set_error("%s", what);
         ecc_matrix_destroy(M);
@@ -691,6 +976,13 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     }
     if (n_pieces > 0 && hipMalloc((void **)&M->d_pieces, sizeof(double2) * n_pieces) != hipSuccess)
         return fail("hipMalloc of piece sums failed");
+    if (!rowlist.empty()) {
+        if (hipMalloc((void **)&M->d_rowlist, sizeof(int32_t) * rowlist.size()) != hipSuccess)
+            return fail("hipMalloc of the row list failed");
+        if (hipMemcpy(M->d_rowlist, rowlist.data(), sizeof(int32_t) * rowlist.size(),
+                      hipMemcpyHostToDevice) != hipSuccess)
+            return fail("copy of the row list failed");
+    }
     // two buffers of G + 1 partials: a loop iteration writes one while the
     // next launch reduces the other
     if (hipMalloc((void **)&M->d_partials, sizeof(double) * 2 * (M->grid + 1)) != hipSuccess)
@@ -706,6 +998,7 @@ ecc_status_t ecc_matrix_destroy(ecc_matrix_t M) {
     (void)hipFree(M->d_fixups);
     (void)hipFree(M->d_pieces);
     (void)hipFree(M->d_partials);
+    (void)hipFree(M->d_rowlist);
     delete M;
     return ECC_OK;
 }
