@@ -101,23 +101,33 @@ __global__ __launch_bounds__(kReduceThreads) void k_allreduce(
     const int vec = __syncthreads_and(ok);
 
     const int64_t base = (int64_t)(blockIdx.x - 1) * (kReduceThreads * kReduceElems);
-    constexpr int U = 4;  // ranks whose loads are in flight together
+    constexpr int U = kReduceU;
+    constexpr int VP = kReduceElems / 2;  // 16-byte pairs per thread
+    static_assert(kReduceElems % 2 == 0, "pairs of elements");
     if (vec) {
-        // element pairs q0 and q0 + kReduceThreads of this chunk
-        const int64_t q0 = base / 2 + tid, q1 = q0 + kReduceThreads;
-        const bool a0 = 2 * q0 < m, a1 = 2 * q1 < m;
-        double2 acc0 = make_double2(0.0, 0.0), acc1 = acc0;
+        // element pairs q[j] = chunk pair offset + tid + j * kReduceThreads
+        int64_t q[VP];
+        bool in[VP];
+        double2 acc[VP];
+#pragma unroll
+        for (int j = 0; j < VP; ++j) {
+            q[j] = base / 2 + tid + (int64_t)j * kReduceThreads;
+            in[j] = 2 * q[j] < m;
+            acc[j] = make_double2(0.0, 0.0);
+        }
         for (int32_t p0 = 0; p0 < P; p0 += U) {
-            double2 v0[U], v1[U];
+            double2 v[U][VP];
             bool e[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int32_t p = p0 + u;
                 if (p < P) {
                     e[u] = stale_select(ver_in[p], arrived[p], t, S);
-                    const double2 *src = reinterpret_cast<const double2 *>(e[u] ? fresh[p] : slots[p]);
-                    if (a0) v0[u] = src[q0];
-                    if (a1) v1[u] = src[q1];
+                    const double2 *src =
+                        reinterpret_cast<const double2 *>(e[u] ? fresh[p] : slots[p]);
+#pragma unroll
+                    for (int j = 0; j < VP; ++j)
+                        if (in[j]) v[u][j] = src[q[j]];
                 }
             }
 #pragma unroll
@@ -126,24 +136,34 @@ __global__ __launch_bounds__(kReduceThreads) void k_allreduce(
                 if (p < P) {
                     if (e[u]) {
                         double2 *dst = reinterpret_cast<double2 *>(slots[p]);
-                        if (a0) dst[q0] = v0[u];
-                        if (a1) dst[q1] = v1[u];
+#pragma unroll
+                        for (int j = 0; j < VP; ++j) {
+                            if (in[j]) {
+#if ECC_RED_NT
+                                __builtin_nontemporal_store(v[u][j].x, &dst[q[j]].x);
+                                __builtin_nontemporal_store(v[u][j].y, &dst[q[j]].y);
+#else
+                                dst[q[j]] = v[u][j];
+#endif
+                            }
+                        }
                     }
-                    if (p == 0) {
-                        acc0 = v0[u];
-                        acc1 = v1[u];
-                    } else {
-                        acc0.x = acc0.x + v0[u].x;
-                        acc0.y = acc0.y + v0[u].y;
-                        acc1.x = acc1.x + v1[u].x;
-                        acc1.y = acc1.y + v1[u].y;
+#pragma unroll
+                    for (int j = 0; j < VP; ++j) {
+                        if (p == 0) {
+                            acc[j] = v[u][j];
+                        } else {
+                            acc[j].x = acc[j].x + v[u][j].x;
+                            acc[j].y = acc[j].y + v[u][j].y;
+                        }
                     }
                 }
             }
         }
         double2 *r2 = reinterpret_cast<double2 *>(result);
-        if (a0) r2[q0] = acc0;
-        if (a1) r2[q1] = acc1;
+#pragma unroll
+        for (int j = 0; j < VP; ++j)
+            if (in[j]) r2[q[j]] = acc[j];
     } else {
         int64_t idx[kReduceElems];
         double acc[kReduceElems];
