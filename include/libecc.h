@@ -257,10 +257,11 @@ ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double *d_b, doubl
                        uint8_t *d_eff_hist, int32_t *d_age_hist, int32_t *h_iters);
 
 /* ---------------------------------------------------------------------------
- * Measurement utility: a plain streaming copy d_dst[i] = d_src[i], 0 <= i < n,
- * with 16-byte accesses (both buffers 16-byte aligned, n even, no overlap),
- * enqueued on hip_stream.  Benchmarks use it as the copy ceiling of the
- * device memory and to calibrate hardware byte counters.
+ * Plain streaming copy d_dst[i] = d_src[i], 0 <= i < n, enqueued on
+ * hip_stream.  Both buffers 8-byte aligned and not overlapping
+ * (ECC_ERR_ARG otherwise); 16-byte accesses when both are 16-byte aligned.
+ * Used to restart an iteration from a resident initial vector, as the copy
+ * ceiling of the device memory, and to calibrate hardware byte counters.
  * ------------------------------------------------------------------------- */
 ecc_status_t ecc_stream_copy(double *d_dst, const double *d_src, int64_t n, void *hip_stream);
 

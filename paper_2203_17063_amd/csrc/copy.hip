@@ -1,6 +1,8 @@
 // Plain streaming copy (16-byte accesses, four per thread in flight): the
 // reference kernel for the measured copy ceiling and for calibrating the
 // HBM byte counters against a kernel of known traffic.
+#include <algorithm>
+
 #include "ecc_common.h"
 
 namespace ecc {
@@ -8,9 +10,15 @@ namespace ecc {
 constexpr int kCopyThreads = 256;
 constexpr int kCopyPairs = 4;  // 16-byte pairs per thread
 
+// Copies npair 16-byte pairs; an odd trailing element (tail != 0) is copied
+// by thread 0 of block 0.
 __global__ __launch_bounds__(kCopyThreads) void k_stream_copy(double2 *__restrict__ dst,
                                                               const double2 *__restrict__ src,
-                                                              int64_t npair) {
+                                                              int64_t npair, int tail) {
+    if (tail && blockIdx.x == 0 && threadIdx.x == 0)
+        reinterpret_cast<double *>(dst)[2 * npair] =
+            reinterpret_cast<const double *>(src)[2 * npair];
+    if (npair == 0) return;
     const int64_t base = (int64_t)blockIdx.x * (kCopyThreads * kCopyPairs) + threadIdx.x;
     double2 v[kCopyPairs];
 #pragma unroll
@@ -25,6 +33,14 @@ __global__ __launch_bounds__(kCopyThreads) void k_stream_copy(double2 *__restric
     }
 }
 
+// Copy of 8-byte elements for buffers that are not 16-byte aligned.
+__global__ __launch_bounds__(kCopyThreads) void k_copy_f64(double *__restrict__ dst,
+                                                           const double *__restrict__ src,
+                                                           int64_t n) {
+    const int64_t k = (int64_t)blockIdx.x * kCopyThreads + threadIdx.x;
+    if (k < n) dst[k] = src[k];
+}
+
 }  // namespace ecc
 
 using namespace ecc;
@@ -35,14 +51,25 @@ extern "C" ecc_status_t ecc_stream_copy(double *d_dst, const double *d_src, int6
     ECC_ARG(n >= 0, "n must be >= 0");
     if (n == 0) return ECC_OK;
     ECC_ARG(d_dst && d_src, "NULL pointer");
-    ECC_ARG((((uintptr_t)d_dst | (uintptr_t)d_src) & 15) == 0 && (n & 1) == 0,
-            "the copy needs 16-byte aligned buffers and an even element count");
+    ECC_ARG((((uintptr_t)d_dst | (uintptr_t)d_src) & 7) == 0, "buffers must be 8-byte aligned");
+    const uintptr_t lo = (uintptr_t)d_dst, hi = lo + 8 * (uintptr_t)n;
+    const uintptr_t slo = (uintptr_t)d_src, shi = slo + 8 * (uintptr_t)n;
+    ECC_ARG(hi <= slo || shi <= lo, "source and destination overlap");
+    if ((((uintptr_t)d_dst | (uintptr_t)d_src) & 15) != 0) {
+        const int64_t grid = (n + kCopyThreads - 1) / kCopyThreads;
+        ECC_ARG(grid < 0x7fffffff, "n too large");
+        hipLaunchKernelGGL(k_copy_f64, dim3((unsigned)grid), dim3(kCopyThreads), 0,
+                           (hipStream_t)hip_stream, d_dst, d_src, n);
+        ECC_LAUNCH_CHECK();
+        return ECC_OK;
+    }
     const int64_t npair = n / 2;
-    const int64_t grid = (npair + kCopyThreads * kCopyPairs - 1) / (kCopyThreads * kCopyPairs);
+    const int64_t grid =
+        std::max<int64_t>(1, (npair + kCopyThreads * kCopyPairs - 1) / (kCopyThreads * kCopyPairs));
     ECC_ARG(grid < 0x7fffffff, "n too large");
     hipLaunchKernelGGL(k_stream_copy, dim3((unsigned)grid), dim3(kCopyThreads), 0,
                        (hipStream_t)hip_stream, reinterpret_cast<double2 *>(d_dst),
-                       reinterpret_cast<const double2 *>(d_src), npair);
+                       reinterpret_cast<const double2 *>(d_src), npair, (int)(n & 1));
     ECC_LAUNCH_CHECK();
     return ECC_OK;
 }

@@ -88,6 +88,16 @@ struct Tile {
 // rows (entries [k0, k1) of the row list: rows of similar length, `slot`
 // lanes each).
 enum { kItemStream = 0, kItemVector = 1, kItemPiece = 2, kItemRows = 3 };
+// Sweep layouts of a matrix: stream items staged through LDS; row-list items
+// binned by length (very uneven rows); short-row items, one lane per row
+// read directly (every row holds at most kShortRow entries).
+enum { kLayStream = 0, kLayRows = 1, kLayShort = 2 };
+#ifndef ECC_SHORT_ROW
+#define ECC_SHORT_ROW 8
+#endif
+constexpr int kShortRow = ECC_SHORT_ROW;
+static_assert(kShortRow <= 8, "a short row is summed from eight registers");
+static_assert(kStreamRows <= 256 && kStreamRows <= kSweepThreads, "one lane per short row");
 struct WorkItem {
     int32_t row0;
     int32_t nrows;
@@ -293,6 +303,7 @@ struct ecc_matrix_s {
     int64_t n_pieces = 0;
     int32_t grid = 1;               // workgroups of a sweep launch
     bool irregular = false;         // row lengths vary widely: row-list items
+    int layout = 0;                 // kLayStream, kLayRows or kLayShort
     int64_t bandwidth = 0;          // max |col - row|
     int32_t *d_rowlist = nullptr;   // rows of the row-list items, by rank and length class
     double *d_partials = nullptr;   // internal partials of ecc_solve: 2 x (grid + 1)

@@ -42,6 +42,9 @@
 #ifndef ECC_GRID_PER_ITEM
 #define ECC_GRID_PER_ITEM 0
 #endif
+#ifndef ECC_WG0_IDLE
+#define ECC_WG0_IDLE 0
+#endif
 
 namespace ecc {
 
@@ -418,13 +421,36 @@ __device__ __forceinline__ double rows_compute(const WorkItem &it, const SweepAr
     return row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
 }
 
-// ROWS selects the layout: row-list items (matrices with very uneven rows) or
-// stream items; both may contain vector items and pieces.
-template <int KIND, bool STEP, bool ROWS>
-__global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
+// A run of at most kSweepThreads consecutive rows of one rank in a matrix
+// whose rows all hold at most kShortRow entries: one lane per row reads the
+// row's entries straight from memory (the lanes of a wave cover one
+// contiguous stretch of the CSR arrays) and sums them in CSR order.  No LDS
+// and no barrier, so the kernel keeps more waves in flight.  rp0/rp1 are
+// the row's bounds, loaded ahead by the caller.
+template <int KIND, bool STEP>
+__device__ __forceinline__ double short_compute(const WorkItem &it, int32_t rp0, int32_t rp1,
+                                                const SweepArgs &a, const StepView &sv,
+                                                RankCache &rc, bool own_arrives) {
+    const int32_t rr = threadIdx.x;
+    if (rr >= it.nrows) return 0.0;
+    const int32_t i = it.row0 + rr;
+    const double xo = a.x_own[i];
+    const double bi = (KIND == ECC_KIND_JACOBI) ? ld_stream(a.b + i) : 0.0;
+    double s = 0.0, dg = 0.0;
+    short_row<KIND, STEP>(i, rp0, rp1, a, it.lo, it.hi, sv, rc, s, dg);
+    if (STEP && own_arrives) a.x_hat[i] = xo;
+    return row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+}
+
+// LAY selects the layout: stream items staged through LDS (kLayStream),
+// row-list items for matrices with very uneven rows (kLayRows) -- both may
+// contain vector items and pieces -- or short-row items (kLayShort).
+template <int KIND, bool STEP, int LAY>
+__device__ __forceinline__ void sweep_body(const SweepArgs &a) {
+    constexpr bool STAGED = LAY == kLayStream;
     // padded by 8 so that a row's first eight entries can be read unclamped
-    __shared__ int32_t s_col[kStreamCap + 8];
-    __shared__ double s_val[kStreamCap + 8];
+    __shared__ int32_t s_col[STAGED ? kStreamCap + 8 : 1];
+    __shared__ double s_val[STAGED ? kStreamCap + 8 : 1];
     __shared__ double s_red[kSweepThreads / 64];
     __shared__ uint8_t s_eff[STEP ? kFusedMaxP : 1];
     __shared__ int32_t s_bs[STEP ? kFusedMaxP + 1 : 1];
@@ -445,15 +471,26 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
         i_end = (int64_t)a.n_items * (xcd + 1) / 8;
         w_first = (int32_t)(i_begin + blockIdx.x / 8);
         w_step = G / 8;
+#if ECC_WG0_IDLE
+        if (xcd == 0 && G / 8 >= 2) {
+            w_first = blockIdx.x == 0 ? (int32_t)i_end : (int32_t)(i_begin + blockIdx.x / 8 - 1);
+            w_step = G / 8 - 1;
+        }
+#endif
     }
     // the first item's loads go out before the prologue below
     int32_t w = w_first;
     WorkItem cur{}, nxt{};
     StreamPrefetch pf;
     const bool have0 = w < i_end;
+    int32_t rp0 = 0, rp1 = 0;  // short layout: this thread's row bounds in the current item
     if (have0) {
         cur = a.items[w];
-        if (!ROWS && cur.kind == kItemStream) stream_load<KIND>(cur, a, pf);
+        if (STAGED && cur.kind == kItemStream) stream_load<KIND>(cur, a, pf);
+        if (LAY == kLayShort && (int32_t)tid < cur.nrows) {
+            rp0 = a.row_ptr[cur.row0 + tid];
+            rp1 = a.row_ptr[cur.row0 + tid + 1];
+        }
     }
     bool have_next = (int64_t)w + w_step < i_end;
     if (have_next) nxt = a.items[w + w_step];
@@ -487,10 +524,21 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
     bool have = have0;
     while (have) {
         const bool own_arrives = STEP && s_eff[cur.rank] != 0;
-        const bool next_stream = !ROWS && have_next && nxt.kind == kItemStream;
+        const bool next_stream = STAGED && have_next && nxt.kind == kItemStream;
         WorkItem nn{};
         const bool have_nn = (int64_t)w + 2 * (int64_t)w_step < i_end;
-        if (!ROWS && cur.kind == kItemStream) {
+        if (LAY == kLayShort) {
+            // the next item's row bounds are in flight while this one is summed
+            int32_t np0 = 0, np1 = 0;
+            if (have_next && (int32_t)tid < nxt.nrows) {
+                np0 = a.row_ptr[nxt.row0 + tid];
+                np1 = a.row_ptr[nxt.row0 + tid + 1];
+            }
+            if (have_nn) nn = a.items[w + 2 * w_step];
+            contrib += short_compute<KIND, STEP>(cur, rp0, rp1, a, sv, rc, own_arrives);
+            rp0 = np0;
+            rp1 = np1;
+        } else if (STAGED && cur.kind == kItemStream) {
             stream_stage(cur, pf, s_col, s_val);
             const int32_t rp0 = pf.rp0, rp1 = pf.rp1;
             const double bi = pf.bi, xo = pf.xo;
@@ -500,7 +548,7 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
             contrib += stream_compute<KIND, STEP>(cur, rp0, rp1, bi, xo, a, s_col, s_val, sv, rc,
                                                   own_arrives);
             __syncthreads();  // LDS is reused by the next item
-        } else if (ROWS && cur.kind == kItemRows) {
+        } else if (LAY == kLayRows && cur.kind == kItemRows) {
             if (have_nn) nn = a.items[w + 2 * w_step];
             contrib += rows_compute<KIND, STEP>(cur, a, sv, rc, own_arrives);
             if (next_stream) stream_load<KIND>(nxt, a, pf);
@@ -518,6 +566,22 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
 
     const double total = block_sum<kSweepThreads>(contrib, s_red);
     if (tid == 0) a.partials[blockIdx.x] = total;
+}
+
+template <int KIND, bool STEP, int LAY>
+__global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
+    sweep_body<KIND, STEP, LAY>(a);
+}
+
+// The short-row layout holds few values per lane: the register budget is
+// capped so that ECC_SHORT_WAVES waves share each SIMD.
+#ifndef ECC_SHORT_WAVES
+#define ECC_SHORT_WAVES 6
+#endif
+template <int KIND, bool STEP>
+__global__ __launch_bounds__(kSweepThreads) __attribute__((amdgpu_waves_per_eu(ECC_SHORT_WAVES)))
+void k_sweep_short(SweepArgs a) {
+    sweep_body<KIND, STEP, kLayShort>(a);
 }
 
 // Second pass of a sweep, one workgroup of kNormThreads.  (1) Rows split into
@@ -731,22 +795,30 @@ static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_
 // Workgroups of a sweep: as many as the device holds at once (each then
 // walks several items through the load/compute pipeline), at most one per
 // item, rounded down to a multiple of the 8 XCDs.
-static int32_t sweep_grid(int64_t n_items, int kind, bool rows) {
+template <int LAY>
+static hipError_t sweep_occupancy(int *per_cu, int kind) {
+    if constexpr (LAY == kLayShort)
+        return kind == ECC_KIND_JACOBI
+                   ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                         per_cu, k_sweep_short<ECC_KIND_JACOBI, true>, kSweepThreads, 0)
+                   : hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                         per_cu, k_sweep_short<ECC_KIND_POWER, true>, kSweepThreads, 0);
+    else
+        return kind == ECC_KIND_JACOBI
+                   ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                         per_cu, k_sweep<ECC_KIND_JACOBI, true, LAY>, kSweepThreads, 0)
+                   : hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                         per_cu, k_sweep<ECC_KIND_POWER, true, LAY>, kSweepThreads, 0);
+}
+
+static int32_t sweep_grid(int64_t n_items, int kind, int layout) {
     int dev = 0, cus = 0, per_cu = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         cus = 256;
-    hipError_t e;
-    if (kind == ECC_KIND_JACOBI)
-        e = rows ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                       &per_cu, k_sweep<ECC_KIND_JACOBI, true, true>, kSweepThreads, 0)
-                 : hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                       &per_cu, k_sweep<ECC_KIND_JACOBI, true, false>, kSweepThreads, 0);
-    else
-        e = rows ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                       &per_cu, k_sweep<ECC_KIND_POWER, true, true>, kSweepThreads, 0)
-                 : hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                       &per_cu, k_sweep<ECC_KIND_POWER, true, false>, kSweepThreads, 0);
+    const hipError_t e = layout == kLayRows    ? sweep_occupancy<kLayRows>(&per_cu, kind)
+                         : layout == kLayShort ? sweep_occupancy<kLayShort>(&per_cu, kind)
+                                               : sweep_occupancy<kLayStream>(&per_cu, kind);
     if (e != hipSuccess || per_cu < 1) per_cu = 4;
     const int64_t resident = (int64_t)std::max(cus, 1) * per_cu;
 #if ECC_GRID_PER_ITEM
@@ -806,26 +878,23 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     TimedLaunch timed(pl, ECC_TIMING_SWEEP);
     const dim3 grid(M->grid), block(kSweepThreads);
     hipStream_t st = pl->stream;
-    const bool rows = M->irregular;
 #define ECC_SWEEP_LAUNCH(K, S, R) \
     hipLaunchKernelGGL((k_sweep<K, S, R>), grid, block, 0, st, a)
+#define ECC_SWEEP_LAYOUTS(K, S)                                        \
+    do {                                                               \
+        if (M->layout == kLayRows) ECC_SWEEP_LAUNCH(K, S, kLayRows);   \
+        else if (M->layout == kLayShort)                               \
+            hipLaunchKernelGGL((k_sweep_short<K, S>), grid, block, 0, st, a); \
+        else ECC_SWEEP_LAUNCH(K, S, kLayStream);                       \
+    } while (0)
     if (M->kind == ECC_KIND_JACOBI) {
-        if (step) {
-            if (rows) ECC_SWEEP_LAUNCH(ECC_KIND_JACOBI, true, true);
-            else ECC_SWEEP_LAUNCH(ECC_KIND_JACOBI, true, false);
-        } else {
-            if (rows) ECC_SWEEP_LAUNCH(ECC_KIND_JACOBI, false, true);
-            else ECC_SWEEP_LAUNCH(ECC_KIND_JACOBI, false, false);
-        }
+        if (step) ECC_SWEEP_LAYOUTS(ECC_KIND_JACOBI, true);
+        else ECC_SWEEP_LAYOUTS(ECC_KIND_JACOBI, false);
     } else {
-        if (step) {
-            if (rows) ECC_SWEEP_LAUNCH(ECC_KIND_POWER, true, true);
-            else ECC_SWEEP_LAUNCH(ECC_KIND_POWER, true, false);
-        } else {
-            if (rows) ECC_SWEEP_LAUNCH(ECC_KIND_POWER, false, true);
-            else ECC_SWEEP_LAUNCH(ECC_KIND_POWER, false, false);
-        }
+        if (step) ECC_SWEEP_LAYOUTS(ECC_KIND_POWER, true);
+        else ECC_SWEEP_LAYOUTS(ECC_KIND_POWER, false);
     }
+#undef ECC_SWEEP_LAYOUTS
 #undef ECC_SWEEP_LAUNCH
     ECC_LAUNCH_CHECK();
     if (step) pl->clock += 1;
@@ -935,6 +1004,18 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     std::vector<int32_t> rowlist;
     int64_t n_pieces = 0;
     const bool irregular = rows_irregular(rp);
+    // Short-row layout for matrices whose rows all hold at most kShortRow
+    // entries.  Measured on MI355X (Jacobi on 2-D 5-point and 3-D 7-point
+    // Laplacians, 0.26M-64M rows): it beats the LDS-staged stream layout for
+    // every 5-entry matrix and for 7-entry ones up to a few hundred MB of
+    // CSR arrays; beyond that, for rows of 7 or 8 entries, the coalesced
+    // loads of the stream layout draw more bandwidth from HBM.
+    int32_t max_row = 0;
+    for (int64_t i = 0; i < n; ++i) max_row = std::max(max_row, rp[i + 1] - rp[i]);
+    const int64_t csr_bytes = 12 * (int64_t)A->nnz + 4 * (n + 1);
+    const bool short_rows =
+        max_row <= kShortRow && (max_row <= 6 || csr_bytes <= (int64_t(1) << 29));
+    const int layout = irregular ? kLayRows : (short_rows ? kLayShort : kLayStream);
     build_items(rp, plan->counts, irregular, items, fixups, rowlist, n_pieces);
     if ((int64_t)items.size() >= (int64_t(1) << 31)) {
         set_error("too many work items");
@@ -953,8 +1034,9 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     M->n_fixups = (int64_t)fixups.size();
     M->n_pieces = n_pieces;
     M->irregular = irregular;
+    M->layout = layout;
     M->bandwidth = bandwidth;
-    M->grid = sweep_grid(M->n_items, kind, irregular);
+    M->grid = sweep_grid(M->n_items, kind, layout);
     auto fail = [&](const char *what) {
         set_error("%s", what);
         ecc_matrix_destroy(M);

@@ -72,6 +72,8 @@ class Iterative:
         self.T = int(mask.shape[0])
         self.d_b = _dev(b, device=device) if b is not None else None
         self.x0 = np.zeros(self.n) if x0 is None else np.asarray(x0, dtype=np.float64)
+        # x0 stays resident: each solve restarts from it with a device copy
+        self.d_x0 = _dev(self.x0, device=device)
         self.d_x = torch.empty(self.n, dtype=torch.float64, device=device)
         self.d_x_tmp = torch.empty_like(self.d_x)
         self.d_x_hat = torch.empty_like(self.d_x)
@@ -84,7 +86,8 @@ class Iterative:
                                       device=device)
 
     def load_x0(self):
-        self.d_x.copy_(torch.from_numpy(self.x0).to(self.d_x.device))
+        if self.n:
+            E.ecc_stream_copy(self.d_x, self.d_x0, self.n, current_stream())
 
     def solve(self, T=None, tol=0.0, histories=False):
         """Reset the plan, load x0 and run T iterations through ecc_solve.

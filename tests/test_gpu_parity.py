@@ -344,6 +344,46 @@ def _arrow_problem(n=40000, T=40, P=7, S=2):
                        T, np.zeros(n), b=rng.standard_normal(n), norm=2)
 
 
+def _banded_problem(kind, n, lmin, lmax, P=13, T=40, S=3, seed=5):
+    """Rows of lmin..lmax entries (at most 64: a regular matrix) at random
+    columns within a band of +-1500 around the diagonal, so that rows read
+    neighbouring ranks: the LDS-staged stream layout."""
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(lmin, lmax + 1, n)
+    cols, vals = [], []
+    for i in range(n):
+        lo, hi = max(0, i - 1500), min(n, i + 1501)
+        c = np.sort(rng.choice(np.arange(lo, hi), int(lens[i]), replace=False))
+        if kind == "jacobi" and i not in c:
+            c[rng.integers(0, c.size)] = i
+            c = np.sort(c)
+        v = rng.uniform(0.05, 1.0, c.size) / c.size
+        if kind == "jacobi":
+            v = -v
+            v[c == i] = 2.0 * np.abs(v).sum() + 1.0
+        cols.append(c)
+        vals.append(v)
+    rp = np.zeros(n + 1, dtype=np.int32)
+    rp[1:] = np.cumsum([c.size for c in cols])
+    A = W.CSR(n, n, rp, np.concatenate(cols).astype(np.int32), np.concatenate(vals))
+    counts = W.dirichlet_partition(n, P, seed)
+    mask = (rng.random((T, P)) < 0.7).astype(np.uint8)
+    mask[0] = 1
+    if kind == "jacobi":
+        return W.Iterative("banded-jacobi", "jacobi", A, counts, W.exclusive_scan(counts), S,
+                           mask, T, np.zeros(n), b=rng.standard_normal(n), norm=2)
+    return W.Iterative("banded-power", "power", A, counts, W.exclusive_scan(counts), S, mask, T,
+                       np.full(n, 1.0 / n), alpha=0.85, beta=0.15 / n, norm=1)
+
+
+@pytest.mark.parametrize("kind", ["jacobi", "power"])
+@pytest.mark.parametrize("lmin,lmax", [(9, 16), (20, 60)])
+def test_solve_stream_layout(kind, lmin, lmax):
+    """Regular rows longer than eight entries: rows of up to 16 entries are
+    summed by one lane in CSR order (bitwise), longer ones by several lanes."""
+    _solve_and_compare(_banded_problem(kind, 30000, lmin, lmax), bitwise=(lmax <= 16))
+
+
 def test_solve_arrow_split_rows():
     _solve_and_compare(_arrow_problem(), bitwise=False)
 
@@ -408,3 +448,22 @@ def test_matrix_checks():
     assert ei.value.status == E.ECC_ERR_STATE
     plan.close()
     run.close()
+
+
+@pytest.mark.parametrize("n,off", [(0, 0), (1, 0), (3, 0), (1001, 0), (1001, 1), (65536 * 3 + 5, 0),
+                                   (65536 * 3 + 5, 1)])
+def test_stream_copy(n, off):
+    """ecc_stream_copy: exact copy for odd lengths and 8-byte (not 16-byte)
+    aligned buffers; nothing outside [0, n) is written."""
+    E, R = _capi(), _runner()
+    announce("stream copy", n, off)
+    src = torch.randn(n + 4, dtype=torch.float64, device="cuda")
+    dst = torch.full((n + 4,), float("nan"), dtype=torch.float64, device="cuda")
+    E.ecc_stream_copy(dst[off:], src[off:], n, R.current_stream())
+    torch.cuda.synchronize()
+    assert torch.equal(dst[off:off + n], src[off:off + n])
+    assert bool(torch.isnan(dst[:off]).all()) and bool(torch.isnan(dst[off + n:]).all())
+    if n > 1:
+        with pytest.raises(E.EccError) as ei:
+            E.ecc_stream_copy(src[1:], src, n, R.current_stream())
+        assert ei.value.status == E.ECC_ERR_ARG
