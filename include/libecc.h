@@ -43,6 +43,7 @@ extern "C" {
 
 typedef struct ecc_plan_s *ecc_plan_t;
 typedef struct ecc_matrix_s *ecc_matrix_t;
+typedef struct ecc_hypercube_s *ecc_hypercube_t;
 
 typedef enum {
     ECC_OK = 0,
@@ -255,6 +256,66 @@ ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double *d_b, doubl
                        double beta, double *d_x, double *d_x_tmp, double *d_x_hat,
                        const uint8_t *d_mask, int32_t T, double tol, double *d_rho,
                        uint8_t *d_eff_hist, int32_t *d_age_hist, int32_t *h_iters);
+
+/* ---------------------------------------------------------------------------
+ * SSP hypercube allreduce with one view per receiver: Algorithm 1
+ * (allreduce_SSP, Section III-A) for P = 2^d processes emulated on one GPU.
+ *
+ * Every process owns d receive slots, one per hypercube step (the paper's
+ * rcv_data_vec): m doubles plus the clock of the message that last landed
+ * there.  One ecc_allreduce_ssp call is one call of every process, with
+ * clock t = number of earlier calls since create/reset:
+ *   - the partial reduction starts as the process's contribution (clock t);
+ *   - at step k = 0 .. d-1 process r sends its partial reduction and clock to
+ *     process r XOR 2^k, whose slot k it overwrites -- if that message has
+ *     landed before r' reads its slot (d_delivered[r'][k] != 0); otherwise r'
+ *     reuses the slot's last message when its clock >= t - slack, and waits
+ *     for this call's message when it is older (or when the slot was never
+ *     written: a first receipt);
+ *   - partial := partial + received (fp64, in that order); its clock becomes
+ *     the smaller of the two (the minimum-clock rule of Section III-A).
+ * All processes take the steps of one call in lock step: the message of step
+ * k of call t is the sender's partial reduction at step k of call t.
+ * --------------------------------------------------------------------------- */
+
+/* Create the hypercube state for P processes (a power of two, 1..64) with
+ * vectors of m doubles and the given slack (ECC_UNBOUNDED: never wait for a
+ * slot that holds a message).  Allocates P * d * m doubles of receive slots
+ * (d = log2 P) and their clocks on the current device; work is enqueued on
+ * hip_stream.  ECC_ERR_ARG for a bad P, m or slack; ECC_ERR_RANGE when the
+ * slots would exceed 2^40 elements; ECC_ERR_ALLOC when allocation fails. */
+ecc_status_t ecc_hypercube_create(int32_t P, int64_t m, int32_t slack, void *hip_stream,
+                                  ecc_hypercube_t *out);
+ecc_status_t ecc_hypercube_destroy(ecc_hypercube_t h);
+/* Clock back to 0, every slot "never written", wait counters to 0. */
+ecc_status_t ecc_hypercube_reset(ecc_hypercube_t h);
+
+/* One call of every process (enqueued; asynchronous).
+ *   d_contrib     [P][m] doubles, row r = process r's new contribution.
+ *   d_delivered   [P][d] bytes (device): != 0 when the message process
+ *                 r XOR 2^k sends at step k of this call lands in slot k of
+ *                 process r before r reads it.  Ignored when P = 1.
+ *   d_result      [P][m] doubles: row r = process r's reduction result.  May
+ *                 be d_contrib itself (in place); must not overlap it
+ *                 otherwise (ECC_ERR_ARG).
+ *   d_result_clock [P] int32 or NULL: the clock of each result, the oldest
+ *                 clock of the data it contains.
+ *   d_outcome     [P][d] bytes or NULL: 0 the slot's last message was reused,
+ *                 1 this call's message had landed, 2 the slot was older than
+ *                 the slack and the process waited, 3 first receipt (waited
+ *                 for a slot that had never been written).
+ * The results are bitwise reproducible: the same fp64 operations in the
+ * same order as the sequential definition. */
+ecc_status_t ecc_allreduce_ssp(ecc_hypercube_t h, const double *d_contrib,
+                               const uint8_t *d_delivered, double *d_result,
+                               int32_t *d_result_clock, uint8_t *d_outcome);
+
+/* Synchronises the stream.  clock: calls so far; waits_total: waits for a
+ * too-old slot (outcome 2) summed over processes and steps; h_slot_clock
+ * [P][d] (host, or NULL): clock of each slot's last message (INT32_MIN when
+ * never written); h_waits [P][d] (host, or NULL): waits per slot. */
+ecc_status_t ecc_hypercube_stats(ecc_hypercube_t h, int64_t *clock, uint64_t *waits_total,
+                                 int32_t *h_slot_clock, uint64_t *h_waits);
 
 /* ---------------------------------------------------------------------------
  * Plain streaming copy d_dst[i] = d_src[i], 0 <= i < n, enqueued on

@@ -64,6 +64,11 @@ _SIGS = [
     ("ecc_iterate_spmv", ctypes.c_int, [_VP, _VP, _D, _D, _VP, _VP, _VP, _VP]),
     ("ecc_residual", ctypes.c_int, [_VP, _VP, _I64, _I32, _VP, _VP]),
     ("ecc_stream_copy", ctypes.c_int, [_VP, _VP, _I64, _VP]),
+    ("ecc_hypercube_create", ctypes.c_int, [_I32, _I64, _I32, _VP, ctypes.POINTER(_VP)]),
+    ("ecc_hypercube_destroy", ctypes.c_int, [_VP]),
+    ("ecc_hypercube_reset", ctypes.c_int, [_VP]),
+    ("ecc_allreduce_ssp", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP]),
+    ("ecc_hypercube_stats", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP]),
     ("ecc_solve", ctypes.c_int, [_VP, _VP, _VP, _D, _D, _VP, _VP, _VP, _VP, _I32, _D, _VP, _VP,
                                  _VP, _VP]),
 ]
@@ -235,3 +240,34 @@ def ecc_solve(plan, mat, d_b, alpha, beta, d_x, d_x_tmp, d_x_hat, d_mask, T, tol
 
 def ecc_stream_copy(d_dst, d_src, n, stream=None):
     _check(lib().ecc_stream_copy(_ptr(d_dst), _ptr(d_src), n, stream))
+
+
+def ecc_hypercube_create(P, m, slack, stream=None) -> int:
+    out = _VP()
+    _check(lib().ecc_hypercube_create(P, m, slack, stream, ctypes.byref(out)))
+    return out.value
+
+
+def ecc_hypercube_destroy(h):
+    _check(lib().ecc_hypercube_destroy(h))
+
+
+def ecc_hypercube_reset(h):
+    _check(lib().ecc_hypercube_reset(h))
+
+
+def ecc_allreduce_ssp(h, d_contrib, d_delivered, d_result, d_result_clock=None, d_outcome=None):
+    _check(lib().ecc_allreduce_ssp(h, _ptr(d_contrib), _ptr(d_delivered), _ptr(d_result),
+                                   _ptr(d_result_clock), _ptr(d_outcome)))
+
+
+def ecc_hypercube_stats(h, P: int):
+    """Returns (clock, waits_total, slot_clock[P][d], waits[P][d])."""
+    d = P.bit_length() - 1
+    clock = ctypes.c_int64()
+    waits = ctypes.c_uint64()
+    clk = np.empty((P, d), dtype=np.int32)
+    w = np.empty((P, d), dtype=np.uint64)
+    _check(lib().ecc_hypercube_stats(h, ctypes.addressof(clock), ctypes.addressof(waits),
+                                     _ptr(clk), _ptr(w)))
+    return clock.value, waits.value, clk, w

@@ -1,0 +1,356 @@
+// SSP hypercube allreduce with one view per receiver (Section III-A,
+// Algorithm 1): P = 2^d virtual processes on one GPU, each with d dedicated
+// receive slots (data and clock of the last message that landed there).
+//
+// One call is one iteration of every process, as one kernel launch:
+//  (1) every workgroup replays the scalar part of the call in LDS -- which
+//      slot of which process takes this call's message from its partner
+//      (process XOR 2^k) and which reuses its last message -- from the slot
+//      clocks of the previous call (read-only in this launch; workgroup 0
+//      writes the new ones into the other half of a double buffer);
+//  (2) the data part is elementwise: element j of every result depends only
+//      on element j of the contributions and slots, so a wave carries a
+//      chunk of elements of all P partial reductions through the d steps
+//      (partners exchange partials by wave shuffles), storing each arriving
+//      message into its slot and reading each reused slot, and no workgroup
+//      waits for another.
+// A partial reduction is updated as partial + received, in that order, in
+// fp64 without contraction: the same operations as the sequential
+// definition, so results are bitwise reproducible.
+#include <algorithm>
+
+#include "ecc_common.h"
+
+namespace ecc {
+
+constexpr int kHcThreads = 256;
+constexpr int kHcMaxDims = 6;  // P <= 64: one lane per process in the scalar phase
+constexpr int32_t kHcNever = INT32_MIN;  // clock of a slot that was never written
+
+struct HcArgs {
+    int32_t P, D, slack;
+    int32_t t;
+    int64_t m;
+    const double *contrib;      // [P][m]
+    const uint8_t *delivered;   // [P][D]: the partner's message of this call has landed
+    double *slots;              // [P][D][m]
+    const int32_t *clk_in;      // [P][D] slot clocks before the call
+    int32_t *clk_out;           // [P][D] after the call (workgroup 0)
+    unsigned long long *waits;  // [P][D] cumulative waits (workgroup 0)
+    double *result;             // [P][m] (may alias contrib)
+    int32_t *result_clock;      // [P] or null (workgroup 0)
+    uint8_t *outcome;           // [P][D] or null (workgroup 0)
+};
+
+// Scalar phase on wave 0, lane r = process r.  Returns nothing; leaves in
+// s_fresh[k] the set of processes whose slot k takes this call's message.
+__device__ __forceinline__ void hc_decide(const HcArgs &a, unsigned long long *s_fresh) {
+    const int lane = threadIdx.x;
+    if (lane >= 64) return;
+    const bool live = lane < a.P;
+    // slack is at most INT32_MAX; ECC_UNBOUNDED accepts every received message
+    const int64_t min_accepted =
+        a.slack == ECC_UNBOUNDED ? INT64_MIN : (int64_t)a.t - (int64_t)a.slack;
+    int32_t pc = a.t;  // clock of this process's partial reduction
+    for (int k = 0; k < a.D; ++k) {
+        const int partner = lane ^ (1 << k);
+        const int32_t sent_clock = __shfl(pc, partner, 64);
+        int32_t sc = live ? a.clk_in[lane * a.D + k] : 0;
+        const bool arrived = live && a.delivered[lane * a.D + k] != 0;
+        uint8_t how;
+        if (arrived) how = 1;                                   // delivered
+        else if (sc == kHcNever) how = 3;                       // first receipt: wait
+        else if ((int64_t)sc < min_accepted) how = 2;           // too old: wait
+        else how = 0;                                           // reuse the slot
+        const bool fresh = live && how != 0;
+        if (fresh) sc = sent_clock;
+        const unsigned long long mask = __ballot(fresh);
+        if (lane == 0) s_fresh[k] = mask;
+        if (live) pc = min(pc, sc);
+        if (blockIdx.x == 0 && live) {
+            a.clk_out[lane * a.D + k] = sc;
+            if (how == 2) a.waits[lane * a.D + k] += 1;
+            if (a.outcome) a.outcome[lane * a.D + k] = how;
+        }
+    }
+    if (blockIdx.x == 0 && live && a.result_clock) a.result_clock[lane] = pc;
+}
+
+__device__ __forceinline__ unsigned long long uniform64(unsigned long long v) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+// Data phase.  A wave holds element chunks of all P processes: lane
+// = r * L + e with L = 64 / P lanes per process, and lane e of process r
+// carries elements j0 + u * L + e (u < kHcV) of r's partial reduction, so
+// the L lanes of one process read consecutive elements.  Process r's
+// partner r XOR 2^k sits L * 2^k lanes away: its partial reduction arrives
+// through one wave shuffle.  At step k a process whose slot takes the
+// message stores the partner's partial into the slot; one that reuses its
+// slot loads it; both add what they received to their own partial.
+constexpr int kHcV = 8;  // elements per lane and chunk
+
+template <int D>
+__global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp(HcArgs a) {
+    constexpr int LOGL = 6 - D;
+    constexpr int L = 1 << LOGL;
+    __shared__ unsigned long long s_fresh[kHcMaxDims];
+    hc_decide(a, s_fresh);
+    __syncthreads();
+    const int lane = threadIdx.x & 63;
+    const int r = lane >> LOGL, e = lane & (L - 1);
+    bool fresh[D > 0 ? D : 1];
+#pragma unroll
+    for (int k = 0; k < D; ++k) fresh[k] = (s_fresh[k] >> r) & 1ull;
+
+    const int64_t m = a.m;
+    const int64_t chunk = (int64_t)L * kHcV;
+    const int64_t n_chunks = (m + chunk - 1) / chunk;
+    const int64_t n_waves = (int64_t)gridDim.x * (kHcThreads / 64);
+    const double *crow = a.contrib + (int64_t)r * m;
+    double *rrow = a.result + (int64_t)r * m;
+    for (int64_t c = (int64_t)blockIdx.x * (kHcThreads / 64) + (threadIdx.x >> 6); c < n_chunks;
+         c += n_waves) {
+        const int64_t j0 = c * chunk + e;
+        double part[kHcV];
+#pragma unroll
+        for (int u = 0; u < kHcV; ++u) {
+            const int64_t j = j0 + (int64_t)u * L;
+            part[u] = j < m ? crow[j] : 0.0;
+        }
+#pragma unroll
+        for (int k = 0; k < D; ++k) {
+            double *srow = a.slots + ((int64_t)r * D + k) * m;
+            double got[kHcV];
+            if (!fresh[k]) {
+#pragma unroll
+                for (int u = 0; u < kHcV; ++u) {
+                    const int64_t j = j0 + (int64_t)u * L;
+                    got[u] = j < m ? srow[j] : 0.0;
+                }
+            }
+            double sent[kHcV];
+#pragma unroll
+            for (int u = 0; u < kHcV; ++u) sent[u] = __shfl_xor(part[u], L << k, 64);
+            if (fresh[k]) {
+#pragma unroll
+                for (int u = 0; u < kHcV; ++u) {
+                    const int64_t j = j0 + (int64_t)u * L;
+                    got[u] = sent[u];
+                    if (j < m) srow[j] = sent[u];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kHcV; ++u) part[u] = part[u] + got[u];
+        }
+#pragma unroll
+        for (int u = 0; u < kHcV; ++u) {
+            const int64_t j = j0 + (int64_t)u * L;
+            if (j < m) rrow[j] = part[u];
+        }
+    }
+}
+
+}  // namespace ecc
+
+using namespace ecc;
+
+struct ecc_hypercube_s {
+    int32_t P = 0, D = 0, slack = 0;
+    int64_t m = 0;
+    int64_t clock = 0;
+    hipStream_t stream = nullptr;
+    int32_t grid = 1;
+    double *d_slots = nullptr;               // [P][D][m]
+    int32_t *d_clk = nullptr;                // [2][P][D]
+    unsigned long long *d_waits = nullptr;   // [P][D]
+};
+
+namespace {
+
+__global__ void k_hc_reset(int32_t n, int32_t *clk, unsigned long long *waits) {
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+        clk[i] = kHcNever;
+        clk[n + i] = kHcNever;
+        waits[i] = 0;
+    }
+}
+
+ecc_status_t hc_reset(ecc_hypercube_t h) {
+    const int32_t n = h->P * h->D;
+    if (n > 0) {
+        hipLaunchKernelGGL(k_hc_reset, dim3(1), dim3(256), 0, h->stream, n, h->d_clk, h->d_waits);
+        ECC_LAUNCH_CHECK();
+    }
+    h->clock = 0;
+    return ECC_OK;
+}
+
+template <int D>
+hipError_t hc_occupancy(int *per_cu) {
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(per_cu, k_allreduce_ssp<D>, kHcThreads, 0);
+}
+
+}  // namespace
+
+extern "C" {
+
+ecc_status_t ecc_hypercube_create(int32_t P, int64_t m, int32_t slack, void *hip_stream,
+                                  ecc_hypercube_t *out) {
+    clear_error();
+    ECC_ARG(out != nullptr, "out is NULL");
+    *out = nullptr;
+    ECC_ARG(P >= 1 && P <= (1 << kHcMaxDims) && (P & (P - 1)) == 0,
+            "P = %d must be a power of two in [1, 64]", P);
+    ECC_ARG(m >= 0, "m must be >= 0");
+    ECC_ARG(slack >= 0, "slack must be >= 0 (ECC_UNBOUNDED for no limit)");
+    int D = 0;
+    while ((1 << D) < P) ++D;
+    const int64_t slot_elems = (int64_t)P * D * m;
+    if (m > (int64_t(1) << 40) / std::max(1, P * std::max(D, 1))) {
+        set_error("P * d * m too large");
+        return ECC_ERR_RANGE;
+    }
+    ecc_hypercube_s *h = new (std::nothrow) ecc_hypercube_s();
+    if (!h) {
+        set_error("host allocation failed");
+        return ECC_ERR_ALLOC;
+    }
+    h->P = P;
+    h->D = D;
+    h->m = m;
+    h->slack = slack;
+    h->stream = (hipStream_t)hip_stream;
+    auto fail = [&](const char *what) {
+        set_error("%s", what);
+        ecc_hypercube_destroy(h);
+        return ECC_ERR_ALLOC;
+    };
+    if (slot_elems > 0 && hipMalloc((void **)&h->d_slots, sizeof(double) * slot_elems) != hipSuccess)
+        return fail("hipMalloc of the receive slots failed");
+    const int32_t n = P * D;
+    if (n > 0) {
+        if (hipMalloc((void **)&h->d_clk, sizeof(int32_t) * 2 * n) != hipSuccess)
+            return fail("hipMalloc of the slot clocks failed");
+        if (hipMalloc((void **)&h->d_waits, sizeof(unsigned long long) * n) != hipSuccess)
+            return fail("hipMalloc of the wait counters failed");
+    }
+    // grid: as many workgroups as fit at once, at most one per four chunks
+    int dev = 0, cus = 256, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        cus = 256;
+    hipError_t e;
+    switch (D) {
+        case 0: e = hc_occupancy<0>(&per_cu); break;
+        case 1: e = hc_occupancy<1>(&per_cu); break;
+        case 2: e = hc_occupancy<2>(&per_cu); break;
+        case 3: e = hc_occupancy<3>(&per_cu); break;
+        case 4: e = hc_occupancy<4>(&per_cu); break;
+        case 5: e = hc_occupancy<5>(&per_cu); break;
+        default: e = hc_occupancy<6>(&per_cu); break;
+    }
+    if (e != hipSuccess || per_cu < 1) per_cu = 2;
+    const int64_t chunk = (int64_t)(64 / P) * kHcV;  // elements of one process per wave
+    const int64_t need = std::max<int64_t>(1, (m + 4 * chunk - 1) / (4 * chunk));
+    h->grid = (int32_t)std::min<int64_t>(need, (int64_t)cus * per_cu);
+    ecc_status_t st = hc_reset(h);
+    if (st != ECC_OK) {
+        ecc_hypercube_destroy(h);
+        return st;
+    }
+    *out = h;
+    return ECC_OK;
+}
+
+ecc_status_t ecc_hypercube_destroy(ecc_hypercube_t h) {
+    if (!h) return ECC_OK;
+    (void)hipStreamSynchronize(h->stream);
+    (void)hipFree(h->d_slots);
+    (void)hipFree(h->d_clk);
+    (void)hipFree(h->d_waits);
+    delete h;
+    return ECC_OK;
+}
+
+ecc_status_t ecc_hypercube_reset(ecc_hypercube_t h) {
+    clear_error();
+    ECC_ARG(h != nullptr, "hypercube is NULL");
+    return hc_reset(h);
+}
+
+ecc_status_t ecc_allreduce_ssp(ecc_hypercube_t h, const double *d_contrib,
+                               const uint8_t *d_delivered, double *d_result,
+                               int32_t *d_result_clock, uint8_t *d_outcome) {
+    clear_error();
+    ECC_ARG(h != nullptr, "hypercube is NULL");
+    ECC_ARG(h->m == 0 || (d_contrib && d_result), "NULL contribution or result");
+    ECC_ARG(h->D == 0 || d_delivered, "d_delivered is NULL");
+    if (h->clock >= INT32_MAX - 1) {
+        set_error("clock overflow");
+        return ECC_ERR_RANGE;
+    }
+    if (h->m > 0 && d_result != d_contrib) {
+        const uintptr_t a0 = (uintptr_t)d_contrib, a1 = a0 + 8 * (uintptr_t)h->P * h->m;
+        const uintptr_t b0 = (uintptr_t)d_result, b1 = b0 + 8 * (uintptr_t)h->P * h->m;
+        ECC_ARG(a1 <= b0 || b1 <= a0, "result overlaps the contributions without being them");
+    }
+    HcArgs a{};
+    a.P = h->P;
+    a.D = h->D;
+    a.slack = h->slack;
+    a.t = (int32_t)h->clock;
+    a.m = h->m;
+    a.contrib = d_contrib;
+    a.delivered = d_delivered;
+    a.slots = h->d_slots;
+    const int32_t n = h->P * h->D;
+    a.clk_in = h->d_clk ? h->d_clk + (h->clock & 1) * n : nullptr;
+    a.clk_out = h->d_clk ? h->d_clk + ((h->clock + 1) & 1) * n : nullptr;
+    a.waits = h->d_waits;
+    a.result = d_result;
+    a.result_clock = d_result_clock;
+    a.outcome = d_outcome;
+    const dim3 grid(h->grid), block(kHcThreads);
+    switch (h->D) {
+        case 0: hipLaunchKernelGGL(k_allreduce_ssp<0>, grid, block, 0, h->stream, a); break;
+        case 1: hipLaunchKernelGGL(k_allreduce_ssp<1>, grid, block, 0, h->stream, a); break;
+        case 2: hipLaunchKernelGGL(k_allreduce_ssp<2>, grid, block, 0, h->stream, a); break;
+        case 3: hipLaunchKernelGGL(k_allreduce_ssp<3>, grid, block, 0, h->stream, a); break;
+        case 4: hipLaunchKernelGGL(k_allreduce_ssp<4>, grid, block, 0, h->stream, a); break;
+        case 5: hipLaunchKernelGGL(k_allreduce_ssp<5>, grid, block, 0, h->stream, a); break;
+        default: hipLaunchKernelGGL(k_allreduce_ssp<6>, grid, block, 0, h->stream, a); break;
+    }
+    ECC_LAUNCH_CHECK();
+    h->clock += 1;
+    return ECC_OK;
+}
+
+ecc_status_t ecc_hypercube_stats(ecc_hypercube_t h, int64_t *clock, uint64_t *waits_total,
+                                 int32_t *h_slot_clock, uint64_t *h_waits) {
+    clear_error();
+    ECC_ARG(h != nullptr, "hypercube is NULL");
+    const int32_t n = h->P * h->D;
+    std::vector<int32_t> clk(n);
+    std::vector<unsigned long long> w(n);
+    if (n > 0) {
+        ECC_HIP(hipStreamSynchronize(h->stream));
+        ECC_HIP(hipMemcpy(clk.data(), h->d_clk + (h->clock & 1) * n, sizeof(int32_t) * n,
+                          hipMemcpyDeviceToHost));
+        ECC_HIP(hipMemcpy(w.data(), h->d_waits, sizeof(unsigned long long) * n,
+                          hipMemcpyDeviceToHost));
+    }
+    if (clock) *clock = h->clock;
+    uint64_t tot = 0;
+    for (int32_t i = 0; i < n; ++i) tot += w[i];
+    if (waits_total) *waits_total = tot;
+    if (h_slot_clock)
+        for (int32_t i = 0; i < n; ++i) h_slot_clock[i] = clk[i];
+    if (h_waits)
+        for (int32_t i = 0; i < n; ++i) h_waits[i] = w[i];
+    return ECC_OK;
+}
+
+}  // extern "C"

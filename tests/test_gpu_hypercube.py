@@ -1,0 +1,111 @@
+"""GPU parity of the SSP hypercube allreduce (Algorithm 1, per-receiver
+views) through the C ABI against the oracle: results, result clocks,
+per-slot outcomes, slot clocks and wait counts, bit for bit."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import hypercube as H                         # noqa: E402
+from gpu_common import announce                           # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def _E():
+    from paper_2203_17063_amd import capi
+    return capi
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _run_and_compare(P, m, slack, q, T, seed, in_place=False):
+    E = _E()
+    d = H.dims(P)
+    announce("hypercube", P, m, slack, q, T, in_place)
+    rng = np.random.default_rng(seed)
+    contribs = rng.standard_normal((T, P, m))
+    delivered = rng.random((T, P, d)) < q
+    ref_res, ref_clk, ref_out, ref_state = H.run(P, slack, contribs, delivered)
+    h = E.ecc_hypercube_create(P, m, slack if slack != H.UNBOUNDED else E.ECC_UNBOUNDED,
+                               _stream())
+    try:
+        d_res = torch.empty((P, m), dtype=torch.float64, device="cuda")
+        d_clk = torch.empty(P, dtype=torch.int32, device="cuda")
+        d_out = torch.empty((P, max(d, 1)), dtype=torch.uint8, device="cuda")
+        d_del = torch.from_numpy(delivered.astype(np.uint8)).cuda()
+        for t in range(T):
+            d_c = torch.from_numpy(contribs[t]).cuda()
+            target = d_c if in_place else d_res
+            E.ecc_allreduce_ssp(h, d_c, d_del[t] if d else None, target, d_clk,
+                                d_out if d else None)
+            torch.cuda.synchronize()
+            got = target.cpu().numpy()
+            assert np.array_equal(got, ref_res[t]), (t, np.abs(got - ref_res[t]).max())
+            assert np.array_equal(d_clk.cpu().numpy(), ref_clk[t]), t
+            if d:
+                assert np.array_equal(d_out.cpu().numpy()[:, :d], ref_out[t]), t
+        clock, waits, slot_clk, w = E.ecc_hypercube_stats(h, P)
+        assert clock == T
+        assert waits == int(ref_state.waits.sum())
+        if d:
+            assert np.array_equal(w.astype(np.int64), ref_state.waits)
+            never = ref_state.slot_clock == H.NEVER
+            assert np.array_equal(slot_clk[never], np.full(never.sum(), np.iinfo(np.int32).min))
+            assert np.array_equal(slot_clk[~never].astype(np.int64), ref_state.slot_clock[~never])
+    finally:
+        E.ecc_hypercube_destroy(h)
+
+
+@pytest.mark.parametrize("P", [1, 2, 4, 8, 16, 32, 64])
+@pytest.mark.parametrize("slack,q", [(0, 0.5), (2, 0.7), (H.UNBOUNDED, 0.3)])
+def test_parity_processes(P, slack, q):
+    _run_and_compare(P, 1000 + P, slack, q, T=10, seed=P * 7 + slack % 13)
+
+
+@pytest.mark.parametrize("m", [0, 1, 7, 65, 4097])
+def test_parity_ragged_lengths(m):
+    _run_and_compare(32, m, 1, 0.6, T=8, seed=m)
+
+
+def test_parity_larger_vector_in_place():
+    _run_and_compare(16, 200003, 3, 0.8, T=6, seed=3, in_place=True)
+
+
+def test_reset_and_errors():
+    E = _E()
+    announce("hypercube errors")
+    for bad in (0, 3, 12, 128):
+        with pytest.raises(E.EccError) as ei:
+            E.ecc_hypercube_create(bad, 10, 1, _stream())
+        assert ei.value.status == E.ECC_ERR_ARG
+    with pytest.raises(E.EccError):
+        E.ecc_hypercube_create(8, -1, 1, _stream())
+    with pytest.raises(E.EccError):
+        E.ecc_hypercube_create(8, 10, -2, _stream())
+    h = E.ecc_hypercube_create(4, 10, 1, _stream())
+    try:
+        c = torch.zeros((4, 10), dtype=torch.float64, device="cuda")
+        big = torch.zeros(4 * 10 + 5, dtype=torch.float64, device="cuda")
+        dl = torch.ones((4, 2), dtype=torch.uint8, device="cuda")
+        with pytest.raises(E.EccError) as ei:      # result overlaps, not in place
+            E.ecc_allreduce_ssp(h, big, dl, big[3:])
+        assert ei.value.status == E.ECC_ERR_ARG
+        E.ecc_allreduce_ssp(h, c, dl, c)
+        E.ecc_hypercube_reset(h)
+        clock, waits, slot_clk, _ = E.ecc_hypercube_stats(h, 4)
+        assert clock == 0 and waits == 0
+        assert (slot_clk == np.iinfo(np.int32).min).all()
+    finally:
+        E.ecc_hypercube_destroy(h)
