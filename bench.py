@@ -11,7 +11,7 @@ Metric: assembled+iterated GB/s (algorithmic bytes of assembly + sweep + norm,
 each distinct element counted once) and iterations/s, with the dominant
 kernel's achieved bandwidth against the HBM roofline.  Prints one JSON line.
 
-    python bench.py [--steps K] [--warmup W] [--config 1|2|3|4a|4b|5]
+    python bench.py [--steps K] [--warmup W] [--config 1|2|3|4a|4b|5|ssp]
 """
 from __future__ import annotations
 
@@ -83,6 +83,8 @@ def build_workload(cfg):
         return W.config4a()
     if cfg == "4b":
         return W.config4b()
+    if cfg == "ssp":
+        return W.hypercube_ssp()
     raise ValueError(cfg)
 
 
@@ -105,6 +107,12 @@ def describe(cfg, prob):
         return {"workload": "allgatherv assembly, P=%d lognormal counts, %d elements, %d reps"
                             % (prob.P, int(prob.counts.sum()), prob.reps),
                 "P": prob.P, "elements": int(prob.counts.sum()), "reps": prob.reps,
+                "config_id": cfg}
+    if cfg == "ssp":
+        return {"workload": "hypercube allreduce_SSP with per-receiver views, P=%d processes x "
+                            "%d elements, slack %d, Bernoulli(%.1f) message delivery, %d calls"
+                            % (prob.P, prob.m, prob.slack, prob.q, prob.calls),
+                "P": prob.P, "m": prob.m, "slack": prob.slack, "calls": prob.calls,
                 "config_id": cfg}
     return {"workload": "partial allreduce-sum, P=%d x %d elements, Bernoulli(%.1f), stale "
                         "substitution, %d reps" % (prob.P, prob.m, prob.q, prob.reps),
@@ -273,6 +281,60 @@ def run_allreduce_gpu(prob, steps, warmup):
             "unit_per_step": prob.reps}
 
 
+def run_hypercube_gpu(prob, steps, warmup):
+    """One step = a reset and prob.calls calls of every process.  Two
+    contribution sets alternate between calls (the bytes moved do not depend
+    on the values)."""
+    import torch
+    from paper_2203_17063_amd import capi as E
+
+    mem0 = torch.cuda.mem_get_info()[0]
+    P, m, d = prob.P, prob.m, prob.d
+    contrib = [torch.from_numpy(prob.contrib(t)).cuda() for t in range(2)]
+    result = torch.empty((P, m), dtype=torch.float64, device="cuda")
+    d_del = torch.from_numpy(prob.delivered.astype(np.uint8)).cuda()
+    stream = torch.cuda.current_stream().cuda_stream
+    h = E.ecc_hypercube_create(P, m, prob.slack, stream)
+    torch.cuda.synchronize()
+    footprint = mem0 - torch.cuda.mem_get_info()[0]
+
+    def step(events=None):
+        E.ecc_hypercube_reset(h)
+        for t in range(prob.calls):
+            if events is not None:
+                events[t][0].record()
+            E.ecc_allreduce_ssp(h, contrib[t & 1], d_del[t], result)
+            if events is not None:
+                events[t][1].record()
+
+    for _ in range(max(warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    # the same steps with events around every call (one kernel launch each)
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(prob.calls)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for s_ in range(steps):
+        step(ev[s_])
+    torch.cuda.synchronize()
+    wall_events = time.perf_counter() - t1
+    ms = sum(a.elapsed_time(b) for row in ev for a, b in row)
+    _, waits, _, _ = E.ecc_hypercube_stats(h, P)
+    E.ecc_hypercube_destroy(h)
+    per_call = 8.0 * m * P * (d + 2) + 2.0 * P * d
+    return {"iters": prob.calls, "wall": wall, "wall_events": wall_events,
+            "times": {"ALLREDUCE_SSP": (ms, steps * prob.calls)},
+            "bytes_per_step": per_call * prob.calls, "dominant": "allreduce_ssp",
+            "dominant_bytes": per_call, "footprint": footprint, "unit_per_step": prob.calls,
+            "waits_per_step": waits}
+
+
 # ----------------------------------------------------------------------------
 # CPU baseline: the oracle as it stands, on a bounded sample
 # ----------------------------------------------------------------------------
@@ -314,6 +376,22 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
         return {"value": round(per_rep * reps / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
                 "kind": "oracle", "sample": "%d of %d repetitions, 1 thread, %.1f s"
                                             % (reps, prob.reps, dt)}
+    if cfg == "ssp":
+        # whole calls of the oracle over the full vectors, from a reset
+        from oracle import hypercube as HC
+        P, m, d = prob.P, prob.m, prob.d
+        contrib = [prob.contrib(t) for t in range(2)]
+        st = HC.HypercubeSSP(P, m, prob.slack)
+        t0 = time.perf_counter()
+        calls = 0
+        while time.perf_counter() - t0 < budget_s and calls < prob.calls:
+            st.call(contrib[calls & 1], prob.delivered[calls])
+            calls += 1
+        dt = time.perf_counter() - t0
+        per_call = res["bytes_per_step"] / res["iters"]
+        return {"value": round(per_call * calls / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
+                "kind": "oracle", "sample": "the first %d of %d calls, 1 thread, %.1f s"
+                                            % (calls, prob.calls, dt)}
     # 4b: a few repetitions over stored vectors
     P, m = prob.P, prob.m
     fresh = [prob.fresh(p, 0) for p in range(P)]
@@ -371,7 +449,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="2", choices=["1", "2", "3", "4a", "4b", "5"])
+    ap.add_argument("--config", default="2", choices=["1", "2", "3", "4a", "4b", "5", "ssp"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only measure a plain 4 GiB device copy (copy ceiling)")
@@ -407,6 +485,11 @@ def main():
         digest = kernel_source_digest(["collectives.hip", "ecc_common.h"])
         tag = "assemble_cfg4a"
         dom_ms, dom_n = res["times"]["ASSEMBLE"]
+    elif cfg == "ssp":
+        res = run_hypercube_gpu(prob, args.steps, args.warmup)
+        digest = kernel_source_digest(["hypercube.hip", "ecc_common.h"])
+        tag = "allreduce_ssp_p32"
+        dom_ms, dom_n = res["times"]["ALLREDUCE_SSP"]
     else:
         res = run_allreduce_gpu(prob, args.steps, args.warmup)
         digest = kernel_source_digest(["collectives.hip", "ecc_common.h"])

@@ -9,11 +9,10 @@
 //      clocks of the previous call (read-only in this launch; workgroup 0
 //      writes the new ones into the other half of a double buffer);
 //  (2) the data part is elementwise: element j of every result depends only
-//      on element j of the contributions and slots, so a wave carries a
-//      chunk of elements of all P partial reductions through the d steps
-//      (partners exchange partials by wave shuffles), storing each arriving
-//      message into its slot and reading each reused slot, and no workgroup
-//      waits for another.
+//      on element j of the contributions and slots, so one thread (or a few
+//      lanes) carries element j of all P partial reductions through the d
+//      steps, storing each arriving message into its slot and reading each
+//      reused slot, and no workgroup waits for another.
 // A partial reduction is updated as partial + received, in that order, in
 // fp64 without contraction: the same operations as the sequential
 // definition, so results are bitwise reproducible.
@@ -82,74 +81,71 @@ __device__ __forceinline__ unsigned long long uniform64(unsigned long long v) {
     return ((unsigned long long)hi << 32) | lo;
 }
 
-// Data phase.  A wave holds element chunks of all P processes: lane
-// = r * L + e with L = 64 / P lanes per process, and lane e of process r
-// carries elements j0 + u * L + e (u < kHcV) of r's partial reduction, so
-// the L lanes of one process read consecutive elements.  Process r's
-// partner r XOR 2^k sits L * 2^k lanes away: its partial reduction arrives
-// through one wave shuffle.  At step k a process whose slot takes the
-// message stores the partner's partial into the slot; one that reuses its
-// slot loads it; both add what they received to their own partial.
-constexpr int kHcV = 8;  // elements per lane and chunk
-
-template <int D>
-__global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp(HcArgs a) {
-    constexpr int LOGL = 6 - D;
-    constexpr int L = 1 << LOGL;
+// Column layout: 2^S lanes share element j; lane h (= lane mod 2^S) carries
+// element j of the partial reductions of processes h * Pt .. h * Pt + Pt - 1
+// (Pt = P / 2^S, at most 32) in registers.  Every load and store of a wave
+// covers contiguous bytes of at most 2^S rows.  At steps k < log2(Pt) the
+// two processes of a pair (r, r XOR 2^k) sit in one thread and are updated
+// together from their old partials; at the higher steps the partner's
+// partial comes from lane h XOR 2^(k - log2 Pt) through a wave shuffle.  A
+// scheduling barrier between steps keeps the loads of a step from being
+// hoisted above the stores of the previous one (register pressure).
+template <int D, int S>
+__global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp_col(HcArgs a) {
+    constexpr int LT = D - S;  // dimensions inside a thread
+    constexpr int Pt = 1 << LT;
+    constexpr int H = 1 << S;
     __shared__ unsigned long long s_fresh[kHcMaxDims];
     hc_decide(a, s_fresh);
     __syncthreads();
-    const int lane = threadIdx.x & 63;
-    const int r = lane >> LOGL, e = lane & (L - 1);
-    bool fresh[D > 0 ? D : 1];
+    unsigned long long fresh[D > 0 ? D : 1];
 #pragma unroll
-    for (int k = 0; k < D; ++k) fresh[k] = (s_fresh[k] >> r) & 1ull;
-
+    for (int k = 0; k < D; ++k) fresh[k] = uniform64(s_fresh[k]);
+    const int h = threadIdx.x & (H - 1);
+    const int r0 = h * Pt;
     const int64_t m = a.m;
-    const int64_t chunk = (int64_t)L * kHcV;
-    const int64_t n_chunks = (m + chunk - 1) / chunk;
-    const int64_t n_waves = (int64_t)gridDim.x * (kHcThreads / 64);
-    const double *crow = a.contrib + (int64_t)r * m;
-    double *rrow = a.result + (int64_t)r * m;
-    for (int64_t c = (int64_t)blockIdx.x * (kHcThreads / 64) + (threadIdx.x >> 6); c < n_chunks;
-         c += n_waves) {
-        const int64_t j0 = c * chunk + e;
-        double part[kHcV];
+    const int64_t stride = (int64_t)gridDim.x * (kHcThreads / H);
+    // the 2^S lanes that exchange partials share one element, so they enter
+    // and leave the loop together
+    for (int64_t j = ((int64_t)blockIdx.x * kHcThreads + threadIdx.x) / H; j < m; j += stride) {
+        double part[Pt];
 #pragma unroll
-        for (int u = 0; u < kHcV; ++u) {
-            const int64_t j = j0 + (int64_t)u * L;
-            part[u] = j < m ? crow[j] : 0.0;
-        }
+        for (int i = 0; i < Pt; ++i) part[i] = a.contrib[(r0 + i) * m + j];
 #pragma unroll
         for (int k = 0; k < D; ++k) {
-            double *srow = a.slots + ((int64_t)r * D + k) * m;
-            double got[kHcV];
-            if (!fresh[k]) {
+            double *srow = a.slots + (int64_t)k * m + j;  // + r * D * m
+            if (k < LT) {
+                const int bit = 1 << k;
 #pragma unroll
-                for (int u = 0; u < kHcV; ++u) {
-                    const int64_t j = j0 + (int64_t)u * L;
-                    got[u] = j < m ? srow[j] : 0.0;
+                for (int i = 0; i < Pt; ++i) {
+                    if (i & bit) continue;
+                    const int r = r0 + i, q = r0 + (i | bit);
+                    const bool fr = (fresh[k] >> r) & 1ull, fq = (fresh[k] >> q) & 1ull;
+                    double *sr = srow + (int64_t)r * D * m, *sq = srow + (int64_t)q * D * m;
+                    const double gr = fr ? part[i | bit] : *sr;
+                    const double gq = fq ? part[i] : *sq;
+                    if (fr) *sr = gr;
+                    if (fq) *sq = gq;
+                    part[i] = part[i] + gr;
+                    part[i | bit] = part[i | bit] + gq;
+                }
+            } else {
+                const int lanebit = 1 << (k - LT);
+#pragma unroll
+                for (int i = 0; i < Pt; ++i) {
+                    const int r = r0 + i;
+                    const bool fr = (fresh[k] >> r) & 1ull;
+                    double *sr = srow + (int64_t)r * D * m;
+                    const double other = __shfl_xor(part[i], lanebit, 64);
+                    const double g = fr ? other : *sr;
+                    if (fr) *sr = g;
+                    part[i] = part[i] + g;
                 }
             }
-            double sent[kHcV];
-#pragma unroll
-            for (int u = 0; u < kHcV; ++u) sent[u] = __shfl_xor(part[u], L << k, 64);
-            if (fresh[k]) {
-#pragma unroll
-                for (int u = 0; u < kHcV; ++u) {
-                    const int64_t j = j0 + (int64_t)u * L;
-                    got[u] = sent[u];
-                    if (j < m) srow[j] = sent[u];
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < kHcV; ++u) part[u] = part[u] + got[u];
+            __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
-        for (int u = 0; u < kHcV; ++u) {
-            const int64_t j = j0 + (int64_t)u * L;
-            if (j < m) rrow[j] = part[u];
-        }
+        for (int i = 0; i < Pt; ++i) a.result[(r0 + i) * m + j] = part[i];
     }
 }
 
@@ -188,9 +184,35 @@ ecc_status_t hc_reset(ecc_hypercube_t h) {
     return ECC_OK;
 }
 
+// Lanes per element: 2^split, so that a thread holds at most
+// 2^ECC_HC_THREAD_DIMS partial reductions.  Measured on MI355X (16 MB per
+// process, slack 2, 80% delivery): P = 32 in one thread, 168 VGPRs, 3.68
+// TB/s; P = 64 over two lanes, 2.08 TB/s (over four lanes, or with P = 32
+// over two, the per-lane delivery bits make every slot access divergent
+// and the registers run out).
+#ifndef ECC_HC_THREAD_DIMS
+#define ECC_HC_THREAD_DIMS 5
+#endif
+constexpr int hc_split(int D) { return D > ECC_HC_THREAD_DIMS ? D - ECC_HC_THREAD_DIMS : 0; }
+
 template <int D>
 hipError_t hc_occupancy(int *per_cu) {
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(per_cu, k_allreduce_ssp<D>, kHcThreads, 0);
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        per_cu, k_allreduce_ssp_col<D, hc_split(D)>, kHcThreads, 0);
+}
+
+template <int D>
+void hc_launch(dim3 grid, hipStream_t st, const HcArgs &a) {
+    hipLaunchKernelGGL((k_allreduce_ssp_col<D, hc_split(D)>), grid, dim3(kHcThreads), 0, st, a);
+}
+
+// Elements one workgroup covers per pass.
+int64_t hc_wg_elems(int D) {
+    switch (D) {
+        case 5: return kHcThreads >> hc_split(5);
+        case 6: return kHcThreads >> hc_split(6);
+        default: return kHcThreads >> hc_split(4);
+    }
 }
 
 }  // namespace
@@ -253,8 +275,8 @@ ecc_status_t ecc_hypercube_create(int32_t P, int64_t m, int32_t slack, void *hip
         default: e = hc_occupancy<6>(&per_cu); break;
     }
     if (e != hipSuccess || per_cu < 1) per_cu = 2;
-    const int64_t chunk = (int64_t)(64 / P) * kHcV;  // elements of one process per wave
-    const int64_t need = std::max<int64_t>(1, (m + 4 * chunk - 1) / (4 * chunk));
+    const int64_t per_wg = hc_wg_elems(D);
+    const int64_t need = std::max<int64_t>(1, (m + per_wg - 1) / per_wg);
     h->grid = (int32_t)std::min<int64_t>(need, (int64_t)cus * per_cu);
     ecc_status_t st = hc_reset(h);
     if (st != ECC_OK) {
@@ -313,15 +335,15 @@ ecc_status_t ecc_allreduce_ssp(ecc_hypercube_t h, const double *d_contrib,
     a.result = d_result;
     a.result_clock = d_result_clock;
     a.outcome = d_outcome;
-    const dim3 grid(h->grid), block(kHcThreads);
+    const dim3 grid(h->grid);
     switch (h->D) {
-        case 0: hipLaunchKernelGGL(k_allreduce_ssp<0>, grid, block, 0, h->stream, a); break;
-        case 1: hipLaunchKernelGGL(k_allreduce_ssp<1>, grid, block, 0, h->stream, a); break;
-        case 2: hipLaunchKernelGGL(k_allreduce_ssp<2>, grid, block, 0, h->stream, a); break;
-        case 3: hipLaunchKernelGGL(k_allreduce_ssp<3>, grid, block, 0, h->stream, a); break;
-        case 4: hipLaunchKernelGGL(k_allreduce_ssp<4>, grid, block, 0, h->stream, a); break;
-        case 5: hipLaunchKernelGGL(k_allreduce_ssp<5>, grid, block, 0, h->stream, a); break;
-        default: hipLaunchKernelGGL(k_allreduce_ssp<6>, grid, block, 0, h->stream, a); break;
+        case 0: hc_launch<0>(grid, h->stream, a); break;
+        case 1: hc_launch<1>(grid, h->stream, a); break;
+        case 2: hc_launch<2>(grid, h->stream, a); break;
+        case 3: hc_launch<3>(grid, h->stream, a); break;
+        case 4: hc_launch<4>(grid, h->stream, a); break;
+        case 5: hc_launch<5>(grid, h->stream, a); break;
+        default: hc_launch<6>(grid, h->stream, a); break;
     }
     ECC_LAUNCH_CHECK();
     h->clock += 1;

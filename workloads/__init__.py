@@ -33,6 +33,8 @@ STREAM_EDGES = 4
 STREAM_COUNTS = 5
 STREAM_PAYLOAD = 6
 STREAM_PAYLOAD_REDUCE = 7
+STREAM_PAYLOAD_HC = 8
+STREAM_DELIVERY = 9
 
 SEED_BASE = 2203170630
 
@@ -417,3 +419,37 @@ def config4b(P: int = 256, m: int = 1 << 22, reps: int = 1000, q: float = 0.7,
              S: int = UNBOUNDED) -> Allreduce:
     seed = seed_of(4)
     return Allreduce(P, m, reps, arrival_mask(seed, reps, np.full(P, q)), S, seed, q)
+
+
+@dataclass
+class HypercubeSSP:
+    """SSP hypercube allreduce (Algorithm 1) for P = 2^d processes: process
+    p's contribution at call t is U[-1,1) from its payload stream at
+    counters (t*P + p)*m + i; the message of step k of call t reaches process
+    r's slot k in time with probability q (Bernoulli, independent per call,
+    process and step; call 0 of every slot included)."""
+    P: int
+    m: int
+    calls: int
+    slack: int
+    q: float
+    seed: int
+    delivered: np.ndarray     # bool [calls][P][d]
+
+    @property
+    def d(self) -> int:
+        return int(self.P).bit_length() - 1
+
+    def contrib(self, t: int) -> np.ndarray:
+        return uniform(self.seed, STREAM_PAYLOAD_HC, self.P * self.m, ctr0=t * self.P * self.m,
+                       lo=-1.0, hi=1.0).reshape(self.P, self.m)
+
+
+def hypercube_ssp(P: int = 32, m: int = 1 << 21, calls: int = 100, slack: int = 2,
+                  q: float = 0.8) -> HypercubeSSP:
+    """32 processes as in the paper's allreduce_SSP run; slack 2, one of the
+    paper's settings; 16 MB vectors (the paper's model size is not stated)."""
+    seed = seed_of(6)
+    d = int(P).bit_length() - 1
+    u = uniform(seed, STREAM_DELIVERY, calls * P * max(d, 1)).reshape(calls, P, max(d, 1))
+    return HypercubeSSP(P, m, calls, slack, q, seed, (u < q)[:, :, :d])
