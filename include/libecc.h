@@ -318,6 +318,61 @@ ecc_status_t ecc_hypercube_stats(ecc_hypercube_t h, int64_t *clock, uint64_t *wa
                                  int32_t *h_slot_clock, uint64_t *h_waits);
 
 /* ---------------------------------------------------------------------------
+ * Eventually consistent Broadcast and Reduce with a threshold (Section
+ * III-B; threshold and status parameters of Section III), and the partial
+ * allreduce that drops what did not arrive.
+ *
+ * Binomial spanning tree over P processes numbered relative to the root
+ * (q = (p - root) mod P): the children of q are q + 2^i for every i above
+ * q's highest set bit (every i for the root) with q + 2^i < P; stage s
+ * involves min(2^s, P) processes.  All sums are fp64, in the order stated,
+ * and bitwise reproducible.  The calls are enqueued on hip_stream; the status
+ * outputs are computed on the host and valid on return.
+ * ------------------------------------------------------------------------- */
+
+#define ECC_THRESHOLD_DATA 0   /* reduce the first ceil(theta * m) elements  */
+#define ECC_THRESHOLD_PROCS 1  /* reduce whole vectors of the first stages   */
+
+/* Broadcast of the first k = ceil(theta * m) elements (theta in [0, 1]) of
+ * the root's vector d_src to every other process: d_dst[p][0, k) = d_src[0,
+ * k) for p != root; elements beyond k keep what they held (the eventually
+ * consistent part).  d_dst is a device array of P device pointers (entry
+ * root is not used); the buffers must not overlap d_src[0, k) or each other
+ * (not checked).  *h_count (host, may be NULL) receives k.  ECC_ERR_ARG for
+ * P < 1, root outside [0, P), m < 0 or theta outside [0, 1]. */
+ecc_status_t ecc_bcast_threshold(int32_t P, int32_t root, int64_t m, double theta,
+                                 const double *d_src, double *const *d_dst, int64_t *h_count,
+                                 void *hip_stream);
+
+/* Reduce (sum) to the root over the binomial spanning tree, 1 <= P <= 64.
+ *   mode ECC_THRESHOLD_DATA:  theta in [0, 1]; the first k = ceil(theta * m)
+ *     elements of all P processes are reduced; d_result[k, m) untouched.
+ *   mode ECC_THRESHOLD_PROCS: theta in (0, 1]; the full vectors (k = m) of
+ *     relative ranks 0 .. n-1 are reduced, n = min(P, the smallest power of
+ *     two >= ceil(theta * P)): whole stages, at least ceil(theta * P)
+ *     processes; the leaves far from the root drop out.
+ * Order: a parent adds its children's partial sums leaves first -- stage by
+ * stage from the last, q += partial(q + 2^s) for every q < 2^s -- so
+ * d_result[i] is the partial of relative rank 0.  d_src is a device array
+ * of P device pointers (process p's vector); d_result must not overlap them.
+ * h_elements / h_processes (host, may be NULL) receive k and n: the status
+ * of the call.  ECC_ERR_ARG for a bad P, root, m, theta or mode. */
+ecc_status_t ecc_reduce_threshold(int32_t P, int32_t root, int64_t m, double theta, int32_t mode,
+                                  const double *const *d_src, double *d_result,
+                                  int64_t *h_elements, int32_t *h_processes, void *hip_stream);
+
+/* Partial allreduce that drops the contributions that did not arrive:
+ * d_result[i] = +0.0 + sum over p with d_arrived[p] != 0, in rank order, of
+ * d_fresh[p][i] (+0.0 when nothing arrived).  No slot, clock or version is
+ * kept: this is the stateless counterpart of ecc_allreduce_partial.
+ * d_fresh: device array of P device pointers; d_arrived: device array of P
+ * bytes; d_count (device int32, may be NULL) receives the number of ranks
+ * that arrived.  ECC_ERR_ARG for P < 1, m < 0 or a NULL required array. */
+ecc_status_t ecc_allreduce_drop(int32_t P, int64_t m, const double *const *d_fresh,
+                                const uint8_t *d_arrived, double *d_result, int32_t *d_count,
+                                void *hip_stream);
+
+/* ---------------------------------------------------------------------------
  * Plain streaming copy d_dst[i] = d_src[i], 0 <= i < n, enqueued on
  * hip_stream.  Both buffers 8-byte aligned and not overlapping
  * (ECC_ERR_ARG otherwise); 16-byte accesses when both are 16-byte aligned.

@@ -21,6 +21,7 @@ ECC_UNBOUNDED = 0x7FFFFFFF
 ECC_NORM_L1, ECC_NORM_L2 = 1, 2
 ECC_KIND_JACOBI, ECC_KIND_POWER = 0, 1
 ECC_TIMING_ASSEMBLE, ECC_TIMING_ALLREDUCE, ECC_TIMING_SWEEP, ECC_TIMING_NORM = 0, 1, 2, 3
+ECC_THRESHOLD_DATA, ECC_THRESHOLD_PROCS = 0, 1
 
 STATUS_NAMES = {0: "ECC_OK", 1: "ECC_ERR_ARG", 2: "ECC_ERR_OVERLAP", 3: "ECC_ERR_RANGE",
                 4: "ECC_ERR_ALLOC", 5: "ECC_ERR_DEVICE", 6: "ECC_ERR_STATE"}
@@ -69,6 +70,10 @@ _SIGS = [
     ("ecc_hypercube_reset", ctypes.c_int, [_VP]),
     ("ecc_allreduce_ssp", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP]),
     ("ecc_hypercube_stats", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP]),
+    ("ecc_bcast_threshold", ctypes.c_int, [_I32, _I32, _I64, _D, _VP, _VP, _VP, _VP]),
+    ("ecc_reduce_threshold", ctypes.c_int, [_I32, _I32, _I64, _D, _I32, _VP, _VP, _VP, _VP,
+                                            _VP]),
+    ("ecc_allreduce_drop", ctypes.c_int, [_I32, _I64, _VP, _VP, _VP, _VP, _VP]),
     ("ecc_solve", ctypes.c_int, [_VP, _VP, _VP, _D, _D, _VP, _VP, _VP, _VP, _I32, _D, _VP, _VP,
                                  _VP, _VP]),
 ]
@@ -271,3 +276,25 @@ def ecc_hypercube_stats(h, P: int):
     _check(lib().ecc_hypercube_stats(h, ctypes.addressof(clock), ctypes.addressof(waits),
                                      _ptr(clk), _ptr(w)))
     return clock.value, waits.value, clk, w
+
+
+def ecc_bcast_threshold(P, root, m, theta, d_src, d_dst, stream=None) -> int:
+    """Returns the number of elements delivered."""
+    k = ctypes.c_int64()
+    _check(lib().ecc_bcast_threshold(P, root, m, theta, _ptr(d_src), _ptr(d_dst),
+                                     ctypes.addressof(k), stream))
+    return k.value
+
+
+def ecc_reduce_threshold(P, root, m, theta, mode, d_src, d_result, stream=None):
+    """Returns (elements reduced, processes involved)."""
+    k = ctypes.c_int64()
+    n = ctypes.c_int32()
+    _check(lib().ecc_reduce_threshold(P, root, m, theta, mode, _ptr(d_src), _ptr(d_result),
+                                      ctypes.addressof(k), ctypes.addressof(n), stream))
+    return k.value, n.value
+
+
+def ecc_allreduce_drop(P, m, d_fresh, d_arrived, d_result, d_count=None, stream=None):
+    _check(lib().ecc_allreduce_drop(P, m, _ptr(d_fresh), _ptr(d_arrived), _ptr(d_result),
+                                    _ptr(d_count), stream))

@@ -1,0 +1,219 @@
+// Eventually consistent Broadcast and Reduce with a threshold (Section III-B,
+// with the threshold/status parameters of Section III), and the partial
+// allreduce that drops the contributions that did not arrive.
+//
+// Binomial spanning tree (BST) over P processes numbered relative to the
+// root: the children of q are q + 2^i for every i above q's highest set bit
+// with q + 2^i < P, so stage s involves min(2^s, P) processes.
+//  - Broadcast delivers the first ceil(theta * m) elements of the root's
+//    vector to every other process: on one GPU the tree's forwarding
+//    reduces to prefix copies (every receiver gets the root's data).
+//  - Reduce sums either the first ceil(theta * m) elements of every process
+//    or the full vectors of the processes of the first stages of the tree
+//    (at least ceil(theta * P) of them).  The order is the tree's: a parent
+//    adds its children's partial sums leaves first, which is, stage by stage
+//    from the last one, q += partial(q + 2^s) for every q < 2^s.  A thread
+//    carries one element of every involved process in registers.
+//  - The dropping allreduce sums, in rank order from +0.0, the contributions
+//    of the ranks that arrived in this step.
+// All sums are fp64 without contraction, in the order stated, so results
+// are bitwise reproducible.
+#include <algorithm>
+#include <cmath>
+
+#include "ecc_common.h"
+
+namespace ecc {
+
+constexpr int kThrThreads = 256;
+constexpr int kThrMaxStages = 6;  // Reduce: at most 64 processes in registers
+constexpr int kBcastTile = 4096;  // elements one workgroup copies
+
+// blockIdx.y = destination process (the root's row returns at once);
+// blockIdx.x = tile of the prefix.  16-byte accesses when both rows are
+// 16-byte aligned, else 8-byte.
+__global__ __launch_bounds__(kThrThreads) void k_bcast_prefix(int32_t root, int64_t k,
+                                                              const double *__restrict__ src,
+                                                              double *const *__restrict__ dst) {
+    const int32_t p = blockIdx.y;
+    if (p == root) return;
+    double *__restrict__ d = dst[p];
+    const int64_t t0 = (int64_t)blockIdx.x * kBcastTile;
+    const int64_t t1 = min<int64_t>(k, t0 + kBcastTile);
+    if (t0 >= t1) return;
+    const bool vec = (((uintptr_t)(src + t0) | (uintptr_t)(d + t0)) & 15) == 0;
+    if (vec) {
+        const int64_t npair = (t1 - t0) / 2;
+        const double2 *s2 = reinterpret_cast<const double2 *>(src + t0);
+        double2 *d2 = reinterpret_cast<double2 *>(d + t0);
+        for (int64_t i = threadIdx.x; i < npair; i += kThrThreads) d2[i] = s2[i];
+        if (((t1 - t0) & 1) && threadIdx.x == 0) d[t1 - 1] = src[t1 - 1];
+    } else {
+        for (int64_t i = t0 + threadIdx.x; i < t1; i += kThrThreads) d[i] = src[i];
+    }
+}
+
+// Reduce over relative ranks 0 .. n-1 (n <= 2^S) of the first k elements.
+template <int S>
+__global__ __launch_bounds__(kThrThreads) void k_reduce_bst(int32_t P, int32_t root, int32_t n,
+                                                            int64_t k,
+                                                            const double *const *__restrict__ src,
+                                                            double *__restrict__ result) {
+    constexpr int N = 1 << S;
+    const int64_t stride = (int64_t)gridDim.x * kThrThreads;
+    for (int64_t j = (int64_t)blockIdx.x * kThrThreads + threadIdx.x; j < k; j += stride) {
+        double part[N];
+#pragma unroll
+        for (int q = 0; q < N; ++q) {
+            if (q < n) {
+                const int32_t p = (q + root) % P;
+                part[q] = src[p][j];
+            }
+        }
+#pragma unroll
+        for (int s = S - 1; s >= 0; --s) {
+#pragma unroll
+            for (int q = 0; q < (1 << s); ++q)
+                if (q + (1 << s) < n) part[q] = part[q] + part[q + (1 << s)];
+        }
+        result[j] = part[0];
+    }
+}
+
+// Dropping partial allreduce: eight ranks' loads in flight, summed in rank
+// order; only arrived ranks are added.
+constexpr int kDropU = 8;
+
+__global__ __launch_bounds__(kThrThreads) void k_allreduce_drop(int32_t P, int64_t m,
+                                                                const double *const *__restrict__ fresh,
+                                                                const uint8_t *__restrict__ arrived,
+                                                                double *__restrict__ result,
+                                                                int32_t *__restrict__ count) {
+    if (count && blockIdx.x == 0 && threadIdx.x == 0) {
+        int32_t c = 0;
+        for (int32_t p = 0; p < P; ++p) c += arrived[p] != 0;
+        *count = c;
+    }
+    const int64_t stride = (int64_t)gridDim.x * kThrThreads;
+    for (int64_t j = (int64_t)blockIdx.x * kThrThreads + threadIdx.x; j < m; j += stride) {
+        double acc = 0.0;
+        for (int32_t p0 = 0; p0 < P; p0 += kDropU) {
+            bool on[kDropU];
+            double v[kDropU];
+#pragma unroll
+            for (int u = 0; u < kDropU; ++u) {
+                const int32_t p = p0 + u;
+                on[u] = p < P && arrived[p] != 0;
+                v[u] = on[u] ? fresh[p][j] : 0.0;
+            }
+#pragma unroll
+            for (int u = 0; u < kDropU; ++u)
+                if (on[u]) acc = acc + v[u];
+        }
+        result[j] = acc;
+    }
+}
+
+int64_t thr_prefix(double theta, int64_t m) {
+    const double x = std::ceil(theta * (double)m);
+    return std::min<int64_t>(m, (int64_t)x);
+}
+
+int32_t thr_involved(double theta, int32_t P) {
+    const int64_t need = std::max<int64_t>(1, (int64_t)std::ceil(theta * (double)P));
+    int64_t n = 1;
+    while (n < need) n *= 2;
+    return (int32_t)std::min<int64_t>(n, P);
+}
+
+int32_t thr_grid(int64_t elems) {
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        cus = 256;
+    const int64_t need = std::max<int64_t>(1, (elems + kThrThreads - 1) / kThrThreads);
+    return (int32_t)std::min<int64_t>(need, (int64_t)cus * 8);
+}
+
+}  // namespace ecc
+
+using namespace ecc;
+
+extern "C" {
+
+ecc_status_t ecc_bcast_threshold(int32_t P, int32_t root, int64_t m, double theta,
+                                 const double *d_src, double *const *d_dst, int64_t *h_count,
+                                 void *hip_stream) {
+    clear_error();
+    ECC_ARG(P >= 1, "P must be >= 1");
+    ECC_ARG(root >= 0 && root < P, "root %d outside [0, P)", root);
+    ECC_ARG(m >= 0, "m must be >= 0");
+    ECC_ARG(theta >= 0.0 && theta <= 1.0, "theta must lie in [0, 1]");
+    const int64_t k = thr_prefix(theta, m);
+    if (h_count) *h_count = k;
+    if (k == 0 || P == 1) return ECC_OK;
+    ECC_ARG(d_src != nullptr && d_dst != nullptr, "NULL source or destination array");
+    const int64_t tiles = (k + kBcastTile - 1) / kBcastTile;
+    ECC_ARG(tiles < 0x7fffffff && P <= 65535, "too many tiles or processes");
+    hipLaunchKernelGGL(k_bcast_prefix, dim3((unsigned)tiles, (unsigned)P), dim3(kThrThreads), 0,
+                       (hipStream_t)hip_stream, root, k, d_src, d_dst);
+    ECC_LAUNCH_CHECK();
+    return ECC_OK;
+}
+
+ecc_status_t ecc_reduce_threshold(int32_t P, int32_t root, int64_t m, double theta, int32_t mode,
+                                  const double *const *d_src, double *d_result,
+                                  int64_t *h_elements, int32_t *h_processes, void *hip_stream) {
+    clear_error();
+    ECC_ARG(P >= 1 && P <= (1 << kThrMaxStages), "P = %d must lie in [1, 64]", P);
+    ECC_ARG(root >= 0 && root < P, "root %d outside [0, P)", root);
+    ECC_ARG(m >= 0, "m must be >= 0");
+    ECC_ARG(mode == ECC_THRESHOLD_DATA || mode == ECC_THRESHOLD_PROCS, "unknown mode %d", mode);
+    int64_t k;
+    int32_t n;
+    if (mode == ECC_THRESHOLD_DATA) {
+        ECC_ARG(theta >= 0.0 && theta <= 1.0, "theta must lie in [0, 1]");
+        k = thr_prefix(theta, m);
+        n = P;
+    } else {
+        ECC_ARG(theta > 0.0 && theta <= 1.0, "theta must lie in (0, 1]");
+        k = m;
+        n = thr_involved(theta, P);
+    }
+    if (h_elements) *h_elements = k;
+    if (h_processes) *h_processes = n;
+    if (k == 0) return ECC_OK;
+    ECC_ARG(d_src != nullptr && d_result != nullptr, "NULL source array or result");
+    int S = 0;
+    while ((1 << S) < n) ++S;
+    const dim3 grid(thr_grid(k)), block(kThrThreads);
+    hipStream_t st = (hipStream_t)hip_stream;
+    switch (S) {
+        case 0: hipLaunchKernelGGL(k_reduce_bst<0>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        case 1: hipLaunchKernelGGL(k_reduce_bst<1>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        case 2: hipLaunchKernelGGL(k_reduce_bst<2>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        case 3: hipLaunchKernelGGL(k_reduce_bst<3>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        case 4: hipLaunchKernelGGL(k_reduce_bst<4>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        case 5: hipLaunchKernelGGL(k_reduce_bst<5>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        default: hipLaunchKernelGGL(k_reduce_bst<6>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+    }
+    ECC_LAUNCH_CHECK();
+    return ECC_OK;
+}
+
+ecc_status_t ecc_allreduce_drop(int32_t P, int64_t m, const double *const *d_fresh,
+                                const uint8_t *d_arrived, double *d_result, int32_t *d_count,
+                                void *hip_stream) {
+    clear_error();
+    ECC_ARG(P >= 1, "P must be >= 1");
+    ECC_ARG(m >= 0, "m must be >= 0");
+    ECC_ARG(d_arrived != nullptr, "d_arrived is NULL");
+    ECC_ARG(m == 0 || (d_fresh && d_result), "NULL contribution array or result");
+    if (m == 0 && !d_count) return ECC_OK;
+    hipLaunchKernelGGL(k_allreduce_drop, dim3(thr_grid(m)), dim3(kThrThreads), 0,
+                       (hipStream_t)hip_stream, P, m, d_fresh, d_arrived, d_result, d_count);
+    ECC_LAUNCH_CHECK();
+    return ECC_OK;
+}
+
+}  // extern "C"
