@@ -11,7 +11,7 @@ Metric: assembled+iterated GB/s (algorithmic bytes of assembly + sweep + norm,
 each distinct element counted once) and iterations/s, with the dominant
 kernel's achieved bandwidth against the HBM roofline.  Prints one JSON line.
 
-    python bench.py [--steps K] [--warmup W] [--config 1|2|3|4a|4b|5|ssp]
+    python bench.py [--steps K] [--warmup W] [--config 1|2|3|4a|4b|5|ssp|thr]
 """
 from __future__ import annotations
 
@@ -85,6 +85,8 @@ def build_workload(cfg):
         return W.config4b()
     if cfg == "ssp":
         return W.hypercube_ssp()
+    if cfg == "thr":
+        return W.threshold_collectives()
     raise ValueError(cfg)
 
 
@@ -107,6 +109,12 @@ def describe(cfg, prob):
         return {"workload": "allgatherv assembly, P=%d lognormal counts, %d elements, %d reps"
                             % (prob.P, int(prob.counts.sum()), prob.reps),
                 "P": prob.P, "elements": int(prob.counts.sum()), "reps": prob.reps,
+                "config_id": cfg}
+    if cfg == "thr":
+        return {"workload": "threshold broadcast + reduce over a binomial tree, P=%d processes x "
+                            "%d elements, data fraction %.2f, %d repetitions"
+                            % (prob.P, prob.m, prob.theta, prob.reps),
+                "P": prob.P, "m": prob.m, "theta": prob.theta, "reps": prob.reps,
                 "config_id": cfg}
     if cfg == "ssp":
         return {"workload": "hypercube allreduce_SSP with per-receiver views, P=%d processes x "
@@ -335,6 +343,61 @@ def run_hypercube_gpu(prob, steps, warmup):
             "waits_per_step": waits}
 
 
+def run_threshold_gpu(prob, steps, warmup):
+    """One step = prob.reps x [threshold broadcast from process 0, then
+    threshold reduce to process 0, both with data fraction theta]."""
+    import torch
+    from paper_2203_17063_amd import capi as E
+
+    mem0 = torch.cuda.mem_get_info()[0]
+    P, m, theta = prob.P, prob.m, prob.theta
+    vecs = [torch.from_numpy(prob.vector(p)).cuda() for p in range(P)]
+    result = torch.empty(m, dtype=torch.float64, device="cuda")
+    d_vecs = torch.tensor([v.data_ptr() for v in vecs], dtype=torch.int64, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    torch.cuda.synchronize()
+    footprint = mem0 - torch.cuda.mem_get_info()[0]
+    k_b = k_r = n_r = 0
+
+    def step(ev=None):
+        nonlocal k_b, k_r, n_r
+        for r in range(prob.reps):
+            if ev is not None:
+                ev[r][0].record()
+            k_b = E.ecc_bcast_threshold(P, 0, m, theta, vecs[0], d_vecs, stream)
+            if ev is not None:
+                ev[r][1].record()
+            k_r, n_r = E.ecc_reduce_threshold(P, 0, m, theta, E.ECC_THRESHOLD_DATA, d_vecs,
+                                              result, stream)
+            if ev is not None:
+                ev[r][2].record()
+
+    for _ in range(max(warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(prob.reps)]
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for s_ in range(steps):
+        step(ev[s_])
+    torch.cuda.synchronize()
+    wall_events = time.perf_counter() - t1
+    ms_b = sum(e[0].elapsed_time(e[1]) for row in ev for e in row)
+    ms_r = sum(e[1].elapsed_time(e[2]) for row in ev for e in row)
+    bytes_b = 8.0 * k_b * P                 # the root's prefix read once, P - 1 copies written
+    bytes_r = 8.0 * k_r * (n_r + 1)         # n prefixes read, the result written
+    return {"iters": prob.reps, "wall": wall, "wall_events": wall_events,
+            "times": {"REDUCE": (ms_r, steps * prob.reps), "BCAST": (ms_b, steps * prob.reps)},
+            "bytes_per_step": (bytes_b + bytes_r) * prob.reps, "dominant": "reduce",
+            "dominant_bytes": bytes_r, "footprint": footprint, "unit_per_step": prob.reps}
+
+
 # ----------------------------------------------------------------------------
 # CPU baseline: the oracle as it stands, on a bounded sample
 # ----------------------------------------------------------------------------
@@ -370,6 +433,23 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
         while time.perf_counter() - t0 < budget_s and reps < prob.reps:
             eff, _, _ = oracle.select(prob.S, reps, prob.mask[reps], version)
             oracle.allgatherv(prob.counts, prob.displs, eff, sends, recv)
+            reps += 1
+        dt = time.perf_counter() - t0
+        per_rep = res["bytes_per_step"] / res["iters"]
+        return {"value": round(per_rep * reps / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
+                "kind": "oracle", "sample": "%d of %d repetitions, 1 thread, %.1f s"
+                                            % (reps, prob.reps, dt)}
+    if cfg == "thr":
+        from oracle import threshold as THO
+        P, m = prob.P, prob.m
+        vecs = [prob.vector(p) for p in range(P)]
+        bufs = [v.copy() for v in vecs]
+        result = np.zeros(m)
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < budget_s and reps < prob.reps:
+            THO.bcast(P, 0, prob.theta, vecs[0], bufs)
+            THO.reduce(P, 0, prob.theta, THO.DATA, vecs, result)
             reps += 1
         dt = time.perf_counter() - t0
         per_rep = res["bytes_per_step"] / res["iters"]
@@ -449,7 +529,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="2", choices=["1", "2", "3", "4a", "4b", "5", "ssp"])
+    ap.add_argument("--config", default="2", choices=["1", "2", "3", "4a", "4b", "5", "ssp", "thr"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only measure a plain 4 GiB device copy (copy ceiling)")
@@ -485,6 +565,11 @@ def main():
         digest = kernel_source_digest(["collectives.hip", "ecc_common.h"])
         tag = "assemble_cfg4a"
         dom_ms, dom_n = res["times"]["ASSEMBLE"]
+    elif cfg == "thr":
+        res = run_threshold_gpu(prob, args.steps, args.warmup)
+        digest = kernel_source_digest(["threshold.hip", "ecc_common.h"])
+        tag = "reduce_threshold_p32"
+        dom_ms, dom_n = res["times"]["REDUCE"]
     elif cfg == "ssp":
         res = run_hypercube_gpu(prob, args.steps, args.warmup)
         digest = kernel_source_digest(["hypercube.hip", "ecc_common.h"])

@@ -7,7 +7,8 @@
 // with q + 2^i < P, so stage s involves min(2^s, P) processes.
 //  - Broadcast delivers the first ceil(theta * m) elements of the root's
 //    vector to every other process: on one GPU the tree's forwarding
-//    reduces to prefix copies (every receiver gets the root's data).
+//    reduces to prefix copies (every receiver gets the root's data); each
+//    tile of the prefix is read once and written P - 1 times.
 //  - Reduce sums either the first ceil(theta * m) elements of every process
 //    or the full vectors of the processes of the first stages of the tree
 //    (at least ceil(theta * P) of them).  The order is the tree's: a parent
@@ -29,27 +30,45 @@ constexpr int kThrThreads = 256;
 constexpr int kThrMaxStages = 6;  // Reduce: at most 64 processes in registers
 constexpr int kBcastTile = 4096;  // elements one workgroup copies
 
-// blockIdx.y = destination process (the root's row returns at once);
-// blockIdx.x = tile of the prefix.  16-byte accesses when both rows are
-// 16-byte aligned, else 8-byte.
-__global__ __launch_bounds__(kThrThreads) void k_bcast_prefix(int32_t root, int64_t k,
+// One workgroup per tile of kBcastTile elements of the prefix: the tile is
+// loaded from the root's vector once, into registers (kBcastPairs pairs per
+// thread), and stored into every other process's buffer -- 16-byte stores
+// where the destination row allows, else 8-byte.
+constexpr int kBcastPairs = kBcastTile / (2 * kThrThreads);
+
+__global__ __launch_bounds__(kThrThreads) void k_bcast_prefix(int32_t P, int32_t root, int64_t k,
                                                               const double *__restrict__ src,
                                                               double *const *__restrict__ dst) {
-    const int32_t p = blockIdx.y;
-    if (p == root) return;
-    double *__restrict__ d = dst[p];
     const int64_t t0 = (int64_t)blockIdx.x * kBcastTile;
-    const int64_t t1 = min<int64_t>(k, t0 + kBcastTile);
-    if (t0 >= t1) return;
-    const bool vec = (((uintptr_t)(src + t0) | (uintptr_t)(d + t0)) & 15) == 0;
-    if (vec) {
-        const int64_t npair = (t1 - t0) / 2;
-        const double2 *s2 = reinterpret_cast<const double2 *>(src + t0);
-        double2 *d2 = reinterpret_cast<double2 *>(d + t0);
-        for (int64_t i = threadIdx.x; i < npair; i += kThrThreads) d2[i] = s2[i];
-        if (((t1 - t0) & 1) && threadIdx.x == 0) d[t1 - 1] = src[t1 - 1];
-    } else {
-        for (int64_t i = t0 + threadIdx.x; i < t1; i += kThrThreads) d[i] = src[i];
+    const bool src16 = ((uintptr_t)src & 15) == 0;
+    double2 v[kBcastPairs];
+#pragma unroll
+    for (int u = 0; u < kBcastPairs; ++u) {
+        const int64_t e = t0 + 2 * ((int64_t)threadIdx.x + (int64_t)u * kThrThreads);
+        if (e + 1 < k) {
+            if (src16) v[u] = *reinterpret_cast<const double2 *>(src + e);
+            else v[u] = make_double2(src[e], src[e + 1]);
+        } else {
+            v[u] = make_double2(e < k ? src[e] : 0.0, 0.0);
+        }
+    }
+    for (int32_t p = 0; p < P; ++p) {
+        if (p == root) continue;
+        double *__restrict__ d = dst[p];
+        const bool d16 = ((uintptr_t)d & 15) == 0;
+#pragma unroll
+        for (int u = 0; u < kBcastPairs; ++u) {
+            const int64_t e = t0 + 2 * ((int64_t)threadIdx.x + (int64_t)u * kThrThreads);
+            if (e + 1 < k) {
+                if (d16) *reinterpret_cast<double2 *>(d + e) = v[u];
+                else {
+                    d[e] = v[u].x;
+                    d[e + 1] = v[u].y;
+                }
+            } else if (e < k) {
+                d[e] = v[u].x;
+            }
+        }
     }
 }
 
@@ -154,9 +173,9 @@ ecc_status_t ecc_bcast_threshold(int32_t P, int32_t root, int64_t m, double thet
     if (k == 0 || P == 1) return ECC_OK;
     ECC_ARG(d_src != nullptr && d_dst != nullptr, "NULL source or destination array");
     const int64_t tiles = (k + kBcastTile - 1) / kBcastTile;
-    ECC_ARG(tiles < 0x7fffffff && P <= 65535, "too many tiles or processes");
-    hipLaunchKernelGGL(k_bcast_prefix, dim3((unsigned)tiles, (unsigned)P), dim3(kThrThreads), 0,
-                       (hipStream_t)hip_stream, root, k, d_src, d_dst);
+    ECC_ARG(tiles < 0x7fffffff, "too many tiles");
+    hipLaunchKernelGGL(k_bcast_prefix, dim3((unsigned)tiles), dim3(kThrThreads), 0,
+                       (hipStream_t)hip_stream, P, root, k, d_src, d_dst);
     ECC_LAUNCH_CHECK();
     return ECC_OK;
 }

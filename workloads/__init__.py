@@ -35,6 +35,7 @@ STREAM_PAYLOAD = 6
 STREAM_PAYLOAD_REDUCE = 7
 STREAM_PAYLOAD_HC = 8
 STREAM_DELIVERY = 9
+STREAM_PAYLOAD_THR = 10
 
 SEED_BASE = 2203170630
 
@@ -453,3 +454,25 @@ def hypercube_ssp(P: int = 32, m: int = 1 << 21, calls: int = 100, slack: int = 
     d = int(P).bit_length() - 1
     u = uniform(seed, STREAM_DELIVERY, calls * P * max(d, 1)).reshape(calls, P, max(d, 1))
     return HypercubeSSP(P, m, calls, slack, q, seed, (u < q)[:, :, :d])
+
+
+@dataclass
+class ThresholdCollectives:
+    """Threshold Broadcast and Reduce (Section III-B) over P processes with
+    vectors of m doubles, U[-1,1) from process p's payload stream at counters
+    p*m + i; theta is the data (or process) fraction."""
+    P: int
+    m: int
+    theta: float
+    reps: int
+    seed: int
+
+    def vector(self, p: int) -> np.ndarray:
+        return uniform(self.seed, STREAM_PAYLOAD_THR, self.m, ctr0=p * self.m, lo=-1.0, hi=1.0)
+
+
+def threshold_collectives(P: int = 32, m: int = 1 << 23, theta: float = 0.5,
+                          reps: int = 100) -> ThresholdCollectives:
+    """32 processes; 8,388,608 doubles, the largest message size of the
+    paper's experiments; half of the data."""
+    return ThresholdCollectives(P, m, theta, reps, seed_of(7))
