@@ -36,6 +36,12 @@ STREAM_PAYLOAD_REDUCE = 7
 STREAM_PAYLOAD_HC = 8
 STREAM_DELIVERY = 9
 STREAM_PAYLOAD_THR = 10
+STREAM_MF_USERS = 11
+STREAM_MF_ITEMS = 12
+STREAM_MF_NOISE = 13
+STREAM_MF_TRUTH = 14
+STREAM_MF_INIT = 15
+STREAM_MF_PERM = 16
 
 SEED_BASE = 2203170630
 
@@ -476,3 +482,80 @@ def threshold_collectives(P: int = 32, m: int = 1 << 23, theta: float = 0.5,
     """32 processes; 8,388,608 doubles, the largest message size of the
     paper's experiments; half of the data."""
     return ThresholdCollectives(P, m, theta, reps, seed_of(7))
+
+
+@dataclass
+class MFProblem:
+    """Matrix factorisation by gradient steps, data parallel over P workers
+    (the paper's allreduce_SSP experiment, Section IV, on synthetic ratings).
+
+    Ratings (users[k], items[k], ratings[k]), k < N, are stored in shard order:
+    worker p holds k in [p*N/P, (p+1)*N/P).  The model W = [U; V] is
+    (n_users + n_items) x rank doubles, row-major, U first.  One iteration at
+    model W: every worker p computes the gradient of its shard's squared error
+    sum_k (r_k - U[u_k].V[i_k])^2; the partial allreduce combines the workers'
+    gradients (stale ones substituted, slack S, arrivals `mask`); the step is
+    W := W - eta * (G_row / n_row + 2 lam W), n_row = the row's number of
+    ratings (1 if none)."""
+    n_users: int
+    n_items: int
+    rank: int
+    P: int
+    users: np.ndarray        # int32 [N]
+    items: np.ndarray        # int32 [N]
+    ratings: np.ndarray      # float64 [N], centred
+    W0: np.ndarray           # float64 [(n_users + n_items) * rank]
+    eta: float
+    lam: float
+    S: int
+    mask: np.ndarray         # uint8 [T][P]
+    T: int
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def N(self) -> int:
+        return int(self.ratings.shape[0])
+
+    @property
+    def m(self) -> int:
+        return (self.n_users + self.n_items) * self.rank
+
+    def shard(self, p: int):
+        return self.N * p // self.P, self.N * (p + 1) // self.P
+
+
+def _zipf_pick(seed: int, stream: int, n_draws: int, n: int, s: float) -> np.ndarray:
+    """Indices in [0, n) drawn with probability proportional to 1/(k+1)^s,
+    then relabelled by a seeded permutation (popularity is not id order)."""
+    w = 1.0 / np.power(np.arange(1, n + 1, dtype=np.float64), s)
+    cdf = np.cumsum(w)
+    cdf /= cdf[-1]
+    k = np.searchsorted(cdf, uniform(seed, stream, n_draws), side="right")
+    k = np.minimum(k, n - 1)
+    perm = np.argsort(uniform(seed, STREAM_MF_PERM, n, ctr0=stream * (1 << 32)), kind="stable")
+    return perm[k].astype(np.int32)
+
+
+def mf_problem(n_users: int = 160_000, n_items: int = 60_000, n_ratings: int = 25_000_000,
+               rank: int = 16, P: int = 32, S: int = 2, q: float = 0.8, T: int = 100,
+               eta: float = 0.5, lam: float = 1e-4, true_rank: int = 8, seed: int = None
+               ) -> MFProblem:
+    """Synthetic ratings shaped like a large movie-rating set (25M ratings;
+    Zipf user activity, exponent 0.5, and item popularity, exponent 0.6):
+    half-star ratings in [0.5, 5] from a planted rank-`true_rank` model plus
+    noise, centred; uniformly shuffled into P equal shards; the model starts
+    at N(0, 0.1^2)."""
+    seed = seed_of(8) if seed is None else seed
+    users = _zipf_pick(seed, STREAM_MF_USERS, n_ratings, n_users, 0.5)
+    items = _zipf_pick(seed, STREAM_MF_ITEMS, n_ratings, n_items, 0.6)
+    tu = normal(seed, STREAM_MF_TRUTH, (n_users + n_items) * true_rank) / np.sqrt(true_rank)
+    tU = tu[:n_users * true_rank].reshape(n_users, true_rank)
+    tV = tu[n_users * true_rank:].reshape(n_items, true_rank)
+    raw = 3.5 + np.einsum("kj,kj->k", tU[users], tV[items]) + 0.5 * normal(seed, STREAM_MF_NOISE,
+                                                                         n_ratings)
+    r = np.clip(np.round(raw * 2.0) / 2.0, 0.5, 5.0)
+    ratings = r - r.mean()
+    W0 = 0.1 * normal(seed, STREAM_MF_INIT, (n_users + n_items) * rank)
+    mask = arrival_mask(seed, T, np.full(P, q))
+    return MFProblem(n_users, n_items, rank, P, users, items, ratings, W0, eta, lam, S, mask, T,
+                     meta={"q": q, "true_rank": true_rank, "rating_mean": float(r.mean())})
