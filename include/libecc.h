@@ -44,6 +44,7 @@ extern "C" {
 typedef struct ecc_plan_s *ecc_plan_t;
 typedef struct ecc_matrix_s *ecc_matrix_t;
 typedef struct ecc_hypercube_s *ecc_hypercube_t;
+typedef struct ecc_mf_s *ecc_mf_t;
 
 typedef enum {
     ECC_OK = 0,
@@ -371,6 +372,44 @@ ecc_status_t ecc_reduce_threshold(int32_t P, int32_t root, int64_t m, double the
 ecc_status_t ecc_allreduce_drop(int32_t P, int64_t m, const double *const *d_fresh,
                                 const uint8_t *d_arrived, double *d_result, int32_t *d_count,
                                 void *hip_stream);
+
+/* ---------------------------------------------------------------------------
+ * Data-parallel matrix factorisation over the partial allreduce: the
+ * workload of the paper's allreduce_SSP experiment (Section IV), P workers,
+ * each holding a shard of the ratings and a replica of the model
+ * W = [U; V] ((n_users + n_items) rows of `rank` doubles, row-major, U
+ * first).  Ratings k < N are (d_users[k], d_items[k], d_ratings[k]); worker
+ * p's shard is k in [N p / P, N (p + 1) / P).
+ * --------------------------------------------------------------------------- */
+
+/* Build the per-worker gradient index (ratings of every (worker, row) in
+ * shard order, by counting sorts on the host; the rating arrays are read
+ * once and must stay valid and unchanged while the state is used).
+ * rank: a power of two in [1, 64]; N in [1, 2^30).  ECC_ERR_ARG for bad
+ * sizes or an out-of-range user/item index; ECC_ERR_RANGE when
+ * P * (n_users + n_items) reaches 2^31; ECC_ERR_ALLOC on allocation
+ * failure.  Synchronous. */
+ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32_t P, int64_t N,
+                           const int32_t *d_users, const int32_t *d_items,
+                           const double *d_ratings, ecc_mf_t *out);
+ecc_status_t ecc_mf_destroy(ecc_mf_t h);
+
+/* One iteration, enqueued on the plan's stream (the plan has P ranks and
+ * carries the slack and the clock):
+ *   e_k = r_k - U[u_k] . V[i_k]        (products added for j = 0 .. rank-1);
+ *   *d_rmse = sqrt(sum_k e_k^2 / N)    (the error at the model on entry);
+ *   d_grads[p] := worker p's gradient of sum over its shard of e_k^2: row
+ *     U[u] accumulates (-2 e_k) V[i_k] and row V[i] accumulates (-2 e_k)
+ *     U[u_k] over the worker's ratings in shard order (0 for rows without);
+ *   d_G := ecc_allreduce_partial(plan, m, d_grads, d_slots, ..., d_arrived,
+ *     d_eff_out) with m = (n_users + n_items) * rank (stale gradients
+ *     substituted from the slots; the plan's clock advances);
+ *   W := W - eta * (G * c_row + 2 lam W), c_row = 1 / max(1, ratings of
+ *     the row).
+ * d_grads, d_slots: device arrays of P device pointers to m doubles each. */
+ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam, double *d_W,
+                            double *const *d_grads, double *const *d_slots, double *d_G,
+                            const uint8_t *d_arrived, double *d_rmse, uint8_t *d_eff_out);
 
 /* ---------------------------------------------------------------------------
  * Plain streaming copy d_dst[i] = d_src[i], 0 <= i < n, enqueued on

@@ -131,3 +131,58 @@ class Iterative:
             self.close()
         except Exception:
             pass
+
+
+class MatrixFactorization:
+    """Data-parallel matrix factorisation over the partial allreduce: ratings,
+    model, per-worker gradient and slot buffers resident in HBM; every
+    iteration is enqueued through ecc_mf_iterate."""
+
+    def __init__(self, prob, device="cuda"):
+        self.prob = prob
+        P, m = prob.P, prob.m
+        self.d_users = _dev(prob.users, device=device)
+        self.d_items = _dev(prob.items, device=device)
+        self.d_ratings = _dev(prob.ratings, device=device)
+        self.d_W0 = _dev(prob.W0, device=device)
+        self.d_W = self.d_W0.clone()
+        self.grads = [torch.empty(m, dtype=torch.float64, device=device) for _ in range(P)]
+        self.slots = [torch.zeros(m, dtype=torch.float64, device=device) for _ in range(P)]
+        self.d_grads = ptr_array(self.grads, device)
+        self.d_slots = ptr_array(self.slots, device)
+        self.d_G = torch.empty(m, dtype=torch.float64, device=device)
+        self.d_mask = _dev(np.asarray(prob.mask, dtype=np.uint8), device=device)
+        self.d_rmse = torch.zeros(max(prob.T, 1), dtype=torch.float64, device=device)
+        self.d_eff = torch.zeros((max(prob.T, 1), P), dtype=torch.uint8, device=device)
+        self.plan = Plan(P, None, None, prob.S)
+        self.handle = E.ecc_mf_create(prob.n_users, prob.n_items, prob.rank, P, prob.N,
+                                      self.d_users, self.d_items, self.d_ratings)
+
+    def reset(self):
+        self.plan.reset()
+        self.d_W.copy_(self.d_W0)
+
+    def iterate(self, t, record=True):
+        E.ecc_mf_iterate(self.handle, self.plan.handle, self.prob.eta, self.prob.lam, self.d_W,
+                         self.d_grads, self.d_slots, self.d_G, self.d_mask[t].data_ptr(),
+                         self.d_rmse[t].data_ptr(), self.d_eff[t] if record else None)
+
+    def run(self, T=None, record=True):
+        T = self.prob.T if T is None else T
+        self.reset()
+        for t in range(T):
+            self.iterate(t, record)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            E.ecc_mf_destroy(self.handle)
+            self.handle = None
+        if getattr(self, "plan", None):
+            self.plan.close()
+            self.plan = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

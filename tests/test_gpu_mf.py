@@ -1,0 +1,80 @@
+"""GPU parity of the data-parallel matrix factorisation over the partial
+allreduce (Section IV's workload) through the C ABI against the oracle: the
+model after every iteration and the staleness decisions bit for bit, the
+error within 1e-12 (its sum is reduced in another order)."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import workloads as W                                     # noqa: E402
+from oracle import mf as M                                # noqa: E402
+from gpu_common import announce                           # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def _compare(prob):
+    from paper_2203_17063_amd import runner as R
+    announce("mf", prob.n_users, prob.n_items, prob.N, prob.rank, prob.P, prob.S, prob.T)
+    ref = M.run(prob, keep_W=tuple(range(prob.T + 1)))
+    run = R.MatrixFactorization(prob)
+    try:
+        run.reset()
+        for t in range(prob.T):
+            run.iterate(t)
+            torch.cuda.synchronize()
+            got = run.d_W.cpu().numpy()
+            assert np.array_equal(got, ref["kept"][t + 1]), \
+                (t, np.abs(got - ref["kept"][t + 1]).max())
+        rmse = run.d_rmse.cpu().numpy()[:prob.T]
+        assert np.allclose(rmse, ref["rmse"], rtol=1e-12, atol=0)
+        assert np.array_equal(run.d_eff.cpu().numpy()[:prob.T], ref["eff"])
+        clock, forced, _, _ = run.plan.stats()
+        assert clock == prob.T and forced == int(ref["forced"].sum())
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("rank", [1, 4, 16, 32])
+def test_mf_synchronous(rank):
+    _compare(W.mf_problem(n_users=300, n_items=120, n_ratings=20011, rank=rank, P=8, S=0, q=1.0,
+                          T=6, eta=1.0, seed=rank))
+
+
+@pytest.mark.parametrize("S,q", [(0, 0.5), (2, 0.6), (5, 0.3)])
+def test_mf_stale(S, q):
+    _compare(W.mf_problem(n_users=700, n_items=250, n_ratings=40009, rank=16, P=32, S=S, q=q,
+                          T=10, eta=1.0, seed=7 + S))
+
+
+def test_mf_one_worker_and_idle_rows():
+    """P = 1; many users and items without ratings (their rows only decay)."""
+    _compare(W.mf_problem(n_users=5000, n_items=3000, n_ratings=3001, rank=8, P=1, S=0, q=1.0,
+                          T=4, eta=1.0, seed=2))
+
+
+def test_mf_errors():
+    from paper_2203_17063_amd import capi as E
+    announce("mf errors")
+    u = torch.zeros(10, dtype=torch.int32, device="cuda")
+    i = torch.zeros(10, dtype=torch.int32, device="cuda")
+    r = torch.zeros(10, dtype=torch.float64, device="cuda")
+    for args in [(4, 4, 3, 2, 10), (4, 4, 128, 2, 10), (0, 4, 4, 2, 10), (4, 4, 4, 0, 10)]:
+        with pytest.raises(E.EccError) as ei:
+            E.ecc_mf_create(*args, u, i, r)
+        assert ei.value.status == E.ECC_ERR_ARG
+    bad = u.clone()
+    bad[7] = 4
+    with pytest.raises(E.EccError) as ei:
+        E.ecc_mf_create(4, 4, 4, 2, 10, bad, i, r)
+    assert ei.value.status == E.ECC_ERR_ARG
