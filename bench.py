@@ -11,7 +11,7 @@ Metric: assembled+iterated GB/s (algorithmic bytes of assembly + sweep + norm,
 each distinct element counted once) and iterations/s, with the dominant
 kernel's achieved bandwidth against the HBM roofline.  Prints one JSON line.
 
-    python bench.py [--steps K] [--warmup W] [--config 1|2|3|4a|4b|5|ssp|thr]
+    python bench.py [--steps K] [--warmup W] [--config 1|2|3|4a|4b|5|ssp|thr|mf]
 """
 from __future__ import annotations
 
@@ -87,6 +87,8 @@ def build_workload(cfg):
         return W.hypercube_ssp()
     if cfg == "thr":
         return W.threshold_collectives()
+    if cfg == "mf":
+        return W.mf_problem()
     raise ValueError(cfg)
 
 
@@ -110,6 +112,14 @@ def describe(cfg, prob):
                             % (prob.P, int(prob.counts.sum()), prob.reps),
                 "P": prob.P, "elements": int(prob.counts.sum()), "reps": prob.reps,
                 "config_id": cfg}
+    if cfg == "mf":
+        return {"workload": "data-parallel matrix factorisation over the partial allreduce: %d "
+                            "synthetic ratings (%d users x %d items), rank %d, P=%d workers, slack "
+                            "%d, Bernoulli(%.1f) arrivals, %d iterations"
+                            % (prob.N, prob.n_users, prob.n_items, prob.rank, prob.P, prob.S,
+                               prob.meta["q"], prob.T),
+                "N": prob.N, "n_users": prob.n_users, "n_items": prob.n_items, "rank": prob.rank,
+                "P": prob.P, "slack": prob.S, "iterations": prob.T, "config_id": cfg}
     if cfg == "thr":
         return {"workload": "threshold broadcast + reduce over a binomial tree, P=%d processes x "
                             "%d elements, data fraction %.2f, %d repetitions"
@@ -398,6 +408,85 @@ def run_threshold_gpu(prob, steps, warmup):
             "dominant_bytes": bytes_r, "footprint": footprint, "unit_per_step": prob.reps}
 
 
+def mf_bytes(prob, arrivals):
+    """Algorithmic bytes of one factorisation iteration, per kernel."""
+    N, m, P = prob.N, prob.m, prob.P
+    rows = prob.n_users + prob.n_items
+    return {"MF_ERROR": 24.0 * N + 8.0 * m,                       # u, i, r read, e written, model
+            "MF_GRAD": 32.0 * N + 8.0 * m + 8.0 * m * P,           # 2 x (perm, e, index), model, P gradients
+            "ALLREDUCE": 8.0 * m * (P + arrivals + 1),
+            "MF_STEP": 24.0 * m + 8.0 * rows}
+
+
+def run_mf_gpu(prob, steps, warmup):
+    """One step = a reset and prob.T iterations.  Afterwards, a slack study:
+    the iterations needed at slack 0 / 2 / 32 / 64 to reach the error that
+    slack 0 reaches after prob.T iterations (same arrival probability)."""
+    import dataclasses
+    import torch
+    import workloads as W
+    from paper_2203_17063_amd import capi as E
+    from paper_2203_17063_amd import runner as R
+
+    mem0 = torch.cuda.mem_get_info()[0]
+    run = R.MatrixFactorization(prob)
+    torch.cuda.synchronize()
+    footprint = mem0 - torch.cuda.mem_get_info()[0]
+    run.run()
+    torch.cuda.synchronize()
+    arrivals = run.d_eff.sum(dim=1).cpu().numpy().astype(np.int64)
+    rmse_T = float(run.d_rmse[prob.T - 1].item())
+    for _ in range(warmup):
+        run.run(record=False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        run.run(record=False)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ph = run.plan.handle
+    E.ecc_plan_set_timing(ph, True)
+    kinds = {"MF_ERROR": E.ECC_TIMING_MF_ERROR, "MF_GRAD": E.ECC_TIMING_MF_GRAD,
+             "ALLREDUCE": E.ECC_TIMING_ALLREDUCE, "MF_STEP": E.ECC_TIMING_MF_STEP}
+    for k in kinds.values():
+        E.ecc_plan_timing(ph, k, reset=True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(steps):
+        run.run(record=False)
+    torch.cuda.synchronize()
+    wall_events = time.perf_counter() - t1
+    times = {name: E.ecc_plan_timing(ph, k) for name, k in kinds.items()}
+    E.ecc_plan_set_timing(ph, False)
+    run.close()
+    per = mf_bytes(prob, float(arrivals.mean()))
+    # slack study, 3 x T iterations each, arrivals Bernoulli(q) per (iteration, worker)
+    T3 = 3 * prob.T
+    study = {}
+    target = None
+    for S in (0, 2, 32, 64):
+        pS = dataclasses.replace(prob, S=S, T=T3,
+                                 mask=W.arrival_mask(W.seed_of(8), T3, np.full(prob.P, prob.meta["q"])))
+        rs = R.MatrixFactorization(pS)
+        rs.run()
+        torch.cuda.synchronize()
+        rm = rs.d_rmse.cpu().numpy()
+        _, forced, _, _ = rs.plan.stats()
+        rs.close()
+        if target is None:
+            target = float(rm[prob.T - 1])
+        hit = np.nonzero(rm <= target)[0]
+        study[str(S)] = {"iterations_to_target": int(hit[0]) + 1 if hit.size else None,
+                         "forced_arrivals_in_%d" % T3: int(forced),
+                         "rmse_at_%d" % prob.T: round(float(rm[prob.T - 1]), 6)}
+    return {"iters": prob.T, "wall": wall, "wall_events": wall_events, "times": times,
+            "bytes_per_step": sum(per.values()) * prob.T, "dominant": "mf_grad",
+            "dominant_bytes": per["MF_GRAD"], "footprint": footprint, "unit_per_step": prob.T,
+            "extra": {"rmse_after_T": round(rmse_T, 6), "target_rmse": round(target, 6),
+                      "slack_study": study,
+                      "kernel_bytes": {k: round(v) for k, v in per.items()}}}
+
+
 # ----------------------------------------------------------------------------
 # CPU baseline: the oracle as it stands, on a bounded sample
 # ----------------------------------------------------------------------------
@@ -439,6 +528,21 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
         return {"value": round(per_rep * reps / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
                 "kind": "oracle", "sample": "%d of %d repetitions, 1 thread, %.1f s"
                                             % (reps, prob.reps, dt)}
+    if cfg == "mf":
+        # worker 0's share of iteration 0: the errors and gradient of its shard
+        from oracle import mf as MFO
+        a, b = prob.shard(0)
+        t0 = time.perf_counter()
+        e = np.zeros(prob.N)
+        e[a:b] = MFO.errors(prob, prob.W0, a, b)
+        MFO.worker_gradient(prob, prob.W0, e, 0)
+        dt = time.perf_counter() - t0
+        per = mf_bytes(prob, prob.P)
+        sample_bytes = (per["MF_ERROR"] - 8.0 * prob.m) / prob.P + \
+            (per["MF_GRAD"] - 8.0 * prob.m * (prob.P - 1)) / prob.P
+        return {"value": round(sample_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
+                "kind": "oracle", "sample": "worker 0's errors and gradient at iteration 0 "
+                                            "(1/%d of the ratings), 1 thread, %.1f s" % (prob.P, dt)}
     if cfg == "thr":
         from oracle import threshold as THO
         P, m = prob.P, prob.m
@@ -529,7 +633,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="2", choices=["1", "2", "3", "4a", "4b", "5", "ssp", "thr"])
+    ap.add_argument("--config", default="2", choices=["1", "2", "3", "4a", "4b", "5", "ssp", "thr", "mf"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only measure a plain 4 GiB device copy (copy ceiling)")
@@ -565,6 +669,11 @@ def main():
         digest = kernel_source_digest(["collectives.hip", "ecc_common.h"])
         tag = "assemble_cfg4a"
         dom_ms, dom_n = res["times"]["ASSEMBLE"]
+    elif cfg == "mf":
+        res = run_mf_gpu(prob, args.steps, args.warmup)
+        digest = kernel_source_digest(["mf.hip", "ecc_common.h"])
+        tag = "mf_grad_p32"
+        dom_ms, dom_n = res["times"]["MF_GRAD"]
     elif cfg == "thr":
         res = run_threshold_gpu(prob, args.steps, args.warmup)
         digest = kernel_source_digest(["threshold.hip", "ecc_common.h"])
@@ -624,6 +733,8 @@ def main():
                       "region of the same K steps",
         },
     }
+    if "extra" in res:
+        line.update(res["extra"])
     if not args.no_cpu_baseline:
         print("[bench] oracle CPU baseline", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(cfg, prob, res)

@@ -285,10 +285,10 @@ struct ecc_plan_s {
 
     // optional event timing per kernel kind
     bool timing = false;
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> pending[4];
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> pending[ECC_TIMING_KINDS];
     std::vector<hipEvent_t> event_pool;
-    double timed_ms[4] = {0, 0, 0, 0};
-    int64_t timed_launches[4] = {0, 0, 0, 0};
+    double timed_ms[ECC_TIMING_KINDS] = {};
+    int64_t timed_launches[ECC_TIMING_KINDS] = {};
 };
 
 struct ecc_matrix_s {

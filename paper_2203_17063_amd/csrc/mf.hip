@@ -274,12 +274,17 @@ ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam,
     while ((1 << log2r) < h->rank) ++log2r;
 #define ECC_MF_RANKS(X) X(1) X(2) X(4) X(8) X(16) X(32) X(64)
 #define ECC_MF_LAUNCH(R)                                                                      \
-    case R:                                                                                   \
-        hipLaunchKernelGGL(k_mf_err<R>, dim3(h->err_grid), dim3(kMfThreads), 0, s, v,         \
-                           h->d_err, h->d_partials);                                          \
+    case R: {                                                                                 \
+        {                                                                                     \
+            TimedLaunch timed(plan, ECC_TIMING_MF_ERROR);                                     \
+            hipLaunchKernelGGL(k_mf_err<R>, dim3(h->err_grid), dim3(kMfThreads), 0, s, v,     \
+                               h->d_err, h->d_partials);                                      \
+        }                                                                                     \
+        TimedLaunch timed(plan, ECC_TIMING_MF_GRAD);                                          \
         hipLaunchKernelGGL(k_mf_grad<R>, dim3(h->grad_grid), dim3(kMfThreads), 0, s, v,       \
                            h->d_err, h->d_perm, h->d_rp, n_rows, d_grads);                    \
-        break;
+        break;                                                                                \
+    }
     switch (h->rank) {
         ECC_MF_RANKS(ECC_MF_LAUNCH)
         default:
@@ -289,13 +294,15 @@ ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam,
 #undef ECC_MF_LAUNCH
 #undef ECC_MF_RANKS
     ECC_LAUNCH_CHECK();
-    hipLaunchKernelGGL(k_mf_rmse, dim3(1), dim3(kNormThreads), 0, s, h->d_partials,
-                       (int64_t)h->err_grid, h->N, d_rmse);
-    ECC_LAUNCH_CHECK();
     st = ecc_allreduce_partial(plan, m, d_grads, d_slots, d_G, d_arrived, d_eff_out, nullptr);
     if (st != ECC_OK) return st;
-    hipLaunchKernelGGL(k_mf_step, dim3(h->step_grid), dim3(kMfThreads), 0, s, m, log2r, eta,
-                       2.0 * lam, d_G, h->d_scale, d_W);
+    {
+        TimedLaunch timed(plan, ECC_TIMING_MF_STEP);
+        hipLaunchKernelGGL(k_mf_rmse, dim3(1), dim3(kNormThreads), 0, s, h->d_partials,
+                           (int64_t)h->err_grid, h->N, d_rmse);
+        hipLaunchKernelGGL(k_mf_step, dim3(h->step_grid), dim3(kMfThreads), 0, s, m, log2r, eta,
+                           2.0 * lam, d_G, h->d_scale, d_W);
+    }
     ECC_LAUNCH_CHECK();
     return ECC_OK;
 }

@@ -276,9 +276,9 @@ ecc_status_t ecc_plan_timing(ecc_plan_t plan, int32_t kernel, double *total_ms,
     clear_error();
     ecc_status_t st = check_plan(plan);
     if (st != ECC_OK) return st;
-    ECC_ARG(kernel >= 0 && kernel < 4, "unknown kernel %d", kernel);
+    ECC_ARG(kernel >= 0 && kernel < ECC_TIMING_KINDS, "unknown kernel %d", kernel);
     ECC_HIP(hipStreamSynchronize(plan->stream));
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < ECC_TIMING_KINDS; ++k) {
         for (auto &pr : plan->pending[k]) {
             float ms = 0.f;
             ECC_HIP(hipEventElapsedTime(&ms, pr.first, pr.second));

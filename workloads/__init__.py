@@ -538,7 +538,7 @@ def _zipf_pick(seed: int, stream: int, n_draws: int, n: int, s: float) -> np.nda
 
 def mf_problem(n_users: int = 160_000, n_items: int = 60_000, n_ratings: int = 25_000_000,
                rank: int = 16, P: int = 32, S: int = 2, q: float = 0.8, T: int = 100,
-               eta: float = 0.5, lam: float = 1e-4, true_rank: int = 8, seed: int = None
+               eta: float = 1.0, lam: float = 1e-4, true_rank: int = 8, seed: int = None
                ) -> MFProblem:
     """Synthetic ratings shaped like a large movie-rating set (25M ratings;
     Zipf user activity, exponent 0.5, and item popularity, exponent 0.6):
