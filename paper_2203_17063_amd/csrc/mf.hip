@@ -58,10 +58,12 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_err(MfView v, double *__restr
 }
 
 // Row r of the gradient index: worker p = r / E, entity e = r % E (E =
-// n_users + n_items; users first).  Its ratings are perm[rp[r] .. rp[r+1]).
+// n_users + n_items; users first).  Its ratings are perm[rp[r] .. rp[r+1]),
+// and oidx holds, in the same order, the index of the other factor's row.
 template <int R>
 __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfView v, const double *__restrict__ err,
                                                         const int32_t *__restrict__ perm,
+                                                        const int32_t *__restrict__ oidx,
                                                         const int32_t *__restrict__ rp,
                                                         int64_t n_rows,
                                                         double *const *__restrict__ grads) {
@@ -75,7 +77,6 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfView v, const double *
         const int64_t e = row - (int64_t)p * E;
         const bool user = e < v.n_users;
         const double *other = user ? V : U;
-        const int32_t *idx = user ? v.items : v.users;
         const int32_t a = rp[row], b = rp[row + 1];
         double acc = 0.0;
         int32_t x = a;
@@ -88,14 +89,14 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfView v, const double *
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 t[u] = -2.0 * err[k[u]];
-                o[u] = other[(int64_t)idx[k[u]] * R + lane];
+                o[u] = other[(int64_t)oidx[x + u] * R + lane];
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u) acc = acc + t[u] * o[u];
         }
         for (; x < b; ++x) {
             const int32_t k = perm[x];
-            acc = acc + (-2.0 * err[k]) * other[(int64_t)idx[k] * R + lane];
+            acc = acc + (-2.0 * err[k]) * other[(int64_t)oidx[x] * R + lane];
         }
         grads[p][e * R + lane] = acc;
     }
@@ -140,6 +141,7 @@ struct ecc_mf_s {
     const double *d_ratings = nullptr;
     double *d_err = nullptr;        // [N]
     int32_t *d_perm = nullptr;      // [2N]
+    int32_t *d_oidx = nullptr;      // [2N] other factor's row of perm[x]
     int32_t *d_rp = nullptr;        // [P * (n_users + n_items) + 1]
     double *d_scale = nullptr;      // [n_users + n_items]
     double *d_partials = nullptr;   // [err_grid]
@@ -153,6 +155,7 @@ ecc_status_t ecc_mf_destroy(ecc_mf_t h) {
     (void)hipDeviceSynchronize();
     (void)hipFree(h->d_err);
     (void)hipFree(h->d_perm);
+    (void)hipFree(h->d_oidx);
     (void)hipFree(h->d_rp);
     (void)hipFree(h->d_scale);
     (void)hipFree(h->d_partials);
@@ -212,6 +215,13 @@ ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32
         }
     }
     rp[n_rows] = (int32_t)pos;
+    std::vector<int32_t> oidx(2 * N);
+    for (int32_t p = 0; p < P; ++p) {
+        const int64_t base = (int64_t)p * E;
+        for (int64_t e = 0; e < E; ++e)
+            for (int32_t x = rp[base + e]; x < rp[base + e + 1]; ++x)
+                oidx[x] = e < n_users ? items[perm[x]] : users[perm[x]];
+    }
     std::vector<double> scale(E);
     for (int64_t e = 0; e < E; ++e) scale[e] = 1.0 / (double)std::max<int64_t>(1, cnt[e]);
 
@@ -238,11 +248,14 @@ ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32
     };
     if (hipMalloc((void **)&h->d_err, sizeof(double) * N) != hipSuccess ||
         hipMalloc((void **)&h->d_perm, sizeof(int32_t) * 2 * N) != hipSuccess ||
+        hipMalloc((void **)&h->d_oidx, sizeof(int32_t) * 2 * N) != hipSuccess ||
         hipMalloc((void **)&h->d_rp, sizeof(int32_t) * (n_rows + 1)) != hipSuccess ||
         hipMalloc((void **)&h->d_scale, sizeof(double) * E) != hipSuccess ||
         hipMalloc((void **)&h->d_partials, sizeof(double) * h->err_grid) != hipSuccess)
         return fail("hipMalloc of the factorisation state failed");
     if (hipMemcpy(h->d_perm, perm.data(), sizeof(int32_t) * 2 * N, hipMemcpyHostToDevice) !=
+            hipSuccess ||
+        hipMemcpy(h->d_oidx, oidx.data(), sizeof(int32_t) * 2 * N, hipMemcpyHostToDevice) !=
             hipSuccess ||
         hipMemcpy(h->d_rp, rp.data(), sizeof(int32_t) * (n_rows + 1), hipMemcpyHostToDevice) !=
             hipSuccess ||
@@ -282,7 +295,7 @@ ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam,
         }                                                                                     \
         TimedLaunch timed(plan, ECC_TIMING_MF_GRAD);                                          \
         hipLaunchKernelGGL(k_mf_grad<R>, dim3(h->grad_grid), dim3(kMfThreads), 0, s, v,       \
-                           h->d_err, h->d_perm, h->d_rp, n_rows, d_grads);                    \
+                           h->d_err, h->d_perm, h->d_oidx, h->d_rp, n_rows, d_grads);         \
         break;                                                                                \
     }
     switch (h->rank) {

@@ -543,8 +543,8 @@ def mf_problem(n_users: int = 160_000, n_items: int = 60_000, n_ratings: int = 2
     """Synthetic ratings shaped like a large movie-rating set (25M ratings;
     Zipf user activity, exponent 0.5, and item popularity, exponent 0.6):
     half-star ratings in [0.5, 5] from a planted rank-`true_rank` model plus
-    noise, centred; uniformly shuffled into P equal shards; the model starts
-    at N(0, 0.1^2)."""
+    noise, centred; uniformly shuffled into P equal shards, each stored by
+    user then item; the model starts at N(0, 0.1^2)."""
     seed = seed_of(8) if seed is None else seed
     users = _zipf_pick(seed, STREAM_MF_USERS, n_ratings, n_users, 0.5)
     items = _zipf_pick(seed, STREAM_MF_ITEMS, n_ratings, n_items, 0.6)
@@ -555,6 +555,11 @@ def mf_problem(n_users: int = 160_000, n_items: int = 60_000, n_ratings: int = 2
                                                                          n_ratings)
     r = np.clip(np.round(raw * 2.0) / 2.0, 0.5, 5.0)
     ratings = r - r.mean()
+    # within each worker's shard, ratings are stored by user, then item
+    for p in range(P):
+        a, b = n_ratings * p // P, n_ratings * (p + 1) // P
+        o = np.lexsort((items[a:b], users[a:b]))
+        users[a:b], items[a:b], ratings[a:b] = users[a:b][o], items[a:b][o], ratings[a:b][o]
     W0 = 0.1 * normal(seed, STREAM_MF_INIT, (n_users + n_items) * rank)
     mask = arrival_mask(seed, T, np.full(P, q))
     return MFProblem(n_users, n_items, rank, P, users, items, ratings, W0, eta, lam, S, mask, T,
