@@ -304,6 +304,7 @@ struct ecc_matrix_s {
     int32_t grid = 1;               // workgroups of a sweep launch
     bool irregular = false;         // row lengths vary widely: row-list items
     int layout = 0;                 // kLayStream, kLayRows or kLayShort
+    int32_t short_r = ecc::kShortRow;  // short layout: entries per row the kernel holds (>= longest row)
     int64_t bandwidth = 0;          // max |col - row|
     int32_t *d_rowlist = nullptr;   // rows of the row-list items, by rank and length class
     double *d_partials = nullptr;   // internal partials of ecc_solve: 2 x (grid + 1)

@@ -39,11 +39,10 @@
 #ifndef ECC_STREAM_NT
 #define ECC_STREAM_NT 0
 #endif
-#ifndef ECC_GRID_PER_ITEM
-#define ECC_GRID_PER_ITEM 0
-#endif
-#ifndef ECC_WG0_IDLE
-#define ECC_WG0_IDLE 0
+// Largest CSR (bytes of col, val and row_ptr) that rows of 7 or 8 entries
+// sweep in the short-row layout.
+#ifndef ECC_SHORT_CSR_LIMIT
+#define ECC_SHORT_CSR_LIMIT (int64_t(1) << 29)
 #endif
 
 namespace ecc {
@@ -421,81 +420,37 @@ __device__ __forceinline__ double rows_compute(const WorkItem &it, const SweepAr
     return row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
 }
 
-// A run of at most kSweepThreads consecutive rows of one rank in a matrix
-// whose rows all hold at most kShortRow entries: one lane per row reads the
-// row's entries straight from memory (the lanes of a wave cover one
-// contiguous stretch of the CSR arrays) and sums them in CSR order.  No LDS
-// and no barrier, so the kernel keeps more waves in flight.  rp0/rp1 are
-// the row's bounds, loaded ahead by the caller.
-template <int KIND, bool STEP>
-__device__ __forceinline__ double short_compute(const WorkItem &it, int32_t rp0, int32_t rp1,
-                                                const SweepArgs &a, const StepView &sv,
-                                                RankCache &rc, bool own_arrives) {
-    const int32_t rr = threadIdx.x;
-    if (rr >= it.nrows) return 0.0;
-    const int32_t i = it.row0 + rr;
-    const double xo = a.x_own[i];
-    const double bi = (KIND == ECC_KIND_JACOBI) ? ld_stream(a.b + i) : 0.0;
-    double s = 0.0, dg = 0.0;
-    short_row<KIND, STEP>(i, rp0, rp1, a, it.lo, it.hi, sv, rc, s, dg);
-    if (STEP && own_arrives) a.x_hat[i] = xo;
-    return row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
-}
-
-// LAY selects the layout: stream items staged through LDS (kLayStream),
-// row-list items for matrices with very uneven rows (kLayRows) -- both may
-// contain vector items and pieces -- or short-row items (kLayShort).
-template <int KIND, bool STEP, int LAY>
-__device__ __forceinline__ void sweep_body(const SweepArgs &a) {
-    constexpr bool STAGED = LAY == kLayStream;
-    // padded by 8 so that a row's first eight entries can be read unclamped
-    __shared__ int32_t s_col[STAGED ? kStreamCap + 8 : 1];
-    __shared__ double s_val[STAGED ? kStreamCap + 8 : 1];
-    __shared__ double s_red[kSweepThreads / 64];
-    __shared__ uint8_t s_eff[STEP ? kFusedMaxP : 1];
-    __shared__ int32_t s_bs[STEP ? kFusedMaxP + 1 : 1];
-    if (a.done && *a.done) return;
-    const int tid = threadIdx.x;
+// Items a workgroup walks: w_first, w_first + w_step, ... below i_end.
+// XCD-aware order: workgroups are dispatched round-robin over the 8 XCDs
+// (blockIdx mod 8).  The items are split into 8 contiguous ranges, one per
+// XCD, and the XCD's workgroups walk its range together, so each XCD's L2
+// sees consecutive rows and their neighbours.  Matrices with very uneven
+// rows deal items round-robin instead, so that the heavy items (listed
+// first) spread over every XCD.
+__device__ __forceinline__ void item_walk(const SweepArgs &a, int64_t &i_end, int32_t &w_first,
+                                          int32_t &w_step) {
     const int32_t G = gridDim.x;
-    // XCD-aware order: workgroups are dispatched round-robin over the 8 XCDs
-    // (blockIdx mod 8).  The items are split into 8 contiguous ranges, one
-    // per XCD, and the XCD's workgroups walk its range together, so each
-    // XCD's L2 sees consecutive rows and their neighbours.  Matrices with
-    // very uneven rows deal items round-robin instead, so that the heavy
-    // items (listed first) spread over every XCD.
-    int64_t i_begin = 0, i_end = a.n_items;
-    int32_t w_first = blockIdx.x, w_step = G;
+    i_end = a.n_items;
+    w_first = blockIdx.x;
+    w_step = G;
     if (!a.interleave && G % 8 == 0 && G >= 8) {
         const int32_t xcd = blockIdx.x % 8;
-        i_begin = (int64_t)a.n_items * xcd / 8;
+        const int64_t i_begin = (int64_t)a.n_items * xcd / 8;
         i_end = (int64_t)a.n_items * (xcd + 1) / 8;
         w_first = (int32_t)(i_begin + blockIdx.x / 8);
         w_step = G / 8;
-#if ECC_WG0_IDLE
-        if (xcd == 0 && G / 8 >= 2) {
-            w_first = blockIdx.x == 0 ? (int32_t)i_end : (int32_t)(i_begin + blockIdx.x / 8 - 1);
-            w_step = G / 8 - 1;
-        }
-#endif
     }
-    // the first item's loads go out before the prologue below
-    int32_t w = w_first;
-    WorkItem cur{}, nxt{};
-    StreamPrefetch pf;
-    const bool have0 = w < i_end;
-    int32_t rp0 = 0, rp1 = 0;  // short layout: this thread's row bounds in the current item
-    if (have0) {
-        cur = a.items[w];
-        if (STAGED && cur.kind == kItemStream) stream_load<KIND>(cur, a, pf);
-        if (LAY == kLayShort && (int32_t)tid < cur.nrows) {
-            rp0 = a.row_ptr[cur.row0 + tid];
-            rp1 = a.row_ptr[cur.row0 + tid + 1];
-        }
-    }
-    bool have_next = (int64_t)w + w_step < i_end;
-    if (have_next) nxt = a.items[w + w_step];
+}
 
-    StepView sv{s_eff, s_bs, a.P};
+// Work every workgroup does before its items: a fused step stages this
+// step's arrival decision and the block starts in LDS (workgroup 0 also
+// records the step's versions, ages and forced arrivals); workgroup 0 zeroes
+// partial G and reduces the previous loop iteration's partials.
+template <bool STEP>
+__device__ __forceinline__ void sweep_prologue(const SweepArgs &a, uint8_t *s_eff, int32_t *s_bs,
+                                               double *s_red) {
+    const int tid = threadIdx.x;
+    const int32_t G = gridDim.x;
     if constexpr (STEP) {
         for (int32_t p = tid; p < a.P; p += kSweepThreads)
             s_eff[p] = stale_select(a.ver_in[p], a.arrived[p], a.t, a.S) ? 1 : 0;
@@ -515,6 +470,39 @@ __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
         }
     }
     if constexpr (STEP) __syncthreads();
+}
+
+// LAY selects the layout: stream items staged through LDS (kLayStream) or
+// row-list items for matrices with very uneven rows (kLayRows); both may
+// contain vector items and pieces.  The short-row layout has its own body.
+template <int KIND, bool STEP, int LAY>
+__device__ __forceinline__ void sweep_body(const SweepArgs &a) {
+    constexpr bool STAGED = LAY == kLayStream;
+    // padded by 8 so that a row's first eight entries can be read unclamped
+    __shared__ int32_t s_col[STAGED ? kStreamCap + 8 : 1];
+    __shared__ double s_val[STAGED ? kStreamCap + 8 : 1];
+    __shared__ double s_red[kSweepThreads / 64];
+    __shared__ uint8_t s_eff[STEP ? kFusedMaxP : 1];
+    __shared__ int32_t s_bs[STEP ? kFusedMaxP + 1 : 1];
+    if (a.done && *a.done) return;
+    const int tid = threadIdx.x;
+    int64_t i_end;
+    int32_t w_first, w_step;
+    item_walk(a, i_end, w_first, w_step);
+    // the first item's loads go out before the prologue below
+    int32_t w = w_first;
+    WorkItem cur{}, nxt{};
+    StreamPrefetch pf;
+    const bool have0 = w < i_end;
+    if (have0) {
+        cur = a.items[w];
+        if (STAGED && cur.kind == kItemStream) stream_load<KIND>(cur, a, pf);
+    }
+    bool have_next = (int64_t)w + w_step < i_end;
+    if (have_next) nxt = a.items[w + w_step];
+
+    StepView sv{s_eff, s_bs, a.P};
+    sweep_prologue<STEP>(a, s_eff, s_bs, s_red);
 
     // Software pipeline over this workgroup's items: while an item is computed
     // from LDS, the loads of the next one (and the descriptor of the one
@@ -527,18 +515,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
         const bool next_stream = STAGED && have_next && nxt.kind == kItemStream;
         WorkItem nn{};
         const bool have_nn = (int64_t)w + 2 * (int64_t)w_step < i_end;
-        if (LAY == kLayShort) {
-            // the next item's row bounds are in flight while this one is summed
-            int32_t np0 = 0, np1 = 0;
-            if (have_next && (int32_t)tid < nxt.nrows) {
-                np0 = a.row_ptr[nxt.row0 + tid];
-                np1 = a.row_ptr[nxt.row0 + tid + 1];
-            }
-            if (have_nn) nn = a.items[w + 2 * w_step];
-            contrib += short_compute<KIND, STEP>(cur, rp0, rp1, a, sv, rc, own_arrives);
-            rp0 = np0;
-            rp1 = np1;
-        } else if (STAGED && cur.kind == kItemStream) {
+        if (STAGED && cur.kind == kItemStream) {
             stream_stage(cur, pf, s_col, s_val);
             const int32_t rp0 = pf.rp0, rp1 = pf.rp1;
             const double bi = pf.bi, xo = pf.xo;
@@ -573,15 +550,136 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
     sweep_body<KIND, STEP, LAY>(a);
 }
 
+// Entries of one short row, at most R of them (R >= the matrix's longest
+// row), loaded an item ahead of their use.
+template <int R>
+struct ShortEntries {
+    int32_t c[R];
+    double v[R];
+    int32_t len;
+};
+
+template <int R>
+__device__ __forceinline__ void short_entries(const SweepArgs &a, int32_t ks, int32_t ke,
+                                              ShortEntries<R> &e) {
+    e.len = ke - ks;
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+        e.c[j] = (j < e.len) ? ld_stream(a.col + ks + j) : 0;
+        e.v[j] = (j < e.len) ? ld_stream(a.val + ks + j) : 0.0;
+    }
+}
+
+// Short-row layout, one lane per row, as a three-deep pipeline over the
+// workgroup's items: while the gathers of item n are in flight, the entries
+// of item n + 1 (whose row bounds arrived during item n - 1) and the row
+// bounds of item n + 2 are loaded.  A lane's row then waits on one memory
+// latency per item instead of three (bounds, entries, gathers).
+template <int KIND, bool STEP, int R>
+__device__ __forceinline__ void short_body(const SweepArgs &a) {
+    __shared__ double s_red[kSweepThreads / 64];
+    __shared__ uint8_t s_eff[STEP ? kFusedMaxP : 1];
+    __shared__ int32_t s_bs[STEP ? kFusedMaxP + 1 : 1];
+    if (a.done && *a.done) return;
+    const int tid = threadIdx.x;
+    int64_t i_end;
+    int32_t w, w_step;
+    item_walk(a, i_end, w, w_step);
+    bool have = w < i_end;
+    bool have_next = have && (int64_t)w + w_step < i_end;
+    bool have_nn = have_next && (int64_t)w + 2 * (int64_t)w_step < i_end;
+    WorkItem cur{}, nxt{}, nn{};
+    ShortEntries<R> E;
+    E.len = 0;
+    int32_t np0 = 0, np1 = 0;  // row bounds of this lane's row in `nxt`
+    if (have) {
+        cur = a.items[w];
+        int32_t r0 = 0, r1 = 0;
+        if (tid < cur.nrows) {
+            r0 = a.row_ptr[cur.row0 + tid];
+            r1 = a.row_ptr[cur.row0 + tid + 1];
+        }
+        short_entries<R>(a, r0, r1, E);
+    }
+    if (have_next) {
+        nxt = a.items[w + w_step];
+        if (tid < nxt.nrows) {
+            np0 = a.row_ptr[nxt.row0 + tid];
+            np1 = a.row_ptr[nxt.row0 + tid + 1];
+        }
+    }
+    if (have_nn) nn = a.items[w + 2 * w_step];
+    StepView sv{s_eff, s_bs, a.P};
+    sweep_prologue<STEP>(a, s_eff, s_bs, s_red);
+
+    double contrib = 0.0;
+    RankCache rc;
+    while (have) {
+        const bool have_n3 = have_nn && (int64_t)w + 3 * (int64_t)w_step < i_end;
+        WorkItem n3{};
+        if (have_n3) n3 = a.items[w + 3 * w_step];
+        const bool live = tid < cur.nrows;
+        const int32_t i = cur.row0 + tid;
+        // this item's gathers first, then the loads for the next two items
+        double y[R];
+#pragma unroll
+        for (int j = 0; j < R; ++j)
+            y[j] = (j < E.len) ? view_load<STEP>(E.c[j], cur.lo, cur.hi, a.x_own, a.x_hat, sv, rc)
+                               : 0.0;
+        double xo = 0.0, bi = 0.0;
+        if (live) {
+            xo = a.x_own[i];
+            if (KIND == ECC_KIND_JACOBI) bi = ld_stream(a.b + i);
+        }
+        ShortEntries<R> En;
+        En.len = 0;
+        if (have_next) short_entries<R>(a, np0, np1, En);
+        int32_t q0 = 0, q1 = 0;
+        if (have_nn && tid < nn.nrows) {
+            q0 = a.row_ptr[nn.row0 + tid];
+            q1 = a.row_ptr[nn.row0 + tid + 1];
+        }
+        if (live) {
+            double s = 0.0, dg = 0.0;
+#pragma unroll
+            for (int j = 0; j < R; ++j) {
+                if (j < E.len) {
+                    if (KIND == ECC_KIND_JACOBI && E.c[j] == i) dg = E.v[j];
+                    else s = s + E.v[j] * y[j];
+                }
+            }
+            if (STEP && s_eff[cur.rank] != 0) a.x_hat[i] = xo;
+            contrib += row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+        }
+        w += w_step;
+        have = have_next;
+        have_next = have_nn;
+        have_nn = have_n3;
+        cur = nxt;
+        nxt = nn;
+        nn = n3;
+        E = En;
+        np0 = q0;
+        np1 = q1;
+    }
+    const double total = block_sum<kSweepThreads>(contrib, s_red);
+    if (tid == 0) a.partials[blockIdx.x] = total;
+}
+
 // The short-row layout holds few values per lane: the register budget is
-// capped so that ECC_SHORT_WAVES waves share each SIMD.
-#ifndef ECC_SHORT_WAVES
-#define ECC_SHORT_WAVES 6
+// capped so that several waves share each SIMD -- as many as the row's
+// registers allow without spilling.
+#ifndef ECC_SHORT_WAVES5
+#define ECC_SHORT_WAVES5 5
 #endif
-template <int KIND, bool STEP>
-__global__ __launch_bounds__(kSweepThreads) __attribute__((amdgpu_waves_per_eu(ECC_SHORT_WAVES)))
+template <int R>
+constexpr int short_waves() {
+    return R <= 3 ? 8 : (R == 4 ? 7 : (R == 5 ? ECC_SHORT_WAVES5 : 4));
+}
+template <int KIND, bool STEP, int R>
+__global__ __launch_bounds__(kSweepThreads) __attribute__((amdgpu_waves_per_eu(short_waves<R>())))
 void k_sweep_short(SweepArgs a) {
-    sweep_body<KIND, STEP, kLayShort>(a);
+    short_body<KIND, STEP, R>(a);
 }
 
 // Second pass of a sweep, one workgroup of kNormThreads.  (1) Rows split into
@@ -797,36 +895,49 @@ static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_
 // item, rounded down to a multiple of the 8 XCDs.
 template <int LAY>
 static hipError_t sweep_occupancy(int *per_cu, int kind) {
-    if constexpr (LAY == kLayShort)
-        return kind == ECC_KIND_JACOBI
-                   ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                         per_cu, k_sweep_short<ECC_KIND_JACOBI, true>, kSweepThreads, 0)
-                   : hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                         per_cu, k_sweep_short<ECC_KIND_POWER, true>, kSweepThreads, 0);
-    else
-        return kind == ECC_KIND_JACOBI
-                   ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                         per_cu, k_sweep<ECC_KIND_JACOBI, true, LAY>, kSweepThreads, 0)
-                   : hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                         per_cu, k_sweep<ECC_KIND_POWER, true, LAY>, kSweepThreads, 0);
+    return kind == ECC_KIND_JACOBI
+               ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                     per_cu, k_sweep<ECC_KIND_JACOBI, true, LAY>, kSweepThreads, 0)
+               : hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                     per_cu, k_sweep<ECC_KIND_POWER, true, LAY>, kSweepThreads, 0);
 }
 
-static int32_t sweep_grid(int64_t n_items, int kind, int layout) {
+template <int R>
+static hipError_t short_occupancy_r(int *per_cu, int kind) {
+    return kind == ECC_KIND_JACOBI
+               ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                     per_cu, k_sweep_short<ECC_KIND_JACOBI, true, R>, kSweepThreads, 0)
+               : hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                     per_cu, k_sweep_short<ECC_KIND_POWER, true, R>, kSweepThreads, 0);
+}
+
+// Entries per row of the short-layout kernel that serves rows of at most
+// `max_row` entries (the launch below uses the same classes).
+static int short_class(int32_t max_row) {
+    return max_row <= 3 ? 3 : max_row == 4 ? 4 : max_row == 5 ? 5 : max_row <= 7 ? 7 : 8;
+}
+
+static hipError_t short_occupancy(int *per_cu, int kind, int32_t short_r) {
+    switch (short_class(short_r)) {
+        case 3: return short_occupancy_r<3>(per_cu, kind);
+        case 4: return short_occupancy_r<4>(per_cu, kind);
+        case 5: return short_occupancy_r<5>(per_cu, kind);
+        case 7: return short_occupancy_r<7>(per_cu, kind);
+        default: return short_occupancy_r<8>(per_cu, kind);
+    }
+}
+
+static int32_t sweep_grid(int64_t n_items, int kind, int layout, int32_t short_r) {
     int dev = 0, cus = 0, per_cu = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         cus = 256;
     const hipError_t e = layout == kLayRows    ? sweep_occupancy<kLayRows>(&per_cu, kind)
-                         : layout == kLayShort ? sweep_occupancy<kLayShort>(&per_cu, kind)
+                         : layout == kLayShort ? short_occupancy(&per_cu, kind, short_r)
                                                : sweep_occupancy<kLayStream>(&per_cu, kind);
     if (e != hipSuccess || per_cu < 1) per_cu = 4;
     const int64_t resident = (int64_t)std::max(cus, 1) * per_cu;
-#if ECC_GRID_PER_ITEM
-    (void)resident;
-    int64_t g = std::max<int64_t>(1, std::min<int64_t>(n_items, (int64_t)1 << 20));
-#else
     int64_t g = std::max<int64_t>(1, std::min<int64_t>({n_items, resident, (int64_t)kMaxSweepBlocks}));
-#endif
     if (g >= 8) g -= g % 8;
     return (int32_t)g;
 }
@@ -880,12 +991,20 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     hipStream_t st = pl->stream;
 #define ECC_SWEEP_LAUNCH(K, S, R) \
     hipLaunchKernelGGL((k_sweep<K, S, R>), grid, block, 0, st, a)
+#define ECC_SHORT_LAUNCH(K, S, R) \
+    hipLaunchKernelGGL((k_sweep_short<K, S, R>), grid, block, 0, st, a)
 #define ECC_SWEEP_LAYOUTS(K, S)                                        \
     do {                                                               \
         if (M->layout == kLayRows) ECC_SWEEP_LAUNCH(K, S, kLayRows);   \
-        else if (M->layout == kLayShort)                               \
-            hipLaunchKernelGGL((k_sweep_short<K, S>), grid, block, 0, st, a); \
-        else ECC_SWEEP_LAUNCH(K, S, kLayStream);                       \
+        else if (M->layout == kLayShort) {                             \
+            switch (short_class(M->short_r)) {                         \
+                case 3: ECC_SHORT_LAUNCH(K, S, 3); break;              \
+                case 4: ECC_SHORT_LAUNCH(K, S, 4); break;              \
+                case 5: ECC_SHORT_LAUNCH(K, S, 5); break;              \
+                case 7: ECC_SHORT_LAUNCH(K, S, 7); break;              \
+                default: ECC_SHORT_LAUNCH(K, S, 8); break;             \
+            }                                                          \
+        } else ECC_SWEEP_LAUNCH(K, S, kLayStream);                     \
     } while (0)
     if (M->kind == ECC_KIND_JACOBI) {
         if (step) ECC_SWEEP_LAYOUTS(ECC_KIND_JACOBI, true);
@@ -895,6 +1014,7 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
         else ECC_SWEEP_LAYOUTS(ECC_KIND_POWER, false);
     }
 #undef ECC_SWEEP_LAYOUTS
+#undef ECC_SHORT_LAUNCH
 #undef ECC_SWEEP_LAUNCH
     ECC_LAUNCH_CHECK();
     if (step) pl->clock += 1;
@@ -1014,7 +1134,7 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     for (int64_t i = 0; i < n; ++i) max_row = std::max(max_row, rp[i + 1] - rp[i]);
     const int64_t csr_bytes = 12 * (int64_t)A->nnz + 4 * (n + 1);
     const bool short_rows =
-        max_row <= kShortRow && (max_row <= 6 || csr_bytes <= (int64_t(1) << 29));
+        max_row <= kShortRow && (max_row <= 6 || csr_bytes <= (int64_t)ECC_SHORT_CSR_LIMIT);
     const int layout = irregular ? kLayRows : (short_rows ? kLayShort : kLayStream);
     build_items(rp, plan->counts, irregular, items, fixups, rowlist, n_pieces);
     if ((int64_t)items.size() >= (int64_t(1) << 31)) {
@@ -1035,8 +1155,9 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     M->n_pieces = n_pieces;
     M->irregular = irregular;
     M->layout = layout;
+    M->short_r = std::max(1, max_row);
     M->bandwidth = bandwidth;
-    M->grid = sweep_grid(M->n_items, kind, layout);
+    M->grid = sweep_grid(M->n_items, kind, layout, M->short_r);
     auto fail = [&](const char *what) {
         set_error("%s", what);
         ecc_matrix_destroy(M);
