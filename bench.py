@@ -412,8 +412,9 @@ def mf_bytes(prob, arrivals):
     """Algorithmic bytes of one factorisation iteration, per kernel."""
     N, m, P = prob.N, prob.m, prob.P
     rows = prob.n_users + prob.n_items
-    return {"MF_ERROR": 24.0 * N + 8.0 * m,                       # u, i, r read, e written, model
-            "MF_GRAD": 32.0 * N + 8.0 * m + 8.0 * m * P,           # 2 x (perm, e, index), model, P gradients
+    return {"MF_GRAD": 24.0 * N + 12.0 * P * rows + 8.0 * m + 8.0 * m * P,
+            # 2 x (other row, rating) per rating, (row, start, length) per
+            # (worker, row), the model, P gradients written
             "ALLREDUCE": 8.0 * m * (P + arrivals + 1),
             "MF_STEP": 24.0 * m + 8.0 * rows}
 
@@ -446,8 +447,8 @@ def run_mf_gpu(prob, steps, warmup):
     wall = time.perf_counter() - t0
     ph = run.plan.handle
     E.ecc_plan_set_timing(ph, True)
-    kinds = {"MF_ERROR": E.ECC_TIMING_MF_ERROR, "MF_GRAD": E.ECC_TIMING_MF_GRAD,
-             "ALLREDUCE": E.ECC_TIMING_ALLREDUCE, "MF_STEP": E.ECC_TIMING_MF_STEP}
+    kinds = {"MF_GRAD": E.ECC_TIMING_MF_GRAD, "ALLREDUCE": E.ECC_TIMING_ALLREDUCE,
+             "MF_STEP": E.ECC_TIMING_MF_STEP}
     for k in kinds.values():
         E.ecc_plan_timing(ph, k, reset=True)
     torch.cuda.synchronize()
@@ -537,9 +538,9 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
         e[a:b] = MFO.errors(prob, prob.W0, a, b)
         MFO.worker_gradient(prob, prob.W0, e, 0)
         dt = time.perf_counter() - t0
-        per = mf_bytes(prob, prob.P)
-        sample_bytes = (per["MF_ERROR"] - 8.0 * prob.m) / prob.P + \
-            (per["MF_GRAD"] - 8.0 * prob.m * (prob.P - 1)) / prob.P
+        # worker 0's share of the index and ratings, the model read, its gradient written
+        rows = prob.n_users + prob.n_items
+        sample_bytes = (24.0 * prob.N + 12.0 * prob.P * rows) / prob.P + 16.0 * prob.m
         return {"value": round(sample_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
                 "kind": "oracle", "sample": "worker 0's errors and gradient at iteration 0 "
                                             "(1/%d of the ratings), 1 thread, %.1f s" % (prob.P, dt)}

@@ -134,10 +134,9 @@ ecc_status_t ecc_plan_stats(ecc_plan_t plan, int64_t *clock, int64_t *forced_tot
 #define ECC_TIMING_ALLREDUCE 1  /* partial allreduce             */
 #define ECC_TIMING_SWEEP 2      /* Jacobi / power-iteration sweep */
 #define ECC_TIMING_NORM 3       /* split-row fix-up + norm pass  */
-#define ECC_TIMING_MF_ERROR 4   /* factorisation: rating errors   */
-#define ECC_TIMING_MF_GRAD 5    /* factorisation: worker gradients */
-#define ECC_TIMING_MF_STEP 6    /* factorisation: model step + RMSE */
-#define ECC_TIMING_KINDS 7
+#define ECC_TIMING_MF_GRAD 4    /* factorisation: errors + worker gradients */
+#define ECC_TIMING_MF_STEP 5    /* factorisation: model step + RMSE */
+#define ECC_TIMING_KINDS 6
 ecc_status_t ecc_plan_set_timing(ecc_plan_t plan, int32_t enable);
 ecc_status_t ecc_plan_timing(ecc_plan_t plan, int32_t kernel, double *total_ms,
                              int64_t *launches, int32_t reset);

@@ -4,20 +4,36 @@
 // and a replica of the model W = [U; V] (rows of `rank` doubles).
 //
 // One iteration, enqueued on the plan's stream:
-//  (1) k_mf_err: e_k = r_k - U[u_k] . V[i_k] for every rating (products
-//      added for j = 0 .. rank-1 in order), and per-workgroup sums of e_k^2;
-//  (2) k_mf_grad: every worker's gradient of its shard's squared error --
-//      row (p, entity) accumulates (-2 e_k) times the other factor's row
-//      over the worker's ratings of that entity, in shard order; `rank`
-//      lanes per row, one per column; rows without ratings are written 0;
-//  (3) the partial allreduce of the workers' gradients (ecc_allreduce_partial:
+//  (1) k_mf_grad: every row (p, entity) of every worker's gradient of its
+//      shard's squared error.  For the worker's ratings of that entity, in
+//      shard order, the rating's error e_k = r_k - U[u_k] . V[i_k] (products
+//      added for j = 0 .. rank-1 in order) and then row += (-2 e_k) times the
+//      other factor's row; rows without ratings are 0.  The errors met in
+//      user rows (every rating lies in exactly one) also feed per-workgroup
+//      sums of e_k^2.
+//  (2) the partial allreduce of the workers' gradients (ecc_allreduce_partial:
 //      staleness decision, stale gradients substituted from the slots);
-//  (4) k_mf_step: W := W - eta * (G * c_row + 2 lam W), c_row = 1 / (number
-//      of ratings of the row, at least 1);
-//  (5) k_mf_rmse: sqrt(sum e_k^2 / N) from the workgroup sums in a fixed
-//      order.
-// The per-worker row index (ratings of each (worker, entity) row in shard
-// order) is built once, on the host, by counting sorts.
+//  (3) k_mf_rmse: sqrt(sum e_k^2 / N) from the workgroup sums in a fixed
+//      order; k_mf_step: W := W - eta * (G * c_row + 2 lam W), c_row = 1 /
+//      (number of ratings of the row, at least 1).
+//
+// The gradient index is built once, on the host: the ratings of each row in
+// shard order (other factor's row index and rating value, stored in that
+// order), and the rows sorted by their number of ratings, longest first.
+//  - A row of more than kMfHeavy ratings takes a whole workgroup: chunks of
+//    its ratings are spread over the workgroup, whose lane groups compute
+//    the errors and products into LDS, and then `rank` lanes add the
+//    products in shard order.  The longest rows (thousands of ratings for
+//    the most popular items) thus wait on a few memory latencies per chunk
+//    instead of a serial chain of loads per rating.
+//  - Other rows take a group of rank / 4 lanes (4 columns each; one lane
+//    for rank < 4), so a wave of rank 16 carries 16 rows of similar
+//    length (rows sorted by length); kMfBatch ratings' loads
+//    are in flight and the next batch's indices are loaded while one is
+//    summed; the next item's row descriptors are loaded one item ahead.
+// A rating's dot product is the running sum of the group's lanes in column
+// order, handed from lane to lane by shuffles, so errors and gradients are
+// the sequential definition's, bit for bit.
 #include <algorithm>
 #include <vector>
 
@@ -27,79 +43,209 @@ namespace ecc {
 
 constexpr int kMfThreads = 256;
 constexpr int kMfMaxRank = 64;
+constexpr int kMfHeavy = 128;   // rows with more ratings take a whole workgroup
+constexpr int kMfStage = 2048;  // doubles of LDS for one chunk of a heavy row
+constexpr int kMfBatch = 4;     // ratings of a light row in flight together
 
-struct MfView {
-    int32_t n_users, n_items;
-    int64_t N;
-    const int32_t *users, *items;
-    const double *ratings;
-    const double *W;  // [U; V]
+template <int R>
+struct MfShape {
+    static constexpr int C = R < 4 ? R : 4;               // columns per lane
+    static constexpr int LPR = R / C;                     // lanes per row
+    static constexpr int GROUPS = kMfThreads / LPR;       // rows of a light item
+    static constexpr int CHUNK = kMfStage / R;            // ratings of a heavy chunk
+    static constexpr int J = CHUNK / GROUPS > 0 ? CHUNK / GROUPS : 1;  // per group and chunk
 };
 
+struct MfGradArgs {
+    int32_t n_users;
+    int64_t E;                    // n_users + n_items
+    const double *W;              // [U; V]
+    const int32_t *oidx;          // [2N] other factor's row, ratings of each row in shard order
+    const double *rv;             // [2N] rating values, same order
+    const int32_t *row_of;        // [n_rows] rows (p * E + entity), longest first
+    const int32_t *start_of;      // [n_rows] first rating of that row in oidx / rv
+    const int32_t *len_of;        // [n_rows] its number of ratings
+    int64_t n_rows;
+    int64_t n_heavy;              // the first n_heavy rows take a workgroup each
+    int64_t n_work;               // n_heavy + light items of GROUPS rows
+    double *const *grads;         // [P] -> m doubles
+    double *partials;             // [gridDim.x] sums of e^2 over user rows
+};
+
+// own . other over a lane group: lane l holds columns l*C .. l*C + C-1 of
+// both rows; lane s continues the running sum of lane s - 1 (received by a
+// shuffle), so the products are added for j = 0 .. R-1 in order from +0.0.
 template <int R>
-__global__ __launch_bounds__(kMfThreads) void k_mf_err(MfView v, double *__restrict__ err,
-                                                       double *__restrict__ partials) {
-    __shared__ double s_red[kMfThreads / 64];
-    const double *U = v.W, *V = v.W + (int64_t)v.n_users * R;
-    double sq = 0.0;
-    const int64_t stride = (int64_t)gridDim.x * kMfThreads;
-    for (int64_t k = (int64_t)blockIdx.x * kMfThreads + threadIdx.x; k < v.N; k += stride) {
-        const double *ur = U + (int64_t)v.users[k] * R;
-        const double *vr = V + (int64_t)v.items[k] * R;
-        double acc = 0.0;
+__device__ __forceinline__ double mf_dot(const double (&ow)[MfShape<R>::C],
+                                         const double (&o)[MfShape<R>::C]) {
+    constexpr int LPR = MfShape<R>::LPR, C = MfShape<R>::C;
+    double d = 0.0;
 #pragma unroll
-        for (int j = 0; j < R; ++j) acc = acc + ur[j] * vr[j];
-        const double e = v.ratings[k] - acc;
-        err[k] = e;
-        sq = sq + e * e;
+    for (int s = 0; s < LPR; ++s) {
+        double v = d;
+#pragma unroll
+        for (int c = 0; c < C; ++c) v = v + ow[c] * o[c];
+        d = (LPR == 1) ? v : __shfl(v, s, LPR);
     }
-    const double tot = block_sum<kMfThreads>(sq, s_red);
-    if (threadIdx.x == 0) partials[blockIdx.x] = tot;
+    return d;
 }
 
-// Row r of the gradient index: worker p = r / E, entity e = r % E (E =
-// n_users + n_items; users first).  Its ratings are perm[rp[r] .. rp[r+1]),
-// and oidx holds, in the same order, the index of the other factor's row.
+// One light row on the lane group (lane = column block); returns the lane's
+// sum of e^2 (user rows, lane 0 only).
 template <int R>
-__global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfView v, const double *__restrict__ err,
-                                                        const int32_t *__restrict__ perm,
-                                                        const int32_t *__restrict__ oidx,
-                                                        const int32_t *__restrict__ rp,
-                                                        int64_t n_rows,
-                                                        double *const *__restrict__ grads) {
-    constexpr int ROWS = kMfThreads / R;  // rows per workgroup and pass
-    const int lane = threadIdx.x % R;
-    const int64_t E = (int64_t)v.n_users + v.n_items;
-    const double *U = v.W, *V = v.W + (int64_t)v.n_users * R;
-    for (int64_t row = (int64_t)blockIdx.x * ROWS + threadIdx.x / R; row < n_rows;
-         row += (int64_t)gridDim.x * ROWS) {
-        const int32_t p = (int32_t)(row / E);
-        const int64_t e = row - (int64_t)p * E;
-        const bool user = e < v.n_users;
-        const double *other = user ? V : U;
-        const int32_t a = rp[row], b = rp[row + 1];
-        double acc = 0.0;
-        int32_t x = a;
-        // four ratings' loads in flight, added in order
-        for (; x + 4 <= b; x += 4) {
-            int32_t k[4];
-            double t[4], o[4];
+__device__ __forceinline__ double mf_light_row(const MfGradArgs &a, int32_t row, int32_t x0,
+                                               int32_t len, int lane) {
+    constexpr int C = MfShape<R>::C, K = kMfBatch;
+    const int32_t p = (int32_t)(row / a.E);
+    const int64_t e = row - (int64_t)p * a.E;
+    const bool user = e < a.n_users;
+    const double *own = a.W + e * R + lane * C;
+    const double *other = (user ? a.W + (int64_t)a.n_users * R : a.W) + lane * C;
+    const int32_t x1 = x0 + len;
+    double acc[C], ow[C];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) k[u] = perm[x + u];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                t[u] = -2.0 * err[k[u]];
-                o[u] = other[(int64_t)oidx[x + u] * R + lane];
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) acc = acc + t[u] * o[u];
-        }
-        for (; x < b; ++x) {
-            const int32_t k = perm[x];
-            acc = acc + (-2.0 * err[k]) * other[(int64_t)oidx[x] * R + lane];
-        }
-        grads[p][e * R + lane] = acc;
+    for (int c = 0; c < C; ++c) {
+        acc[c] = 0.0;
+        ow[c] = len > 0 ? own[c] : 0.0;
     }
+    int32_t ki[K];
+    double kr[K];
+#pragma unroll
+    for (int u = 0; u < K; ++u) {
+        ki[u] = (x0 + u < x1) ? a.oidx[x0 + u] : 0;
+        kr[u] = (x0 + u < x1) ? a.rv[x0 + u] : 0.0;
+    }
+    double sq = 0.0;
+    for (int32_t x = x0; x < x1; x += K) {
+        double o[K][C], r[K];
+#pragma unroll
+        for (int u = 0; u < K; ++u) {
+            r[u] = kr[u];
+#pragma unroll
+            for (int c = 0; c < C; ++c)
+                o[u][c] = (x + u < x1) ? other[(int64_t)ki[u] * R + c] : 0.0;
+        }
+        const int32_t xn = x + K;
+#pragma unroll
+        for (int u = 0; u < K; ++u) {
+            ki[u] = (xn + u < x1) ? a.oidx[xn + u] : 0;
+            kr[u] = (xn + u < x1) ? a.rv[xn + u] : 0.0;
+        }
+#pragma unroll
+        for (int u = 0; u < K; ++u) {
+            if (x + u < x1) {
+                const double err = r[u] - mf_dot<R>(ow, o[u]);
+                const double t = -2.0 * err;
+#pragma unroll
+                for (int c = 0; c < C; ++c) acc[c] = acc[c] + t * o[u][c];
+                if (user) sq = sq + err * err;
+            }
+        }
+    }
+    double *g = a.grads[p] + e * R + lane * C;
+#pragma unroll
+    for (int c = 0; c < C; ++c) g[c] = acc[c];
+    return lane == 0 ? sq : 0.0;
+}
+
+// One heavy row on the whole workgroup; returns the thread's sum of e^2.
+template <int R>
+__device__ __forceinline__ double mf_heavy_row(const MfGradArgs &a, int32_t row, int32_t x0,
+                                               int32_t len, double *s_prod) {
+    constexpr int LPR = MfShape<R>::LPR, C = MfShape<R>::C, NG = MfShape<R>::GROUPS;
+    constexpr int CH = MfShape<R>::CHUNK, J = MfShape<R>::J;
+    const int tid = threadIdx.x, lane = tid % LPR, grp = tid / LPR;
+    const int32_t p = (int32_t)(row / a.E);
+    const int64_t e = row - (int64_t)p * a.E;
+    const bool user = e < a.n_users;
+    const double *own = a.W + e * R + lane * C;
+    const double *other = (user ? a.W + (int64_t)a.n_users * R : a.W) + lane * C;
+    double ow[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) ow[c] = own[c];
+    double acc = 0.0, sq = 0.0;
+    for (int32_t xb = 0; xb < len; xb += CH) {
+        const int32_t n = min(CH, len - xb);
+        // ratings grp, grp + NG, ... of the chunk: loads first, then products
+        int32_t ki[J];
+        double kr[J], o[J][C];
+#pragma unroll
+        for (int q = 0; q < J; ++q) {
+            const int32_t j = grp + q * NG;
+            ki[q] = j < n ? a.oidx[x0 + xb + j] : 0;
+            kr[q] = j < n ? a.rv[x0 + xb + j] : 0.0;
+        }
+#pragma unroll
+        for (int q = 0; q < J; ++q) {
+            const int32_t j = grp + q * NG;
+#pragma unroll
+            for (int c = 0; c < C; ++c)
+                o[q][c] = j < n ? other[(int64_t)ki[q] * R + c] : 0.0;
+        }
+#pragma unroll
+        for (int q = 0; q < J; ++q) {
+            const int32_t j = grp + q * NG;
+            if (j < n) {
+                const double err = kr[q] - mf_dot<R>(ow, o[q]);
+                const double t = -2.0 * err;
+#pragma unroll
+                for (int c = 0; c < C; ++c) s_prod[j * R + lane * C + c] = t * o[q][c];
+                if (user && lane == 0) sq = sq + err * err;
+            }
+        }
+        __syncthreads();
+        if (tid < R)
+            for (int32_t j = 0; j < n; ++j) acc = acc + s_prod[j * R + tid];
+        __syncthreads();
+    }
+    if (tid < R) a.grads[p][e * R + tid] = acc;
+    return sq;
+}
+
+template <int R>
+__global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfGradArgs a) {
+    __shared__ double s_prod[kMfStage];
+    __shared__ double s_red[kMfThreads / 64];
+    constexpr int LPR = MfShape<R>::LPR, G = MfShape<R>::GROUPS;
+    static_assert(MfShape<R>::CHUNK * R == kMfStage, "a heavy chunk fills the stage");
+    const int lane = threadIdx.x % LPR, grp = threadIdx.x / LPR;
+    double sq = 0.0;
+    // this lane group's row in a light item w (descriptors one item ahead)
+    auto light_q = [&](int64_t w) { return a.n_heavy + (w - a.n_heavy) * G + grp; };
+    int32_t nrow = 0, nx0 = 0, nlen = -1;
+    int64_t w = blockIdx.x;
+    if (w < a.n_work && w >= a.n_heavy && light_q(w) < a.n_rows) {
+        const int64_t q = light_q(w);
+        nrow = a.row_of[q];
+        nx0 = a.start_of[q];
+        nlen = a.len_of[q];
+    }
+    for (; w < a.n_work; w += gridDim.x) {
+        if (w < a.n_heavy) {
+            sq += mf_heavy_row<R>(a, a.row_of[w], a.start_of[w], a.len_of[w], s_prod);
+            const int64_t wn = w + gridDim.x;
+            nlen = -1;
+            if (wn < a.n_work && wn >= a.n_heavy && light_q(wn) < a.n_rows) {
+                const int64_t q = light_q(wn);
+                nrow = a.row_of[q];
+                nx0 = a.start_of[q];
+                nlen = a.len_of[q];
+            }
+            continue;
+        }
+        const int32_t row = nrow, x0 = nx0, len = nlen;
+        const int64_t wn = w + gridDim.x;
+        nlen = -1;
+        if (wn < a.n_work && light_q(wn) < a.n_rows) {
+            const int64_t q = light_q(wn);
+            nrow = a.row_of[q];
+            nx0 = a.start_of[q];
+            nlen = a.len_of[q];
+        }
+        if (len >= 0) sq += mf_light_row<R>(a, row, x0, len, lane);
+    }
+    const double tot = block_sum<kMfThreads>(sq, s_red);
+    if (threadIdx.x == 0) a.partials[blockIdx.x] = tot;
 }
 
 __global__ __launch_bounds__(kMfThreads) void k_mf_step(int64_t m, int log2r, double eta,
@@ -137,15 +283,15 @@ using namespace ecc;
 struct ecc_mf_s {
     int32_t n_users = 0, n_items = 0, rank = 0, P = 0;
     int64_t N = 0;
-    const int32_t *d_users = nullptr, *d_items = nullptr;
-    const double *d_ratings = nullptr;
-    double *d_err = nullptr;        // [N]
-    int32_t *d_perm = nullptr;      // [2N]
-    int32_t *d_oidx = nullptr;      // [2N] other factor's row of perm[x]
-    int32_t *d_rp = nullptr;        // [P * (n_users + n_items) + 1]
+    int32_t *d_oidx = nullptr;      // [2N] other factor's row, ratings of each row in shard order
+    double *d_rv = nullptr;         // [2N] rating values, same order
+    int32_t *d_row_of = nullptr;    // [P * (n_users + n_items)] rows, longest first
+    int32_t *d_start_of = nullptr;  // same order: first rating in d_oidx / d_rv
+    int32_t *d_len_of = nullptr;    // same order: number of ratings
+    int64_t n_heavy = 0;            // rows of more than kMfHeavy ratings
     double *d_scale = nullptr;      // [n_users + n_items]
-    double *d_partials = nullptr;   // [err_grid]
-    int32_t err_grid = 1, grad_grid = 1, step_grid = 1;
+    double *d_partials = nullptr;   // [grad_grid]
+    int32_t grad_grid = 1, step_grid = 1;
 };
 
 extern "C" {
@@ -153,10 +299,11 @@ extern "C" {
 ecc_status_t ecc_mf_destroy(ecc_mf_t h) {
     if (!h) return ECC_OK;
     (void)hipDeviceSynchronize();
-    (void)hipFree(h->d_err);
-    (void)hipFree(h->d_perm);
     (void)hipFree(h->d_oidx);
-    (void)hipFree(h->d_rp);
+    (void)hipFree(h->d_rv);
+    (void)hipFree(h->d_row_of);
+    (void)hipFree(h->d_start_of);
+    (void)hipFree(h->d_len_of);
     (void)hipFree(h->d_scale);
     (void)hipFree(h->d_partials);
     delete h;
@@ -182,8 +329,10 @@ ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32
         return ECC_ERR_RANGE;
     }
     std::vector<int32_t> users(N), items(N);
+    std::vector<double> ratings(N);
     ECC_HIP(hipMemcpy(users.data(), d_users, sizeof(int32_t) * N, hipMemcpyDeviceToHost));
     ECC_HIP(hipMemcpy(items.data(), d_items, sizeof(int32_t) * N, hipMemcpyDeviceToHost));
+    ECC_HIP(hipMemcpy(ratings.data(), d_ratings, sizeof(double) * N, hipMemcpyDeviceToHost));
     std::vector<int64_t> cnt(E, 0);
     for (int64_t k = 0; k < N; ++k) {
         ECC_ARG(users[k] >= 0 && users[k] < n_users, "users[%lld] out of range", (long long)k);
@@ -192,8 +341,9 @@ ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32
         ++cnt[(int64_t)n_users + items[k]];
     }
     // rows (p, entity): users then items of worker p; their ratings in shard
-    // order, user rows' in perm[2 a_p ...] and item rows' after them
-    std::vector<int32_t> rp(n_rows + 1, 0), perm(2 * N);
+    // order (counting sort), stored as the other factor's row and the value
+    std::vector<int32_t> rp(n_rows + 1, 0), oidx(2 * N);
+    std::vector<double> rv(2 * N);
     std::vector<int32_t> fill(E);
     int64_t pos = 0;
     for (int32_t p = 0; p < P; ++p) {
@@ -210,17 +360,41 @@ ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32
             fill[e] = rp[base + e];
         }
         for (int64_t k = a; k < b; ++k) {
-            perm[fill[users[k]]++] = (int32_t)k;
-            perm[fill[(int64_t)n_users + items[k]]++] = (int32_t)k;
+            const int32_t xu = fill[users[k]]++;
+            const int32_t xi = fill[(int64_t)n_users + items[k]]++;
+            oidx[xu] = items[k];
+            rv[xu] = ratings[k];
+            oidx[xi] = users[k];
+            rv[xi] = ratings[k];
         }
     }
     rp[n_rows] = (int32_t)pos;
-    std::vector<int32_t> oidx(2 * N);
-    for (int32_t p = 0; p < P; ++p) {
-        const int64_t base = (int64_t)p * E;
-        for (int64_t e = 0; e < E; ++e)
-            for (int32_t x = rp[base + e]; x < rp[base + e + 1]; ++x)
-                oidx[x] = e < n_users ? items[perm[x]] : users[perm[x]];
+    // rows by number of ratings, longest first (rows of equal length in row
+    // order): heavy rows by a sort, the rest by a counting sort
+    std::vector<int32_t> heavy, by_len(kMfHeavy + 2, 0);
+    for (int64_t r = 0; r < n_rows; ++r) {
+        const int32_t len = rp[r + 1] - rp[r];
+        if (len > kMfHeavy) heavy.push_back((int32_t)r);
+        else ++by_len[len];
+    }
+    std::stable_sort(heavy.begin(), heavy.end(), [&](int32_t x, int32_t y) {
+        return rp[x + 1] - rp[x] > rp[y + 1] - rp[y];
+    });
+    std::vector<int32_t> row_of(n_rows), start_of(n_rows), len_of(n_rows);
+    int64_t next = (int64_t)heavy.size();
+    std::vector<int64_t> slot(kMfHeavy + 1);
+    for (int32_t len = kMfHeavy; len >= 0; --len) {
+        slot[len] = next;
+        next += by_len[len];
+    }
+    for (size_t j = 0; j < heavy.size(); ++j) row_of[j] = heavy[j];
+    for (int64_t r = 0; r < n_rows; ++r) {
+        const int32_t len = rp[r + 1] - rp[r];
+        if (len <= kMfHeavy) row_of[slot[len]++] = (int32_t)r;
+    }
+    for (int64_t q = 0; q < n_rows; ++q) {
+        start_of[q] = rp[row_of[q]];
+        len_of[q] = rp[row_of[q] + 1] - rp[row_of[q]];
     }
     std::vector<double> scale(E);
     for (int64_t e = 0; e < E; ++e) scale[e] = 1.0 / (double)std::max<int64_t>(1, cnt[e]);
@@ -235,29 +409,33 @@ ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32
     h->rank = rank;
     h->P = P;
     h->N = N;
-    h->d_users = d_users;
-    h->d_items = d_items;
-    h->d_ratings = d_ratings;
-    h->err_grid = mf_grid((N + kMfThreads - 1) / kMfThreads, 8);
-    h->grad_grid = mf_grid((n_rows + kMfThreads / rank - 1) / (kMfThreads / rank), 8);
+    h->n_heavy = (int64_t)heavy.size();
+    const int64_t groups = kMfThreads / (rank < 4 ? 1 : rank / 4);
+    const int64_t n_work = h->n_heavy + (n_rows - h->n_heavy + groups - 1) / groups;
+    h->grad_grid = mf_grid(n_work, 8);
     h->step_grid = mf_grid((E * rank + kMfThreads - 1) / kMfThreads, 8);
     auto fail = [&](const char *what) {
         set_error("%s", what);
         ecc_mf_destroy(h);
         return ECC_ERR_ALLOC;
     };
-    if (hipMalloc((void **)&h->d_err, sizeof(double) * N) != hipSuccess ||
-        hipMalloc((void **)&h->d_perm, sizeof(int32_t) * 2 * N) != hipSuccess ||
-        hipMalloc((void **)&h->d_oidx, sizeof(int32_t) * 2 * N) != hipSuccess ||
-        hipMalloc((void **)&h->d_rp, sizeof(int32_t) * (n_rows + 1)) != hipSuccess ||
+    if (hipMalloc((void **)&h->d_oidx, sizeof(int32_t) * 2 * N) != hipSuccess ||
+        hipMalloc((void **)&h->d_rv, sizeof(double) * 2 * N) != hipSuccess ||
+        hipMalloc((void **)&h->d_row_of, sizeof(int32_t) * n_rows) != hipSuccess ||
+        hipMalloc((void **)&h->d_start_of, sizeof(int32_t) * n_rows) != hipSuccess ||
+        hipMalloc((void **)&h->d_len_of, sizeof(int32_t) * n_rows) != hipSuccess ||
         hipMalloc((void **)&h->d_scale, sizeof(double) * E) != hipSuccess ||
-        hipMalloc((void **)&h->d_partials, sizeof(double) * h->err_grid) != hipSuccess)
+        hipMalloc((void **)&h->d_partials, sizeof(double) * h->grad_grid) != hipSuccess)
         return fail("hipMalloc of the factorisation state failed");
-    if (hipMemcpy(h->d_perm, perm.data(), sizeof(int32_t) * 2 * N, hipMemcpyHostToDevice) !=
+    if (hipMemcpy(h->d_oidx, oidx.data(), sizeof(int32_t) * 2 * N, hipMemcpyHostToDevice) !=
             hipSuccess ||
-        hipMemcpy(h->d_oidx, oidx.data(), sizeof(int32_t) * 2 * N, hipMemcpyHostToDevice) !=
+        hipMemcpy(h->d_rv, rv.data(), sizeof(double) * 2 * N, hipMemcpyHostToDevice) !=
             hipSuccess ||
-        hipMemcpy(h->d_rp, rp.data(), sizeof(int32_t) * (n_rows + 1), hipMemcpyHostToDevice) !=
+        hipMemcpy(h->d_row_of, row_of.data(), sizeof(int32_t) * n_rows, hipMemcpyHostToDevice) !=
+            hipSuccess ||
+        hipMemcpy(h->d_start_of, start_of.data(), sizeof(int32_t) * n_rows,
+                  hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(h->d_len_of, len_of.data(), sizeof(int32_t) * n_rows, hipMemcpyHostToDevice) !=
             hipSuccess ||
         hipMemcpy(h->d_scale, scale.data(), sizeof(double) * E, hipMemcpyHostToDevice) !=
             hipSuccess)
@@ -279,40 +457,49 @@ ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam,
     }
     ECC_ARG(d_W && d_grads && d_slots && d_G && d_arrived && d_rmse, "NULL argument");
     hipStream_t s = plan->stream;
-    MfView v{h->n_users, h->n_items, h->N, h->d_users, h->d_items, h->d_ratings, d_W};
     const int64_t E = (int64_t)h->n_users + h->n_items;
     const int64_t n_rows = (int64_t)h->P * E;
     const int64_t m = E * h->rank;
     int log2r = 0;
     while ((1 << log2r) < h->rank) ++log2r;
-#define ECC_MF_RANKS(X) X(1) X(2) X(4) X(8) X(16) X(32) X(64)
-#define ECC_MF_LAUNCH(R)                                                                      \
-    case R: {                                                                                 \
-        {                                                                                     \
-            TimedLaunch timed(plan, ECC_TIMING_MF_ERROR);                                     \
-            hipLaunchKernelGGL(k_mf_err<R>, dim3(h->err_grid), dim3(kMfThreads), 0, s, v,     \
-                               h->d_err, h->d_partials);                                      \
-        }                                                                                     \
-        TimedLaunch timed(plan, ECC_TIMING_MF_GRAD);                                          \
-        hipLaunchKernelGGL(k_mf_grad<R>, dim3(h->grad_grid), dim3(kMfThreads), 0, s, v,       \
-                           h->d_err, h->d_perm, h->d_oidx, h->d_rp, n_rows, d_grads);         \
-        break;                                                                                \
+    const int64_t groups = kMfThreads / (h->rank < 4 ? 1 : h->rank / 4);
+    MfGradArgs ga{};
+    ga.n_users = h->n_users;
+    ga.E = E;
+    ga.W = d_W;
+    ga.oidx = h->d_oidx;
+    ga.rv = h->d_rv;
+    ga.row_of = h->d_row_of;
+    ga.start_of = h->d_start_of;
+    ga.len_of = h->d_len_of;
+    ga.n_rows = n_rows;
+    ga.n_heavy = h->n_heavy;
+    ga.n_work = h->n_heavy + (n_rows - h->n_heavy + groups - 1) / groups;
+    ga.grads = d_grads;
+    ga.partials = h->d_partials;
+    {
+        TimedLaunch timed(plan, ECC_TIMING_MF_GRAD);
+        const dim3 grid(h->grad_grid), block(kMfThreads);
+        switch (h->rank) {
+            case 1: hipLaunchKernelGGL(k_mf_grad<1>, grid, block, 0, s, ga); break;
+            case 2: hipLaunchKernelGGL(k_mf_grad<2>, grid, block, 0, s, ga); break;
+            case 4: hipLaunchKernelGGL(k_mf_grad<4>, grid, block, 0, s, ga); break;
+            case 8: hipLaunchKernelGGL(k_mf_grad<8>, grid, block, 0, s, ga); break;
+            case 16: hipLaunchKernelGGL(k_mf_grad<16>, grid, block, 0, s, ga); break;
+            case 32: hipLaunchKernelGGL(k_mf_grad<32>, grid, block, 0, s, ga); break;
+            case 64: hipLaunchKernelGGL(k_mf_grad<64>, grid, block, 0, s, ga); break;
+            default:
+                set_error("internal: rank %d", h->rank);
+                return ECC_ERR_STATE;
+        }
+        ECC_LAUNCH_CHECK();
     }
-    switch (h->rank) {
-        ECC_MF_RANKS(ECC_MF_LAUNCH)
-        default:
-            set_error("internal: rank %d", h->rank);
-            return ECC_ERR_STATE;
-    }
-#undef ECC_MF_LAUNCH
-#undef ECC_MF_RANKS
-    ECC_LAUNCH_CHECK();
     st = ecc_allreduce_partial(plan, m, d_grads, d_slots, d_G, d_arrived, d_eff_out, nullptr);
     if (st != ECC_OK) return st;
     {
         TimedLaunch timed(plan, ECC_TIMING_MF_STEP);
         hipLaunchKernelGGL(k_mf_rmse, dim3(1), dim3(kNormThreads), 0, s, h->d_partials,
-                           (int64_t)h->err_grid, h->N, d_rmse);
+                           (int64_t)h->grad_grid, h->N, d_rmse);
         hipLaunchKernelGGL(k_mf_step, dim3(h->step_grid), dim3(kMfThreads), 0, s, m, log2r, eta,
                            2.0 * lam, d_G, h->d_scale, d_W);
     }

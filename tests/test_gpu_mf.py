@@ -57,6 +57,23 @@ def test_mf_stale(S, q):
                           T=10, eta=1.0, seed=7 + S))
 
 
+@pytest.mark.parametrize("rank", [1, 16, 64])
+def test_mf_long_rows(rank):
+    """Few users and items: every (worker, row) holds hundreds to thousands
+    of ratings, so each row is summed by a whole workgroup over several
+    chunks of its ratings."""
+    _compare(W.mf_problem(n_users=60, n_items=25, n_ratings=50021, rank=rank, P=2, S=1, q=0.7,
+                          T=4, eta=1.0, seed=11 + rank))
+
+
+@pytest.mark.parametrize("rank", [2, 8, 16])
+def test_mf_long_and_short_rows(rank):
+    """Item rows of hundreds of ratings next to user rows of a few: both
+    row paths in one launch."""
+    _compare(W.mf_problem(n_users=2000, n_items=40, n_ratings=60013, rank=rank, P=4, S=2, q=0.6,
+                          T=5, eta=1.0, seed=23 + rank))
+
+
 def test_mf_one_worker_and_idle_rows():
     """P = 1; many users and items without ratings (their rows only decay)."""
     _compare(W.mf_problem(n_users=5000, n_items=3000, n_ratings=3001, rank=8, P=1, S=0, q=1.0,
