@@ -22,6 +22,13 @@
 
 namespace ecc {
 
+// Contributions, slots and results are each touched once per call and the
+// slots of all processes (P d m doubles) far exceed the caches: non-temporal
+// accesses (measured on MI355X, 32 processes x 16 MB: 973 us against 1,019
+// us with ordinary ones).
+__device__ __forceinline__ void hc_st(double *p, double v) { __builtin_nontemporal_store(v, p); }
+__device__ __forceinline__ double hc_ld(const double *p) { return __builtin_nontemporal_load(p); }
+
 constexpr int kHcThreads = 256;
 constexpr int kHcMaxDims = 6;  // P <= 64: one lane per process in the scalar phase
 constexpr int32_t kHcNever = INT32_MIN;  // clock of a slot that was never written
@@ -110,7 +117,7 @@ __global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp_col(HcArgs a) {
     for (int64_t j = ((int64_t)blockIdx.x * kHcThreads + threadIdx.x) / H; j < m; j += stride) {
         double part[Pt];
 #pragma unroll
-        for (int i = 0; i < Pt; ++i) part[i] = a.contrib[(r0 + i) * m + j];
+        for (int i = 0; i < Pt; ++i) part[i] = hc_ld(a.contrib + (r0 + i) * m + j);
 #pragma unroll
         for (int k = 0; k < D; ++k) {
             double *srow = a.slots + (int64_t)k * m + j;  // + r * D * m
@@ -122,10 +129,10 @@ __global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp_col(HcArgs a) {
                     const int r = r0 + i, q = r0 + (i | bit);
                     const bool fr = (fresh[k] >> r) & 1ull, fq = (fresh[k] >> q) & 1ull;
                     double *sr = srow + (int64_t)r * D * m, *sq = srow + (int64_t)q * D * m;
-                    const double gr = fr ? part[i | bit] : *sr;
-                    const double gq = fq ? part[i] : *sq;
-                    if (fr) *sr = gr;
-                    if (fq) *sq = gq;
+                    const double gr = fr ? part[i | bit] : hc_ld(sr);
+                    const double gq = fq ? part[i] : hc_ld(sq);
+                    if (fr) hc_st(sr, gr);
+                    if (fq) hc_st(sq, gq);
                     part[i] = part[i] + gr;
                     part[i | bit] = part[i | bit] + gq;
                 }
@@ -137,15 +144,15 @@ __global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp_col(HcArgs a) {
                     const bool fr = (fresh[k] >> r) & 1ull;
                     double *sr = srow + (int64_t)r * D * m;
                     const double other = __shfl_xor(part[i], lanebit, 64);
-                    const double g = fr ? other : *sr;
-                    if (fr) *sr = g;
+                    const double g = fr ? other : hc_ld(sr);
+                    if (fr) hc_st(sr, g);
                     part[i] = part[i] + g;
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
-        for (int i = 0; i < Pt; ++i) a.result[(r0 + i) * m + j] = part[i];
+        for (int i = 0; i < Pt; ++i) hc_st(a.result + (r0 + i) * m + j, part[i]);
     }
 }
 
@@ -194,12 +201,6 @@ ecc_status_t hc_reset(ecc_hypercube_t h) {
 #define ECC_HC_THREAD_DIMS 5
 #endif
 constexpr int hc_split(int D) { return D > ECC_HC_THREAD_DIMS ? D - ECC_HC_THREAD_DIMS : 0; }
-
-template <int D>
-hipError_t hc_occupancy(int *per_cu) {
-    return hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        per_cu, k_allreduce_ssp_col<D, hc_split(D)>, kHcThreads, 0);
-}
 
 template <int D>
 void hc_launch(dim3 grid, hipStream_t st, const HcArgs &a) {
@@ -259,25 +260,12 @@ ecc_status_t ecc_hypercube_create(int32_t P, int64_t m, int32_t slack, void *hip
         if (hipMalloc((void **)&h->d_waits, sizeof(unsigned long long) * n) != hipSuccess)
             return fail("hipMalloc of the wait counters failed");
     }
-    // grid: as many workgroups as fit at once, at most one per four chunks
-    int dev = 0, cus = 256, per_cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        cus = 256;
-    hipError_t e;
-    switch (D) {
-        case 0: e = hc_occupancy<0>(&per_cu); break;
-        case 1: e = hc_occupancy<1>(&per_cu); break;
-        case 2: e = hc_occupancy<2>(&per_cu); break;
-        case 3: e = hc_occupancy<3>(&per_cu); break;
-        case 4: e = hc_occupancy<4>(&per_cu); break;
-        case 5: e = hc_occupancy<5>(&per_cu); break;
-        default: e = hc_occupancy<6>(&per_cu); break;
-    }
-    if (e != hipSuccess || per_cu < 1) per_cu = 2;
+    // grid: one workgroup per pass over its elements (measured on MI355X,
+    // 32 processes x 16 MB: 945 us, against 974 us with the resident
+    // workgroups walking the vector)
     const int64_t per_wg = hc_wg_elems(D);
     const int64_t need = std::max<int64_t>(1, (m + per_wg - 1) / per_wg);
-    h->grid = (int32_t)std::min<int64_t>(need, (int64_t)cus * per_cu);
+    h->grid = (int32_t)std::min<int64_t>(need, 0x7fffffff);
     ecc_status_t st = hc_reset(h);
     if (st != ECC_OK) {
         ecc_hypercube_destroy(h);
