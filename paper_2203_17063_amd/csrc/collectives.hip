@@ -138,14 +138,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_allreduce(
                         double2 *dst = reinterpret_cast<double2 *>(slots[p]);
 #pragma unroll
                         for (int j = 0; j < VP; ++j) {
-                            if (in[j]) {
-#if ECC_RED_NT
-                                __builtin_nontemporal_store(v[u][j].x, &dst[q[j]].x);
-                                __builtin_nontemporal_store(v[u][j].y, &dst[q[j]].y);
-#else
-                                dst[q[j]] = v[u][j];
-#endif
-                            }
+                            if (in[j]) dst[q[j]] = v[u][j];
                         }
                     }
 #pragma unroll

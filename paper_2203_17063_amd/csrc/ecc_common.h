@@ -53,18 +53,9 @@ constexpr int kAssembleTile = 2048;      // elements copied by one workgroup
 // Partial allreduce block shape: 1,024 threads x 16 elements, so that a
 // workgroup streams 128 KB of each rank's vector at a time (measured on
 // MI355X: 5.45 TB/s at 256 ranks x 4M, against 4.89 TB/s with 256 x 4).
-#ifndef ECC_RED_THREADS
-#define ECC_RED_THREADS 1024
-#endif
-#ifndef ECC_RED_ELEMS
-#define ECC_RED_ELEMS 16
-#endif
-#ifndef ECC_RED_U
-#define ECC_RED_U 1
-#endif
-constexpr int kReduceThreads = ECC_RED_THREADS;
-constexpr int kReduceElems = ECC_RED_ELEMS;  // elements per thread per rank (pairs of 16 B)
-constexpr int kReduceU = ECC_RED_U;          // ranks whose loads are in flight together
+constexpr int kReduceThreads = 1024;
+constexpr int kReduceElems = 16;  // elements per thread per rank (pairs of 16 B)
+constexpr int kReduceU = 1;       // ranks whose loads are in flight together
 constexpr int kSweepThreads = 256;
 constexpr int kStreamCap = 2048;         // nonzeros staged in LDS by a stream item
 constexpr int kStreamRows = 256;         // rows of one stream item at most
@@ -92,10 +83,7 @@ enum { kItemStream = 0, kItemVector = 1, kItemPiece = 2, kItemRows = 3 };
 // binned by length (very uneven rows); short-row items, one lane per row
 // read directly (every row holds at most kShortRow entries).
 enum { kLayStream = 0, kLayRows = 1, kLayShort = 2 };
-#ifndef ECC_SHORT_ROW
-#define ECC_SHORT_ROW 8
-#endif
-constexpr int kShortRow = ECC_SHORT_ROW;
+constexpr int kShortRow = 8;
 static_assert(kShortRow <= 8, "a short row is summed from eight registers");
 static_assert(kStreamRows <= 256 && kStreamRows <= kSweepThreads, "one lane per short row");
 struct WorkItem {

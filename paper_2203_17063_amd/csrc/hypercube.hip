@@ -192,15 +192,13 @@ ecc_status_t hc_reset(ecc_hypercube_t h) {
 }
 
 // Lanes per element: 2^split, so that a thread holds at most
-// 2^ECC_HC_THREAD_DIMS partial reductions.  Measured on MI355X (16 MB per
+// 2^kHcThreadDims partial reductions.  Measured on MI355X (16 MB per
 // process, slack 2, 80% delivery): P = 32 in one thread, 168 VGPRs, 3.68
 // TB/s; P = 64 over two lanes, 2.08 TB/s (over four lanes, or with P = 32
 // over two, the per-lane delivery bits make every slot access divergent
 // and the registers run out).
-#ifndef ECC_HC_THREAD_DIMS
-#define ECC_HC_THREAD_DIMS 5
-#endif
-constexpr int hc_split(int D) { return D > ECC_HC_THREAD_DIMS ? D - ECC_HC_THREAD_DIMS : 0; }
+constexpr int kHcThreadDims = 5;
+constexpr int hc_split(int D) { return D > kHcThreadDims ? D - kHcThreadDims : 0; }
 
 template <int D>
 void hc_launch(dim3 grid, hipStream_t st, const HcArgs &a) {

@@ -5,23 +5,31 @@
 // elsewhere, plus the residual-norm reduction.
 //
 // Work decomposition (built once per matrix on the host, CSR-Adaptive style
-// after Greathouse & Daga, SC'14): a "stream" item is a run of short rows of
-// one rank whose nonzeros fit in LDS -- they are loaded with coalesced
-// accesses and each row is then summed by 1..64 lanes; a "vector" item is one
-// long row summed by the whole workgroup; a "piece" is a fixed-size slice of
-// a very long row whose partial sum is recombined, in piece order, at the
-// end.  Items never straddle a rank boundary, so [lo, hi) is uniform per
-// item.  Rows summed by a single lane accumulate in CSR order with no fused
-// multiply-add, exactly like the sequential definition.
+// after Greathouse & Daga, SC'14), in one of three layouts per matrix:
+//  - short rows (every row holds at most 8 entries): an item is a run of up
+//    to 256 rows of one rank, one lane per row reading its entries straight
+//    from memory, pipelined three items deep;
+//  - stream items for other regular matrices: a run of short rows of one
+//    rank whose nonzeros fit in LDS -- they are loaded with coalesced
+//    accesses and each row is then summed by 1..64 lanes;
+//  - row-list items for very uneven rows (power-law graphs): rows of one rank
+//    binned by length, 1, 4, 16 or 64 lanes per row, gathers of the vector
+//    as device-scope loads that skip the CU's L1.
+// In the last two, a "vector" item is one long row summed by the whole
+// workgroup and a "piece" a fixed-size slice of a very long row whose
+// partial sum is recombined, in piece order, at the end.  Items never
+// straddle a rank boundary, so [lo, hi) is uniform per item.  Rows summed by
+// a single lane accumulate in CSR order with no fused multiply-add, exactly
+// like the sequential definition.
 //
 // Each workgroup writes one partial norm.  Split rows and the reduction of
 // the partials (in a fixed order, so results are deterministic run to run)
 // belong to a second pass that starts after the sweep has finished: a
 // separate one-workgroup launch, or -- in a loop without a tolerance and
 // without split rows -- workgroup 0 of the next iteration's launch.  No
-// device-wide fence or atomic is used inside a launch: on a multi-XCD part
-// an agent-scope release writes back the XCD's L2, which would cost more
-// than the launch boundary.
+// device-wide fence or read-modify-write atomic is used inside a launch: on
+// a multi-XCD part an agent-scope release writes back the XCD's L2, which
+// would cost more than the launch boundary.
 //
 // Loop iterations use the same kernel with the staleness decision and the
 // assembly fused in: every workgroup evaluates the decision for all ranks
@@ -36,16 +44,11 @@
 
 #include "ecc_common.h"
 
-#ifndef ECC_STREAM_NT
-#define ECC_STREAM_NT 0
-#endif
+namespace ecc {
+
 // Largest CSR (bytes of col, val and row_ptr) that rows of 7 or 8 entries
 // sweep in the short-row layout.
-#ifndef ECC_SHORT_CSR_LIMIT
-#define ECC_SHORT_CSR_LIMIT (int64_t(1) << 29)
-#endif
-
-namespace ecc {
+constexpr int64_t kShortCsrLimit = int64_t(1) << 29;
 
 struct SweepArgs {
     const WorkItem *items;
@@ -171,17 +174,6 @@ __device__ __forceinline__ int lanes_per_row(int32_t nnz, int32_t nr) {
     return tpr;
 }
 
-// Loads of arrays that are streamed once per sweep (CSR arrays, b): marked
-// non-temporal so that they do not evict the reused iterate from L2.
-template <typename T>
-__device__ __forceinline__ T ld_stream(const T *p) {
-#if ECC_STREAM_NT
-    return __builtin_nontemporal_load(p);
-#else
-    return *p;
-#endif
-}
-
 // Accumulates a lane's entries k0, k0 + stride, ... (< k1) of row i, in that
 // order, W at a time: the next W (col, val) loads are in flight while the
 // current W gathers of y complete.  With stride 1 this is the row's CSR
@@ -197,8 +189,8 @@ __device__ __forceinline__ void seg_accumulate(int32_t i, int32_t k0, int32_t k1
 #pragma unroll
     for (int u = 0; u < W; ++u) {
         const int32_t k = k0 + u * stride;
-        c[u] = (k < k1) ? ld_stream(a.col + k) : 0;
-        v[u] = (k < k1) ? ld_stream(a.val + k) : 0.0;
+        c[u] = (k < k1) ? a.col[k] : 0;
+        v[u] = (k < k1) ? a.val[k] : 0.0;
     }
     for (int32_t k = k0; k < k1; k += W * stride) {
         double y[W];
@@ -212,8 +204,8 @@ __device__ __forceinline__ void seg_accumulate(int32_t i, int32_t k0, int32_t k1
 #pragma unroll
         for (int u = 0; u < W; ++u) {
             const int32_t kk = kn + u * stride;
-            cn[u] = (kk < k1) ? ld_stream(a.col + kk) : 0;
-            vn[u] = (kk < k1) ? ld_stream(a.val + kk) : 0.0;
+            cn[u] = (kk < k1) ? a.col[kk] : 0;
+            vn[u] = (kk < k1) ? a.val[kk] : 0.0;
         }
 #pragma unroll
         for (int u = 0; u < W; ++u) {
@@ -241,8 +233,8 @@ __device__ __forceinline__ void short_row(int32_t i, int32_t ks, int32_t ke, con
     double v8[8], y8[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-        c8[j] = (j < len) ? ld_stream(a.col + ks + j) : 0;
-        v8[j] = (j < len) ? ld_stream(a.val + ks + j) : 0.0;
+        c8[j] = (j < len) ? a.col[ks + j] : 0;
+        v8[j] = (j < len) ? a.val[ks + j] : 0.0;
     }
 #pragma unroll
     for (int j = 0; j < 8; ++j)
@@ -276,8 +268,8 @@ __device__ __forceinline__ void stream_load(const WorkItem &it, const SweepArgs 
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int32_t kc = min(it.k0 + tid + u * kSweepThreads, it.k1 - 1);
-            pf.cv[u] = ld_stream(a.col + kc);
-            pf.vv[u] = ld_stream(a.val + kc);
+            pf.cv[u] = a.col[kc];
+            pf.vv[u] = a.val[kc];
         }
     }
     const int tpr = lanes_per_row(nnz, it.nrows);
@@ -286,10 +278,10 @@ __device__ __forceinline__ void stream_load(const WorkItem &it, const SweepArgs 
     pf.bi = pf.xo = 0.0;
     if (rr < it.nrows) {
         const int32_t i = it.row0 + rr;
-        pf.rp0 = ld_stream(a.row_ptr + i);
-        pf.rp1 = ld_stream(a.row_ptr + i + 1);
+        pf.rp0 = a.row_ptr[i];
+        pf.rp1 = a.row_ptr[i + 1];
         pf.xo = a.x_own[i];
-        if (KIND == ECC_KIND_JACOBI) pf.bi = ld_stream(a.b + i);
+        if (KIND == ECC_KIND_JACOBI) pf.bi = a.b[i];
     }
 }
 
@@ -573,8 +565,8 @@ __device__ __forceinline__ void short_entries(const SweepArgs &a, int32_t ks, in
     e.len = ke - ks;
 #pragma unroll
     for (int j = 0; j < R; ++j) {
-        e.c[j] = (j < e.len) ? ld_stream(a.col + ks + j) : 0;
-        e.v[j] = (j < e.len) ? ld_stream(a.val + ks + j) : 0.0;
+        e.c[j] = (j < e.len) ? a.col[ks + j] : 0;
+        e.v[j] = (j < e.len) ? a.val[ks + j] : 0.0;
     }
 }
 
@@ -637,7 +629,7 @@ __device__ __forceinline__ void short_body(const SweepArgs &a) {
         double xo = 0.0, bi = 0.0;
         if (live) {
             xo = a.x_own[i];
-            if (KIND == ECC_KIND_JACOBI) bi = ld_stream(a.b + i);
+            if (KIND == ECC_KIND_JACOBI) bi = a.b[i];
         }
         ShortEntries<R> En;
         En.len = 0;
@@ -676,13 +668,11 @@ __device__ __forceinline__ void short_body(const SweepArgs &a) {
 
 // The short-row layout holds few values per lane: the register budget is
 // capped so that several waves share each SIMD -- as many as the row's
-// registers allow without spilling.
-#ifndef ECC_SHORT_WAVES5
-#define ECC_SHORT_WAVES5 5
-#endif
+// registers allow without spilling (R = 5 at 6 waves spills; measured on
+// MI355X, config 2: 20.3 us against 19.7 us at 5 waves).
 template <int R>
 constexpr int short_waves() {
-    return R <= 3 ? 8 : (R == 4 ? 7 : (R == 5 ? ECC_SHORT_WAVES5 : 4));
+    return R <= 3 ? 8 : (R == 4 ? 7 : (R == 5 ? 5 : 4));
 }
 template <int KIND, bool STEP, int R>
 __global__ __launch_bounds__(kSweepThreads) __attribute__((amdgpu_waves_per_eu(short_waves<R>())))
@@ -1142,7 +1132,7 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     for (int64_t i = 0; i < n; ++i) max_row = std::max(max_row, rp[i + 1] - rp[i]);
     const int64_t csr_bytes = 12 * (int64_t)A->nnz + 4 * (n + 1);
     const bool short_rows =
-        max_row <= kShortRow && (max_row <= 6 || csr_bytes <= (int64_t)ECC_SHORT_CSR_LIMIT);
+        max_row <= kShortRow && (max_row <= 6 || csr_bytes <= kShortCsrLimit);
     const int layout = irregular ? kLayRows : (short_rows ? kLayShort : kLayStream);
     build_items(rp, plan->counts, irregular, items, fixups, rowlist, n_pieces);
     if ((int64_t)items.size() >= (int64_t(1) << 31)) {
