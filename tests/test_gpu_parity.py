@@ -347,7 +347,8 @@ def _arrow_problem(n=40000, T=40, P=7, S=2):
 def _banded_problem(kind, n, lmin, lmax, P=13, T=40, S=3, seed=5):
     """Rows of lmin..lmax entries (at most 64: a regular matrix) at random
     columns within a band of +-1500 around the diagonal, so that rows read
-    neighbouring ranks: the LDS-staged stream layout."""
+    neighbouring ranks: the LDS-staged stream layout for rows of more than
+    eight entries, the short-row layout otherwise."""
     rng = np.random.default_rng(seed)
     lens = rng.integers(lmin, lmax + 1, n)
     cols, vals = [], []
@@ -382,6 +383,17 @@ def test_solve_stream_layout(kind, lmin, lmax):
     """Regular rows longer than eight entries: rows of up to 16 entries are
     summed by one lane in CSR order (bitwise), longer ones by several lanes."""
     _solve_and_compare(_banded_problem(kind, 30000, lmin, lmax), bitwise=(lmax <= 16))
+
+
+@pytest.mark.parametrize("kind,lmin,lmax", [
+    ("jacobi", 1, 2), ("power", 0, 3), ("jacobi", 2, 4), ("power", 3, 6), ("jacobi", 5, 7),
+    ("jacobi", 8, 8), ("power", 1, 8)])
+def test_solve_short_layout(kind, lmin, lmax):
+    """Rows of at most eight entries: the short-row layout, one lane per row
+    summed in CSR order (bitwise).  The kernel holds 3, 4, 5, 7 or 8 entries
+    per row after the longest row; rows may be shorter than that, or empty
+    (power step)."""
+    _solve_and_compare(_banded_problem(kind, 30000, lmin, lmax), bitwise=True)
 
 
 def test_solve_arrow_split_rows():
