@@ -385,9 +385,12 @@ ecc_status_t ecc_allreduce_drop(int32_t P, int64_t m, const double *const *d_fre
  * p's shard is k in [N p / P, N (p + 1) / P).
  * --------------------------------------------------------------------------- */
 
-/* Build the per-worker gradient index (ratings of every (worker, row) in
- * shard order, by counting sorts on the host; the rating arrays are read
- * once and must stay valid and unchanged while the state is used).
+/* Build the per-worker gradient index on the host, by counting sorts: the
+ * ratings of every (worker, row) in shard order, stored as the other
+ * factor's row index and the rating value (12 bytes per rating and side),
+ * and the rows sorted by their number of ratings (12 bytes per row).  The
+ * rating arrays are read once, here; the state keeps its own copy, so the
+ * caller may free or change them afterwards.
  * rank: a power of two in [1, 64]; N in [1, 2^30).  ECC_ERR_ARG for bad
  * sizes or an out-of-range user/item index; ECC_ERR_RANGE when
  * P * (n_users + n_items) reaches 2^31; ECC_ERR_ALLOC on allocation

@@ -23,11 +23,17 @@ def _gpu():
     torch.cuda.synchronize()
 
 
-def _compare(prob):
+def _compare(prob, clobber_inputs=False):
     from paper_2203_17063_amd import runner as R
     announce("mf", prob.n_users, prob.n_items, prob.N, prob.rank, prob.P, prob.S, prob.T)
     ref = M.run(prob, keep_W=tuple(range(prob.T + 1)))
     run = R.MatrixFactorization(prob)
+    if clobber_inputs:
+        # the state keeps its own copy of the ratings: the caller's arrays
+        # may change after ecc_mf_create
+        run.d_users.fill_(0)
+        run.d_items.fill_(0)
+        run.d_ratings.fill_(-1.0)
     try:
         run.reset()
         for t in range(prob.T):
@@ -72,6 +78,11 @@ def test_mf_long_and_short_rows(rank):
     row paths in one launch."""
     _compare(W.mf_problem(n_users=2000, n_items=40, n_ratings=60013, rank=rank, P=4, S=2, q=0.6,
                           T=5, eta=1.0, seed=23 + rank))
+
+
+def test_mf_inputs_copied_at_create():
+    _compare(W.mf_problem(n_users=400, n_items=90, n_ratings=30011, rank=8, P=4, S=1, q=0.7,
+                          T=4, eta=1.0, seed=31), clobber_inputs=True)
 
 
 def test_mf_one_worker_and_idle_rows():
