@@ -88,71 +88,52 @@ __device__ __forceinline__ unsigned long long uniform64(unsigned long long v) {
     return ((unsigned long long)hi << 32) | lo;
 }
 
-// Column layout: 2^S lanes share element j; lane h (= lane mod 2^S) carries
-// element j of the partial reductions of processes h * Pt .. h * Pt + Pt - 1
-// (Pt = P / 2^S, at most 32) in registers.  Every load and store of a wave
-// covers contiguous bytes of at most 2^S rows.  At steps k < log2(Pt) the
-// two processes of a pair (r, r XOR 2^k) sit in one thread and are updated
-// together from their old partials; at the higher steps the partner's
-// partial comes from lane h XOR 2^(k - log2 Pt) through a wave shuffle.  A
-// scheduling barrier between steps keeps the loads of a step from being
-// hoisted above the stores of the previous one (register pressure).
-template <int D, int S>
-__global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp_col(HcArgs a) {
-    constexpr int LT = D - S;  // dimensions inside a thread
-    constexpr int Pt = 1 << LT;
-    constexpr int H = 1 << S;
+// Column layout: a thread carries element j of all P = 2^D partial
+// reductions in registers (P <= 64), so every load and store of a wave
+// covers contiguous bytes of one row.  At step k the two processes of each
+// pair (r, r XOR 2^k) sit in the same thread and are updated together from
+// their old partials.  A scheduling barrier between steps keeps the loads of
+// a step from being hoisted above the stores of the previous one (register
+// pressure).  Measured on MI355X (slack 2, 80 % delivery): P = 32 x 16 MB,
+// 168 VGPRs, 3.98 TB/s; P = 64 x 8 MB, 256 VGPRs, 2.63 TB/s (2.23 TB/s with
+// two lanes per element, whose per-lane delivery bits make every slot
+// access divergent).
+template <int D>
+__global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp(HcArgs a) {
+    constexpr int Pt = 1 << D;
     __shared__ unsigned long long s_fresh[kHcMaxDims];
     hc_decide(a, s_fresh);
     __syncthreads();
     unsigned long long fresh[D > 0 ? D : 1];
 #pragma unroll
     for (int k = 0; k < D; ++k) fresh[k] = uniform64(s_fresh[k]);
-    const int h = threadIdx.x & (H - 1);
-    const int r0 = h * Pt;
     const int64_t m = a.m;
-    const int64_t stride = (int64_t)gridDim.x * (kHcThreads / H);
-    // the 2^S lanes that exchange partials share one element, so they enter
-    // and leave the loop together
-    for (int64_t j = ((int64_t)blockIdx.x * kHcThreads + threadIdx.x) / H; j < m; j += stride) {
+    const int64_t stride = (int64_t)gridDim.x * kHcThreads;
+    for (int64_t j = (int64_t)blockIdx.x * kHcThreads + threadIdx.x; j < m; j += stride) {
         double part[Pt];
 #pragma unroll
-        for (int i = 0; i < Pt; ++i) part[i] = hc_ld(a.contrib + (r0 + i) * m + j);
+        for (int i = 0; i < Pt; ++i) part[i] = hc_ld(a.contrib + i * m + j);
 #pragma unroll
         for (int k = 0; k < D; ++k) {
             double *srow = a.slots + (int64_t)k * m + j;  // + r * D * m
-            if (k < LT) {
-                const int bit = 1 << k;
+            const int bit = 1 << k;
 #pragma unroll
-                for (int i = 0; i < Pt; ++i) {
-                    if (i & bit) continue;
-                    const int r = r0 + i, q = r0 + (i | bit);
-                    const bool fr = (fresh[k] >> r) & 1ull, fq = (fresh[k] >> q) & 1ull;
-                    double *sr = srow + (int64_t)r * D * m, *sq = srow + (int64_t)q * D * m;
-                    const double gr = fr ? part[i | bit] : hc_ld(sr);
-                    const double gq = fq ? part[i] : hc_ld(sq);
-                    if (fr) hc_st(sr, gr);
-                    if (fq) hc_st(sq, gq);
-                    part[i] = part[i] + gr;
-                    part[i | bit] = part[i | bit] + gq;
-                }
-            } else {
-                const int lanebit = 1 << (k - LT);
-#pragma unroll
-                for (int i = 0; i < Pt; ++i) {
-                    const int r = r0 + i;
-                    const bool fr = (fresh[k] >> r) & 1ull;
-                    double *sr = srow + (int64_t)r * D * m;
-                    const double other = __shfl_xor(part[i], lanebit, 64);
-                    const double g = fr ? other : hc_ld(sr);
-                    if (fr) hc_st(sr, g);
-                    part[i] = part[i] + g;
-                }
+            for (int i = 0; i < Pt; ++i) {
+                if (i & bit) continue;
+                const int q = i | bit;
+                const bool fr = (fresh[k] >> i) & 1ull, fq = (fresh[k] >> q) & 1ull;
+                double *sr = srow + (int64_t)i * D * m, *sq = srow + (int64_t)q * D * m;
+                const double gr = fr ? part[q] : hc_ld(sr);
+                const double gq = fq ? part[i] : hc_ld(sq);
+                if (fr) hc_st(sr, gr);
+                if (fq) hc_st(sq, gq);
+                part[i] = part[i] + gr;
+                part[q] = part[q] + gq;
             }
             __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
-        for (int i = 0; i < Pt; ++i) hc_st(a.result + (r0 + i) * m + j, part[i]);
+        for (int i = 0; i < Pt; ++i) hc_st(a.result + i * m + j, part[i]);
     }
 }
 
@@ -191,27 +172,9 @@ ecc_status_t hc_reset(ecc_hypercube_t h) {
     return ECC_OK;
 }
 
-// Lanes per element: 2^split, so that a thread holds at most
-// 2^kHcThreadDims partial reductions.  Measured on MI355X (16 MB per
-// process, slack 2, 80% delivery): P = 32 in one thread, 168 VGPRs, 3.68
-// TB/s; P = 64 over two lanes, 2.08 TB/s (over four lanes, or with P = 32
-// over two, the per-lane delivery bits make every slot access divergent
-// and the registers run out).
-constexpr int kHcThreadDims = 5;
-constexpr int hc_split(int D) { return D > kHcThreadDims ? D - kHcThreadDims : 0; }
-
 template <int D>
 void hc_launch(dim3 grid, hipStream_t st, const HcArgs &a) {
-    hipLaunchKernelGGL((k_allreduce_ssp_col<D, hc_split(D)>), grid, dim3(kHcThreads), 0, st, a);
-}
-
-// Elements one workgroup covers per pass.
-int64_t hc_wg_elems(int D) {
-    switch (D) {
-        case 5: return kHcThreads >> hc_split(5);
-        case 6: return kHcThreads >> hc_split(6);
-        default: return kHcThreads >> hc_split(4);
-    }
+    hipLaunchKernelGGL((k_allreduce_ssp<D>), grid, dim3(kHcThreads), 0, st, a);
 }
 
 }  // namespace
@@ -261,7 +224,7 @@ ecc_status_t ecc_hypercube_create(int32_t P, int64_t m, int32_t slack, void *hip
     // grid: one workgroup per pass over its elements (measured on MI355X,
     // 32 processes x 16 MB: 945 us, against 974 us with the resident
     // workgroups walking the vector)
-    const int64_t per_wg = hc_wg_elems(D);
+    const int64_t per_wg = kHcThreads;  // elements of one workgroup
     const int64_t need = std::max<int64_t>(1, (m + per_wg - 1) / per_wg);
     h->grid = (int32_t)std::min<int64_t>(need, 0x7fffffff);
     ecc_status_t st = hc_reset(h);
