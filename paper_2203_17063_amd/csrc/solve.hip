@@ -2,10 +2,11 @@
 //   staleness decision + assembly  ->  block-row sweep  ->  norm  ->  swap,
 // each on the plan's next clock, enqueued without host round trips.  Each
 // iteration is one fused kernel launch (see sweep.hip) unless the plan has
-// more ranks than a workgroup stages in LDS; then the assembly is its own
-// launch.  A tolerance is checked on the device: the norm pass raises a flag that makes
-// every later kernel of the loop return at entry, so the state (versions,
-// ages, iterate) is exactly that after the first iteration below tolerance.
+// more ranks than a workgroup stages in LDS, or the matrix has very uneven
+// rows; then the assembly is its own launch.  A tolerance is checked on the
+// device: the norm pass raises a flag that makes every later kernel of the
+// loop return at entry, so the state (versions, ages, iterate) is exactly
+// that after the first iteration below tolerance.
 #include <algorithm>
 
 #include "ecc_common.h"
@@ -58,7 +59,12 @@ extern "C" ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double 
     // Otherwise a one-workgroup pass follows each sweep (split rows, norm and
     // the convergence flag).  The assembly is fused into the sweep while the
     // rank state fits in LDS.
-    const bool fused = P <= kFusedMaxP;
+    // For matrices with very uneven rows (power-law graphs), whose columns are
+    // spread at random, the fused kernel's rank lookup of every off-block
+    // gather costs more than assembling first: assemble, then a sweep that
+    // reads every other rank from the assembled vector (measured on MI355X,
+    // PageRank on a scale-22 R-MAT graph: 67.2 against 70.0 ms per solve).
+    const bool fused = P <= kFusedMaxP && A->layout != kLayRows;
     const bool deferred = fused && tol <= 0.0 && A->n_fixups == 0;
     double *cur = d_x, *nxt = d_x_tmp;
     for (int32_t t = 0; t < T; ++t) {

@@ -891,13 +891,16 @@ static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_
 // Workgroups of a sweep: as many as the device holds at once (each then
 // walks several items through the load/compute pipeline), at most one per
 // item, rounded down to a multiple of the 8 XCDs.
+// Occupancy of the kernel a loop iteration launches: the fused one, except
+// for the row-list layout, which is never fused.
 template <int LAY>
 static hipError_t sweep_occupancy(int *per_cu, int kind) {
+    constexpr bool S = LAY != kLayRows;
     return kind == ECC_KIND_JACOBI
                ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                     per_cu, k_sweep<ECC_KIND_JACOBI, true, LAY>, kSweepThreads, 0)
+                     per_cu, k_sweep<ECC_KIND_JACOBI, S, LAY>, kSweepThreads, 0)
                : hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                     per_cu, k_sweep<ECC_KIND_POWER, true, LAY>, kSweepThreads, 0);
+                     per_cu, k_sweep<ECC_KIND_POWER, S, LAY>, kSweepThreads, 0);
 }
 
 template <int R>
@@ -940,6 +943,27 @@ static int32_t sweep_grid(int64_t n_items, int kind, int layout, int32_t short_r
     return (int32_t)g;
 }
 
+// The kernel of a matrix's layout.  Matrices with very uneven rows are only
+// swept after a separate assembly (see ecc_solve), so their fused kernel is
+// never built.
+template <int K, bool S>
+static void launch_layout(ecc_matrix_t M, dim3 grid, dim3 block, hipStream_t st,
+                          const SweepArgs &a) {
+    if (M->layout == kLayRows) {
+        if constexpr (!S) hipLaunchKernelGGL((k_sweep<K, S, kLayRows>), grid, block, 0, st, a);
+    } else if (M->layout == kLayShort) {
+        switch (short_class(M->short_r)) {
+            case 3: hipLaunchKernelGGL((k_sweep_short<K, S, 3>), grid, block, 0, st, a); break;
+            case 4: hipLaunchKernelGGL((k_sweep_short<K, S, 4>), grid, block, 0, st, a); break;
+            case 5: hipLaunchKernelGGL((k_sweep_short<K, S, 5>), grid, block, 0, st, a); break;
+            case 7: hipLaunchKernelGGL((k_sweep_short<K, S, 7>), grid, block, 0, st, a); break;
+            default: hipLaunchKernelGGL((k_sweep_short<K, S, 8>), grid, block, 0, st, a); break;
+        }
+    } else {
+        hipLaunchKernelGGL((k_sweep<K, S, kLayStream>), grid, block, 0, st, a);
+    }
+}
+
 ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     ecc_plan_t pl = M->plan;
     SweepArgs a{};
@@ -966,8 +990,8 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     const bool step = L.arrived != nullptr;
     if (step) {
         const int64_t t = pl->clock;
-        if (pl->P > kFusedMaxP || !pl->d_block_start) {
-            set_error("internal: fused step does not fit the plan");
+        if (pl->P > kFusedMaxP || !pl->d_block_start || M->layout == kLayRows) {
+            set_error("internal: fused step does not fit the plan or the matrix");
             return ECC_ERR_STATE;
         }
         a.step = 1;
@@ -987,33 +1011,13 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     TimedLaunch timed(pl, ECC_TIMING_SWEEP);
     const dim3 grid(M->grid), block(kSweepThreads);
     hipStream_t st = pl->stream;
-#define ECC_SWEEP_LAUNCH(K, S, R) \
-    hipLaunchKernelGGL((k_sweep<K, S, R>), grid, block, 0, st, a)
-#define ECC_SHORT_LAUNCH(K, S, R) \
-    hipLaunchKernelGGL((k_sweep_short<K, S, R>), grid, block, 0, st, a)
-#define ECC_SWEEP_LAYOUTS(K, S)                                        \
-    do {                                                               \
-        if (M->layout == kLayRows) ECC_SWEEP_LAUNCH(K, S, kLayRows);   \
-        else if (M->layout == kLayShort) {                             \
-            switch (short_class(M->short_r)) {                         \
-                case 3: ECC_SHORT_LAUNCH(K, S, 3); break;              \
-                case 4: ECC_SHORT_LAUNCH(K, S, 4); break;              \
-                case 5: ECC_SHORT_LAUNCH(K, S, 5); break;              \
-                case 7: ECC_SHORT_LAUNCH(K, S, 7); break;              \
-                default: ECC_SHORT_LAUNCH(K, S, 8); break;             \
-            }                                                          \
-        } else ECC_SWEEP_LAUNCH(K, S, kLayStream);                     \
-    } while (0)
     if (M->kind == ECC_KIND_JACOBI) {
-        if (step) ECC_SWEEP_LAYOUTS(ECC_KIND_JACOBI, true);
-        else ECC_SWEEP_LAYOUTS(ECC_KIND_JACOBI, false);
+        if (step) launch_layout<ECC_KIND_JACOBI, true>(M, grid, block, st, a);
+        else launch_layout<ECC_KIND_JACOBI, false>(M, grid, block, st, a);
     } else {
-        if (step) ECC_SWEEP_LAYOUTS(ECC_KIND_POWER, true);
-        else ECC_SWEEP_LAYOUTS(ECC_KIND_POWER, false);
+        if (step) launch_layout<ECC_KIND_POWER, true>(M, grid, block, st, a);
+        else launch_layout<ECC_KIND_POWER, false>(M, grid, block, st, a);
     }
-#undef ECC_SWEEP_LAYOUTS
-#undef ECC_SHORT_LAUNCH
-#undef ECC_SWEEP_LAUNCH
     ECC_LAUNCH_CHECK();
     if (step) pl->clock += 1;
     return ECC_OK;
