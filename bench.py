@@ -32,9 +32,13 @@ METRIC = "assembled+iterated GB/s and iterations/s at 1 GPU; % of HBM peak"
 PROFILES = os.path.join(ROOT, "profiles")
 
 
-def sweep_bytes(n, nnz):
+def sweep_bytes(n, nnz, slots=0):
     """Algorithmic bytes of one sweep: col + val per nonzero, row_ptr, the x view,
-    b (or x_own for the update norm), the written iterate."""
+    b (or x_own for the update norm), the written iterate.  With the short-row
+    layout (slots = entries held per row) the entries are read from the
+    column-major copy, padding included, and row_ptr is not read."""
+    if slots:
+        return 12 * slots * n + 24 * n
     return 12 * nnz + 28 * n + 4
 
 
@@ -181,6 +185,7 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
     E.ecc_plan_set_timing(run.plan.handle, False)
     rho = run.d_rho.cpu().numpy()[:iters]
     n_part = int(run.d_partials.numel())
+    layout, slots = E.ecc_matrix_layout(run.mat)
     run.close()
 
     counts = prob.counts
@@ -188,7 +193,7 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
     # algorithmic bytes of the data path: assembly (read + write of every
     # arrived element), sweep, norm partials
     b_assemble = float(np.sum(16 * eff_elems + 14 * prob.P))
-    b_sweep = float(sweep_bytes(prob.n, prob.A.nnz))
+    b_sweep = float(sweep_bytes(prob.n, prob.A.nnz, slots if layout == E.ECC_LAYOUT_SHORT else 0))
     b_norm = 8.0 * n_part
     bytes_per_step = b_assemble + iters * (b_sweep + b_norm)
     # one fused launch per iteration: the sweep plus the write of the arrived

@@ -207,11 +207,26 @@ ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *con
  * row-block work list (blocks never straddle a rank boundary; rows longer
  * than one work item are split and recombined in a fixed order), and for
  * ECC_KIND_JACOBI checks that every row has exactly one diagonal entry and
- * that it is non-zero (else ECC_ERR_ARG).  The matrix arrays are referenced,
- * not copied: they must outlive the handle and stay unchanged. */
+ * that it is non-zero (else ECC_ERR_ARG).  It chooses the sweep layout:
+ *   ECC_LAYOUT_SHORT   every row holds at most 8 entries: the entries are
+ *                      copied, column-major and padded to the longest row's
+ *                      class R in {3, 4, 5, 7, 8} (12 bytes x R x n_rows of
+ *                      device memory), one lane per row;
+ *   ECC_LAYOUT_ROWS    very uneven rows (longest > 64 and > 8 x (mean + 1)):
+ *                      rows binned by length;
+ *   ECC_LAYOUT_STREAM  otherwise: runs of rows staged in LDS.
+ * The matrix arrays must outlive the handle and stay unchanged (the last two
+ * layouts read them at every sweep). */
+#define ECC_LAYOUT_STREAM 0
+#define ECC_LAYOUT_ROWS 1
+#define ECC_LAYOUT_SHORT 2
 ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
                                ecc_matrix_t *out);
 ecc_status_t ecc_matrix_destroy(ecc_matrix_t A);
+
+/* The layout ecc_matrix_create chose (ECC_LAYOUT_*) and, for
+ * ECC_LAYOUT_SHORT, the entries held per row R (0 otherwise).  Host only. */
+ecc_status_t ecc_matrix_layout(ecc_matrix_t A, int32_t *layout, int32_t *row_slots);
 
 /* Number of doubles a d_partials buffer for this matrix must hold. */
 int64_t ecc_partials_size(ecc_matrix_t A);

@@ -23,6 +23,7 @@ ECC_KIND_JACOBI, ECC_KIND_POWER = 0, 1
 ECC_TIMING_ASSEMBLE, ECC_TIMING_ALLREDUCE, ECC_TIMING_SWEEP, ECC_TIMING_NORM = 0, 1, 2, 3
 ECC_TIMING_MF_GRAD, ECC_TIMING_MF_STEP = 4, 5
 ECC_THRESHOLD_DATA, ECC_THRESHOLD_PROCS = 0, 1
+ECC_LAYOUT_STREAM, ECC_LAYOUT_ROWS, ECC_LAYOUT_SHORT = 0, 1, 2
 
 STATUS_NAMES = {0: "ECC_OK", 1: "ECC_ERR_ARG", 2: "ECC_ERR_OVERLAP", 3: "ECC_ERR_RANGE",
                 4: "ECC_ERR_ALLOC", 5: "ECC_ERR_DEVICE", 6: "ECC_ERR_STATE"}
@@ -62,6 +63,7 @@ _SIGS = [
     ("ecc_matrix_create", ctypes.c_int, [_VP, ctypes.POINTER(ecc_csr_t), _I32, ctypes.POINTER(_VP)]),
     ("ecc_matrix_destroy", ctypes.c_int, [_VP]),
     ("ecc_partials_size", _I64, [_VP]),
+    ("ecc_matrix_layout", ctypes.c_int, [_VP, _VP, _VP]),
     ("ecc_iterate_jacobi", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     ("ecc_iterate_spmv", ctypes.c_int, [_VP, _VP, _D, _D, _VP, _VP, _VP, _VP]),
     ("ecc_residual", ctypes.c_int, [_VP, _VP, _I64, _I32, _VP, _VP]),
@@ -219,6 +221,13 @@ def ecc_matrix_destroy(mat):
 
 def ecc_partials_size(mat) -> int:
     return int(lib().ecc_partials_size(mat))
+
+
+def ecc_matrix_layout(mat):
+    """(layout, entries held per row) of a matrix handle."""
+    layout, slots = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(lib().ecc_matrix_layout(mat, ctypes.byref(layout), ctypes.byref(slots)))
+    return layout.value, slots.value
 
 
 def ecc_iterate_jacobi(plan, mat, d_b, d_x_own, d_x_hat, d_x_next, d_partials):

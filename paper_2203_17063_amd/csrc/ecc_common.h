@@ -295,6 +295,8 @@ struct ecc_matrix_s {
     int32_t short_r = ecc::kShortRow;  // short layout: entries per row the kernel holds (>= longest row)
     int64_t bandwidth = 0;          // max |col - row|
     int32_t *d_rowlist = nullptr;   // rows of the row-list items, by rank and length class
+    int32_t *d_ell_col = nullptr;   // short layout: entries column-major, [R][n] (-1: padding)
+    double *d_ell_val = nullptr;    // short layout: their values, [R][n]
     double *d_partials = nullptr;   // internal partials of ecc_solve: 2 x (grid + 1)
 };
 

@@ -68,6 +68,7 @@ def test_null_handles_are_rejected_without_device():
     assert L.ecc_partials_size(None) == 0
     assert L.ecc_allgatherv_assemble(None, None, None, None, None, None) == E.ECC_ERR_ARG
     assert L.ecc_residual(None, None, 1, 2, None, None) == E.ECC_ERR_ARG
+    assert L.ecc_matrix_layout(None, None, None) == E.ECC_ERR_ARG
 
 
 def test_product_path_does_not_touch_oracle():

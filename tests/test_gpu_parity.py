@@ -431,6 +431,26 @@ def test_step_api_matches_solve():
         run.close()
 
 
+def test_layout_choice():
+    """The layout each kind of matrix gets: rows of at most 8 entries the
+    short-row layout (entries held per row after the longest row), regular
+    longer rows the stream layout, power-law rows the row-list layout."""
+    E, R = _capi(), _runner()
+    cases = [(W.config1(), E.ECC_LAYOUT_SHORT, 3), (W.config2(N=33, T=2), E.ECC_LAYOUT_SHORT, 5),
+             (W.config5(N=12, T=2, P=8), E.ECC_LAYOUT_SHORT, 7),
+             (_banded_problem("jacobi", 3000, 4, 4, T=2), E.ECC_LAYOUT_SHORT, 4),
+             (_banded_problem("power", 3000, 6, 6, T=2), E.ECC_LAYOUT_SHORT, 7),
+             (_banded_problem("jacobi", 3000, 9, 16, T=2), E.ECC_LAYOUT_STREAM, 0),
+             (W.config3(scale=10, T=2), E.ECC_LAYOUT_ROWS, 0)]
+    for prob, layout, slots in cases:
+        announce("layout", prob.name)
+        run = R.Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts, prob.S,
+                          prob.mask, prob.kind, b=prob.b, alpha=prob.alpha, beta=prob.beta,
+                          x0=prob.x0)
+        assert E.ecc_matrix_layout(run.mat) == (layout, slots), prob.name
+        run.close()
+
+
 def test_matrix_checks():
     E, R = _capi(), _runner()
     prob = W.config2(N=8, T=2)
