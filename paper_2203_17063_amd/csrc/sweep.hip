@@ -6,9 +6,9 @@
 //
 // Work decomposition (built once per matrix on the host, CSR-Adaptive style
 // after Greathouse & Daga, SC'14), in one of three layouts per matrix:
-//  - short rows (every row holds at most 8 entries): an item is a run of up
-//    to 256 rows of one rank, one lane per row reading its entries straight
-//    from memory, pipelined three items deep;
+//  - short rows (every row holds at most 8 entries): the entries are copied
+//    column-major at set-up; an item is a run of up to 256 rows of one rank,
+//    one lane per row, pipelined two items deep;
 //  - stream items for other regular matrices: a run of short rows of one
 //    rank whose nonzeros fit in LDS -- they are loaded with coalesced
 //    accesses and each row is then summed by 1..64 lanes;
