@@ -653,12 +653,13 @@ __global__ void k_build_ell(int32_t n, int32_t R, const int32_t *__restrict__ ro
 }
 
 // The short-row layout holds few values per lane: the register budget is
-// capped so that several waves share each SIMD -- as many as the row's
-// registers allow without spilling (R = 5 at 6 waves spills; measured on
-// MI355X, config 2: 20.3 us against 19.7 us at 5 waves).
+// capped so that as many waves share each SIMD as the row's registers allow
+// without spilling -- 8 for rows of up to 4 entries, 7 for 5, 5 for 7 or 8
+// (the fused Jacobi kernel: 61, 69 and 85-93 VGPRs; 8 waves at R = 5 would
+// spill).
 template <int R>
 constexpr int short_waves() {
-    return R <= 3 ? 8 : (R == 4 ? 7 : (R == 5 ? 5 : 4));
+    return R <= 4 ? 8 : (R == 5 ? 7 : 5);
 }
 template <int KIND, bool STEP, int R>
 __global__ __launch_bounds__(kSweepThreads) __attribute__((amdgpu_waves_per_eu(short_waves<R>())))
