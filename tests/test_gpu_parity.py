@@ -396,6 +396,39 @@ def test_solve_short_layout(kind, lmin, lmax):
     _solve_and_compare(_banded_problem(kind, 30000, lmin, lmax), bitwise=True)
 
 
+@pytest.mark.parametrize("kind", ["jacobi", "power"])
+@pytest.mark.parametrize("n,counts", [(1, [1]), (2, [0, 2, 0]), (255, [100, 0, 155]),
+                                      (257, [257]), (513, [0, 256, 1, 256])])
+def test_solve_tiny_and_ragged(kind, n, counts):
+    """Matrices of one row, a few rows, and just under / over a 256-row item,
+    with single-rank plans and ranks that own no rows: one-item grids, ragged
+    last items and empty ranks in the short-row layout."""
+    rng = np.random.default_rng(n + 7 * len(counts))
+    rows = []
+    for i in range(n):
+        c = np.unique(np.clip(np.array([i - 1, i, i + 1, i + 37]), 0, n - 1))
+        v = -rng.uniform(0.1, 1.0, c.size) / c.size
+        if kind == "jacobi":
+            v[c == i] = 2.0 * np.abs(v).sum() + 1.0
+        rows.append((c, v))
+    rp = np.zeros(n + 1, dtype=np.int32)
+    rp[1:] = np.cumsum([c.size for c, _ in rows])
+    A = W.CSR(n, n, rp, np.concatenate([c for c, _ in rows]).astype(np.int32),
+              np.abs(np.concatenate([v for _, v in rows])) if kind == "power"
+              else np.concatenate([v for _, v in rows]))
+    counts = np.array(counts, dtype=np.int64)
+    P, T = counts.size, 12
+    mask = (rng.random((T, P)) < 0.6).astype(np.uint8)
+    mask[0] = 1
+    if kind == "jacobi":
+        prob = W.Iterative("tiny-jacobi", "jacobi", A, counts, W.exclusive_scan(counts), 2, mask,
+                           T, np.zeros(n), b=rng.standard_normal(n), norm=2)
+    else:
+        prob = W.Iterative("tiny-power", "power", A, counts, W.exclusive_scan(counts), 2, mask, T,
+                           np.full(n, 1.0 / n), alpha=0.85, beta=0.15 / n, norm=1)
+    _solve_and_compare(prob, bitwise=True)
+
+
 def test_solve_arrow_split_rows():
     _solve_and_compare(_arrow_problem(), bitwise=False)
 
