@@ -429,6 +429,48 @@ def test_solve_tiny_and_ragged(kind, n, counts):
     _solve_and_compare(prob, bitwise=True)
 
 
+@pytest.mark.parametrize("seed", range(20))
+def test_solve_random_shapes(seed):
+    """Random sizes (1-5,000 rows), row lengths (0-12 entries, so both the
+    short-row and the stream layouts), rank counts (1-12, some empty),
+    staleness bounds and arrival rates, Jacobi or PageRank; compared with the
+    oracle at every iteration."""
+    rng = np.random.default_rng(1000 + seed)
+    n = int(rng.integers(1, 5001))
+    kind = "jacobi" if seed % 2 == 0 else "power"
+    lmax = int(rng.integers(1, 13))
+    band = int(rng.integers(1, max(2, n)))
+    rows = []
+    for i in range(n):
+        ln = int(rng.integers(0 if kind == "power" else 1, lmax + 1))
+        lo, hi = max(0, i - band), min(n, i + band + 1)
+        c = np.sort(rng.choice(np.arange(lo, hi), min(ln, hi - lo), replace=False))
+        if kind == "jacobi" and i not in c:
+            c = np.sort(np.concatenate([c[1:], [i]])) if c.size else np.array([i])
+        v = rng.uniform(0.05, 1.0, c.size) / max(c.size, 1)
+        if kind == "jacobi":
+            v = -v
+            v[c == i] = 2.0 * np.abs(v).sum() + 1.0
+        rows.append((c.astype(np.int64), v))
+    rp = np.zeros(n + 1, dtype=np.int32)
+    rp[1:] = np.cumsum([c.size for c, _ in rows])
+    A = W.CSR(n, n, rp, np.concatenate([c for c, _ in rows]).astype(np.int32),
+              np.concatenate([v for _, v in rows]))
+    P = int(rng.integers(1, 13))
+    cuts = np.sort(rng.integers(0, n + 1, P - 1))
+    counts = np.diff(np.concatenate([[0], cuts, [n]])).astype(np.int64)
+    T, S = 15, int(rng.integers(0, 4))
+    mask = (rng.random((T, P)) < rng.uniform(0.3, 1.0)).astype(np.uint8)
+    mask[0] = 1
+    if kind == "jacobi":
+        prob = W.Iterative("random-jacobi", "jacobi", A, counts, W.exclusive_scan(counts), S,
+                           mask, T, np.zeros(n), b=rng.standard_normal(n), norm=2)
+    else:
+        prob = W.Iterative("random-power", "power", A, counts, W.exclusive_scan(counts), S,
+                           mask, T, np.full(n, 1.0 / n), alpha=0.85, beta=0.15 / n, norm=1)
+    _solve_and_compare(prob, bitwise=lmax <= 16)
+
+
 def test_solve_arrow_split_rows():
     _solve_and_compare(_arrow_problem(), bitwise=False)
 
