@@ -212,13 +212,16 @@ ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *con
  *                      copied, column-major and padded to the longest row's
  *                      class R in {3, 4, 5, 7, 8} (12 bytes x R x n_rows of
  *                      device memory), one lane per row;
- *   ECC_LAYOUT_ROWS    very uneven rows (longest > 64 and > 8 x (mean + 1)):
- *                      rows binned by length;
+ *   ECC_LAYOUT_SORTED  very uneven rows (longest > 64 and > 8 x (mean + 1)):
+ *                      the rows of every rank are copied in order of
+ *                      decreasing length (12 bytes x nnz + 8 bytes x n_rows
+ *                      of device memory) and swept in runs staged in LDS;
  *   ECC_LAYOUT_STREAM  otherwise: runs of rows staged in LDS.
- * The matrix arrays must outlive the handle and stay unchanged (the last two
- * layouts read them at every sweep). */
+ * ECC_LAYOUT_STREAM reads the matrix arrays at every sweep: they must then
+ * outlive the handle and stay unchanged.  The other two layouts sweep the
+ * copy made here. */
 #define ECC_LAYOUT_STREAM 0
-#define ECC_LAYOUT_ROWS 1
+#define ECC_LAYOUT_SORTED 1
 #define ECC_LAYOUT_SHORT 2
 ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
                                ecc_matrix_t *out);

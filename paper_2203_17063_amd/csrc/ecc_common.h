@@ -74,15 +74,17 @@ struct Tile {
 
 // One sweep work item: rows [row0, row0 + nrows) of rank `rank`, whose block
 // is [lo, hi), touching nonzeros [k0, k1).  kind: stream (many short rows
-// staged in LDS), vector (one long row, whole workgroup), piece (slice
-// [k0, k1) of a very long row; its partial sum goes to piece slot `slot`) or
-// rows (entries [k0, k1) of the row list: rows of similar length, `slot`
-// lanes each).
-enum { kItemStream = 0, kItemVector = 1, kItemPiece = 2, kItemRows = 3 };
-// Sweep layouts of a matrix: stream items staged through LDS; row-list items
-// binned by length (very uneven rows); short-row items, one lane per row
-// read directly (every row holds at most kShortRow entries).
-enum { kLayStream = 0, kLayRows = 1, kLayShort = 2 };
+// staged in LDS), vector (one long row, whole workgroup) or piece (slice
+// [k0, k1) of a very long row; its partial sum goes to piece slot `slot`).
+// In the sorted layout, row0 of a stream item and [k0, k1) of every item
+// refer to the sorted copy of the matrix; row0 of a vector item or a piece
+// is the row itself.
+enum { kItemStream = 0, kItemVector = 1, kItemPiece = 2 };
+// Sweep layouts of a matrix: stream items staged through LDS; the same over
+// a copy whose rows are sorted by decreasing length within each rank (very
+// uneven rows); short-row items, one lane per row read directly (every row
+// holds at most kShortRow entries).
+enum { kLayStream = 0, kLaySorted = 1, kLayShort = 2 };
 constexpr int kShortRow = 8;
 static_assert(kShortRow <= 8, "a short row is summed from eight registers");
 static_assert(kStreamRows <= 256 && kStreamRows <= kSweepThreads, "one lane per short row");
@@ -290,11 +292,14 @@ struct ecc_matrix_s {
     double2 *d_pieces = nullptr;    // (partial sum, diagonal) per piece
     int64_t n_pieces = 0;
     int32_t grid = 1;               // workgroups of a sweep launch
-    bool irregular = false;         // row lengths vary widely: row-list items
-    int layout = 0;                 // kLayStream, kLayRows or kLayShort
+    bool irregular = false;         // row lengths vary widely: sorted layout, items dealt round-robin
+    int layout = 0;                 // kLayStream, kLaySorted or kLayShort
     int32_t short_r = ecc::kShortRow;  // short layout: entries per row the kernel holds (>= longest row)
     int64_t bandwidth = 0;          // max |col - row|
-    int32_t *d_rowlist = nullptr;   // rows of the row-list items, by rank and length class
+    int32_t *d_order = nullptr;     // sorted layout: the row at each sorted position, [n]
+    int32_t *d_srow_ptr = nullptr;  // sorted layout: row pointers of the sorted copy, [n + 1]
+    int32_t *d_scol = nullptr;      // sorted layout: its column indices, [nnz]
+    double *d_sval = nullptr;       // sorted layout: its values, [nnz]
     int32_t *d_ell_col = nullptr;   // short layout: entries column-major, [R][n] (-1: padding)
     double *d_ell_val = nullptr;    // short layout: their values, [R][n]
     double *d_partials = nullptr;   // internal partials of ecc_solve: 2 x (grid + 1)

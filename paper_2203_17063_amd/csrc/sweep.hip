@@ -12,9 +12,11 @@
 //  - stream items for other regular matrices: a run of short rows of one
 //    rank whose nonzeros fit in LDS -- they are loaded with coalesced
 //    accesses and each row is then summed by 1..64 lanes;
-//  - row-list items for very uneven rows (power-law graphs): rows of one rank
-//    binned by length, 1, 4, 16 or 64 lanes per row, gathers of the vector
-//    as device-scope loads that skip the CU's L1.
+//  - sorted stream items for very uneven rows (power-law graphs): the same
+//    items over a copy of the matrix, made at set-up, whose rows are ordered
+//    by decreasing length within each rank, so that an item holds rows of
+//    similar length and its lanes split evenly over them; a map from sorted
+//    position to row places each result.
 // In the last two, a "vector" item is one long row summed by the whole
 // workgroup and a "piece" a fixed-size slice of a very long row whose
 // partial sum is recombined, in piece order, at the end.  Items never
@@ -60,7 +62,7 @@ struct SweepArgs {
     double *x_next;
     double *partials;
     double2 *pieces;
-    const int32_t *rowlist;
+    const int32_t *order;    // sorted layout: the row at each sorted position
     const int32_t *ell_col;  // short layout: column-major copy of the entries
     const double *ell_val;
     int64_t ell_n;
@@ -127,11 +129,8 @@ __device__ __forceinline__ bool col_arrives(const StepView &v, int32_t c, RankCa
     return e;
 }
 
-// A gather of the assembled vector.  DEV: a relaxed device-scope load, which
-// skips the CU's L1 -- for matrices with very uneven rows, whose random
-// gathers see little reuse there (measured on MI355X, PageRank on a scale-22
-// R-MAT graph: 683 against 709 us per sweep).
-template <bool STEP, bool DEV = false>
+// A gather of the assembled vector.
+template <bool STEP>
 __device__ __forceinline__ double view_load(int32_t c, int32_t lo, int32_t hi,
                                             const double *__restrict__ x_own,
                                             const double *__restrict__ x_hat,
@@ -140,9 +139,7 @@ __device__ __forceinline__ double view_load(int32_t c, int32_t lo, int32_t hi,
     if constexpr (STEP) {
         if (!own) own = col_arrives(sv, c, rc);
     }
-    const double *p = (own ? x_own : x_hat) + c;
-    if constexpr (DEV) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    else return *p;
+    return (own ? x_own : x_hat)[c];
 }
 
 // Row epilogue; returns the row's contribution to the norm (r_i^2 for Jacobi,
@@ -178,7 +175,7 @@ __device__ __forceinline__ int lanes_per_row(int32_t nnz, int32_t nr) {
 // order, W at a time: the next W (col, val) loads are in flight while the
 // current W gathers of y complete.  With stride 1 this is the row's CSR
 // order.  Jacobi skips (and records) the diagonal entry.
-template <int KIND, bool STEP, int W, bool DEV>
+template <int KIND, bool STEP, int W>
 __device__ __forceinline__ void seg_accumulate(int32_t i, int32_t k0, int32_t k1, int32_t stride,
                                                const SweepArgs &a, int32_t lo, int32_t hi,
                                                const StepView &sv, RankCache &rc, double &s,
@@ -196,7 +193,7 @@ __device__ __forceinline__ void seg_accumulate(int32_t i, int32_t k0, int32_t k1
         double y[W];
 #pragma unroll
         for (int u = 0; u < W; ++u)
-            y[u] = (k + u * stride < k1) ? view_load<STEP, DEV>(c[u], lo, hi, a.x_own, a.x_hat, sv, rc)
+            y[u] = (k + u * stride < k1) ? view_load<STEP>(c[u], lo, hi, a.x_own, a.x_hat, sv, rc)
                                           : 0.0;
         const int32_t kn = k + W * stride;
         int32_t cn[W];
@@ -222,43 +219,18 @@ __device__ __forceinline__ void seg_accumulate(int32_t i, int32_t k0, int32_t k1
     }
 }
 
-// A short row (at most 8 entries) on one lane, in CSR order, all gathers in
-// flight together.
-template <int KIND, bool STEP, bool DEV>
-__device__ __forceinline__ void short_row(int32_t i, int32_t ks, int32_t ke, const SweepArgs &a,
-                                          int32_t lo, int32_t hi, const StepView &sv,
-                                          RankCache &rc, double &s, double &dg) {
-    const int32_t len = ke - ks;
-    int32_t c8[8];
-    double v8[8], y8[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        c8[j] = (j < len) ? a.col[ks + j] : 0;
-        v8[j] = (j < len) ? a.val[ks + j] : 0.0;
-    }
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-        y8[j] = (j < len) ? view_load<STEP, DEV>(c8[j], lo, hi, a.x_own, a.x_hat, sv, rc) : 0.0;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        if (j < len) {
-            if (KIND == ECC_KIND_JACOBI && c8[j] == i) dg = v8[j];
-            else s = s + v8[j] * y8[j];
-        }
-    }
-}
-
 // Registers that carry the next stream item's data while the current one is
 // computed: its nonzeros (eight per thread, coalesced) and the per-row values
-// of the row this thread will finish.
+// of the row this thread will finish (ri: that row's index, which in the
+// sorted layout differs from its position).
 struct StreamPrefetch {
     int32_t cv[8];
     double vv[8];
-    int32_t rp0, rp1;
+    int32_t rp0, rp1, ri;
     double bi, xo;
 };
 
-template <int KIND>
+template <int KIND, int LAY>
 __device__ __forceinline__ void stream_load(const WorkItem &it, const SweepArgs &a,
                                             StreamPrefetch &pf) {
     const int tid = threadIdx.x;
@@ -274,12 +246,14 @@ __device__ __forceinline__ void stream_load(const WorkItem &it, const SweepArgs 
     }
     const int tpr = lanes_per_row(nnz, it.nrows);
     const int32_t rr = tid / tpr;
-    pf.rp0 = pf.rp1 = 0;
+    pf.rp0 = pf.rp1 = pf.ri = 0;
     pf.bi = pf.xo = 0.0;
     if (rr < it.nrows) {
-        const int32_t i = it.row0 + rr;
-        pf.rp0 = a.row_ptr[i];
-        pf.rp1 = a.row_ptr[i + 1];
+        const int32_t r = it.row0 + rr;
+        pf.rp0 = a.row_ptr[r];
+        pf.rp1 = a.row_ptr[r + 1];
+        const int32_t i = (LAY == kLaySorted) ? a.order[r] : r;
+        pf.ri = i;
         pf.xo = a.x_own[i];
         if (KIND == ECC_KIND_JACOBI) pf.bi = a.b[i];
     }
@@ -299,10 +273,11 @@ __device__ __forceinline__ void stream_stage(const WorkItem &it, const StreamPre
 }
 
 // The rows of a stream item from the staged nonzeros; returns this thread's
-// norm contribution.
+// norm contribution.  i: the index of the row this thread finishes.
 template <int KIND, bool STEP>
 __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0, int32_t rp1,
-                                                 double bi, double xo, const SweepArgs &a,
+                                                 int32_t i, double bi, double xo,
+                                                 const SweepArgs &a,
                                                  const int32_t *s_col, const double *s_val,
                                                  const StepView &sv, RankCache &rc,
                                                  bool own_arrives) {
@@ -312,7 +287,6 @@ __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0
     const int lane = tid & (tpr - 1);
     const int32_t rr = tid / tpr;
     if (rr >= it.nrows) return 0.0;
-    const int32_t i = it.row0 + rr;
     const int32_t lo = it.lo, hi = it.hi;
     const int32_t rs = rp0 - it.k0, re = rp1 - it.k0;
     double s = 0.0, dg = 0.0;
@@ -367,15 +341,14 @@ __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0
 
 // One long row (or a slice of it) by the whole workgroup; returns the norm
 // contribution (in thread 0).
-template <int KIND, bool STEP, bool DEV>
+template <int KIND, bool STEP>
 __device__ __forceinline__ double long_compute(const WorkItem &it, const SweepArgs &a,
                                                const StepView &sv, RankCache &rc,
                                                bool own_arrives, double *s_red) {
     const int tid = threadIdx.x;
     const int32_t i = it.row0, lo = it.lo, hi = it.hi;
     double s = 0.0, dg = 0.0;
-    seg_accumulate<KIND, STEP, 4, DEV>(i, it.k0 + tid, it.k1, kSweepThreads, a, lo, hi, sv, rc, s,
-                                       dg);
+    seg_accumulate<KIND, STEP, 4>(i, it.k0 + tid, it.k1, kSweepThreads, a, lo, hi, sv, rc, s, dg);
     s = block_sum<kSweepThreads>(s, s_red);
     if (KIND == ECC_KIND_JACOBI) dg = block_sum<kSweepThreads>(dg, s_red);
     if (tid != 0) return 0.0;
@@ -383,36 +356,6 @@ __device__ __forceinline__ double long_compute(const WorkItem &it, const SweepAr
         a.pieces[it.slot] = make_double2(s, dg);
         return 0.0;
     }
-    const double xo = a.x_own[i];
-    const double bi = (KIND == ECC_KIND_JACOBI) ? a.b[i] : 0.0;
-    if (STEP && own_arrives) a.x_hat[i] = xo;
-    return row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
-}
-
-// A row-list item: rows of similar length, `tpr` lanes per row reading the
-// row's nonzeros directly (contiguous per row); rows of one lane are summed
-// in CSR order.  Returns this thread's norm contribution.
-template <int KIND, bool STEP>
-__device__ __forceinline__ double rows_compute(const WorkItem &it, const SweepArgs &a,
-                                               const StepView &sv, RankCache &rc,
-                                               bool own_arrives) {
-    const int tid = threadIdx.x;
-    const int tpr = it.slot;
-    const int lane = tid & (tpr - 1);
-    const int32_t li = it.k0 + tid / tpr;
-    if (li >= it.k1) return 0.0;
-    const int32_t i = a.rowlist[li];
-    const int32_t lo = it.lo, hi = it.hi;
-    const int32_t ks = a.row_ptr[i], ke = a.row_ptr[i + 1];
-    double s = 0.0, dg = 0.0;
-    if (tpr == 1) {
-        short_row<KIND, STEP, true>(i, ks, ke, a, lo, hi, sv, rc, s, dg);  // class of rows <= 8
-    } else {
-        seg_accumulate<KIND, STEP, 4, true>(i, ks + lane, ke, tpr, a, lo, hi, sv, rc, s, dg);
-        s = group_sum_dyn(s, tpr);
-        if (KIND == ECC_KIND_JACOBI) dg = group_sum_dyn(dg, tpr);
-    }
-    if (lane != 0) return 0.0;
     const double xo = a.x_own[i];
     const double bi = (KIND == ECC_KIND_JACOBI) ? a.b[i] : 0.0;
     if (STEP && own_arrives) a.x_hat[i] = xo;
@@ -471,15 +414,15 @@ __device__ __forceinline__ void sweep_prologue(const SweepArgs &a, uint8_t *s_ef
     if constexpr (STEP) __syncthreads();
 }
 
-// LAY selects the layout: stream items staged through LDS (kLayStream) or
-// row-list items for matrices with very uneven rows (kLayRows); both may
-// contain vector items and pieces.  The short-row layout has its own body.
+// LAY selects the layout: stream items over the matrix (kLayStream) or over
+// its sorted copy (kLaySorted); both may contain vector items and pieces.
+// The short-row layout has its own body.
 template <int KIND, bool STEP, int LAY>
 __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
-    constexpr bool STAGED = LAY == kLayStream;
+    static_assert(LAY == kLayStream || LAY == kLaySorted, "stream layouts only");
     // padded by 8 so that a row's first eight entries can be read unclamped
-    __shared__ int32_t s_col[STAGED ? kStreamCap + 8 : 1];
-    __shared__ double s_val[STAGED ? kStreamCap + 8 : 1];
+    __shared__ int32_t s_col[kStreamCap + 8];
+    __shared__ double s_val[kStreamCap + 8];
     __shared__ double s_red[kSweepThreads / 64];
     __shared__ uint8_t s_eff[STEP ? kFusedMaxP : 1];
     __shared__ int32_t s_bs[STEP ? kFusedMaxP + 1 : 1];
@@ -495,7 +438,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
     const bool have0 = w < i_end;
     if (have0) {
         cur = a.items[w];
-        if (STAGED && cur.kind == kItemStream) stream_load<KIND>(cur, a, pf);
+        if (cur.kind == kItemStream) stream_load<KIND, LAY>(cur, a, pf);
     }
     bool have_next = (int64_t)w + w_step < i_end;
     if (have_next) nxt = a.items[w + w_step];
@@ -511,28 +454,23 @@ __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
     bool have = have0;
     while (have) {
         const bool own_arrives = STEP && s_eff[cur.rank] != 0;
-        const bool next_stream = STAGED && have_next && nxt.kind == kItemStream;
+        const bool next_stream = have_next && nxt.kind == kItemStream;
         WorkItem nn{};
         const bool have_nn = (int64_t)w + 2 * (int64_t)w_step < i_end;
-        if (STAGED && cur.kind == kItemStream) {
+        if (cur.kind == kItemStream) {
             stream_stage(cur, pf, s_col, s_val);
-            const int32_t rp0 = pf.rp0, rp1 = pf.rp1;
+            const int32_t rp0 = pf.rp0, rp1 = pf.rp1, ri = pf.ri;
             const double bi = pf.bi, xo = pf.xo;
             __syncthreads();
-            if (next_stream) stream_load<KIND>(nxt, a, pf);
+            if (next_stream) stream_load<KIND, LAY>(nxt, a, pf);
             if (have_nn) nn = a.items[w + 2 * w_step];
-            contrib += stream_compute<KIND, STEP>(cur, rp0, rp1, bi, xo, a, s_col, s_val, sv, rc,
-                                                  own_arrives);
+            contrib += stream_compute<KIND, STEP>(cur, rp0, rp1, ri, bi, xo, a, s_col, s_val, sv,
+                                                  rc, own_arrives);
             __syncthreads();  // LDS is reused by the next item
-        } else if (LAY == kLayRows && cur.kind == kItemRows) {
-            if (have_nn) nn = a.items[w + 2 * w_step];
-            contrib += rows_compute<KIND, STEP>(cur, a, sv, rc, own_arrives);
-            if (next_stream) stream_load<KIND>(nxt, a, pf);
         } else {
             if (have_nn) nn = a.items[w + 2 * w_step];
-            contrib += long_compute<KIND, STEP, LAY == kLayRows>(cur, a, sv, rc, own_arrives,
-                                                                 s_red);
-            if (next_stream) stream_load<KIND>(nxt, a, pf);
+            contrib += long_compute<KIND, STEP>(cur, a, sv, rc, own_arrives, s_red);
+            if (next_stream) stream_load<KIND, LAY>(nxt, a, pf);
         }
         w += w_step;
         have = have_next;
@@ -777,11 +715,11 @@ __global__ void k_check(int32_t n_rows, int32_t n_cols, const int32_t *__restric
 
 // Work items of a matrix for a plan's row blocks.  Rows longer than one LDS
 // stage become vector items (one workgroup) or pieces of kVectorCap nonzeros
-// (recombined in order); they come first.  The other rows form, for a
-// regular matrix, runs of consecutive short rows (stream items); for a
-// matrix whose row lengths vary widely (longest row > 64 and > 8 x (mean +
-// 1)), row-list items of one length class per rank: <= 8 nonzeros with one
-// lane per row, <= 32 with 4, <= 128 with 16, longer with 64.
+// (recombined in order); they come first.  The other rows form runs of
+// consecutive rows (stream items) of up to kStreamRows rows and kStreamCap
+// nonzeros.  rp holds the row pointers the items address; with `order` (the
+// sorted layout) row position r holds row order[r]: stream items keep
+// positions, vector items, pieces and fixups name the row itself.
 static bool rows_irregular(const std::vector<int32_t> &rp) {
     const int64_t n = (int64_t)rp.size() - 1;
     if (n <= 0) return false;
@@ -792,15 +730,10 @@ static bool rows_irregular(const std::vector<int32_t> &rp) {
 }
 
 static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_t> &counts,
-                        bool irregular, std::vector<WorkItem> &items,
-                        std::vector<Fixup> &fixups, std::vector<int32_t> &rowlist,
-                        int64_t &n_pieces) {
+                        const std::vector<int32_t> *order, std::vector<WorkItem> &items,
+                        std::vector<Fixup> &fixups, int64_t &n_pieces) {
     std::vector<WorkItem> big, vec, stream;
-    std::vector<WorkItem> cls[4];
-    static const int kClassMax[4] = {8, 32, 128, kStreamCap};
-    static const int kClassLanes[4] = {1, 4, 16, 64};
     n_pieces = 0;
-    rowlist.clear();
     int64_t row = 0;
     auto make = [](int64_t r0, int64_t nr, int64_t k0, int64_t k1, int64_t lo, int64_t hi,
                    int kind, int64_t p, int64_t slot) {
@@ -818,30 +751,23 @@ static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_
     };
     for (size_t p = 0; p < counts.size(); ++p) {
         const int64_t lo = row, hi = row + counts[p];
-        std::vector<int32_t> by_class[4];
         int64_t i = lo;
         while (i < hi) {
             const int64_t len = (int64_t)rp[i + 1] - rp[i];
             if (len > kStreamCap) {
+                const int64_t ri = order ? (*order)[i] : i;
                 if (len <= kVectorCap) {
-                    vec.push_back(make(i, 1, rp[i], rp[i + 1], lo, hi, kItemVector, p, 0));
+                    vec.push_back(make(ri, 1, rp[i], rp[i + 1], lo, hi, kItemVector, p, 0));
                 } else {
                     const int32_t np = (int32_t)((len + kVectorCap - 1) / kVectorCap);
-                    fixups.push_back({(int32_t)i, (int32_t)n_pieces, np, (int32_t)p});
+                    fixups.push_back({(int32_t)ri, (int32_t)n_pieces, np, (int32_t)p});
                     for (int32_t j = 0; j < np; ++j) {
                         const int64_t ka = rp[i] + (int64_t)j * kVectorCap;
                         const int64_t kb = std::min<int64_t>(rp[i + 1], ka + kVectorCap);
-                        big.push_back(make(i, 1, ka, kb, lo, hi, kItemPiece, p, n_pieces + j));
+                        big.push_back(make(ri, 1, ka, kb, lo, hi, kItemPiece, p, n_pieces + j));
                     }
                     n_pieces += np;
                 }
-                ++i;
-                continue;
-            }
-            if (irregular) {
-                int c = 0;
-                while (len > kClassMax[c]) ++c;
-                by_class[c].push_back((int32_t)i);
                 ++i;
                 continue;
             }
@@ -855,34 +781,62 @@ static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_
             }
             stream.push_back(make(start, i - start, rp[start], rp[i], lo, hi, kItemStream, p, 0));
         }
-        for (int c = 0; c < 4; ++c) {
-            const int64_t per_item = kSweepThreads / kClassLanes[c];
-            const std::vector<int32_t> &rows = by_class[c];
-            for (size_t s0 = 0; s0 < rows.size(); s0 += per_item) {
-                const int64_t l0 = (int64_t)rowlist.size() + 0;
-                const size_t s1 = std::min(rows.size(), s0 + (size_t)per_item);
-                rowlist.insert(rowlist.end(), rows.begin() + s0, rows.begin() + s1);
-                cls[c].push_back(make(rows[s0], (int64_t)(s1 - s0), l0, l0 + (int64_t)(s1 - s0),
-                                      lo, hi, kItemRows, p, kClassLanes[c]));
-            }
-        }
         row = hi;
     }
     items.clear();
     items.insert(items.end(), big.begin(), big.end());
     items.insert(items.end(), vec.begin(), vec.end());
-    for (int c = 3; c >= 0; --c) items.insert(items.end(), cls[c].begin(), cls[c].end());
     items.insert(items.end(), stream.begin(), stream.end());
+}
+
+// Sorted layout: the rows of every rank ordered by decreasing length, ties in
+// row order.  Returns the row at each position and the row pointers of the
+// sorted copy.
+static void sort_rows(const std::vector<int32_t> &rp, const std::vector<int64_t> &counts,
+                      std::vector<int32_t> &order, std::vector<int32_t> &srp) {
+    const int64_t n = (int64_t)rp.size() - 1;
+    order.resize(n);
+    srp.assign(n + 1, 0);
+    int64_t lo = 0;
+    for (size_t p = 0; p < counts.size(); ++p) {
+        const int64_t hi = lo + counts[p];
+        for (int64_t i = lo; i < hi; ++i) order[i] = (int32_t)i;
+        std::stable_sort(order.begin() + lo, order.begin() + hi, [&](int32_t x, int32_t y) {
+            return rp[x + 1] - rp[x] > rp[y + 1] - rp[y];
+        });
+        lo = hi;
+    }
+    for (int64_t r = 0; r < n; ++r) srp[r + 1] = srp[r] + (rp[order[r] + 1] - rp[order[r]]);
+}
+
+// Copies row order[r] of the matrix to position r of the sorted copy, one
+// wave per row.
+__global__ void k_sort_rows(int32_t n, const int32_t *__restrict__ order,
+                            const int32_t *__restrict__ row_ptr,
+                            const int32_t *__restrict__ srow_ptr, const int32_t *__restrict__ col,
+                            const double *__restrict__ val, int32_t *__restrict__ scol,
+                            double *__restrict__ sval) {
+    const int lane = threadIdx.x & 63;
+    const int64_t per_block = blockDim.x / 64;
+    const int64_t waves = (int64_t)gridDim.x * per_block;
+    for (int64_t r = (int64_t)blockIdx.x * per_block + threadIdx.x / 64; r < n; r += waves) {
+        const int32_t i = order[r];
+        const int32_t src = row_ptr[i], len = row_ptr[i + 1] - src, dst = srow_ptr[r];
+        for (int32_t k = lane; k < len; k += 64) {
+            scol[dst + k] = col[src + k];
+            sval[dst + k] = val[src + k];
+        }
+    }
 }
 
 // Workgroups of a sweep: as many as the device holds at once (each then
 // walks several items through the load/compute pipeline), at most one per
 // item, rounded down to a multiple of the 8 XCDs.
 // Occupancy of the kernel a loop iteration launches: the fused one, except
-// for the row-list layout, which is never fused.
+// for the sorted layout, which is never fused.
 template <int LAY>
 static hipError_t sweep_occupancy(int *per_cu, int kind) {
-    constexpr bool S = LAY != kLayRows;
+    constexpr bool S = LAY != kLaySorted;
     return kind == ECC_KIND_JACOBI
                ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
                      per_cu, k_sweep<ECC_KIND_JACOBI, S, LAY>, kSweepThreads, 0)
@@ -920,7 +874,7 @@ static int32_t sweep_grid(int64_t n_items, int kind, int layout, int32_t short_r
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         cus = 256;
-    const hipError_t e = layout == kLayRows    ? sweep_occupancy<kLayRows>(&per_cu, kind)
+    const hipError_t e = layout == kLaySorted  ? sweep_occupancy<kLaySorted>(&per_cu, kind)
                          : layout == kLayShort ? short_occupancy(&per_cu, kind, short_r)
                                                : sweep_occupancy<kLayStream>(&per_cu, kind);
     if (e != hipSuccess || per_cu < 1) per_cu = 4;
@@ -936,8 +890,8 @@ static int32_t sweep_grid(int64_t n_items, int kind, int layout, int32_t short_r
 template <int K, bool S>
 static void launch_layout(ecc_matrix_t M, dim3 grid, dim3 block, hipStream_t st,
                           const SweepArgs &a) {
-    if (M->layout == kLayRows) {
-        if constexpr (!S) hipLaunchKernelGGL((k_sweep<K, S, kLayRows>), grid, block, 0, st, a);
+    if (M->layout == kLaySorted) {
+        if constexpr (!S) hipLaunchKernelGGL((k_sweep<K, S, kLaySorted>), grid, block, 0, st, a);
     } else if (M->layout == kLayShort) {
         switch (short_class(M->short_r)) {
             case 3: hipLaunchKernelGGL((k_sweep_short<K, S, 3>), grid, block, 0, st, a); break;
@@ -956,9 +910,10 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     SweepArgs a{};
     a.items = M->d_items;
     a.n_items = (int32_t)M->n_items;
-    a.row_ptr = M->A.d_row_ptr;
-    a.col = M->A.d_col;
-    a.val = M->A.d_val;
+    const bool sorted = M->layout == kLaySorted;
+    a.row_ptr = sorted ? M->d_srow_ptr : M->A.d_row_ptr;
+    a.col = sorted ? M->d_scol : M->A.d_col;
+    a.val = sorted ? M->d_sval : M->A.d_val;
     a.b = L.b;
     a.alpha = L.alpha;
     a.beta = L.beta;
@@ -967,7 +922,7 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     a.x_next = L.x_next;
     a.partials = L.partials;
     a.pieces = M->d_pieces;
-    a.rowlist = M->d_rowlist;
+    a.order = M->d_order;
     a.ell_col = M->d_ell_col;
     a.ell_val = M->d_ell_val;
     a.ell_n = M->A.n_rows;
@@ -980,7 +935,7 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     const bool step = L.arrived != nullptr;
     if (step) {
         const int64_t t = pl->clock;
-        if (pl->P > kFusedMaxP || !pl->d_block_start || M->layout == kLayRows) {
+        if (pl->P > kFusedMaxP || !pl->d_block_start || M->layout == kLaySorted) {
             set_error("internal: fused step does not fit the plan or the matrix");
             return ECC_ERR_STATE;
         }
@@ -1113,8 +1068,14 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
 
     std::vector<WorkItem> items;
     std::vector<Fixup> fixups;
-    std::vector<int32_t> rowlist;
     int64_t n_pieces = 0;
+    // Sorted layout for matrices whose row lengths vary widely (power-law
+    // graphs): in row order, neighbouring rows differ so much in length that
+    // no split of an item's lanes suits them all.  Measured on MI355X
+    // (PageRank on a scale-22 R-MAT graph, 64 ranks): 544 against 644 us per
+    // sweep for rows binned into length classes read in place, whose
+    // scattered row reads kept the texture address units busier than the
+    // gathers of x do.
     const bool irregular = rows_irregular(rp);
     // Short-row layout, over a column-major copy of the entries, for
     // matrices whose rows all hold at most kShortRow entries.  Measured on
@@ -1124,8 +1085,14 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     int32_t max_row = 0;
     for (int64_t i = 0; i < n; ++i) max_row = std::max(max_row, rp[i + 1] - rp[i]);
     const bool short_rows = max_row <= kShortRow;
-    const int layout = irregular ? kLayRows : (short_rows ? kLayShort : kLayStream);
-    build_items(rp, plan->counts, irregular, items, fixups, rowlist, n_pieces);
+    const int layout = irregular ? kLaySorted : (short_rows ? kLayShort : kLayStream);
+    std::vector<int32_t> order, srp;
+    if (irregular) {
+        sort_rows(rp, plan->counts, order, srp);
+        build_items(srp, plan->counts, &order, items, fixups, n_pieces);
+    } else {
+        build_items(rp, plan->counts, nullptr, items, fixups, n_pieces);
+    }
     if ((int64_t)items.size() >= (int64_t(1) << 31)) {
         set_error("too many work items");
         return ECC_ERR_RANGE;
@@ -1168,12 +1135,25 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     }
     if (n_pieces > 0 && hipMalloc((void **)&M->d_pieces, sizeof(double2) * n_pieces) != hipSuccess)
         return fail("hipMalloc of piece sums failed");
-    if (!rowlist.empty()) {
-        if (hipMalloc((void **)&M->d_rowlist, sizeof(int32_t) * rowlist.size()) != hipSuccess)
-            return fail("hipMalloc of the row list failed");
-        if (hipMemcpy(M->d_rowlist, rowlist.data(), sizeof(int32_t) * rowlist.size(),
+    if (layout == kLaySorted && n > 0) {
+        if (hipMalloc((void **)&M->d_order, sizeof(int32_t) * n) != hipSuccess ||
+            hipMalloc((void **)&M->d_srow_ptr, sizeof(int32_t) * (n + 1)) != hipSuccess ||
+            hipMalloc((void **)&M->d_scol, sizeof(int32_t) * std::max<int64_t>(1, A->nnz)) !=
+                hipSuccess ||
+            hipMalloc((void **)&M->d_sval, sizeof(double) * std::max<int64_t>(1, A->nnz)) !=
+                hipSuccess)
+            return fail("hipMalloc of the sorted copy failed");
+        if (hipMemcpy(M->d_order, order.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice) !=
+                hipSuccess ||
+            hipMemcpy(M->d_srow_ptr, srp.data(), sizeof(int32_t) * (n + 1),
                       hipMemcpyHostToDevice) != hipSuccess)
-            return fail("copy of the row list failed");
+            return fail("copy of the row order failed");
+        const int blocks = (int)std::min<int64_t>(65536, (n + 3) / 4);
+        hipLaunchKernelGGL(k_sort_rows, dim3(blocks), dim3(256), 0, plan->stream, (int32_t)n,
+                           M->d_order, A->d_row_ptr, M->d_srow_ptr, A->d_col, A->d_val, M->d_scol,
+                           M->d_sval);
+        if (hipGetLastError() != hipSuccess || hipStreamSynchronize(plan->stream) != hipSuccess)
+            return fail("building the sorted copy failed");
     }
     if (layout == kLayShort && n > 0) {
         const int32_t R = short_class(M->short_r);
@@ -1201,7 +1181,10 @@ ecc_status_t ecc_matrix_destroy(ecc_matrix_t M) {
     (void)hipFree(M->d_fixups);
     (void)hipFree(M->d_pieces);
     (void)hipFree(M->d_partials);
-    (void)hipFree(M->d_rowlist);
+    (void)hipFree(M->d_order);
+    (void)hipFree(M->d_srow_ptr);
+    (void)hipFree(M->d_scol);
+    (void)hipFree(M->d_sval);
     (void)hipFree(M->d_ell_col);
     (void)hipFree(M->d_ell_val);
     delete M;
@@ -1213,7 +1196,7 @@ ecc_status_t ecc_matrix_layout(ecc_matrix_t M, int32_t *layout, int32_t *row_slo
     ECC_ARG(M != nullptr, "matrix is NULL");
     ECC_ARG(layout != nullptr && row_slots != nullptr, "NULL output");
     *layout = M->layout == kLayShort ? ECC_LAYOUT_SHORT
-              : M->layout == kLayRows ? ECC_LAYOUT_ROWS
+              : M->layout == kLaySorted ? ECC_LAYOUT_SORTED
                                       : ECC_LAYOUT_STREAM;
     *row_slots = M->layout == kLayShort ? short_class(M->short_r) : 0;
     return ECC_OK;

@@ -255,12 +255,15 @@ def _floor(prob, x):
     return float(np.sum(prob.alpha * wx + prob.beta + np.abs(x)))
 
 
-def _solve_and_compare(prob, bitwise, threads=8):
+def _solve_and_compare(prob, bitwise, threads=8, layout=None):
     R = _runner()
     announce("solve", prob.name, prob.n, prob.A.nnz, prob.P, prob.T)
     run = R.Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts, prob.S,
                       prob.mask, prob.kind, b=prob.b, alpha=prob.alpha, beta=prob.beta,
                       x0=prob.x0)
+    if layout is not None:  # the layout by name: "SHORT", "STREAM" or "SORTED"
+        E = _capi()
+        assert E.ecc_matrix_layout(run.mat)[0] == getattr(E, "ECC_LAYOUT_" + layout)
     iters = run.solve(tol=prob.tol, histories=True)
     torch.cuda.synchronize()
     x = run.d_x.cpu().numpy()
@@ -310,7 +313,7 @@ def test_solve_config5_small(N, P):
 def test_solve_config3_small(scale):
     """Scale 15 has rows summed by a whole workgroup; scale 17 also has rows
     longer than one work item, split into pieces and recombined."""
-    _solve_and_compare(W.config3(scale=scale, T=60), bitwise=False)
+    _solve_and_compare(W.config3(scale=scale, T=60), bitwise=False, layout="SORTED")
 
 
 def test_solve_many_ranks_unfused():
@@ -472,7 +475,52 @@ def test_solve_random_shapes(seed):
 
 
 def test_solve_arrow_split_rows():
-    _solve_and_compare(_arrow_problem(), bitwise=False)
+    _solve_and_compare(_arrow_problem(), bitwise=False, layout="SORTED")
+
+
+def _powerlaw_problem(kind, n, counts, seed, T=25, S=2):
+    """Rows whose lengths follow a heavy tail (most hold a few entries, a few
+    hold thousands, one is split into pieces) at random columns: very uneven
+    rows, swept in the sorted layout.  PageRank rows may be empty."""
+    rng = np.random.default_rng(seed)
+    lens = np.minimum((rng.pareto(1.1, n) * 2.0).astype(np.int64), n - 1)
+    lens[rng.integers(0, n)] = n - 1                       # longer than one vector item
+    lens[rng.choice(n, 6, replace=False)] = rng.integers(2049, 9000, 6)  # whole-workgroup rows
+    rows = []
+    for i in range(n):
+        c = np.sort(rng.choice(n, int(lens[i]), replace=False))
+        if kind == "jacobi" and i not in c:
+            c = np.sort(np.concatenate([c[1:], [i]])) if c.size else np.array([i])
+        v = rng.uniform(0.05, 1.0, c.size) / max(c.size, 1)
+        if kind == "jacobi":
+            v = -v
+            v[c == i] = 2.0 * np.abs(v).sum() + 1.0
+        rows.append((c.astype(np.int64), v))
+    rp = np.zeros(n + 1, dtype=np.int32)
+    rp[1:] = np.cumsum([c.size for c, _ in rows])
+    A = W.CSR(n, n, rp, np.concatenate([c for c, _ in rows]).astype(np.int32),
+              np.concatenate([v for _, v in rows]))
+    counts = (W.dirichlet_partition(n, counts, seed) if isinstance(counts, int)
+              else np.array(counts, dtype=np.int64))
+    P = counts.size
+    mask = (rng.random((T, P)) < 0.7).astype(np.uint8)
+    mask[0] = 1
+    if kind == "jacobi":
+        return W.Iterative("powerlaw-jacobi", "jacobi", A, counts, W.exclusive_scan(counts), S,
+                           mask, T, np.zeros(n), b=rng.standard_normal(n), norm=2)
+    return W.Iterative("powerlaw-power", "power", A, counts, W.exclusive_scan(counts), S, mask, T,
+                       np.full(n, 1.0 / n), alpha=0.85, beta=0.15 / n, norm=1)
+
+
+@pytest.mark.parametrize("kind", ["jacobi", "power"])
+@pytest.mark.parametrize("counts", [[20000], [0, 3000, 0, 9000, 1000, 7000], 9])
+def test_solve_sorted_layout(kind, counts):
+    """Very uneven rows: each rank's rows are swept in order of decreasing
+    length from a copy, and every result goes back to its own row (Jacobi
+    finds each row's diagonal by the row's index).  One rank, ranks that own
+    no rows, and nine uneven ranks."""
+    prob = _powerlaw_problem(kind, 20000, counts, seed=31 + len(str(counts)))
+    _solve_and_compare(prob, bitwise=False, layout="SORTED")
 
 
 def test_solve_config3_tolerance_stop():
@@ -509,14 +557,14 @@ def test_step_api_matches_solve():
 def test_layout_choice():
     """The layout each kind of matrix gets: rows of at most 8 entries the
     short-row layout (entries held per row after the longest row), regular
-    longer rows the stream layout, power-law rows the row-list layout."""
+    longer rows the stream layout, power-law rows the sorted layout."""
     E, R = _capi(), _runner()
     cases = [(W.config1(), E.ECC_LAYOUT_SHORT, 3), (W.config2(N=33, T=2), E.ECC_LAYOUT_SHORT, 5),
              (W.config5(N=12, T=2, P=8), E.ECC_LAYOUT_SHORT, 7),
              (_banded_problem("jacobi", 3000, 4, 4, T=2), E.ECC_LAYOUT_SHORT, 4),
              (_banded_problem("power", 3000, 6, 6, T=2), E.ECC_LAYOUT_SHORT, 7),
              (_banded_problem("jacobi", 3000, 9, 16, T=2), E.ECC_LAYOUT_STREAM, 0),
-             (W.config3(scale=10, T=2), E.ECC_LAYOUT_ROWS, 0)]
+             (W.config3(scale=10, T=2), E.ECC_LAYOUT_SORTED, 0)]
     for prob, layout, slots in cases:
         announce("layout", prob.name)
         run = R.Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts, prob.S,
