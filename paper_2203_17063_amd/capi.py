@@ -21,7 +21,7 @@ ECC_UNBOUNDED = 0x7FFFFFFF
 ECC_NORM_L1, ECC_NORM_L2 = 1, 2
 ECC_KIND_JACOBI, ECC_KIND_POWER = 0, 1
 ECC_TIMING_ASSEMBLE, ECC_TIMING_ALLREDUCE, ECC_TIMING_SWEEP, ECC_TIMING_NORM = 0, 1, 2, 3
-ECC_TIMING_MF_GRAD, ECC_TIMING_MF_STEP = 4, 5
+ECC_TIMING_MF_GRAD, ECC_TIMING_MF_STEP, ECC_TIMING_KINDS = 4, 5, 6
 ECC_THRESHOLD_DATA, ECC_THRESHOLD_PROCS = 0, 1
 ECC_LAYOUT_STREAM, ECC_LAYOUT_SORTED, ECC_LAYOUT_SHORT = 0, 1, 2
 

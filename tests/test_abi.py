@@ -36,6 +36,26 @@ def test_library_loads_and_exports_header():
     assert E.ecc_abi_version() == 1
 
 
+def header_constants():
+    """Every integer constant the header defines: #define lines and the
+    status enum."""
+    text = open(os.path.join(ROOT, "include", "libecc.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    consts = {m.group(1): int(m.group(2), 0)
+              for m in re.finditer(r"^#define\s+(ECC_\w+)\s+((?:0x)?[0-9a-fA-F]+)\s*$", text,
+                                   flags=re.M)}
+    consts.update({m.group(1): int(m.group(2))
+                   for m in re.finditer(r"\b(ECC_(?:OK|ERR_\w+))\s*=\s*(\d+)", text)})
+    return consts
+
+
+def test_binding_constants_match_header():
+    consts = header_constants()
+    assert len(consts) >= 24
+    for name, value in consts.items():
+        assert getattr(E, name) == value, name
+
+
 def test_status_strings():
     for code, name in E.STATUS_NAMES.items():
         assert E.lib().ecc_status_string(code).decode() == name
