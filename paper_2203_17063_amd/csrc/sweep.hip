@@ -244,8 +244,16 @@ __device__ __forceinline__ void stream_load(const WorkItem &it, const SweepArgs 
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int32_t kc = min(it.k0 + tid + u * kSweepThreads, it.k1 - 1);
-            pf.cv[u] = a.col[kc];
-            pf.vv[u] = a.val[kc];
+            if constexpr (LAY == kLaySorted) {
+                // read-once streams that would otherwise evict lines of the
+                // gathered vector from L2 (measured on MI355X, PageRank on a
+                // scale-22 R-MAT graph: 573 against 600 us per sweep)
+                pf.cv[u] = __builtin_nontemporal_load(a.col + kc);
+                pf.vv[u] = __builtin_nontemporal_load(a.val + kc);
+            } else {
+                pf.cv[u] = a.col[kc];
+                pf.vv[u] = a.val[kc];
+            }
         }
     }
     const int tpr = lanes_per_row(nnz, it.nrows);
