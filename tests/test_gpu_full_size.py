@@ -58,3 +58,81 @@ def test_config4a_full():
     assert clock == prob.reps and forced == 0
     assert (version == prob.reps - 1).all() and (age == 0).all()
     plan.close()
+
+
+def test_hypercube_full_sampled():
+    """allreduce_SSP at the benchmark's shape: 32 processes x 16 MB, slack 2,
+    Bernoulli(0.8) delivery, all 100 calls with the benchmark's two
+    contribution sets alternating.  Element j of every result depends only on
+    element j of the contributions and of the slots (the decisions only on
+    clocks), so the oracle runs on 4,096 sampled elements; those results, the
+    result clocks, the slot outcomes and the wait count match bit for bit."""
+    from oracle import hypercube as H
+    from paper_2203_17063_amd import capi as E
+    prob = W.hypercube_ssp()
+    P, m, d, T = prob.P, prob.m, prob.d, prob.calls
+    announce("hypercube full", P, m, prob.slack, T)
+    rng = np.random.default_rng(11)
+    idx = np.unique(np.concatenate([[0, m - 1], rng.choice(m, 4094, replace=False)]))
+    c_h = [prob.contrib(t) for t in range(2)]
+    ref_res, ref_clk, ref_out, ref_state = H.run(
+        P, prob.slack, np.stack([c_h[t & 1][:, idx] for t in range(T)]), prob.delivered[:T])
+    contrib = [torch.from_numpy(c).cuda() for c in c_h]
+    del c_h
+    stream = torch.cuda.current_stream().cuda_stream
+    result = torch.empty((P, m), dtype=torch.float64, device="cuda")
+    d_idx = torch.from_numpy(idx).cuda()
+    d_del = torch.from_numpy(prob.delivered.astype(np.uint8)).cuda()
+    d_clk = torch.empty(P, dtype=torch.int32, device="cuda")
+    d_out = torch.empty((P, d), dtype=torch.uint8, device="cuda")
+    h = E.ecc_hypercube_create(P, m, prob.slack, stream)
+    try:
+        for t in range(T):
+            E.ecc_allreduce_ssp(h, contrib[t & 1], d_del[t], result, d_clk, d_out)
+            got = result[:, d_idx].cpu().numpy()
+            assert np.array_equal(got, ref_res[t]), (t, np.abs(got - ref_res[t]).max())
+            assert np.array_equal(d_clk.cpu().numpy(), ref_clk[t]), t
+            assert np.array_equal(d_out.cpu().numpy(), ref_out[t]), t
+        clock, waits, _, _ = E.ecc_hypercube_stats(h, P)
+        assert clock == T and waits == int(ref_state.waits.sum())
+    finally:
+        E.ecc_hypercube_destroy(h)
+
+
+def test_threshold_full():
+    """Threshold Broadcast then Reduce at the benchmark's shape (32
+    processes, 8,388,608 doubles, data fraction 0.5, root 0), two repetitions
+    in the benchmark's order: the broadcast overwrites every receiver's
+    prefix, which the reduce then sums.  Bit for bit with the oracle on the
+    full vectors, the untouched tail of the result included."""
+    from oracle import threshold as TH
+    from paper_2203_17063_amd import capi as E
+    prob = W.threshold_collectives()
+    P, m, theta = prob.P, prob.m, prob.theta
+    announce("threshold full", P, m, theta)
+    xs_h = [prob.vector(p) for p in range(P)]
+    res_h = np.full(m, -2.5)
+    vecs = [torch.from_numpy(x).cuda() for x in xs_h]
+    result = torch.full((m,), -2.5, dtype=torch.float64, device="cuda")
+    d_vecs = torch.tensor([v.data_ptr() for v in vecs], dtype=torch.int64, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    for r in range(2):
+        k_ref = TH.bcast(P, 0, theta, xs_h[0], xs_h)
+        kr_ref, n_ref = TH.reduce(P, 0, theta, TH.DATA, xs_h, res_h)
+        k = E.ecc_bcast_threshold(P, 0, m, theta, vecs[0], d_vecs, stream)
+        k_r, n_r = E.ecc_reduce_threshold(P, 0, m, theta, E.ECC_THRESHOLD_DATA, d_vecs, result,
+                                          stream)
+        torch.cuda.synchronize()
+        assert k == k_ref and (k_r, n_r) == (kr_ref, n_ref), r
+        assert np.array_equal(result.cpu().numpy(), res_h), r
+        for p in (0, 1, 17, P - 1):
+            assert np.array_equal(vecs[p].cpu().numpy(), xs_h[p]), (r, p)
+
+
+def test_mf_full():
+    """The factorisation at the benchmark's shape (25M ratings, 160,000 users,
+    60,000 items, rank 16, 32 workers, slack 2, Bernoulli(0.8) arrivals), two
+    iterations: the model bit for bit, the decisions exactly, the error
+    within 1e-12."""
+    from test_gpu_mf import _compare
+    _compare(W.mf_problem(T=2))
