@@ -646,7 +646,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the data path runs P virtual ranks inside one "
-              "GPU's HBM and this build has no multi-GPU leg (requested --gpus %d)" % args.gpus,
+              "GPU's HBM and the library has no multi-GPU path (requested --gpus %d)" % args.gpus,
               file=sys.stderr)
         sys.exit(2)
 

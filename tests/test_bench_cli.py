@@ -1,5 +1,5 @@
 """bench.py's command line on the CPU: more than one GPU is refused with a
-message (this build measures one GPU), and the copy probe and configurations
+message (the benchmark measures one GPU), and the copy probe and configurations
 are listed."""
 import os
 import subprocess
