@@ -212,23 +212,38 @@ ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *con
  *                      copied, column-major and padded to the longest row's
  *                      class R in {3, 4, 5, 7, 8} (12 bytes x R x n_rows of
  *                      device memory), one lane per row;
- *   ECC_LAYOUT_SORTED  very uneven rows (longest > 64 and > 8 x (mean + 1)):
+ *   ECC_LAYOUT_SORTED  very uneven rows (longest > 64 and > 8 x (mean + 1))
+ *                      over a vector of at most one column range (below):
  *                      the rows of every rank are copied in order of
  *                      decreasing length (12 bytes x nnz + 8 bytes x n_rows
  *                      of device memory) and swept in runs staged in LDS;
+ *   ECC_LAYOUT_RANGES  very uneven rows over a longer vector: the columns are
+ *                      cut into R = ceil(8 x n_rows / 8 MiB) ranges of equal
+ *                      width (2 <= R <= 16; the environment variable
+ *                      ECC_RANGE_BYTES, read here, replaces the 8 MiB), every
+ *                      row into its entries of each range, and these
+ *                      sub-rows are copied range by range in order of
+ *                      decreasing length class (12 bytes x nnz, 12 bytes per
+ *                      sub-row, 8 x R + 2 bytes x n_rows of device memory,
+ *                      plus 8 bytes x n_rows for Jacobi; the host copies the
+ *                      entries once here).  A sweep sums every sub-row,
+ *                      then adds a row's sub-row sums in range order: the
+ *                      result differs from the CSR-order sum by rounding;
  *   ECC_LAYOUT_STREAM  otherwise: runs of rows staged in LDS.
  * ECC_LAYOUT_STREAM reads the matrix arrays at every sweep: they must then
- * outlive the handle and stay unchanged.  The other two layouts sweep the
- * copy made here. */
+ * outlive the handle and stay unchanged.  The other layouts sweep the copy
+ * made here. */
 #define ECC_LAYOUT_STREAM 0
 #define ECC_LAYOUT_SORTED 1
 #define ECC_LAYOUT_SHORT 2
+#define ECC_LAYOUT_RANGES 3
 ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
                                ecc_matrix_t *out);
 ecc_status_t ecc_matrix_destroy(ecc_matrix_t A);
 
 /* The layout ecc_matrix_create chose (ECC_LAYOUT_*) and, for
- * ECC_LAYOUT_SHORT, the entries held per row R (0 otherwise).  Host only. */
+ * ECC_LAYOUT_SHORT, the entries held per row R, for ECC_LAYOUT_RANGES the
+ * number of column ranges (0 otherwise).  Host only. */
 ecc_status_t ecc_matrix_layout(ecc_matrix_t A, int32_t *layout, int32_t *row_slots);
 
 /* Number of doubles a d_partials buffer for this matrix must hold. */

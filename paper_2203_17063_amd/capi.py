@@ -23,7 +23,7 @@ ECC_KIND_JACOBI, ECC_KIND_POWER = 0, 1
 ECC_TIMING_ASSEMBLE, ECC_TIMING_ALLREDUCE, ECC_TIMING_SWEEP, ECC_TIMING_NORM = 0, 1, 2, 3
 ECC_TIMING_MF_GRAD, ECC_TIMING_MF_STEP, ECC_TIMING_KINDS = 4, 5, 6
 ECC_THRESHOLD_DATA, ECC_THRESHOLD_PROCS = 0, 1
-ECC_LAYOUT_STREAM, ECC_LAYOUT_SORTED, ECC_LAYOUT_SHORT = 0, 1, 2
+ECC_LAYOUT_STREAM, ECC_LAYOUT_SORTED, ECC_LAYOUT_SHORT, ECC_LAYOUT_RANGES = 0, 1, 2, 3
 
 STATUS_NAMES = {0: "ECC_OK", 1: "ECC_ERR_ARG", 2: "ECC_ERR_OVERLAP", 3: "ECC_ERR_RANGE",
                 4: "ECC_ERR_ALLOC", 5: "ECC_ERR_DEVICE", 6: "ECC_ERR_STATE"}

@@ -83,8 +83,11 @@ enum { kItemStream = 0, kItemVector = 1, kItemPiece = 2 };
 // Sweep layouts of a matrix: stream items staged through LDS; the same over
 // a copy whose rows are sorted by decreasing length within each rank (very
 // uneven rows); short-row items, one lane per row read directly (every row
-// holds at most kShortRow entries).
-enum { kLayStream = 0, kLaySorted = 1, kLayShort = 2 };
+// holds at most kShortRow entries); very uneven rows over a large vector cut
+// by column range into sub-rows, summed per range and then per row.
+enum { kLayStream = 0, kLaySorted = 1, kLayShort = 2, kLayRanges = 3 };
+constexpr int kMaxRanges = 16;              // column ranges of the range layout at most
+constexpr int64_t kRangeBytes = 8 << 20;    // bytes of the vector per column range
 constexpr int kShortRow = 8;
 static_assert(kShortRow <= 8, "a short row is summed from eight registers");
 static_assert(kStreamRows <= 256 && kStreamRows <= kSweepThreads, "one lane per short row");
@@ -300,6 +303,15 @@ struct ecc_matrix_s {
     int32_t *d_srow_ptr = nullptr;  // sorted layout: row pointers of the sorted copy, [n + 1]
     int32_t *d_scol = nullptr;      // sorted layout: its column indices, [nnz]
     double *d_sval = nullptr;       // sorted layout: its values, [nnz]
+    // range layout (the sorted copy above holds the sub-rows, range by range)
+    int32_t n_ranges = 0;           // column ranges
+    int64_t n_sub = 0;              // sub-rows
+    int2 *d_sinfo = nullptr;        // [n_sub] (row, rank) of each sub-row
+    double *d_rpart = nullptr;      // [n_ranges][n] sums of each row's sub-rows
+    uint16_t *d_rmask = nullptr;    // [n] the ranges in which each row has entries
+    double *d_diag = nullptr;       // [n] Jacobi: each row's diagonal entry
+    ecc::Fixup *d_rfix = nullptr;   // split sub-rows: (row, first piece, pieces, range)
+    int64_t n_rfix = 0;
     int32_t *d_ell_col = nullptr;   // short layout: entries column-major, [R][n] (-1: padding)
     double *d_ell_val = nullptr;    // short layout: their values, [R][n]
     double *d_partials = nullptr;   // internal partials of ecc_solve: 2 x (grid + 1)

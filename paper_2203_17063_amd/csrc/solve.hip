@@ -64,7 +64,7 @@ extern "C" ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double 
     // gather costs more than assembling first: assemble, then a sweep that
     // reads every other rank from the assembled vector (measured on MI355X,
     // PageRank on a scale-22 R-MAT graph: 67.2 against 70.0 ms per solve).
-    const bool fused = P <= kFusedMaxP && A->layout != kLaySorted;
+    const bool fused = P <= kFusedMaxP && A->layout != kLaySorted && A->layout != kLayRanges;
     const bool deferred = fused && tol <= 0.0 && A->n_fixups == 0;
     double *cur = d_x, *nxt = d_x_tmp;
     for (int32_t t = 0; t < T; ++t) {

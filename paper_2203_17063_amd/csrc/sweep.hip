@@ -42,6 +42,7 @@
 // rank arrives.  No entry of x_hat that is written is read in the same
 // launch, so the fused step equals assemble-then-sweep bit for bit.
 #include <algorithm>
+#include <cstdlib>
 #include <vector>
 
 #include "ecc_common.h"
@@ -66,6 +67,9 @@ struct SweepArgs {
     double *partials;
     double2 *pieces;
     const int32_t *order;    // sorted layout: the row at each sorted position
+    const int2 *sinfo;       // range layout: (row, rank) of each sub-row
+    double *rpart;           // range layout: [ranges][rn] sums of the sub-rows
+    int64_t rn;
     const int32_t *ell_col;  // short layout: column-major copy of the entries
     const double *ell_val;
     int64_t ell_n;
@@ -231,6 +235,7 @@ struct StreamPrefetch {
     int32_t cv[8];
     double vv[8];
     int32_t rp0, rp1, ri;
+    int32_t lo, hi;  // range layout: the row's rank block
     double bi, xo;
 };
 
@@ -244,7 +249,7 @@ __device__ __forceinline__ void stream_load(const WorkItem &it, const SweepArgs 
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int32_t kc = min(it.k0 + tid + u * kSweepThreads, it.k1 - 1);
-            if constexpr (LAY == kLaySorted) {
+            if constexpr (LAY == kLaySorted || LAY == kLayRanges) {
                 // read-once streams that would otherwise evict lines of the
                 // gathered vector from L2 (measured on MI355X, PageRank on a
                 // scale-22 R-MAT graph: 573 against 600 us per sweep)
@@ -258,16 +263,25 @@ __device__ __forceinline__ void stream_load(const WorkItem &it, const SweepArgs 
     }
     const int tpr = lanes_per_row(nnz, it.nrows);
     const int32_t rr = tid / tpr;
-    pf.rp0 = pf.rp1 = pf.ri = 0;
+    pf.rp0 = pf.rp1 = pf.ri = pf.lo = pf.hi = 0;
     pf.bi = pf.xo = 0.0;
     if (rr < it.nrows) {
         const int32_t r = it.row0 + rr;
         pf.rp0 = a.row_ptr[r];
         pf.rp1 = a.row_ptr[r + 1];
-        const int32_t i = (LAY == kLaySorted) ? a.order[r] : r;
-        pf.ri = i;
-        pf.xo = a.x_own[i];
-        if (KIND == ECC_KIND_JACOBI) pf.bi = a.b[i];
+        if constexpr (LAY == kLayRanges) {
+            // a sub-row: its row and that row's rank block; the row's own
+            // values are read by the finishing pass
+            const int2 si = a.sinfo[r];
+            pf.ri = si.x;
+            pf.lo = a.block_start[si.y];
+            pf.hi = a.block_start[si.y + 1];
+        } else {
+            const int32_t i = (LAY == kLaySorted) ? a.order[r] : r;
+            pf.ri = i;
+            pf.xo = a.x_own[i];
+            if (KIND == ECC_KIND_JACOBI) pf.bi = a.b[i];
+        }
     }
 }
 
@@ -285,11 +299,13 @@ __device__ __forceinline__ void stream_stage(const WorkItem &it, const StreamPre
 }
 
 // The rows of a stream item from the staged nonzeros; returns this thread's
-// norm contribution.  i: the index of the row this thread finishes.
-template <int KIND, bool STEP>
+// norm contribution.  i: the index of the row this thread finishes; [lo, hi):
+// its rank block.  The range layout stores the sum of a sub-row instead
+// (item rank = column range), for the finishing pass.
+template <int KIND, bool STEP, int LAY>
 __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0, int32_t rp1,
-                                                 int32_t i, double bi, double xo,
-                                                 const SweepArgs &a,
+                                                 int32_t i, int32_t lo, int32_t hi, double bi,
+                                                 double xo, const SweepArgs &a,
                                                  const int32_t *s_col, const double *s_val,
                                                  const StepView &sv, RankCache &rc,
                                                  bool own_arrives) {
@@ -299,7 +315,6 @@ __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0
     const int lane = tid & (tpr - 1);
     const int32_t rr = tid / tpr;
     if (rr >= it.nrows) return 0.0;
-    const int32_t lo = it.lo, hi = it.hi;
     const int32_t rs = rp0 - it.k0, re = rp1 - it.k0;
     double s = 0.0, dg = 0.0;
     if (tpr == 1) {
@@ -347,13 +362,18 @@ __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0
         if (KIND == ECC_KIND_JACOBI) dg = group_sum_dyn(dg, tpr);
     }
     if (lane != 0) return 0.0;
-    if (STEP && own_arrives) a.x_hat[i] = xo;
-    return row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+    if constexpr (LAY == kLayRanges) {
+        a.rpart[(int64_t)it.rank * a.rn + i] = s;
+        return 0.0;
+    } else {
+        if (STEP && own_arrives) a.x_hat[i] = xo;
+        return row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+    }
 }
 
 // One long row (or a slice of it) by the whole workgroup; returns the norm
 // contribution (in thread 0).
-template <int KIND, bool STEP>
+template <int KIND, bool STEP, int LAY>
 __device__ __forceinline__ double long_compute(const WorkItem &it, const SweepArgs &a,
                                                const StepView &sv, RankCache &rc,
                                                bool own_arrives, double *s_red) {
@@ -366,6 +386,10 @@ __device__ __forceinline__ double long_compute(const WorkItem &it, const SweepAr
     if (tid != 0) return 0.0;
     if (it.kind == kItemPiece) {
         a.pieces[it.slot] = make_double2(s, dg);
+        return 0.0;
+    }
+    if constexpr (LAY == kLayRanges) {
+        a.rpart[(int64_t)it.rank * a.rn + i] = s;
         return 0.0;
     }
     const double xo = a.x_own[i];
@@ -434,12 +458,14 @@ __device__ __forceinline__ void sweep_prologue(const SweepArgs &a, uint8_t *s_ef
     if constexpr (STEP) __syncthreads();
 }
 
-// LAY selects the layout: stream items over the matrix (kLayStream) or over
-// its sorted copy (kLaySorted); both may contain vector items and pieces.
+// LAY selects the layout: stream items over the matrix (kLayStream), over
+// its sorted copy (kLaySorted) or over its sub-rows cut by column range
+// (kLayRanges); all may contain vector items and pieces.
 // The short-row layout has its own body.
 template <int KIND, bool STEP, int LAY>
 __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
-    static_assert(LAY == kLayStream || LAY == kLaySorted, "stream layouts only");
+    static_assert(LAY == kLayStream || LAY == kLaySorted || LAY == kLayRanges,
+                  "stream layouts only");
     // padded by 8 so that a row's first eight entries can be read unclamped
     __shared__ int32_t s_col[kStreamCap + 8];
     __shared__ double s_val[kStreamCap + 8];
@@ -480,16 +506,18 @@ __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
         if (cur.kind == kItemStream) {
             stream_stage(cur, pf, s_col, s_val);
             const int32_t rp0 = pf.rp0, rp1 = pf.rp1, ri = pf.ri;
+            const int32_t lo = LAY == kLayRanges ? pf.lo : cur.lo;
+            const int32_t hi = LAY == kLayRanges ? pf.hi : cur.hi;
             const double bi = pf.bi, xo = pf.xo;
             __syncthreads();
             if (next_stream) stream_load<KIND, LAY>(nxt, a, pf);
             if (have_nn) nn = a.items[w + 2 * w_step];
-            contrib += stream_compute<KIND, STEP>(cur, rp0, rp1, ri, bi, xo, a, s_col, s_val, sv,
-                                                  rc, own_arrives);
+            contrib += stream_compute<KIND, STEP, LAY>(cur, rp0, rp1, ri, lo, hi, bi, xo, a, s_col,
+                                                       s_val, sv, rc, own_arrives);
             __syncthreads();  // LDS is reused by the next item
         } else {
             if (have_nn) nn = a.items[w + 2 * w_step];
-            contrib += long_compute<KIND, STEP>(cur, a, sv, rc, own_arrives, s_red);
+            contrib += long_compute<KIND, STEP, LAY>(cur, a, sv, rc, own_arrives, s_red);
             if (next_stream) stream_load<KIND, LAY>(nxt, a, pf);
         }
         w += w_step;
@@ -506,6 +534,82 @@ __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
 template <int KIND, bool STEP, int LAY>
 __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
     sweep_body<KIND, STEP, LAY>(a);
+}
+
+// Range layout: the sum of a sub-row cut into pieces, its pieces added in
+// order (fixup rank = column range).
+__global__ void k_range_fix(int32_t n_fix, const Fixup *__restrict__ fix,
+                            const double2 *__restrict__ pieces, int64_t rn,
+                            double *__restrict__ rpart, const int32_t *done) {
+    if (done && *done) return;
+    for (int32_t f = blockIdx.x * blockDim.x + threadIdx.x; f < n_fix; f += gridDim.x * blockDim.x) {
+        const Fixup x = fix[f];
+        double s = 0.0;
+        for (int32_t j = 0; j < x.npieces; ++j) s = s + pieces[x.slot0 + j].x;
+        rpart[(int64_t)x.rank * rn + x.row] = s;
+    }
+}
+
+struct RangeFinishArgs {
+    int64_t n;
+    int32_t n_ranges;
+    const uint16_t *rmask;
+    const double *rpart;  // [n_ranges][n]
+    const double *diag;
+    const double *b;
+    double alpha, beta;
+    const double *x_own;
+    double *x_next;
+    double *partials;     // [gridDim.x + 1]
+    const int32_t *done;
+};
+
+// Range layout, second kernel: a row's sum is its sub-rows' sums added in
+// range order; then the row is finished as in the other layouts, with one
+// norm partial per workgroup (and none for split rows, whose sums are
+// already in).  The grid is the sweep's, so workgroups are large and every
+// thread takes kFinishRows rows at a time, all their loads in flight.
+constexpr int kFinishThreads = 1024;
+constexpr int kFinishRows = 4;
+template <int KIND>
+__global__ __launch_bounds__(kFinishThreads) void k_range_finish(RangeFinishArgs a) {
+    __shared__ double s_red[kFinishThreads / 64];
+    if (a.done && *a.done) return;
+    double contrib = 0.0;
+    const int64_t stride = (int64_t)gridDim.x * kFinishThreads;
+    for (int64_t i0 = (int64_t)blockIdx.x * kFinishThreads + threadIdx.x; i0 < a.n;
+         i0 += stride * kFinishRows) {
+        uint32_t mask[kFinishRows];
+        double s[kFinishRows], xo[kFinishRows], dg[kFinishRows], bi[kFinishRows];
+#pragma unroll
+        for (int u = 0; u < kFinishRows; ++u) {
+            const int64_t i = i0 + u * stride;
+            const bool live = i < a.n;
+            mask[u] = live ? a.rmask[i] : 0u;
+            xo[u] = live ? a.x_own[i] : 0.0;
+            dg[u] = (KIND == ECC_KIND_JACOBI && live) ? a.diag[i] : 0.0;
+            bi[u] = (KIND == ECC_KIND_JACOBI && live) ? a.b[i] : 0.0;
+        }
+#pragma unroll
+        for (int u = 0; u < kFinishRows; ++u) {
+            const int64_t i = i0 + u * stride;
+            s[u] = 0.0;
+            for (int x = 0; x < a.n_ranges; ++x)
+                if ((mask[u] >> x) & 1u) s[u] = s[u] + a.rpart[(int64_t)x * a.n + i];
+        }
+#pragma unroll
+        for (int u = 0; u < kFinishRows; ++u) {
+            const int64_t i = i0 + u * stride;
+            if (i < a.n)
+                contrib += row_finish<KIND>((int32_t)i, s[u], dg[u], bi[u], xo[u], a.alpha,
+                                            a.beta, a.x_next);
+        }
+    }
+    const double total = block_sum<kFinishThreads>(contrib, s_red);
+    if (threadIdx.x == 0) {
+        a.partials[blockIdx.x] = total;
+        if (blockIdx.x == 0) a.partials[gridDim.x] = 0.0;
+    }
 }
 
 // Entries of one short row in the column-major copy: entry k of row i sits
@@ -829,6 +933,165 @@ static void sort_rows(const std::vector<int32_t> &rp, const std::vector<int64_t>
     for (int64_t r = 0; r < n; ++r) srp[r + 1] = srp[r] + (rp[order[r] + 1] - rp[order[r]]);
 }
 
+// Range layout: the number of column ranges for a vector of n doubles,
+// about kRangeBytes of it per range (ECC_RANGE_BYTES overrides the size).
+static int32_t range_count(int64_t n) {
+    int64_t bytes = kRangeBytes;
+    if (const char *e = std::getenv("ECC_RANGE_BYTES")) {
+        const long long v = std::atoll(e);
+        if (v > 0) bytes = v;
+    }
+    const int64_t nr = (n * 8 + bytes - 1) / bytes;
+    return (int32_t)std::min<int64_t>(kMaxRanges, std::max<int64_t>(1, nr));
+}
+
+// The column range of column c: NR ranges of equal width over [0, n).
+static inline int32_t range_of(int64_t c, int64_t n, int32_t NR) { return (int32_t)(c * NR / n); }
+
+struct RangeBuild {
+    std::vector<int32_t> srp;     // [n_sub + 1] row pointers of the sub-rows
+    std::vector<int2> sinfo;      // [n_sub] (row, rank)
+    std::vector<int32_t> scol;    // [nnz] entries, sub-row by sub-row
+    std::vector<double> sval;
+    std::vector<uint16_t> rmask;  // [n] ranges in which a row has entries
+    std::vector<double> diag;     // [n] Jacobi diagonal
+    std::vector<Fixup> rfix;      // split sub-rows
+};
+
+// Range layout: every row cut into sub-rows by column range (its entries of
+// one range, in CSR order); the sub-rows of a range ordered by decreasing
+// length class (octaves) across all ranks, in row order within a class;
+// ranges one after another.
+// Items: pieces and vector items first, then stream items range by range, so
+// that the workgroups, walking the items together, gather from one range of
+// the vector at a time.  Item rank = the column range; lo/hi of a vector item
+// or piece = its row's rank block (stream items carry theirs per sub-row).
+static void build_ranges(const std::vector<int32_t> &rp, const std::vector<int32_t> &col,
+                         const std::vector<double> &val, const std::vector<int64_t> &counts,
+                         int32_t NR, bool jacobi, RangeBuild &B, std::vector<WorkItem> &items,
+                         int64_t &n_pieces) {
+    const int64_t n = (int64_t)rp.size() - 1;
+    std::vector<int64_t> bs(counts.size() + 1, 0);
+    for (size_t p = 0; p < counts.size(); ++p) bs[p + 1] = bs[p] + counts[p];
+    std::vector<int32_t> rank_of(n);
+    for (size_t p = 0; p < counts.size(); ++p)
+        for (int64_t i = bs[p]; i < bs[p + 1]; ++i) rank_of[i] = (int32_t)p;
+    // sub-rows of each range in row order: (row, length)
+    std::vector<std::vector<int32_t>> srow(NR), slen(NR);
+    std::vector<int32_t> cnt(NR);
+    B.rmask.assign(n, 0);
+    B.diag.assign(jacobi ? n : 0, 0.0);
+    for (int64_t i = 0; i < n; ++i) {
+        std::fill(cnt.begin(), cnt.end(), 0);
+        for (int32_t k = rp[i]; k < rp[i + 1]; ++k) {
+            ++cnt[range_of(col[k], n, NR)];
+            if (jacobi && col[k] == i) B.diag[i] = val[k];
+        }
+        for (int32_t x = 0; x < NR; ++x)
+            if (cnt[x] > 0) {
+                srow[x].push_back((int32_t)i);
+                slen[x].push_back(cnt[x]);
+                B.rmask[i] |= (uint16_t)(1u << x);
+            }
+    }
+    // sorted position of the j-th sub-row (row order) of range x: base[x] + inv[x][j]
+    std::vector<int64_t> base(NR + 1, 0);
+    std::vector<std::vector<int32_t>> inv(NR);
+    for (int32_t x = 0; x < NR; ++x) base[x + 1] = base[x] + (int64_t)srow[x].size();
+    const int64_t n_sub = base[NR];
+    B.srp.assign(n_sub + 1, 0);
+    B.sinfo.resize(n_sub);
+    for (int32_t x = 0; x < NR; ++x) {
+        const int64_t m = (int64_t)srow[x].size();
+        std::vector<int32_t> perm(m);
+        for (int64_t j = 0; j < m; ++j) perm[j] = (int32_t)j;
+        // decreasing length class (octaves), rows in row order within a class:
+        // neighbouring sub-rows then write their sums close together
+        auto octave = [&](int32_t u) { return 31 - __builtin_clz((uint32_t)slen[x][u]); };
+        std::stable_sort(perm.begin(), perm.end(),
+                         [&](int32_t u, int32_t v) { return octave(u) > octave(v); });
+        inv[x].resize(m);
+        for (int64_t q = 0; q < m; ++q) {
+            const int32_t j = perm[q];
+            inv[x][j] = (int32_t)q;
+            const int64_t r = base[x] + q;
+            B.srp[r + 1] = slen[x][j];
+            B.sinfo[r] = make_int2(srow[x][j], rank_of[srow[x][j]]);
+        }
+    }
+    for (int64_t r = 0; r < n_sub; ++r) B.srp[r + 1] += B.srp[r];
+    // entries: each row's entries of range x to its sub-row, in CSR order
+    B.scol.resize(col.size());
+    B.sval.resize(val.size());
+    std::vector<int32_t> seen(NR, 0);
+    std::vector<int64_t> cur(NR);
+    for (int64_t i = 0; i < n; ++i) {
+        for (int32_t x = 0; x < NR; ++x)
+            if ((B.rmask[i] >> x) & 1u) cur[x] = B.srp[base[x] + inv[x][seen[x]++]];
+        for (int32_t k = rp[i]; k < rp[i + 1]; ++k) {
+            const int64_t d = cur[range_of(col[k], n, NR)]++;
+            B.scol[d] = col[k];
+            B.sval[d] = val[k];
+        }
+    }
+    // items
+    auto make = [](int64_t r0, int64_t nr, int64_t k0, int64_t k1, int64_t lo, int64_t hi,
+                   int kind, int64_t x, int64_t slot) {
+        WorkItem w{};
+        w.row0 = (int32_t)r0;
+        w.nrows = (int32_t)nr;
+        w.k0 = (int32_t)k0;
+        w.k1 = (int32_t)k1;
+        w.lo = (int32_t)lo;
+        w.hi = (int32_t)hi;
+        w.kind = kind;
+        w.rank = (int32_t)x;
+        w.slot = (int32_t)slot;
+        return w;
+    };
+    std::vector<WorkItem> big, vec, stream;
+    n_pieces = 0;
+    for (int32_t x = 0; x < NR; ++x) {
+        int64_t r = base[x];
+        const int64_t end = base[x + 1];
+        while (r < end) {
+            const int64_t len = (int64_t)B.srp[r + 1] - B.srp[r];
+            if (len > kStreamCap) {
+                const int32_t i = B.sinfo[r].x, p = B.sinfo[r].y;
+                if (len <= kVectorCap) {
+                    vec.push_back(make(i, 1, B.srp[r], B.srp[r + 1], bs[p], bs[p + 1], kItemVector,
+                                       x, 0));
+                } else {
+                    const int32_t np = (int32_t)((len + kVectorCap - 1) / kVectorCap);
+                    B.rfix.push_back({i, (int32_t)n_pieces, np, x});
+                    for (int32_t j = 0; j < np; ++j) {
+                        const int64_t ka = B.srp[r] + (int64_t)j * kVectorCap;
+                        const int64_t kb = std::min<int64_t>(B.srp[r + 1], ka + kVectorCap);
+                        big.push_back(make(i, 1, ka, kb, bs[p], bs[p + 1], kItemPiece, x,
+                                           n_pieces + j));
+                    }
+                    n_pieces += np;
+                }
+                ++r;
+                continue;
+            }
+            const int64_t start = r;
+            int64_t nnz = 0;
+            while (r < end && r - start < kStreamRows) {
+                const int64_t l = (int64_t)B.srp[r + 1] - B.srp[r];
+                if (l > kStreamCap || nnz + l > kStreamCap) break;
+                nnz += l;
+                ++r;
+            }
+            stream.push_back(make(start, r - start, B.srp[start], B.srp[r], 0, 0, kItemStream, x, 0));
+        }
+    }
+    items.clear();
+    items.insert(items.end(), big.begin(), big.end());
+    items.insert(items.end(), vec.begin(), vec.end());
+    items.insert(items.end(), stream.begin(), stream.end());
+}
+
 // Copies row order[r] of the matrix to position r of the sorted copy, one
 // wave per row.
 __global__ void k_sort_rows(int32_t n, const int32_t *__restrict__ order,
@@ -853,10 +1116,10 @@ __global__ void k_sort_rows(int32_t n, const int32_t *__restrict__ order,
 // walks several items through the load/compute pipeline), at most one per
 // item, rounded down to a multiple of the 8 XCDs.
 // Occupancy of the kernel a loop iteration launches: the fused one, except
-// for the sorted layout, which is never fused.
+// for the sorted and range layouts, which are never fused.
 template <int LAY>
 static hipError_t sweep_occupancy(int *per_cu, int kind) {
-    constexpr bool S = LAY != kLaySorted;
+    constexpr bool S = LAY != kLaySorted && LAY != kLayRanges;
     return kind == ECC_KIND_JACOBI
                ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
                      per_cu, k_sweep<ECC_KIND_JACOBI, S, LAY>, kSweepThreads, 0)
@@ -895,6 +1158,7 @@ static int32_t sweep_grid(int64_t n_items, int kind, int layout, int32_t short_r
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         cus = 256;
     const hipError_t e = layout == kLaySorted  ? sweep_occupancy<kLaySorted>(&per_cu, kind)
+                         : layout == kLayRanges ? sweep_occupancy<kLayRanges>(&per_cu, kind)
                          : layout == kLayShort ? short_occupancy(&per_cu, kind, short_r)
                                                : sweep_occupancy<kLayStream>(&per_cu, kind);
     if (e != hipSuccess || per_cu < 1) per_cu = 4;
@@ -912,6 +1176,8 @@ static void launch_layout(ecc_matrix_t M, dim3 grid, dim3 block, hipStream_t st,
                           const SweepArgs &a) {
     if (M->layout == kLaySorted) {
         if constexpr (!S) hipLaunchKernelGGL((k_sweep<K, S, kLaySorted>), grid, block, 0, st, a);
+    } else if (M->layout == kLayRanges) {
+        if constexpr (!S) hipLaunchKernelGGL((k_sweep<K, S, kLayRanges>), grid, block, 0, st, a);
     } else if (M->layout == kLayShort) {
         switch (short_class(M->short_r)) {
             case 3: hipLaunchKernelGGL((k_sweep_short<K, S, 3>), grid, block, 0, st, a); break;
@@ -930,7 +1196,7 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     SweepArgs a{};
     a.items = M->d_items;
     a.n_items = (int32_t)M->n_items;
-    const bool sorted = M->layout == kLaySorted;
+    const bool sorted = M->layout == kLaySorted || M->layout == kLayRanges;
     a.row_ptr = sorted ? M->d_srow_ptr : M->A.d_row_ptr;
     a.col = sorted ? M->d_scol : M->A.d_col;
     a.val = sorted ? M->d_sval : M->A.d_val;
@@ -943,6 +1209,10 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     a.partials = L.partials;
     a.pieces = M->d_pieces;
     a.order = M->d_order;
+    a.sinfo = M->d_sinfo;
+    a.rpart = M->d_rpart;
+    a.rn = M->A.n_rows;
+    a.block_start = pl->d_block_start;
     a.ell_col = M->d_ell_col;
     a.ell_val = M->d_ell_val;
     a.ell_n = M->A.n_rows;
@@ -956,7 +1226,8 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     const bool step = L.arrived != nullptr;
     if (step) {
         const int64_t t = pl->clock;
-        if (pl->P > kFusedMaxP || !pl->d_block_start || M->layout == kLaySorted) {
+        if (pl->P > kFusedMaxP || !pl->d_block_start || M->layout == kLaySorted ||
+            M->layout == kLayRanges) {
             set_error("internal: fused step does not fit the plan or the matrix");
             return ECC_ERR_STATE;
         }
@@ -985,6 +1256,34 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
         else launch_layout<ECC_KIND_POWER, false>(M, grid, block, st, a);
     }
     ECC_LAUNCH_CHECK();
+    if (M->layout == kLayRanges) {
+        // the split sub-rows' sums, then every row from its sub-rows' sums
+        if (M->n_rfix > 0) {
+            const int fb = (int)std::min<int64_t>(1024, (M->n_rfix + 255) / 256);
+            hipLaunchKernelGGL(k_range_fix, dim3(fb), dim3(256), 0, st, (int32_t)M->n_rfix,
+                               M->d_rfix, M->d_pieces, (int64_t)M->A.n_rows, M->d_rpart, L.done);
+            ECC_LAUNCH_CHECK();
+        }
+        RangeFinishArgs f{};
+        f.n = M->A.n_rows;
+        f.n_ranges = M->n_ranges;
+        f.rmask = M->d_rmask;
+        f.rpart = M->d_rpart;
+        f.diag = M->d_diag;
+        f.b = L.b;
+        f.alpha = L.alpha;
+        f.beta = L.beta;
+        f.x_own = L.x_own;
+        f.x_next = L.x_next;
+        f.partials = L.partials;
+        f.done = L.done;
+        const dim3 fblock(kFinishThreads);
+        if (M->kind == ECC_KIND_JACOBI)
+            hipLaunchKernelGGL(k_range_finish<ECC_KIND_JACOBI>, grid, fblock, 0, st, f);
+        else
+            hipLaunchKernelGGL(k_range_finish<ECC_KIND_POWER>, grid, fblock, 0, st, f);
+        ECC_LAUNCH_CHECK();
+    }
     if (step) pl->clock += 1;
     return ECC_OK;
 }
@@ -1106,9 +1405,22 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
     int32_t max_row = 0;
     for (int64_t i = 0; i < n; ++i) max_row = std::max(max_row, rp[i + 1] - rp[i]);
     const bool short_rows = max_row <= kShortRow;
-    const int layout = irregular ? kLaySorted : (short_rows ? kLayShort : kLayStream);
+    // Very uneven rows over a vector of more than one range: the range layout
+    // (each range of the vector, about kRangeBytes, is gathered by all
+    // workgroups at once and stays in the XCDs' L2).
+    const int32_t n_ranges = irregular ? range_count(n) : 1;
+    const int layout = irregular ? (n_ranges >= 2 ? kLayRanges : kLaySorted)
+                                 : (short_rows ? kLayShort : kLayStream);
     std::vector<int32_t> order, srp;
-    if (irregular) {
+    RangeBuild RB;
+    if (layout == kLayRanges) {
+        std::vector<int32_t> hcol(A->nnz);
+        std::vector<double> hval(A->nnz);
+        ECC_HIP(hipMemcpy(hcol.data(), A->d_col, sizeof(int32_t) * A->nnz, hipMemcpyDeviceToHost));
+        ECC_HIP(hipMemcpy(hval.data(), A->d_val, sizeof(double) * A->nnz, hipMemcpyDeviceToHost));
+        build_ranges(rp, hcol, hval, plan->counts, n_ranges, kind == ECC_KIND_JACOBI, RB, items,
+                     n_pieces);
+    } else if (irregular) {
         sort_rows(rp, plan->counts, order, srp);
         build_items(srp, plan->counts, &order, items, fixups, n_pieces);
     } else {
@@ -1176,6 +1488,26 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
         if (hipGetLastError() != hipSuccess || hipStreamSynchronize(plan->stream) != hipSuccess)
             return fail("building the sorted copy failed");
     }
+    if (layout == kLayRanges) {
+        M->n_ranges = n_ranges;
+        M->n_sub = (int64_t)RB.sinfo.size();
+        M->n_rfix = (int64_t)RB.rfix.size();
+        auto up = [&](void **dst, const void *src, size_t bytes) {
+            if (hipMalloc(dst, std::max<size_t>(bytes, 8)) != hipSuccess) return false;
+            return bytes == 0 || hipMemcpy(*dst, src, bytes, hipMemcpyHostToDevice) == hipSuccess;
+        };
+        if (!up((void **)&M->d_srow_ptr, RB.srp.data(), sizeof(int32_t) * RB.srp.size()) ||
+            !up((void **)&M->d_sinfo, RB.sinfo.data(), sizeof(int2) * RB.sinfo.size()) ||
+            !up((void **)&M->d_scol, RB.scol.data(), sizeof(int32_t) * RB.scol.size()) ||
+            !up((void **)&M->d_sval, RB.sval.data(), sizeof(double) * RB.sval.size()) ||
+            !up((void **)&M->d_rmask, RB.rmask.data(), sizeof(uint16_t) * RB.rmask.size()) ||
+            !up((void **)&M->d_diag, RB.diag.data(), sizeof(double) * RB.diag.size()) ||
+            !up((void **)&M->d_rfix, RB.rfix.data(), sizeof(Fixup) * RB.rfix.size()))
+            return fail("building the range layout failed");
+        if (hipMalloc((void **)&M->d_rpart, sizeof(double) * (size_t)n_ranges * (size_t)n) !=
+            hipSuccess)
+            return fail("hipMalloc of the range sums failed");
+    }
     if (layout == kLayShort && n > 0) {
         const int32_t R = short_class(M->short_r);
         if (hipMalloc((void **)&M->d_ell_col, sizeof(int32_t) * R * n) != hipSuccess ||
@@ -1206,6 +1538,11 @@ ecc_status_t ecc_matrix_destroy(ecc_matrix_t M) {
     (void)hipFree(M->d_srow_ptr);
     (void)hipFree(M->d_scol);
     (void)hipFree(M->d_sval);
+    (void)hipFree(M->d_sinfo);
+    (void)hipFree(M->d_rpart);
+    (void)hipFree(M->d_rmask);
+    (void)hipFree(M->d_diag);
+    (void)hipFree(M->d_rfix);
     (void)hipFree(M->d_ell_col);
     (void)hipFree(M->d_ell_val);
     delete M;
@@ -1218,8 +1555,11 @@ ecc_status_t ecc_matrix_layout(ecc_matrix_t M, int32_t *layout, int32_t *row_slo
     ECC_ARG(layout != nullptr && row_slots != nullptr, "NULL output");
     *layout = M->layout == kLayShort ? ECC_LAYOUT_SHORT
               : M->layout == kLaySorted ? ECC_LAYOUT_SORTED
+              : M->layout == kLayRanges ? ECC_LAYOUT_RANGES
                                       : ECC_LAYOUT_STREAM;
-    *row_slots = M->layout == kLayShort ? short_class(M->short_r) : 0;
+    *row_slots = M->layout == kLayShort    ? short_class(M->short_r)
+                 : M->layout == kLayRanges ? M->n_ranges
+                                           : 0;
     return ECC_OK;
 }
 

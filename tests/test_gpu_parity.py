@@ -6,6 +6,9 @@ oracle, norms within 1e-12 relative plus 32 units of rounding of the
 problem's scale; stencil sweeps sum every row on one lane in CSR order, so
 their iterates are also checked bit for bit.
 """
+import contextlib
+import os
+
 import numpy as np
 import pytest
 
@@ -512,6 +515,46 @@ def _powerlaw_problem(kind, n, counts, seed, T=25, S=2):
                        np.full(n, 1.0 / n), alpha=0.85, beta=0.15 / n, norm=1)
 
 
+@contextlib.contextmanager
+def _range_bytes(v):
+    """Column ranges of v bytes of the vector for matrices created inside."""
+    old = os.environ.get("ECC_RANGE_BYTES")
+    os.environ["ECC_RANGE_BYTES"] = str(v)
+    try:
+        yield
+    finally:
+        if old is None:
+            del os.environ["ECC_RANGE_BYTES"]
+        else:
+            os.environ["ECC_RANGE_BYTES"] = old
+
+
+@pytest.mark.parametrize("kind", ["jacobi", "power"])
+@pytest.mark.parametrize("counts", [[20000], [0, 3000, 0, 9000, 1000, 7000], 9])
+@pytest.mark.parametrize("range_bytes", [16384, 1])
+def test_solve_range_layout(kind, counts, range_bytes):
+    """Very uneven rows cut by column range into sub-rows (10 ranges of 16 KB
+    of the vector, or the most, 16): each sub-row summed on its own, a row's
+    sums added in range order by a second kernel, split sub-rows recombined
+    first; Jacobi takes the diagonal kept at set-up."""
+    prob = _powerlaw_problem(kind, 20000, counts, seed=31 + len(str(counts)))
+    with _range_bytes(range_bytes):
+        _solve_and_compare(prob, bitwise=False, layout="RANGES")
+
+
+@pytest.mark.parametrize("scale", [12, 15, 17])
+def test_solve_config3_ranges(scale):
+    """R-MAT PageRank in the range layout (scale 15 has sub-rows summed by a
+    whole workgroup, scale 17 split sub-rows)."""
+    with _range_bytes(4096):
+        _solve_and_compare(W.config3(scale=scale, T=60), bitwise=False, layout="RANGES")
+
+
+def test_solve_arrow_ranges():
+    with _range_bytes(8192):
+        _solve_and_compare(_arrow_problem(), bitwise=False, layout="RANGES")
+
+
 @pytest.mark.parametrize("kind", ["jacobi", "power"])
 @pytest.mark.parametrize("counts", [[20000], [0, 3000, 0, 9000, 1000, 7000], 9])
 def test_solve_sorted_layout(kind, counts):
@@ -533,8 +576,19 @@ def test_step_api_matches_solve():
     """assemble -> iterate -> residual through the separate calls reproduce the
     loop-control call bit for bit (fused single-launch loop, the loop with a
     second pass per iteration, and split rows)."""
+    _step_api_matches_solve((W.config2(N=40, T=25), W.config3(scale=11, T=25),
+                             _arrow_problem(T=12)))
+
+
+def test_step_api_matches_solve_ranges():
+    """The same for the range layout (sub-row sums, then rows)."""
+    with _range_bytes(2048):
+        _step_api_matches_solve((W.config3(scale=11, T=25), _arrow_problem(T=12)))
+
+
+def _step_api_matches_solve(problems):
     R = _runner()
-    for prob in (W.config2(N=40, T=25), W.config3(scale=11, T=25), _arrow_problem(T=12)):
+    for prob in problems:
         announce("step api", prob.name)
         run = R.Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts, prob.S,
                           prob.mask, prob.kind, b=prob.b, alpha=prob.alpha, beta=prob.beta,
@@ -557,7 +611,8 @@ def test_step_api_matches_solve():
 def test_layout_choice():
     """The layout each kind of matrix gets: rows of at most 8 entries the
     short-row layout (entries held per row after the longest row), regular
-    longer rows the stream layout, power-law rows the sorted layout."""
+    longer rows the stream layout, power-law rows the sorted layout, or over a
+    vector of several column ranges the range layout."""
     E, R = _capi(), _runner()
     cases = [(W.config1(), E.ECC_LAYOUT_SHORT, 3), (W.config2(N=33, T=2), E.ECC_LAYOUT_SHORT, 5),
              (W.config5(N=12, T=2, P=8), E.ECC_LAYOUT_SHORT, 7),
@@ -566,12 +621,18 @@ def test_layout_choice():
              (_banded_problem("jacobi", 3000, 9, 16, T=2), E.ECC_LAYOUT_STREAM, 0),
              (W.config3(scale=10, T=2), E.ECC_LAYOUT_SORTED, 0)]
     for prob, layout, slots in cases:
-        announce("layout", prob.name)
-        run = R.Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts, prob.S,
-                          prob.mask, prob.kind, b=prob.b, alpha=prob.alpha, beta=prob.beta,
-                          x0=prob.x0)
-        assert E.ecc_matrix_layout(run.mat) == (layout, slots), prob.name
-        run.close()
+        _check_layout(R, E, prob, layout, slots)
+    with _range_bytes(4096):          # 8 KB of vector: two column ranges
+        _check_layout(R, E, W.config3(scale=10, T=2), E.ECC_LAYOUT_RANGES, 2)
+
+
+def _check_layout(R, E, prob, layout, slots):
+    announce("layout", prob.name)
+    run = R.Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts, prob.S,
+                      prob.mask, prob.kind, b=prob.b, alpha=prob.alpha, beta=prob.beta,
+                      x0=prob.x0)
+    assert E.ecc_matrix_layout(run.mat) == (layout, slots), prob.name
+    run.close()
 
 
 def test_matrix_checks():
