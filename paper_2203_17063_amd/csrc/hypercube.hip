@@ -18,6 +18,8 @@
 // definition, so results are bitwise reproducible.
 #include <algorithm>
 
+#include <new>
+
 #include "ecc_common.h"
 
 namespace ecc {
@@ -299,7 +301,7 @@ ecc_status_t ecc_allreduce_ssp(ecc_hypercube_t h, const double *d_contrib,
     return ECC_OK;
 }
 
-ecc_status_t ecc_hypercube_stats(ecc_hypercube_t h, int64_t *clock, uint64_t *waits_total,
+static ecc_status_t ecc_hypercube_stats_impl(ecc_hypercube_t h, int64_t *clock, uint64_t *waits_total,
                                  int32_t *h_slot_clock, uint64_t *h_waits) {
     clear_error();
     ECC_ARG(h != nullptr, "hypercube is NULL");
@@ -322,6 +324,18 @@ ecc_status_t ecc_hypercube_stats(ecc_hypercube_t h, int64_t *clock, uint64_t *wa
     if (h_waits)
         for (int32_t i = 0; i < n; ++i) h_waits[i] = w[i];
     return ECC_OK;
+}
+
+// Host allocations of the set-up throw std::bad_alloc when memory runs
+// out: the C ABI reports ECC_ERR_ALLOC instead of letting it escape.
+ecc_status_t ecc_hypercube_stats(ecc_hypercube_t h, int64_t *clock, uint64_t *waits_total,
+                                 int32_t *h_slot_clock, uint64_t *h_waits) {
+    try {
+        return ecc_hypercube_stats_impl(h, clock, waits_total, h_slot_clock, h_waits);
+    } catch (const std::bad_alloc &) {
+        set_error("host allocation failed");
+        return ECC_ERR_ALLOC;
+    }
 }
 
 }  // extern "C"

@@ -37,6 +37,8 @@
 #include <algorithm>
 #include <vector>
 
+#include <new>
+
 #include "ecc_common.h"
 
 namespace ecc {
@@ -310,7 +312,7 @@ ecc_status_t ecc_mf_destroy(ecc_mf_t h) {
     return ECC_OK;
 }
 
-ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32_t P, int64_t N,
+static ecc_status_t ecc_mf_create_impl(int32_t n_users, int32_t n_items, int32_t rank, int32_t P, int64_t N,
                            const int32_t *d_users, const int32_t *d_items,
                            const double *d_ratings, ecc_mf_t *out) {
     clear_error();
@@ -442,6 +444,19 @@ ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32
         return fail("upload of the factorisation state failed");
     *out = h;
     return ECC_OK;
+}
+
+// Host allocations of the set-up throw std::bad_alloc when memory runs
+// out: the C ABI reports ECC_ERR_ALLOC instead of letting it escape.
+ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32_t P, int64_t N,
+                           const int32_t *d_users, const int32_t *d_items,
+                           const double *d_ratings, ecc_mf_t *out) {
+    try {
+        return ecc_mf_create_impl(n_users, n_items, rank, P, N, d_users, d_items, d_ratings, out);
+    } catch (const std::bad_alloc &) {
+        set_error("host allocation failed");
+        return ECC_ERR_ALLOC;
+    }
 }
 
 ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam, double *d_W,

@@ -7,6 +7,8 @@
 #include <cstring>
 #include <numeric>
 
+#include <new>
+
 #include "ecc_common.h"
 
 namespace ecc {
@@ -119,7 +121,7 @@ const char *ecc_status_string(ecc_status_t s) {
     return "ECC_ERR_UNKNOWN";
 }
 
-ecc_status_t ecc_plan_validate(int32_t P, const int64_t *h_counts, const int64_t *h_displs,
+static ecc_status_t ecc_plan_validate_impl(int32_t P, const int64_t *h_counts, const int64_t *h_displs,
                                int32_t max_staleness) {
     clear_error();
     ECC_ARG(P >= 1, "P must be >= 1 (got %d)", P);
@@ -149,7 +151,19 @@ ecc_status_t ecc_plan_validate(int32_t P, const int64_t *h_counts, const int64_t
     return ECC_OK;
 }
 
-ecc_status_t ecc_plan_create(int32_t P, const int64_t *h_counts, const int64_t *h_displs,
+// Host allocations of the set-up throw std::bad_alloc when memory runs
+// out: the C ABI reports ECC_ERR_ALLOC instead of letting it escape.
+ecc_status_t ecc_plan_validate(int32_t P, const int64_t *h_counts, const int64_t *h_displs,
+                               int32_t max_staleness) {
+    try {
+        return ecc_plan_validate_impl(P, h_counts, h_displs, max_staleness);
+    } catch (const std::bad_alloc &) {
+        set_error("host allocation failed");
+        return ECC_ERR_ALLOC;
+    }
+}
+
+static ecc_status_t ecc_plan_create_impl(int32_t P, const int64_t *h_counts, const int64_t *h_displs,
                              int32_t max_staleness, void *hip_stream, ecc_plan_t *out) {
     ECC_ARG(out != nullptr, "out is NULL");
     *out = nullptr;
@@ -239,6 +253,18 @@ ecc_status_t ecc_plan_create(int32_t P, const int64_t *h_counts, const int64_t *
     }
     *out = pl;
     return ECC_OK;
+}
+
+// Host allocations of the set-up throw std::bad_alloc when memory runs
+// out: the C ABI reports ECC_ERR_ALLOC instead of letting it escape.
+ecc_status_t ecc_plan_create(int32_t P, const int64_t *h_counts, const int64_t *h_displs,
+                             int32_t max_staleness, void *hip_stream, ecc_plan_t *out) {
+    try {
+        return ecc_plan_create_impl(P, h_counts, h_displs, max_staleness, hip_stream, out);
+    } catch (const std::bad_alloc &) {
+        set_error("host allocation failed");
+        return ECC_ERR_ALLOC;
+    }
 }
 
 ecc_status_t ecc_plan_destroy(ecc_plan_t plan) {

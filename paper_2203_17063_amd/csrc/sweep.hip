@@ -45,6 +45,8 @@
 #include <cstdlib>
 #include <vector>
 
+#include <new>
+
 #include "ecc_common.h"
 
 namespace ecc {
@@ -1324,7 +1326,7 @@ using namespace ecc;
 
 extern "C" {
 
-ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
+static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
                                ecc_matrix_t *out) {
     clear_error();
     ECC_ARG(out != nullptr, "out is NULL");
@@ -1525,6 +1527,18 @@ ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind
         return fail("hipMalloc of partials failed");
     *out = M;
     return ECC_OK;
+}
+
+// Host allocations of the set-up throw std::bad_alloc when memory runs
+// out: the C ABI reports ECC_ERR_ALLOC instead of letting it escape.
+ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
+                               ecc_matrix_t *out) {
+    try {
+        return ecc_matrix_create_impl(plan, A, kind, out);
+    } catch (const std::bad_alloc &) {
+        set_error("host allocation failed");
+        return ECC_ERR_ALLOC;
+    }
 }
 
 ecc_status_t ecc_matrix_destroy(ecc_matrix_t M) {
