@@ -11,7 +11,14 @@ Metric: assembled+iterated GB/s (algorithmic bytes of assembly + sweep + norm,
 each distinct element counted once) and iterations/s, with the dominant
 kernel's achieved bandwidth against the HBM roofline.  Prints one JSON line.
 
-    python bench.py [--steps K] [--warmup W] [--config 1|2|3|4a|4b|5|ssp|thr|mf]
+    python bench.py [--steps K] [--warmup W] [--config NAME]
+
+NAME: jacobi-2d (the default above), jacobi-1d (tridiagonal, n = 4096, 4
+ranks, synchronous), pagerank-rmat (R-MAT scale 22, 64 ranks), jacobi-3d (7-point
+400^3, 512 ranks), allgatherv (256 lognormal blocks, 16.5M elements),
+allreduce (partial allreduce of 256 x 4M), hypercube (allreduce_SSP, 32 x
+16 MB), threshold (Broadcast + Reduce, 32 x 8M), mf (matrix factorisation,
+25M ratings, 32 workers).
 """
 from __future__ import annotations
 
@@ -75,21 +82,21 @@ def read_traffic(kernel_tag, digest):
 
 def build_workload(cfg):
     import workloads as W
-    if cfg == "1":
-        return W.config1()
-    if cfg == "2":
-        return W.config2()
-    if cfg == "3":
-        return W.config3()
-    if cfg == "5":
-        return W.config5()
-    if cfg == "4a":
-        return W.config4a()
-    if cfg == "4b":
-        return W.config4b()
-    if cfg == "ssp":
+    if cfg == "jacobi-1d":
+        return W.jacobi_1d()
+    if cfg == "jacobi-2d":
+        return W.jacobi_2d()
+    if cfg == "pagerank-rmat":
+        return W.pagerank_rmat()
+    if cfg == "jacobi-3d":
+        return W.jacobi_3d()
+    if cfg == "allgatherv":
+        return W.allgatherv_lognormal()
+    if cfg == "allreduce":
+        return W.partial_allreduce()
+    if cfg == "hypercube":
         return W.hypercube_ssp()
-    if cfg == "thr":
+    if cfg == "threshold":
         return W.threshold_collectives()
     if cfg == "mf":
         return W.mf_problem()
@@ -97,25 +104,25 @@ def build_workload(cfg):
 
 
 def describe(cfg, prob):
-    if cfg in ("1", "2", "5"):
-        dims = {"1": "1-D tridiagonal", "2": "2-D 5-point", "5": "3-D 7-point"}[cfg]
+    if cfg in ("jacobi-1d", "jacobi-2d", "jacobi-3d"):
+        dims = {"jacobi-1d": "1-D tridiagonal", "jacobi-2d": "2-D 5-point", "jacobi-3d": "3-D 7-point"}[cfg]
         return {"workload": "jacobi %s Laplacian n=%d, P=%d block-row ranks, S=%d, %s arrivals, "
                             "%d iterations" % (dims, prob.n, prob.P, prob.S,
-                                               "all" if cfg == "1" else "Bernoulli",
+                                               "all" if cfg == "jacobi-1d" else "Bernoulli",
                                                prob.T),
                 "n": prob.n, "nnz": prob.A.nnz, "P": prob.P, "max_staleness": prob.S,
-                "iterations": prob.T, "config_id": cfg}
-    if cfg == "3":
+                "iterations": prob.T, "name": cfg}
+    if cfg == "pagerank-rmat":
         return {"workload": "pagerank power iteration on R-MAT scale %d (%d edges), P=%d, S=%d, "
                             "Bernoulli(0.8), <=%d iterations or L1 < 1e-10"
                             % (prob.meta["scale"], prob.A.nnz, prob.P, prob.S, prob.T),
                 "n": prob.n, "nnz": prob.A.nnz, "P": prob.P, "max_staleness": prob.S,
-                "iterations": prob.T, "config_id": cfg}
-    if cfg == "4a":
+                "iterations": prob.T, "name": cfg}
+    if cfg == "allgatherv":
         return {"workload": "allgatherv assembly, P=%d lognormal counts, %d elements, %d reps"
                             % (prob.P, int(prob.counts.sum()), prob.reps),
                 "P": prob.P, "elements": int(prob.counts.sum()), "reps": prob.reps,
-                "config_id": cfg}
+                "name": cfg}
     if cfg == "mf":
         return {"workload": "data-parallel matrix factorisation over the partial allreduce: %d "
                             "synthetic ratings (%d users x %d items), rank %d, P=%d workers, slack "
@@ -123,22 +130,22 @@ def describe(cfg, prob):
                             % (prob.N, prob.n_users, prob.n_items, prob.rank, prob.P, prob.S,
                                prob.meta["q"], prob.T),
                 "N": prob.N, "n_users": prob.n_users, "n_items": prob.n_items, "rank": prob.rank,
-                "P": prob.P, "slack": prob.S, "iterations": prob.T, "config_id": cfg}
-    if cfg == "thr":
+                "P": prob.P, "slack": prob.S, "iterations": prob.T, "name": cfg}
+    if cfg == "threshold":
         return {"workload": "threshold broadcast + reduce over a binomial tree, P=%d processes x "
                             "%d elements, data fraction %.2f, %d repetitions"
                             % (prob.P, prob.m, prob.theta, prob.reps),
                 "P": prob.P, "m": prob.m, "theta": prob.theta, "reps": prob.reps,
-                "config_id": cfg}
-    if cfg == "ssp":
+                "name": cfg}
+    if cfg == "hypercube":
         return {"workload": "hypercube allreduce_SSP with per-receiver views, P=%d processes x "
                             "%d elements, slack %d, Bernoulli(%.1f) message delivery, %d calls"
                             % (prob.P, prob.m, prob.slack, prob.q, prob.calls),
                 "P": prob.P, "m": prob.m, "slack": prob.slack, "calls": prob.calls,
-                "config_id": cfg}
+                "name": cfg}
     return {"workload": "partial allreduce-sum, P=%d x %d elements, Bernoulli(%.1f), stale "
                         "substitution, %d reps" % (prob.P, prob.m, prob.q, prob.reps),
-            "P": prob.P, "m": prob.m, "reps": prob.reps, "config_id": cfg}
+            "P": prob.P, "m": prob.m, "reps": prob.reps, "name": cfg}
 
 
 # ----------------------------------------------------------------------------
@@ -500,12 +507,12 @@ def run_mf_gpu(prob, steps, warmup):
 def cpu_baseline(cfg, prob, res, budget_s=12.0):
     import oracle
     cores = 1
-    if cfg in ("1", "2", "3", "5"):
+    if cfg in ("jacobi-1d", "jacobi-2d", "pagerank-rmat", "jacobi-3d"):
         # whole iterations of the oracle; sample = first k iterations
         per_iter_bytes = res["bytes_per_step"] / res["iters"]
         t0 = time.perf_counter()
         k = 0
-        sample_iters = res["iters"] if cfg in ("1", "2") else min(res["iters"], 8)
+        sample_iters = res["iters"] if cfg in ("jacobi-1d", "jacobi-2d") else min(res["iters"], 8)
         done_iters = 0
         while True:
             oracle.run_iterative(prob, T=sample_iters, threads=cores)
@@ -519,7 +526,7 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
                 "sample": "%d oracle iterations (%d run(s) of %d) of this workload, 1 thread, "
                           "%.1f s; %.3g iterations/s" % (done_iters, k, sample_iters, dt,
                                                          done_iters / dt)}
-    if cfg == "4a":
+    if cfg == "allgatherv":
         version = np.full(prob.P, -1, dtype=np.int32)
         recv = np.empty_like(prob.send)
         sends = [prob.send[d:d + c] for d, c in zip(prob.displs, prob.counts)]
@@ -549,7 +556,7 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
         return {"value": round(sample_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
                 "kind": "oracle", "sample": "worker 0's errors and gradient at iteration 0 "
                                             "(1/%d of the ratings), 1 thread, %.1f s" % (prob.P, dt)}
-    if cfg == "thr":
+    if cfg == "threshold":
         from oracle import threshold as THO
         P, m = prob.P, prob.m
         vecs = [prob.vector(p) for p in range(P)]
@@ -566,7 +573,7 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
         return {"value": round(per_rep * reps / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
                 "kind": "oracle", "sample": "%d of %d repetitions, 1 thread, %.1f s"
                                             % (reps, prob.reps, dt)}
-    if cfg == "ssp":
+    if cfg == "hypercube":
         # whole calls of the oracle over the full vectors, from a reset
         from oracle import hypercube as HC
         P, m, d = prob.P, prob.m, prob.d
@@ -639,7 +646,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="2", choices=["1", "2", "3", "4a", "4b", "5", "ssp", "thr", "mf"])
+    ap.add_argument("--config", default="jacobi-2d",
+                    choices=["jacobi-1d", "jacobi-2d", "pagerank-rmat", "jacobi-3d", "allgatherv",
+                             "allreduce", "hypercube", "threshold", "mf"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only measure a plain 4 GiB device copy (copy ceiling)")
@@ -662,30 +671,30 @@ def main():
         return
 
     cfg = args.config
-    print("[bench] generating workload config %s" % cfg, file=sys.stderr, flush=True)
+    print("[bench] generating workload %s" % cfg, file=sys.stderr, flush=True)
     prob = build_workload(cfg)
     print("[bench] running on GPU", file=sys.stderr, flush=True)
-    if cfg in ("1", "2", "3", "5"):
+    if cfg in ("jacobi-1d", "jacobi-2d", "pagerank-rmat", "jacobi-3d"):
         res = run_iterative_gpu(cfg, prob, args.steps, args.warmup)
         digest = kernel_source_digest(["sweep.hip", "ecc_common.h"])
-        tag = "sweep_%s_cfg%s" % ("jacobi" if prob.kind == "jacobi" else "pagerank", cfg)
+        tag = "sweep_" + cfg.replace("-", "_")
         dom_ms, dom_n = res["times"]["SWEEP"]
-    elif cfg == "4a":
+    elif cfg == "allgatherv":
         res = run_allgatherv_gpu(prob, args.steps, args.warmup)
         digest = kernel_source_digest(["collectives.hip", "ecc_common.h"])
-        tag = "assemble_cfg4a"
+        tag = "assemble_allgatherv"
         dom_ms, dom_n = res["times"]["ASSEMBLE"]
     elif cfg == "mf":
         res = run_mf_gpu(prob, args.steps, args.warmup)
         digest = kernel_source_digest(["mf.hip", "ecc_common.h"])
         tag = "mf_grad_p32"
         dom_ms, dom_n = res["times"]["MF_GRAD"]
-    elif cfg == "thr":
+    elif cfg == "threshold":
         res = run_threshold_gpu(prob, args.steps, args.warmup)
         digest = kernel_source_digest(["threshold.hip", "ecc_common.h"])
         tag = "reduce_threshold_p32"
         dom_ms, dom_n = res["times"]["REDUCE"]
-    elif cfg == "ssp":
+    elif cfg == "hypercube":
         res = run_hypercube_gpu(prob, args.steps, args.warmup)
         digest = kernel_source_digest(["hypercube.hip", "ecc_common.h"])
         tag = "allreduce_ssp_p32"
@@ -693,7 +702,7 @@ def main():
     else:
         res = run_allreduce_gpu(prob, args.steps, args.warmup)
         digest = kernel_source_digest(["collectives.hip", "ecc_common.h"])
-        tag = "allreduce_cfg4b"
+        tag = "allreduce_partial"
         dom_ms, dom_n = res["times"]["ALLREDUCE"]
 
     steps = args.steps

@@ -27,22 +27,22 @@ def _gpu():
     torch.cuda.empty_cache()
 
 
-def test_config3_full():
+def test_pagerank_rmat_full():
     """PageRank on R-MAT scale 22 (2^26 edges), 64 ranks, S = 4."""
-    _solve_and_compare(W.config3(), bitwise=False, threads=THREADS)
+    _solve_and_compare(W.pagerank_rmat(), bitwise=False, threads=THREADS)
 
 
-def test_config5_full():
+def test_jacobi_3d_full():
     """3-D Jacobi, n = 64,000,000, 447,040,000 nonzeros, 512 ranks, S = 5:
     iterates bitwise equal to the oracle."""
-    _solve_and_compare(W.config5(), bitwise=True, threads=THREADS)
+    _solve_and_compare(W.jacobi_3d(), bitwise=True, threads=THREADS)
 
 
-def test_config4a_full():
+def test_allgatherv_full():
     """allgatherv of 256 lognormal blocks (16.5M elements), 1,000 repetitions."""
     from paper_2203_17063_amd import capi as E
     from paper_2203_17063_amd import runner as R
-    prob = W.config4a()
+    prob = W.allgatherv_lognormal()
     announce("4a full", int(prob.counts.sum()), prob.reps)
     send = torch.from_numpy(prob.send).cuda()
     recv = torch.full_like(send, float("nan"))

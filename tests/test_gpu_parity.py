@@ -127,7 +127,7 @@ def test_assemble_parity(P, layout, S, misalign):
 
 def test_assemble_packed_and_empty():
     E, R = _capi(), _runner()
-    prob = W.config4a(P=256, reps=6, mean=700.0)
+    prob = W.allgatherv_lognormal(P=256, reps=6, mean=700.0)
     announce("assemble_packed 4a-small", prob.counts.sum())
     E_tot = int(prob.counts.sum())
     send = torch.from_numpy(prob.send).cuda()
@@ -206,11 +206,11 @@ def test_allreduce_parity(P, m, S, aligned):
     plan.close()
 
 
-def test_allreduce_config4b_sampled():
-    """Config 4b's shape (256 ranks x 4M, 70% arrival, no staleness bound) for a
+def test_partial_allreduce_full_sampled():
+    """The benchmark's partial allreduce shape (256 ranks x 4M, 70% arrival, no staleness bound) for a
     few repetitions, checked at sampled indices against the last-arrival sum."""
     E, R = _capi(), _runner()
-    prob = W.config4b(reps=4)
+    prob = W.partial_allreduce(reps=4)
     P, m = prob.P, prob.m
     announce("allreduce 4b full-size sampled", P, m)
     fresh = [torch.empty(m, dtype=torch.float64, device="cuda") for _ in range(P)]
@@ -294,34 +294,34 @@ def _solve_and_compare(prob, bitwise, threads=8, layout=None):
     return iters
 
 
-def test_solve_config1():
-    _solve_and_compare(W.config1(), bitwise=True)
+def test_solve_jacobi_1d():
+    _solve_and_compare(W.jacobi_1d(), bitwise=True)
 
 
 @pytest.mark.parametrize("N,T", [(33, 40), (64, 80)])
-def test_solve_config2_small(N, T):
-    _solve_and_compare(W.config2(N=N, T=T), bitwise=True)
+def test_solve_jacobi_2d_small(N, T):
+    _solve_and_compare(W.jacobi_2d(N=N, T=T), bitwise=True)
 
 
-def test_solve_config2_full():
-    _solve_and_compare(W.config2(), bitwise=True)
+def test_solve_jacobi_2d_full():
+    _solve_and_compare(W.jacobi_2d(), bitwise=True)
 
 
 @pytest.mark.parametrize("N,P", [(12, 512), (24, 512), (40, 64)])
-def test_solve_config5_small(N, P):
-    _solve_and_compare(W.config5(N=N, T=60, P=P), bitwise=True)
+def test_solve_jacobi_3d_small(N, P):
+    _solve_and_compare(W.jacobi_3d(N=N, T=60, P=P), bitwise=True)
 
 
 @pytest.mark.parametrize("scale", [8, 12, 15, 17])
-def test_solve_config3_small(scale):
+def test_solve_pagerank_rmat_small(scale):
     """Scale 15 has rows summed by a whole workgroup; scale 17 also has rows
     longer than one work item, split into pieces and recombined."""
-    _solve_and_compare(W.config3(scale=scale, T=60), bitwise=False, layout="SORTED")
+    _solve_and_compare(W.pagerank_rmat(scale=scale, T=60), bitwise=False, layout="SORTED")
 
 
 def test_solve_many_ranks_unfused():
     """More ranks than a workgroup stages in LDS: separate assembly launches."""
-    _solve_and_compare(W.config5(N=24, T=30, P=2048), bitwise=True)
+    _solve_and_compare(W.jacobi_3d(N=24, T=30, P=2048), bitwise=True)
 
 
 def _arrow_problem(n=40000, T=40, P=7, S=2):
@@ -543,11 +543,11 @@ def test_solve_range_layout(kind, counts, range_bytes):
 
 
 @pytest.mark.parametrize("scale", [12, 15, 17])
-def test_solve_config3_ranges(scale):
+def test_solve_pagerank_rmat_ranges(scale):
     """R-MAT PageRank in the range layout (scale 15 has sub-rows summed by a
     whole workgroup, scale 17 split sub-rows)."""
     with _range_bytes(4096):
-        _solve_and_compare(W.config3(scale=scale, T=60), bitwise=False, layout="RANGES")
+        _solve_and_compare(W.pagerank_rmat(scale=scale, T=60), bitwise=False, layout="RANGES")
 
 
 def test_solve_arrow_ranges():
@@ -566,8 +566,8 @@ def test_solve_sorted_layout(kind, counts):
     _solve_and_compare(prob, bitwise=False, layout="SORTED")
 
 
-def test_solve_config3_tolerance_stop():
-    prob = W.config3(scale=10, T=200)
+def test_solve_pagerank_rmat_tolerance_stop():
+    prob = W.pagerank_rmat(scale=10, T=200)
     iters = _solve_and_compare(prob, bitwise=False)
     assert iters < 200
 
@@ -576,14 +576,14 @@ def test_step_api_matches_solve():
     """assemble -> iterate -> residual through the separate calls reproduce the
     loop-control call bit for bit (fused single-launch loop, the loop with a
     second pass per iteration, and split rows)."""
-    _step_api_matches_solve((W.config2(N=40, T=25), W.config3(scale=11, T=25),
+    _step_api_matches_solve((W.jacobi_2d(N=40, T=25), W.pagerank_rmat(scale=11, T=25),
                              _arrow_problem(T=12)))
 
 
 def test_step_api_matches_solve_ranges():
     """The same for the range layout (sub-row sums, then rows)."""
     with _range_bytes(2048):
-        _step_api_matches_solve((W.config3(scale=11, T=25), _arrow_problem(T=12)))
+        _step_api_matches_solve((W.pagerank_rmat(scale=11, T=25), _arrow_problem(T=12)))
 
 
 def _step_api_matches_solve(problems):
@@ -614,16 +614,16 @@ def test_layout_choice():
     longer rows the stream layout, power-law rows the sorted layout, or over a
     vector of several column ranges the range layout."""
     E, R = _capi(), _runner()
-    cases = [(W.config1(), E.ECC_LAYOUT_SHORT, 3), (W.config2(N=33, T=2), E.ECC_LAYOUT_SHORT, 5),
-             (W.config5(N=12, T=2, P=8), E.ECC_LAYOUT_SHORT, 7),
+    cases = [(W.jacobi_1d(), E.ECC_LAYOUT_SHORT, 3), (W.jacobi_2d(N=33, T=2), E.ECC_LAYOUT_SHORT, 5),
+             (W.jacobi_3d(N=12, T=2, P=8), E.ECC_LAYOUT_SHORT, 7),
              (_banded_problem("jacobi", 3000, 4, 4, T=2), E.ECC_LAYOUT_SHORT, 4),
              (_banded_problem("power", 3000, 6, 6, T=2), E.ECC_LAYOUT_SHORT, 7),
              (_banded_problem("jacobi", 3000, 9, 16, T=2), E.ECC_LAYOUT_STREAM, 0),
-             (W.config3(scale=10, T=2), E.ECC_LAYOUT_SORTED, 0)]
+             (W.pagerank_rmat(scale=10, T=2), E.ECC_LAYOUT_SORTED, 0)]
     for prob, layout, slots in cases:
         _check_layout(R, E, prob, layout, slots)
     with _range_bytes(4096):          # 8 KB of vector: two column ranges
-        _check_layout(R, E, W.config3(scale=10, T=2), E.ECC_LAYOUT_RANGES, 2)
+        _check_layout(R, E, W.pagerank_rmat(scale=10, T=2), E.ECC_LAYOUT_RANGES, 2)
 
 
 def _check_layout(R, E, prob, layout, slots):
@@ -637,7 +637,7 @@ def _check_layout(R, E, prob, layout, slots):
 
 def test_matrix_checks():
     E, R = _capi(), _runner()
-    prob = W.config2(N=8, T=2)
+    prob = W.jacobi_2d(N=8, T=2)
     announce("matrix checks")
     run = R.Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts, prob.S,
                       prob.mask, "jacobi", b=prob.b)

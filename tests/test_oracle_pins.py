@@ -291,9 +291,9 @@ def test_jacobi_2x2_hand_example(golden):
 
 
 def test_jacobi_1d_fixed_point_thomas():
-    """Config 1 (synchronous) after 50 sweeps is within rho(M)^50 sqrt(n) of the
+    """The synchronous 1-D Jacobi workload after 50 sweeps is within rho(M)^50 sqrt(n) of the
     exact solution from a banded LAPACK solve (rho(M) = cos(pi/(n+1))/2)."""
-    prob = W.config1()
+    prob = W.jacobi_1d()
     h = oracle.run_iterative(prob)
     n = prob.n
     ab = np.zeros((3, n))

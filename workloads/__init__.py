@@ -310,7 +310,7 @@ class Iterative:
         return self.A.n_rows
 
 
-def config1() -> Iterative:
+def jacobi_1d() -> Iterative:
     """1-D tridiag(-1, 4, -1), n = 4096, b ~ U[0,1), P = 4 Dirichlet(1) blocks,
     every block arrives every iteration, S = 0, 50 iterations."""
     seed = seed_of(1)
@@ -318,13 +318,13 @@ def config1() -> Iterative:
     A = stencil_csr(1, n, 4.0)
     counts = dirichlet_partition(n, 4, seed)
     T = 50
-    return Iterative("cfg1-jacobi-1d", "jacobi", A, counts, exclusive_scan(counts), 0,
+    return Iterative("jacobi-1d", "jacobi", A, counts, exclusive_scan(counts), 0,
                      np.ones((T, 4), dtype=np.uint8), T, np.zeros(n),
                      b=uniform(seed, STREAM_B, n), norm=2,
                      meta={"dim": 1, "N": n, "diag": 4.0, "q": 1.0})
 
 
-def config2(N: int = 1024, T: int = 200) -> Iterative:
+def jacobi_2d(N: int = 1024, T: int = 200) -> Iterative:
     """2-D 5-point Laplacian N x N with the diagonal shifted by +4 (diag 8),
     b ~ N(0,1), P = 16 uneven blocks, Bernoulli(0.9) arrivals, S = 3."""
     seed = seed_of(2)
@@ -333,12 +333,12 @@ def config2(N: int = 1024, T: int = 200) -> Iterative:
     P = 16
     counts = dirichlet_partition(n, P, seed)
     q = np.full(P, 0.9)
-    return Iterative("cfg2-jacobi-2d", "jacobi", A, counts, exclusive_scan(counts), 3,
+    return Iterative("jacobi-2d", "jacobi", A, counts, exclusive_scan(counts), 3,
                      arrival_mask(seed, T, q), T, np.zeros(n), b=normal(seed, STREAM_B, n),
                      norm=2, meta={"dim": 2, "N": N, "diag": 8.0, "q": 0.9})
 
 
-def config3(scale: int = 22, edge_factor: int = 16, T: int = 100, P: int = 64) -> Iterative:
+def pagerank_rmat(scale: int = 22, edge_factor: int = 16, T: int = 100, P: int = 64) -> Iterative:
     """PageRank power iteration x <- 0.85 W x + 0.15/n on an R-MAT graph
     (2^scale vertices, edge_factor * 2^scale edges), W = A^T D^-1 in pull CSR,
     P edge-balanced blocks, Bernoulli(0.8) arrivals, S = 4, stop at
@@ -351,13 +351,13 @@ def config3(scale: int = 22, edge_factor: int = 16, T: int = 100, P: int = 64) -
     del src, dst
     counts = edge_balanced_partition(W.row_ptr, P)
     q = np.full(P, 0.8)
-    return Iterative("cfg3-pagerank-rmat", "power", W, counts, exclusive_scan(counts), 4,
+    return Iterative("pagerank-rmat", "power", W, counts, exclusive_scan(counts), 4,
                      arrival_mask(seed, T, q), T, np.full(n, 1.0 / n), alpha=0.85,
                      beta=0.15 / n, tol=1e-10, norm=1,
                      meta={"scale": scale, "edges": E, "q": 0.8})
 
 
-def config5(N: int = 400, T: int = 100, P: int = 512) -> Iterative:
+def jacobi_3d(N: int = 400, T: int = 100, P: int = 512) -> Iterative:
     """3-D 7-point Laplacian N^3 with the diagonal shifted by +6 (diag 12),
     b ~ U[0,1), P uneven blocks, per-rank arrival probability q_p ~ U[0.6, 0.95],
     S = 5."""
@@ -366,7 +366,7 @@ def config5(N: int = 400, T: int = 100, P: int = 512) -> Iterative:
     n = A.n_rows
     counts = dirichlet_partition(n, P, seed)
     q = 0.6 + 0.35 * uniform(seed, STREAM_Q, P)
-    return Iterative("cfg5-jacobi-3d", "jacobi", A, counts, exclusive_scan(counts), 5,
+    return Iterative("jacobi-3d", "jacobi", A, counts, exclusive_scan(counts), 5,
                      arrival_mask(seed, T, q), T, np.zeros(n), b=uniform(seed, STREAM_B, n),
                      norm=2, meta={"dim": 3, "N": N, "diag": 12.0, "q": "U[0.6,0.95]"})
 
@@ -388,7 +388,7 @@ class Allgatherv:
         return int(self.counts.shape[0])
 
 
-def config4a(P: int = 256, reps: int = 1000, mean: float = 65536.0) -> Allgatherv:
+def allgatherv_lognormal(P: int = 256, reps: int = 1000, mean: float = 65536.0) -> Allgatherv:
     seed = seed_of(4)
     counts = lognormal_counts(P, seed, mean=mean)
     displs = exclusive_scan(counts)
@@ -422,7 +422,7 @@ class Allreduce:
         return uniform_at(self.seed, STREAM_PAYLOAD_REDUCE, ctr, lo=-1.0, hi=1.0)
 
 
-def config4b(P: int = 256, m: int = 1 << 22, reps: int = 1000, q: float = 0.7,
+def partial_allreduce(P: int = 256, m: int = 1 << 22, reps: int = 1000, q: float = 0.7,
              S: int = UNBOUNDED) -> Allreduce:
     seed = seed_of(4)
     return Allreduce(P, m, reps, arrival_mask(seed, reps, np.full(P, q)), S, seed, q)
