@@ -5,7 +5,7 @@
 // elsewhere, plus the residual-norm reduction.
 //
 // Work decomposition (built once per matrix on the host, CSR-Adaptive style
-// after Greathouse & Daga, SC'14), in one of three layouts per matrix:
+// after Greathouse & Daga, SC'14), in one of four layouts per matrix:
 //  - short rows (every row holds at most 8 entries): the entries are copied
 //    column-major at set-up; an item is a run of up to 256 rows of one rank,
 //    one lane per row, pipelined two items deep;
@@ -16,11 +16,18 @@
 //    items over a copy of the matrix, made at set-up, whose rows are ordered
 //    by decreasing length within each rank, so that an item holds rows of
 //    similar length and its lanes split evenly over them; a map from sorted
-//    position to row places each result.
-// In the last two, a "vector" item is one long row summed by the whole
+//    position to row places each result;
+//  - range items for very uneven rows over a vector longer than one column
+//    range: every row cut into its entries of each column range (sub-rows),
+//    the sub-rows swept range by range as sorted stream items (so that the
+//    gathers of a time come from one range of the vector, which stays in
+//    L2), each sub-row's sum stored, and every row then finished from its
+//    sub-row sums added in range order by a second kernel.
+// In the last three, a "vector" item is one long row summed by the whole
 // workgroup and a "piece" a fixed-size slice of a very long row whose
 // partial sum is recombined, in piece order, at the end.  Items never
-// straddle a rank boundary, so [lo, hi) is uniform per item.  Rows summed by
+// straddle a rank boundary, so [lo, hi) is uniform per item (range items
+// excepted: a length class mixes ranks, so each sub-row carries its rank).  Rows summed by
 // a single lane accumulate in CSR order with no fused multiply-add, exactly
 // like the sequential definition.
 //
