@@ -208,10 +208,21 @@ ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *con
  * than one work item are split and recombined in a fixed order), and for
  * ECC_KIND_JACOBI checks that every row has exactly one diagonal entry and
  * that it is non-zero (else ECC_ERR_ARG).  It chooses the sweep layout:
- *   ECC_LAYOUT_SHORT   every row holds at most 8 entries: the entries are
- *                      copied, column-major and padded to the longest row's
- *                      class R in {3, 4, 5, 7, 8} (12 bytes x R x n_rows of
- *                      device memory), one lane per row;
+ *   ECC_LAYOUT_SHORT   every row holds at most 8 entries: work items are
+ *                      runs of up to 256 rows of one rank, one lane per row,
+ *                      and the entries are copied item by item in the order
+ *                      the items are swept, each item's entries stored
+ *                      entry-major (entry k of all its rows together) and
+ *                      padded to the longest row's class R in {3, 4, 5, 7, 8}
+ *                      (about 12 bytes x R x n_rows of device memory).  When
+ *                      the columns of every row lie near the row itself or
+ *                      near the rows one "plane" away (the bandwidth B: a
+ *                      3-D grid stencil), and B rows are too many for the
+ *                      rows one plane apart to meet in L2, the items are
+ *                      swept in plane tiles: rows [z B + tau W, z B + (tau
+ *                      + 1) W) for every plane z, tile after tile, so that
+ *                      a row's neighbours one plane away were read a few
+ *                      items earlier (ecc_matrix_tiling reports B and W);
  *   ECC_LAYOUT_SORTED  very uneven rows (longest > 64 and > 8 x (mean + 1))
  *                      over a vector of at most one column range (below):
  *                      the rows of every rank are copied in order of
@@ -219,9 +230,9 @@ ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *con
  *                      of device memory) and swept in runs staged in LDS;
  *   ECC_LAYOUT_RANGES  very uneven rows over a longer vector: the columns are
  *                      cut into R = ceil(8 x n_rows / 8 MiB) ranges of equal
- *                      width (2 <= R <= 16; the environment variable
- *                      ECC_RANGE_BYTES, read here, replaces the 8 MiB), every
- *                      row into its entries of each range, and these
+ *                      width (2 <= R <= 16; ecc_matrix_opts_t.range_bytes
+ *                      replaces the 8 MiB), every row into its entries of
+ *                      each range, and these
  *                      sub-rows are copied range by range in order of
  *                      decreasing length class (12 bytes x nnz, 12 bytes per
  *                      sub-row, 8 x R + 2 bytes x n_rows of device memory,
@@ -240,6 +251,46 @@ ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *con
 ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
                                ecc_matrix_t *out);
 ecc_status_t ecc_matrix_destroy(ecc_matrix_t A);
+
+/* Set-up choices of ecc_matrix_create_ex; all zero gives ecc_matrix_create's
+ * defaults.  They change how a sweep is laid out and ordered, never what it
+ * computes, except that range_bytes changes the ECC_LAYOUT_RANGES rounding
+ * (the number of sub-row sums added per row).
+ *   range_bytes  ECC_LAYOUT_RANGES: bytes of the vector per column range
+ *                (0: 8 MiB).
+ *   tile_rows    ECC_LAYOUT_SHORT plane tiles: 0 chosen from the matrix, > 0
+ *                that many rows per tile (rounded up to a multiple of 256;
+ *                applied only to a matrix that qualifies for tiling), < 0
+ *                items in row order.
+ *   schedule     ECC_LAYOUT_SHORT: how a sweep's workgroups share the items.
+ *                ECC_SCHEDULE_STATIC: each walks a fixed set (items cut into
+ *                eight ranges, one per XCD).  ECC_SCHEDULE_QUEUE: each claims
+ *                the next item of its XCD's range with an atomic ticket (and
+ *                of the other ranges once its own is exhausted); each item
+ *                then writes its own partial norm, so ecc_partials_size is
+ *                the item count + 1.  ECC_SCHEDULE_AUTO (0): the queue when
+ *                a workgroup would walk at least 16 items.
+ * opts may be NULL (the defaults).  ECC_ERR_ARG for a negative range_bytes
+ * or an unknown schedule. */
+#define ECC_SCHEDULE_AUTO 0
+#define ECC_SCHEDULE_STATIC 1
+#define ECC_SCHEDULE_QUEUE 2
+typedef struct {
+    int64_t range_bytes;
+    int64_t tile_rows;
+    int32_t schedule;
+} ecc_matrix_opts_t;
+ecc_status_t ecc_matrix_create_ex(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
+                                  const ecc_matrix_opts_t *opts, ecc_matrix_t *out);
+
+/* ECC_LAYOUT_SHORT plane tiling chosen at set-up (host only): *plane_rows =
+ * the bandwidth B taken as the plane size and *tile_rows = W, both 0 when
+ * the items are swept in row order. */
+ecc_status_t ecc_matrix_tiling(ecc_matrix_t A, int64_t *plane_rows, int64_t *tile_rows);
+
+/* Schedule chosen at set-up (host only): ECC_SCHEDULE_STATIC or
+ * ECC_SCHEDULE_QUEUE. */
+ecc_status_t ecc_matrix_schedule(ecc_matrix_t A, int32_t *schedule);
 
 /* The layout ecc_matrix_create chose (ECC_LAYOUT_*) and, for
  * ECC_LAYOUT_SHORT, the entries held per row R, for ECC_LAYOUT_RANGES the

@@ -24,6 +24,7 @@ ECC_TIMING_ASSEMBLE, ECC_TIMING_ALLREDUCE, ECC_TIMING_SWEEP, ECC_TIMING_NORM = 0
 ECC_TIMING_MF_GRAD, ECC_TIMING_MF_STEP, ECC_TIMING_KINDS = 4, 5, 6
 ECC_THRESHOLD_DATA, ECC_THRESHOLD_PROCS = 0, 1
 ECC_LAYOUT_STREAM, ECC_LAYOUT_SORTED, ECC_LAYOUT_SHORT, ECC_LAYOUT_RANGES = 0, 1, 2, 3
+ECC_SCHEDULE_AUTO, ECC_SCHEDULE_STATIC, ECC_SCHEDULE_QUEUE = 0, 1, 2
 
 STATUS_NAMES = {0: "ECC_OK", 1: "ECC_ERR_ARG", 2: "ECC_ERR_OVERLAP", 3: "ECC_ERR_RANGE",
                 4: "ECC_ERR_ALLOC", 5: "ECC_ERR_DEVICE", 6: "ECC_ERR_STATE"}
@@ -39,6 +40,11 @@ class ecc_csr_t(ctypes.Structure):
     _fields_ = [("n_rows", ctypes.c_int64), ("n_cols", ctypes.c_int64), ("nnz", ctypes.c_int64),
                 ("d_row_ptr", ctypes.c_void_p), ("d_col", ctypes.c_void_p),
                 ("d_val", ctypes.c_void_p)]
+
+
+class ecc_matrix_opts_t(ctypes.Structure):
+    _fields_ = [("range_bytes", ctypes.c_int64), ("tile_rows", ctypes.c_int64),
+                ("schedule", ctypes.c_int32)]
 
 
 _lib = None
@@ -61,7 +67,12 @@ _SIGS = [
     ("ecc_allgatherv_assemble_packed", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP]),
     ("ecc_allreduce_partial", ctypes.c_int, [_VP, _I64, _VP, _VP, _VP, _VP, _VP, _VP]),
     ("ecc_matrix_create", ctypes.c_int, [_VP, ctypes.POINTER(ecc_csr_t), _I32, ctypes.POINTER(_VP)]),
+    ("ecc_matrix_create_ex", ctypes.c_int, [_VP, ctypes.POINTER(ecc_csr_t), _I32,
+                                            ctypes.POINTER(ecc_matrix_opts_t),
+                                            ctypes.POINTER(_VP)]),
     ("ecc_matrix_destroy", ctypes.c_int, [_VP]),
+    ("ecc_matrix_tiling", ctypes.c_int, [_VP, _VP, _VP]),
+    ("ecc_matrix_schedule", ctypes.c_int, [_VP, _VP]),
     ("ecc_partials_size", _I64, [_VP]),
     ("ecc_matrix_layout", ctypes.c_int, [_VP, _VP, _VP]),
     ("ecc_iterate_jacobi", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP]),
@@ -213,6 +224,28 @@ def ecc_matrix_create(plan, csr: ecc_csr_t, kind: int) -> int:
     out = _VP()
     _check(lib().ecc_matrix_create(plan, ctypes.byref(csr), kind, ctypes.byref(out)))
     return out.value
+
+
+def ecc_matrix_create_ex(plan, csr: ecc_csr_t, kind: int, range_bytes: int = 0,
+                         tile_rows: int = 0, schedule: int = 0) -> int:
+    out = _VP()
+    opts = ecc_matrix_opts_t(range_bytes, tile_rows, schedule)
+    _check(lib().ecc_matrix_create_ex(plan, ctypes.byref(csr), kind, ctypes.byref(opts),
+                                      ctypes.byref(out)))
+    return out.value
+
+
+def ecc_matrix_tiling(mat):
+    """(plane rows, tile rows) of a short-layout matrix; (0, 0) in row order."""
+    plane, tile = ctypes.c_int64(0), ctypes.c_int64(0)
+    _check(lib().ecc_matrix_tiling(mat, ctypes.byref(plane), ctypes.byref(tile)))
+    return plane.value, tile.value
+
+
+def ecc_matrix_schedule(mat) -> int:
+    sch = ctypes.c_int32(0)
+    _check(lib().ecc_matrix_schedule(mat, ctypes.byref(sch)))
+    return sch.value
 
 
 def ecc_matrix_destroy(mat):

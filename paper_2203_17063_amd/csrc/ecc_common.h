@@ -88,6 +88,19 @@ enum { kItemStream = 0, kItemVector = 1, kItemPiece = 2 };
 enum { kLayStream = 0, kLaySorted = 1, kLayShort = 2, kLayRanges = 3 };
 constexpr int kMaxRanges = 16;              // column ranges of the range layout at most
 constexpr int64_t kRangeBytes = 8 << 20;    // bytes of the vector per column range
+// Plane tiling of the short-row layout: applied when one plane of rows
+// streams more than kTileMinBytes (the rows one plane apart no longer meet
+// in an XCD's 4 MB L2); tiles of kTileNearFactor times the largest in-plane
+// column offset, at least kTileMinRows rows.
+constexpr int64_t kTileMinBytes = 4 << 20;
+constexpr int64_t kTileNearFactor = 64;
+constexpr int64_t kTileMinRows = 4096;
+// Item queue of a short-layout sweep (see sweep.hip): one ticket counter per
+// XCD range of items, 256 bytes apart, then the count of workgroups done.
+// Taken when a workgroup would otherwise walk at least kQueueMinItems items.
+constexpr int kQueueRanges = 8;
+constexpr int kQueueStride = 64;
+constexpr int64_t kQueueMinItems = 16;
 constexpr int kShortRow = 8;
 static_assert(kShortRow <= 8, "a short row is summed from eight registers");
 static_assert(kStreamRows <= 256 && kStreamRows <= kSweepThreads, "one lane per short row");
@@ -239,11 +252,22 @@ __device__ __forceinline__ void record_step(int32_t P, int32_t S, int64_t t,
 // thread j adds values j, j + kNormThreads, ... in order, then a fixed tree.
 // The value at index `n - 1` may be supplied in a register (`last`, used when
 // `use_last`) instead of being read, with the same order of operations.
+// Loads are issued eight at a time, the additions stay in that order.
 __device__ __forceinline__ double reduce_values(const double *__restrict__ v, int64_t n,
                                                 bool use_last, double last, double *scratch) {
     double acc = 0.0;
-    for (int64_t k = threadIdx.x; k < n; k += kNormThreads)
-        acc += (use_last && k == n - 1) ? last : v[k];
+    int64_t k = threadIdx.x;
+    for (; k + 7 * kNormThreads < n; k += 8 * kNormThreads) {
+        double t[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int64_t q = k + (int64_t)j * kNormThreads;
+            t[j] = (use_last && q == n - 1) ? last : v[q];
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc += t[j];
+    }
+    for (; k < n; k += kNormThreads) acc += (use_last && k == n - 1) ? last : v[k];
     return block_sum<kNormThreads>(acc, scratch);
 }
 
@@ -312,9 +336,14 @@ struct ecc_matrix_s {
     double *d_diag = nullptr;       // [n] Jacobi: each row's diagonal entry
     ecc::Fixup *d_rfix = nullptr;   // split sub-rows: (row, first piece, pieces, range)
     int64_t n_rfix = 0;
-    int32_t *d_ell_col = nullptr;   // short layout: entries column-major, [R][n] (-1: padding)
-    double *d_ell_val = nullptr;    // short layout: their values, [R][n]
-    double *d_partials = nullptr;   // internal partials of ecc_solve: 2 x (grid + 1)
+    int32_t *d_ell_col = nullptr;   // short layout: entries item by item, entry-major (-1: padding)
+    double *d_ell_val = nullptr;    // short layout: their values
+    int64_t tile_plane = 0;         // short layout: plane rows of the tiled item order (0: row order)
+    int64_t tile_rows = 0;          // short layout: rows per tile
+    double *d_partials = nullptr;   // internal partials of ecc_solve: 2 x n_part
+    int64_t n_part = 1;             // partial sums a sweep writes: grid + 1, or n_items + 1 (queue)
+    bool queue = false;             // short layout: items claimed from a run-time queue
+    unsigned *d_queue = nullptr;    // its ticket counters, (kQueueRanges + 1) x kQueueStride
 };
 
 namespace ecc {

@@ -52,7 +52,7 @@ extern "C" ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double 
     hipLaunchKernelGGL(k_ctrl_reset, dim3(1), dim3(64), 0, plan->stream, plan->d_ctrl);
     ECC_LAUNCH_CHECK();
     const int32_t *done = plan->d_ctrl;
-    const int64_t G1 = (int64_t)A->grid + 1;
+    const int64_t G1 = A->n_part;
     // Without a tolerance and without split rows, every iteration is a single
     // launch: workgroup 0 of launch t reduces launch t-1's partials (double
     // buffer), and one last pass reduces those of the final iteration.

@@ -49,7 +49,6 @@
 // rank arrives.  No entry of x_hat that is written is read in the same
 // launch, so the fused step equals assemble-then-sweep bit for bit.
 #include <algorithm>
-#include <cstdlib>
 #include <vector>
 
 #include <new>
@@ -103,6 +102,10 @@ struct SweepArgs {
     double *prev_rho;
     int32_t norm;
     const int32_t *done;
+    // partial sums per launch (the last one is split rows' share) and, for a
+    // queue-scheduled matrix, its ticket counters
+    int64_t n_part;
+    unsigned *queue;
 };
 
 // Rank state staged in LDS by a fused step.
@@ -445,7 +448,6 @@ template <bool STEP>
 __device__ __forceinline__ void sweep_prologue(const SweepArgs &a, uint8_t *s_eff, int32_t *s_bs,
                                                double *s_red) {
     const int tid = threadIdx.x;
-    const int32_t G = gridDim.x;
     if constexpr (STEP) {
         for (int32_t p = tid; p < a.P; p += kSweepThreads)
             s_eff[p] = stale_select(a.ver_in[p], a.arrived[p], a.t, a.S) ? 1 : 0;
@@ -455,12 +457,12 @@ __device__ __forceinline__ void sweep_prologue(const SweepArgs &a, uint8_t *s_ef
                         a.forced, a.eff_user, a.age_user, nullptr);
     }
     if (blockIdx.x == 0) {
-        // no split rows: their norm contribution (partial G) is zero
-        if (a.zero_extra && tid == 0) a.partials[G] = 0.0;
+        // no split rows: their norm contribution (the last partial) is zero
+        if (a.zero_extra && tid == 0) a.partials[a.n_part - 1] = 0.0;
         // deferred norm of the previous loop iteration, whose partials the
         // kernel boundary has made visible (same order as a separate pass)
         if (a.prev_partials) {
-            const double sum = reduce_values(a.prev_partials, (int64_t)G + 1, false, 0.0, s_red);
+            const double sum = reduce_values(a.prev_partials, a.n_part, false, 0.0, s_red);
             if (tid == 0) *a.prev_rho = (a.norm == ECC_NORM_L2) ? sqrt(sum) : sum;
         }
     }
@@ -621,21 +623,29 @@ __global__ __launch_bounds__(kFinishThreads) void k_range_finish(RangeFinishArgs
     }
 }
 
-// Entries of one short row in the column-major copy: entry k of row i sits
-// at ell[k * n + i], so the lanes of a wave (consecutive rows) load
-// consecutive words; padding past the row's end has column -1.
+// Entries of one short row in the item-major copy.  Item w's entries start
+// at row offset base = w.k0 (a multiple of 32) and are stored entry-major
+// over the item's rows padded to a multiple of 32: entry k of the item's
+// row l sits at [base * R + k * pad + l], so the lanes of a wave load
+// consecutive words and an item's entries are one contiguous run of the
+// copy, which is laid out in the order the items are swept.  Padding past a
+// row's end has column -1.
 template <int R>
 struct EllEntries {
     int32_t c[R];
     double v[R];
 };
 
+__device__ __forceinline__ int32_t sell_pad(int32_t nrows) { return (nrows + 31) & ~31; }
+
 template <int R>
-__device__ __forceinline__ void ell_entries(const SweepArgs &a, bool live, int32_t i,
-                                            EllEntries<R> &e) {
+__device__ __forceinline__ void ell_entries(const SweepArgs &a, bool live, const WorkItem &w,
+                                            int32_t l, EllEntries<R> &e) {
+    const int64_t base = (int64_t)w.k0 * R + l;
+    const int32_t pad = sell_pad(w.nrows);
 #pragma unroll
     for (int j = 0; j < R; ++j) {
-        const int64_t k = (int64_t)j * a.ell_n + i;
+        const int64_t k = base + (int64_t)j * pad;
         e.c[j] = live ? a.ell_col[k] : -1;
         e.v[j] = live ? a.ell_val[k] : 0.0;
     }
@@ -660,7 +670,7 @@ __device__ __forceinline__ void short_body(const SweepArgs &a) {
     WorkItem cur{}, nxt{};
     EllEntries<R> E;
     if (have) cur = a.items[w];
-    ell_entries<R>(a, have && tid < cur.nrows, cur.row0 + tid, E);
+    ell_entries<R>(a, have && tid < cur.nrows, cur, tid, E);
     if (have_next) nxt = a.items[w + w_step];
     StepView sv{s_eff, s_bs, a.P};
     sweep_prologue<STEP>(a, s_eff, s_bs, s_red);
@@ -685,7 +695,7 @@ __device__ __forceinline__ void short_body(const SweepArgs &a) {
             if (KIND == ECC_KIND_JACOBI) bi = a.b[i];
         }
         EllEntries<R> En;
-        ell_entries<R>(a, have_next && tid < nxt.nrows, nxt.row0 + tid, En);
+        ell_entries<R>(a, have_next && tid < nxt.nrows, nxt, tid, En);
         if (live) {
             double s = 0.0, dg = 0.0;
 #pragma unroll
@@ -709,16 +719,150 @@ __device__ __forceinline__ void short_body(const SweepArgs &a) {
     if (tid == 0) a.partials[blockIdx.x] = total;
 }
 
-// Column-major copy of a matrix whose rows hold at most R entries.
-__global__ void k_build_ell(int32_t n, int32_t R, const int32_t *__restrict__ row_ptr,
-                            const int32_t *__restrict__ col, const double *__restrict__ val,
-                            int32_t *__restrict__ ell_col, double *__restrict__ ell_val) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t k0 = row_ptr[i], len = row_ptr[i + 1] - k0;
+// Item queue of a short-layout sweep.  With a static walk (item_walk) the
+// workgroups of an XCD drift apart: on MI355X, in a 400^3 Jacobi sweep, the
+// items an XCD's 160 workgroups start within one round span about 4,400
+// items instead of 160, so the rows that neighbour each other one plane
+// apart no longer meet in L2.  Here the items are split into kQueueRanges
+// contiguous ranges (range r for the workgroups of XCD r), and a workgroup
+// claims the next item of its own XCD's range with an agent-scope atomic
+// ticket; once that range is exhausted it moves on to the following ranges.
+// Every item is claimed exactly once whatever the mapping of workgroups to
+// XCDs, and the XCD's active items stay those in flight.  The last workgroup
+// to finish zeroes the counters for the next launch.  Each item writes its
+// own partial norm (its four waves' sums added in wave order), so the norm
+// does not depend on which workgroup took which item.
+// Claims item tickets for thread 0: the next item of range r, moving on
+// while ranges are exhausted; -1 once every range is.
+__device__ __forceinline__ int32_t queue_take(unsigned *q, int64_t n_items, int &r, int &left) {
+    while (left > 0) {
+        const int64_t b = n_items * r / kQueueRanges, e = n_items * (r + 1) / kQueueRanges;
+        const unsigned t = atomicAdd(&q[r * kQueueStride], 1u);
+        if ((int64_t)t < e - b) return (int32_t)(b + t);
+        r = (r + 1) % kQueueRanges;
+        --left;
+    }
+    return -1;
+}
+
+// The hardware id of the XCD running the calling wave (HW_REG_XCC_ID, bits
+// 3:0): a read of a hardware register.
+__device__ __forceinline__ int xcc_id() {
+    return (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) & 15);
+}
+
+// Short-row layout with queue-claimed items.  The same two-deep pipeline as
+// short_body: tickets are taken three items ahead by thread 0 and handed to
+// the workgroup through LDS at the one barrier per item, where the item's
+// partial norm is also assembled.
+template <int KIND, bool STEP, int R>
+__device__ __forceinline__ void short_body_queue(const SweepArgs &a) {
+    __shared__ double s_red[kSweepThreads / 64];
+    __shared__ double s_ws[2][kSweepThreads / 64];
+    __shared__ int32_t s_tk[5];  // [0..1] tickets handed on per item, [2..4] the first three
+    __shared__ uint8_t s_eff[STEP ? kFusedMaxP : 1];
+    __shared__ int32_t s_bs[STEP ? kFusedMaxP + 1 : 1];
+    if (a.done && *a.done) return;
+    const int tid = threadIdx.x;
+    int r = 0, left = kQueueRanges;
+    if (tid == 0) {
+        r = xcc_id() % kQueueRanges;
+        for (int k = 0; k < 3; ++k) s_tk[2 + k] = queue_take(a.queue, a.n_items, r, left);
+    }
+    StepView sv{s_eff, s_bs, a.P};
+    sweep_prologue<STEP>(a, s_eff, s_bs, s_red);
+    __syncthreads();
+    int32_t w = s_tk[2], wn = s_tk[3], wnn = s_tk[4];
+    WorkItem cur{}, nxt{};
+    EllEntries<R> E;
+    if (w >= 0) cur = a.items[w];
+    ell_entries<R>(a, w >= 0 && tid < cur.nrows, cur, tid, E);
+    if (wn >= 0) nxt = a.items[wn];
+    RankCache rc;
+    int kk = 0;
+    while (w >= 0) {
+        int32_t tk = -1;
+        if (tid == 0 && wnn >= 0) tk = queue_take(a.queue, a.n_items, r, left);
+        WorkItem nn{};
+        if (wnn >= 0) nn = a.items[wnn];
+        const bool live = tid < cur.nrows;
+        const int32_t i = cur.row0 + tid;
+        double y[R];
+#pragma unroll
+        for (int j = 0; j < R; ++j)
+            y[j] = (E.c[j] >= 0) ? view_load<STEP>(E.c[j], cur.lo, cur.hi, a.x_own, a.x_hat, sv, rc)
+                                 : 0.0;
+        double xo = 0.0, bi = 0.0;
+        if (live) {
+            xo = a.x_own[i];
+            if (KIND == ECC_KIND_JACOBI) bi = a.b[i];
+        }
+        EllEntries<R> En;
+        ell_entries<R>(a, wn >= 0 && tid < nxt.nrows, nxt, tid, En);
+        double c = 0.0;
+        if (live) {
+            double s = 0.0, dg = 0.0;
+#pragma unroll
+            for (int j = 0; j < R; ++j) {
+                if (E.c[j] >= 0) {
+                    if (KIND == ECC_KIND_JACOBI && E.c[j] == i) dg = E.v[j];
+                    else s = s + E.v[j] * y[j];
+                }
+            }
+            if (STEP && s_eff[cur.rank] != 0) a.x_hat[i] = xo;
+            c = row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+        }
+        c = group_sum<64>(c);
+        const int slot = kk & 1;
+        if ((tid & 63) == 0) s_ws[slot][tid >> 6] = c;
+        if (tid == 0) s_tk[slot] = tk;
+        __syncthreads();
+        if (tid == 0) {
+            double t = s_ws[slot][0];
+#pragma unroll
+            for (int q = 1; q < kSweepThreads / 64; ++q) t += s_ws[slot][q];
+            a.partials[w] = t;
+        }
+        const int32_t w3 = s_tk[slot];
+        ++kk;
+        w = wn;
+        wn = wnn;
+        wnn = w3;
+        cur = nxt;
+        nxt = nn;
+        E = En;
+    }
+    // the last workgroup out zeroes the counters for the next launch
+    if (tid == 0) {
+        unsigned *fin = a.queue + kQueueRanges * kQueueStride;
+        if (atomicAdd(fin, 1u) == gridDim.x - 1) {
+            for (int q = 0; q < kQueueRanges; ++q) atomicExch(a.queue + q * kQueueStride, 0u);
+            atomicExch(fin, 0u);
+        }
+    }
+}
+
+// Item-major copy of a matrix whose rows hold at most R entries (layout as
+// in ell_entries), one workgroup of kSweepThreads per item: lane l copies
+// row row0 + l; lanes of the padding write column -1.
+__global__ void k_build_ell(int64_t n_items, int32_t R, const WorkItem *__restrict__ items,
+                            const int32_t *__restrict__ row_ptr, const int32_t *__restrict__ col,
+                            const double *__restrict__ val, int32_t *__restrict__ ell_col,
+                            double *__restrict__ ell_val) {
+    for (int64_t w = blockIdx.x; w < n_items; w += gridDim.x) {
+        const WorkItem it = items[w];
+        const int32_t pad = sell_pad(it.nrows);
+        const int32_t l = threadIdx.x;
+        if (l >= pad) continue;
+        int32_t k0 = 0, len = 0;
+        if (l < it.nrows) {
+            k0 = row_ptr[it.row0 + l];
+            len = row_ptr[it.row0 + l + 1] - k0;
+        }
+        const int64_t base = (int64_t)it.k0 * R + l;
         for (int32_t j = 0; j < R; ++j) {
-            ell_col[(int64_t)j * n + i] = j < len ? col[k0 + j] : -1;
-            ell_val[(int64_t)j * n + i] = j < len ? val[k0 + j] : 0.0;
+            ell_col[base + (int64_t)j * pad] = j < len ? col[k0 + j] : -1;
+            ell_val[base + (int64_t)j * pad] = j < len ? val[k0 + j] : 0.0;
         }
     }
 }
@@ -732,10 +876,11 @@ template <int R>
 constexpr int short_waves() {
     return R <= 4 ? 8 : (R == 5 ? 7 : 5);
 }
-template <int KIND, bool STEP, int R>
+template <int KIND, bool STEP, int R, bool QUEUE>
 __global__ __launch_bounds__(kSweepThreads) __attribute__((amdgpu_waves_per_eu(short_waves<R>())))
 void k_sweep_short(SweepArgs a) {
-    short_body<KIND, STEP, R>(a);
+    if constexpr (QUEUE) short_body_queue<KIND, STEP, R>(a);
+    else short_body<KIND, STEP, R>(a);
 }
 
 // Second pass of a sweep, one workgroup of kNormThreads.  (1) Rows split into
@@ -842,6 +987,30 @@ __global__ void k_check(int32_t n_rows, int32_t n_cols, const int32_t *__restric
     if (band) atomicMax(&bad[2], band);
 }
 
+// How the columns of a matrix of bandwidth B sit around each row: the
+// distance of an entry from the row is m = min(|d|, ||d| - B|), d = col - row
+// (its offset from the row itself or from the rows one plane of B rows
+// away).  prof[0] = entries with m > lim, prof[1] = the largest m <= lim.
+__global__ void k_band_profile(int32_t n_rows, int64_t B, int64_t lim,
+                               const int32_t *__restrict__ row_ptr,
+                               const int32_t *__restrict__ col,
+                               unsigned long long *__restrict__ prof) {
+    unsigned long long far = 0, near = 0;
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n_rows;
+         i += gridDim.x * blockDim.x) {
+        for (int32_t k = row_ptr[i]; k < row_ptr[i + 1]; ++k) {
+            const int64_t d = (int64_t)col[k] - i;
+            const int64_t a = d < 0 ? -d : d;
+            const int64_t e = a > B ? a - B : B - a;
+            const int64_t m = a < e ? a : e;
+            if (m > lim) ++far;
+            else near = max(near, (unsigned long long)m);
+        }
+    }
+    if (far) atomicAdd(&prof[0], far);
+    if (near) atomicMax(&prof[1], near);
+}
+
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
@@ -922,6 +1091,51 @@ static void build_items(const std::vector<int32_t> &rp, const std::vector<int64_
     items.insert(items.end(), stream.begin(), stream.end());
 }
 
+// Short-row layout: runs of up to kSweepThreads rows of one rank.  With
+// plane tiling (plane B > 0, tile W > 0) the runs are taken segment by
+// segment, tile by tile: for tau = 0, W, 2W, ... below B and every plane z,
+// the rows [z B + tau, z B + min(tau + W, B)) below n.  Each item's k0 is
+// the row offset of its entries in the item-major copy (a multiple of 32);
+// returns the copy's padded row count.
+static int64_t build_short_items(int64_t n, const std::vector<int64_t> &counts, int64_t plane,
+                                 int64_t tile, std::vector<WorkItem> &items) {
+    std::vector<int64_t> bs(counts.size() + 1, 0);
+    for (size_t p = 0; p < counts.size(); ++p) bs[p + 1] = bs[p] + counts[p];
+    items.clear();
+    int64_t base = 0;
+    auto segment = [&](int64_t a, int64_t b) {
+        // the rank holding row a: the last p with bs[p] <= a (after empty ranks)
+        int64_t p = (std::upper_bound(bs.begin(), bs.end(), a) - bs.begin()) - 1;
+        while (a < b) {
+            while (bs[p + 1] <= a) ++p;
+            const int64_t e = std::min({b, bs[p + 1], a + (int64_t)kSweepThreads});
+            WorkItem w{};
+            w.row0 = (int32_t)a;
+            w.nrows = (int32_t)(e - a);
+            w.k0 = (int32_t)std::min<int64_t>(base, INT32_MAX);
+            w.lo = (int32_t)bs[p];
+            w.hi = (int32_t)bs[p + 1];
+            w.kind = kItemStream;
+            w.rank = (int32_t)p;
+            items.push_back(w);
+            base += (e - a + 31) & ~int64_t(31);
+            a = e;
+        }
+    };
+    if (plane > 0 && tile > 0) {
+        const int64_t planes = (n + plane - 1) / plane;
+        for (int64_t tau = 0; tau < plane; tau += tile)
+            for (int64_t z = 0; z < planes; ++z) {
+                const int64_t a = z * plane + tau;
+                const int64_t b = std::min(n, z * plane + std::min(tau + tile, plane));
+                if (a < b) segment(a, b);
+            }
+    } else if (n > 0) {
+        segment(0, n);
+    }
+    return base;
+}
+
 // Sorted layout: the rows of every rank ordered by decreasing length, ties in
 // row order.  Returns the row at each position and the row pointers of the
 // sorted copy.
@@ -943,13 +1157,8 @@ static void sort_rows(const std::vector<int32_t> &rp, const std::vector<int64_t>
 }
 
 // Range layout: the number of column ranges for a vector of n doubles,
-// about kRangeBytes of it per range (ECC_RANGE_BYTES overrides the size).
-static int32_t range_count(int64_t n) {
-    int64_t bytes = kRangeBytes;
-    if (const char *e = std::getenv("ECC_RANGE_BYTES")) {
-        const long long v = std::atoll(e);
-        if (v > 0) bytes = v;
-    }
+// about `bytes` of it per range.
+static int32_t range_count(int64_t n, int64_t bytes) {
     const int64_t nr = (n * 8 + bytes - 1) / bytes;
     return (int32_t)std::min<int64_t>(kMaxRanges, std::max<int64_t>(1, nr));
 }
@@ -1140,9 +1349,9 @@ template <int R>
 static hipError_t short_occupancy_r(int *per_cu, int kind) {
     return kind == ECC_KIND_JACOBI
                ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                     per_cu, k_sweep_short<ECC_KIND_JACOBI, true, R>, kSweepThreads, 0)
+                     per_cu, k_sweep_short<ECC_KIND_JACOBI, true, R, false>, kSweepThreads, 0)
                : hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                     per_cu, k_sweep_short<ECC_KIND_POWER, true, R>, kSweepThreads, 0);
+                     per_cu, k_sweep_short<ECC_KIND_POWER, true, R, false>, kSweepThreads, 0);
 }
 
 // Entries per row of the short-layout kernel that serves rows of at most
@@ -1187,13 +1396,21 @@ static void launch_layout(ecc_matrix_t M, dim3 grid, dim3 block, hipStream_t st,
         if constexpr (!S) hipLaunchKernelGGL((k_sweep<K, S, kLaySorted>), grid, block, 0, st, a);
     } else if (M->layout == kLayRanges) {
         if constexpr (!S) hipLaunchKernelGGL((k_sweep<K, S, kLayRanges>), grid, block, 0, st, a);
+    } else if (M->layout == kLayShort && M->queue) {
+        switch (short_class(M->short_r)) {
+            case 3: hipLaunchKernelGGL((k_sweep_short<K, S, 3, true>), grid, block, 0, st, a); break;
+            case 4: hipLaunchKernelGGL((k_sweep_short<K, S, 4, true>), grid, block, 0, st, a); break;
+            case 5: hipLaunchKernelGGL((k_sweep_short<K, S, 5, true>), grid, block, 0, st, a); break;
+            case 7: hipLaunchKernelGGL((k_sweep_short<K, S, 7, true>), grid, block, 0, st, a); break;
+            default: hipLaunchKernelGGL((k_sweep_short<K, S, 8, true>), grid, block, 0, st, a); break;
+        }
     } else if (M->layout == kLayShort) {
         switch (short_class(M->short_r)) {
-            case 3: hipLaunchKernelGGL((k_sweep_short<K, S, 3>), grid, block, 0, st, a); break;
-            case 4: hipLaunchKernelGGL((k_sweep_short<K, S, 4>), grid, block, 0, st, a); break;
-            case 5: hipLaunchKernelGGL((k_sweep_short<K, S, 5>), grid, block, 0, st, a); break;
-            case 7: hipLaunchKernelGGL((k_sweep_short<K, S, 7>), grid, block, 0, st, a); break;
-            default: hipLaunchKernelGGL((k_sweep_short<K, S, 8>), grid, block, 0, st, a); break;
+            case 3: hipLaunchKernelGGL((k_sweep_short<K, S, 3, false>), grid, block, 0, st, a); break;
+            case 4: hipLaunchKernelGGL((k_sweep_short<K, S, 4, false>), grid, block, 0, st, a); break;
+            case 5: hipLaunchKernelGGL((k_sweep_short<K, S, 5, false>), grid, block, 0, st, a); break;
+            case 7: hipLaunchKernelGGL((k_sweep_short<K, S, 7, false>), grid, block, 0, st, a); break;
+            default: hipLaunchKernelGGL((k_sweep_short<K, S, 8, false>), grid, block, 0, st, a); break;
         }
     } else {
         hipLaunchKernelGGL((k_sweep<K, S, kLayStream>), grid, block, 0, st, a);
@@ -1226,7 +1443,11 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     a.ell_val = M->d_ell_val;
     a.ell_n = M->A.n_rows;
     a.interleave = M->irregular ? 1 : 0;
-    a.reserve0 = M->grid >= kReserveMinGrid ? 1 : 0;
+    // a queue-scheduled sweep needs no reserved workgroup: workgroup 0 takes
+    // items once its reduction of the previous partials is done
+    a.reserve0 = (M->grid >= kReserveMinGrid && !M->queue) ? 1 : 0;
+    a.n_part = M->n_part;
+    a.queue = M->queue ? M->d_queue : nullptr;
     a.zero_extra = M->n_fixups == 0 ? 1 : 0;
     a.prev_partials = L.prev_partials;
     a.prev_rho = L.prev_rho;
@@ -1301,7 +1522,7 @@ ecc_status_t launch_pass2(ecc_matrix_t M, const Pass2Launch &L) {
     ecc_plan_t pl = M->plan;
     Pass2Args a{};
     a.partials = L.partials;
-    a.G = M->grid;
+    a.G = (int32_t)(M->n_part - 1);
     a.fixups = M->d_fixups;
     a.n_fixups = (int32_t)M->n_fixups;
     a.pieces = M->d_pieces;
@@ -1334,13 +1555,19 @@ using namespace ecc;
 extern "C" {
 
 static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
-                               ecc_matrix_t *out) {
+                                           const ecc_matrix_opts_t *opts_in, ecc_matrix_t *out) {
     clear_error();
     ECC_ARG(out != nullptr, "out is NULL");
     *out = nullptr;
     ecc_status_t st = check_plan(plan);
     if (st != ECC_OK) return st;
     ECC_ARG(A != nullptr, "A is NULL");
+    const ecc_matrix_opts_t opts = opts_in ? *opts_in : ecc_matrix_opts_t{0, 0, 0};
+    ECC_ARG(opts.range_bytes >= 0, "range_bytes is negative");
+    ECC_ARG(opts.schedule == ECC_SCHEDULE_AUTO || opts.schedule == ECC_SCHEDULE_STATIC ||
+                opts.schedule == ECC_SCHEDULE_QUEUE,
+            "unknown schedule %d", opts.schedule);
+    const int64_t range_bytes = opts.range_bytes > 0 ? opts.range_bytes : kRangeBytes;
     ECC_ARG(kind == ECC_KIND_JACOBI || kind == ECC_KIND_POWER, "unknown kind %d", kind);
     ECC_ARG(A->n_rows >= 0 && A->n_cols >= 0 && A->nnz >= 0, "negative matrix size");
     if (A->nnz >= (int64_t(1) << 31) || A->n_rows >= (int64_t(1) << 31) ||
@@ -1417,11 +1644,12 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
     // Very uneven rows over a vector of more than one range: the range layout
     // (each range of the vector, about kRangeBytes, is gathered by all
     // workgroups at once and stays in the XCDs' L2).
-    const int32_t n_ranges = irregular ? range_count(n) : 1;
+    const int32_t n_ranges = irregular ? range_count(n, range_bytes) : 1;
     const int layout = irregular ? (n_ranges >= 2 ? kLayRanges : kLaySorted)
                                  : (short_rows ? kLayShort : kLayStream);
     std::vector<int32_t> order, srp;
     RangeBuild RB;
+    int64_t tile_plane = 0, tile_rows = 0, short_rows_total = 0;
     if (layout == kLayRanges) {
         std::vector<int32_t> hcol(A->nnz);
         std::vector<double> hval(A->nnz);
@@ -1432,6 +1660,54 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
     } else if (irregular) {
         sort_rows(rp, plan->counts, order, srp);
         build_items(srp, plan->counts, &order, items, fixups, n_pieces);
+    } else if (layout == kLayShort) {
+        // Plane tiling for a matrix whose columns sit near the row or near
+        // the rows one bandwidth B away (a 3-D grid stencil, B = one plane),
+        // when B rows stream more than an XCD's L2 holds: in row order the
+        // neighbours one plane ahead are read B rows before their own rows
+        // are swept, and have left L2 by then.
+        // A caller's tile size applies whenever the columns qualify.
+        const int64_t row_bytes = 12 * (int64_t)short_class(std::max(1, max_row)) + 24;
+        const bool big = bandwidth >= 1024 && bandwidth * row_bytes > kTileMinBytes;
+        if (opts.tile_rows >= 0 && bandwidth >= 16 && n >= 3 * bandwidth &&
+            (big || opts.tile_rows > 0)) {
+            unsigned long long h_prof[2] = {0, 0};
+            unsigned long long *d_prof = nullptr;
+            ECC_HIP(hipMalloc((void **)&d_prof, sizeof(h_prof)));
+            hipError_t e = hipMemcpy(d_prof, h_prof, sizeof(h_prof), hipMemcpyHostToDevice);
+            if (e == hipSuccess) {
+                const int blocks = (int)std::min<int64_t>(4096, (n + 255) / 256);
+                hipLaunchKernelGGL(k_band_profile, dim3(blocks), dim3(256), 0, plan->stream,
+                                   (int32_t)n, bandwidth, bandwidth / 16, A->d_row_ptr, A->d_col,
+                                   d_prof);
+                e = hipGetLastError();
+                if (e == hipSuccess) e = hipStreamSynchronize(plan->stream);
+                if (e == hipSuccess)
+                    e = hipMemcpy(h_prof, d_prof, sizeof(h_prof), hipMemcpyDeviceToHost);
+            }
+            (void)hipFree(d_prof);
+            if (e != hipSuccess) {
+                set_error("band profile failed: %s", hipGetErrorString(e));
+                return ECC_ERR_DEVICE;
+            }
+            if (h_prof[0] == 0) {
+                // tiles wide against the in-plane offsets (the edge rows of a
+                // tile re-read their neighbours in the next tile)
+                int64_t w = opts.tile_rows > 0 ? opts.tile_rows
+                                               : std::max<int64_t>(kTileMinRows,
+                                                                   kTileNearFactor * (int64_t)h_prof[1]);
+                w = (w + kSweepThreads - 1) / kSweepThreads * kSweepThreads;
+                if (w < bandwidth) {
+                    tile_plane = bandwidth;
+                    tile_rows = w;
+                }
+            }
+        }
+        short_rows_total = build_short_items(n, plan->counts, tile_plane, tile_rows, items);
+        if (short_rows_total >= (int64_t(1) << 31)) {
+            set_error("the short-row copy needs more than 2^31 padded rows");
+            return ECC_ERR_RANGE;
+        }
     } else {
         build_items(rp, plan->counts, nullptr, items, fixups, n_pieces);
     }
@@ -1455,7 +1731,17 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
     M->layout = layout;
     M->short_r = std::max(1, max_row);
     M->bandwidth = bandwidth;
+    M->tile_plane = tile_plane;
+    M->tile_rows = tile_rows;
     M->grid = sweep_grid(M->n_items, kind, layout, M->short_r);
+    // Queue-claimed items for a short-layout matrix that gives each workgroup
+    // many items (the static walk's drift grows with them): measured on
+    // MI355X, Jacobi on the 400^3 7-point stencil, 1.55 against 1.66 ms per
+    // sweep.
+    M->queue = layout == kLayShort && (opts.schedule == ECC_SCHEDULE_QUEUE ||
+                                       (opts.schedule == ECC_SCHEDULE_AUTO &&
+                                        M->n_items >= kQueueMinItems * (int64_t)M->grid));
+    M->n_part = M->queue ? M->n_items + 1 : (int64_t)M->grid + 1;
     auto fail = [&](const char *what) {
         set_error("%s", what);
         ecc_matrix_destroy(M);
@@ -1518,20 +1804,29 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
             return fail("hipMalloc of the range sums failed");
     }
     if (layout == kLayShort && n > 0) {
-        const int32_t R = short_class(M->short_r);
-        if (hipMalloc((void **)&M->d_ell_col, sizeof(int32_t) * R * n) != hipSuccess ||
-            hipMalloc((void **)&M->d_ell_val, sizeof(double) * R * n) != hipSuccess)
-            return fail("hipMalloc of the column-major entries failed");
-        const int blocks = (int)std::min<int64_t>(65536, (n + 255) / 256);
-        hipLaunchKernelGGL(k_build_ell, dim3(blocks), dim3(256), 0, plan->stream, (int32_t)n, R,
-                           A->d_row_ptr, A->d_col, A->d_val, M->d_ell_col, M->d_ell_val);
+        const int64_t R = short_class(M->short_r);
+        if (hipMalloc((void **)&M->d_ell_col, sizeof(int32_t) * R * short_rows_total) !=
+                hipSuccess ||
+            hipMalloc((void **)&M->d_ell_val, sizeof(double) * R * short_rows_total) != hipSuccess)
+            return fail("hipMalloc of the item-major entries failed");
+        const int blocks = (int)std::min<int64_t>(65536, M->n_items);
+        hipLaunchKernelGGL(k_build_ell, dim3(blocks), dim3(kSweepThreads), 0, plan->stream,
+                           M->n_items, (int32_t)R, M->d_items, A->d_row_ptr, A->d_col, A->d_val,
+                           M->d_ell_col, M->d_ell_val);
         if (hipGetLastError() != hipSuccess || hipStreamSynchronize(plan->stream) != hipSuccess)
-            return fail("building the column-major entries failed");
+            return fail("building the item-major entries failed");
     }
     // two buffers of G + 1 partials: a loop iteration writes one while the
     // next launch reduces the other
-    if (hipMalloc((void **)&M->d_partials, sizeof(double) * 2 * (M->grid + 1)) != hipSuccess)
+    if (hipMalloc((void **)&M->d_partials, sizeof(double) * 2 * M->n_part) != hipSuccess)
         return fail("hipMalloc of partials failed");
+    if (M->queue) {
+        const size_t qb = sizeof(unsigned) * (kQueueRanges + 1) * kQueueStride;
+        if (hipMalloc((void **)&M->d_queue, qb) != hipSuccess ||
+            hipMemsetAsync(M->d_queue, 0, qb, plan->stream) != hipSuccess ||
+            hipStreamSynchronize(plan->stream) != hipSuccess)
+            return fail("allocating the item queue failed");
+    }
     *out = M;
     return ECC_OK;
 }
@@ -1540,8 +1835,13 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
 // out: the C ABI reports ECC_ERR_ALLOC instead of letting it escape.
 ecc_status_t ecc_matrix_create(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
                                ecc_matrix_t *out) {
+    return ecc_matrix_create_ex(plan, A, kind, nullptr, out);
+}
+
+ecc_status_t ecc_matrix_create_ex(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
+                                  const ecc_matrix_opts_t *opts, ecc_matrix_t *out) {
     try {
-        return ecc_matrix_create_impl(plan, A, kind, out);
+        return ecc_matrix_create_impl(plan, A, kind, opts, out);
     } catch (const std::bad_alloc &) {
         set_error("host allocation failed");
         return ECC_ERR_ALLOC;
@@ -1566,6 +1866,7 @@ ecc_status_t ecc_matrix_destroy(ecc_matrix_t M) {
     (void)hipFree(M->d_rfix);
     (void)hipFree(M->d_ell_col);
     (void)hipFree(M->d_ell_val);
+    (void)hipFree(M->d_queue);
     delete M;
     return ECC_OK;
 }
@@ -1584,9 +1885,26 @@ ecc_status_t ecc_matrix_layout(ecc_matrix_t M, int32_t *layout, int32_t *row_slo
     return ECC_OK;
 }
 
+ecc_status_t ecc_matrix_tiling(ecc_matrix_t M, int64_t *plane_rows, int64_t *tile_rows) {
+    clear_error();
+    ECC_ARG(M != nullptr, "matrix is NULL");
+    ECC_ARG(plane_rows != nullptr && tile_rows != nullptr, "NULL output");
+    *plane_rows = M->tile_plane;
+    *tile_rows = M->tile_rows;
+    return ECC_OK;
+}
+
+ecc_status_t ecc_matrix_schedule(ecc_matrix_t M, int32_t *schedule) {
+    clear_error();
+    ECC_ARG(M != nullptr, "matrix is NULL");
+    ECC_ARG(schedule != nullptr, "NULL output");
+    *schedule = M->queue ? ECC_SCHEDULE_QUEUE : ECC_SCHEDULE_STATIC;
+    return ECC_OK;
+}
+
 int64_t ecc_partials_size(ecc_matrix_t M) {
     if (!M) return 0;
-    return (int64_t)M->grid + 1;
+    return M->n_part;
 }
 
 static ecc_status_t iterate(ecc_plan_t plan, ecc_matrix_t M, int32_t kind, const double *d_b,

@@ -34,8 +34,11 @@ def test_pagerank_rmat_full():
 
 def test_jacobi_3d_full():
     """3-D Jacobi, n = 64,000,000, 447,040,000 nonzeros, 512 ranks, S = 5:
-    iterates bitwise equal to the oracle."""
-    _solve_and_compare(W.jacobi_3d(), bitwise=True, threads=THREADS)
+    iterates bitwise equal to the oracle.  The set-up sweeps it in plane
+    tiles (planes of 400^2 rows, tiles of 64 x 400 rows)."""
+    from paper_2203_17063_amd import capi as E
+    _solve_and_compare(W.jacobi_3d(), bitwise=True, threads=THREADS, tiling=(160000, 25600),
+                       expect_schedule=E.ECC_SCHEDULE_QUEUE)
 
 
 def test_allgatherv_full():

@@ -6,8 +6,6 @@ oracle, norms within 1e-12 relative plus 32 units of rounding of the
 problem's scale; stencil sweeps sum every row on one lane in CSR order, so
 their iterates are also checked bit for bit.
 """
-import contextlib
-import os
 
 import numpy as np
 import pytest
@@ -258,12 +256,25 @@ def _floor(prob, x):
     return float(np.sum(prob.alpha * wx + prob.beta + np.abs(x)))
 
 
-def _solve_and_compare(prob, bitwise, threads=8, layout=None):
-    R = _runner()
+def _iterative(prob, range_bytes=0, tile_rows=0, schedule=0):
+    """The problem resident on the GPU; range_bytes / tile_rows / schedule are
+    the matrix set-up options (0: the library's choice)."""
+    return _runner().Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts,
+                               prob.S, prob.mask, prob.kind, b=prob.b, alpha=prob.alpha,
+                               beta=prob.beta, x0=prob.x0, range_bytes=range_bytes,
+                               tile_rows=tile_rows, schedule=schedule)
+
+
+def _solve_and_compare(prob, bitwise, threads=8, layout=None, range_bytes=0, tile_rows=0,
+                       tiling=None, schedule=0, expect_schedule=None, solves=1):
     announce("solve", prob.name, prob.n, prob.A.nnz, prob.P, prob.T)
-    run = R.Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts, prob.S,
-                      prob.mask, prob.kind, b=prob.b, alpha=prob.alpha, beta=prob.beta,
-                      x0=prob.x0)
+    run = _iterative(prob, range_bytes, tile_rows, schedule)
+    if tiling is not None:  # (plane rows, tile rows) the set-up must choose
+        assert _capi().ecc_matrix_tiling(run.mat) == tiling
+    if expect_schedule is not None:
+        assert _capi().ecc_matrix_schedule(run.mat) == expect_schedule
+    for _ in range(solves - 1):  # earlier solves of the same handle change nothing
+        run.solve(tol=prob.tol)
     if layout is not None:  # the layout by name: "SHORT", "STREAM" or "SORTED"
         E = _capi()
         assert E.ecc_matrix_layout(run.mat)[0] == getattr(E, "ECC_LAYOUT_" + layout)
@@ -515,20 +526,6 @@ def _powerlaw_problem(kind, n, counts, seed, T=25, S=2):
                        np.full(n, 1.0 / n), alpha=0.85, beta=0.15 / n, norm=1)
 
 
-@contextlib.contextmanager
-def _range_bytes(v):
-    """Column ranges of v bytes of the vector for matrices created inside."""
-    old = os.environ.get("ECC_RANGE_BYTES")
-    os.environ["ECC_RANGE_BYTES"] = str(v)
-    try:
-        yield
-    finally:
-        if old is None:
-            del os.environ["ECC_RANGE_BYTES"]
-        else:
-            os.environ["ECC_RANGE_BYTES"] = old
-
-
 @pytest.mark.parametrize("kind", ["jacobi", "power"])
 @pytest.mark.parametrize("counts", [[20000], [0, 3000, 0, 9000, 1000, 7000], 9])
 @pytest.mark.parametrize("range_bytes", [16384, 1])
@@ -538,21 +535,19 @@ def test_solve_range_layout(kind, counts, range_bytes):
     sums added in range order by a second kernel, split sub-rows recombined
     first; Jacobi takes the diagonal kept at set-up."""
     prob = _powerlaw_problem(kind, 20000, counts, seed=31 + len(str(counts)))
-    with _range_bytes(range_bytes):
-        _solve_and_compare(prob, bitwise=False, layout="RANGES")
+    _solve_and_compare(prob, bitwise=False, layout="RANGES", range_bytes=range_bytes)
 
 
 @pytest.mark.parametrize("scale", [12, 15, 17])
 def test_solve_pagerank_rmat_ranges(scale):
     """R-MAT PageRank in the range layout (scale 15 has sub-rows summed by a
     whole workgroup, scale 17 split sub-rows)."""
-    with _range_bytes(4096):
-        _solve_and_compare(W.pagerank_rmat(scale=scale, T=60), bitwise=False, layout="RANGES")
+    _solve_and_compare(W.pagerank_rmat(scale=scale, T=60), bitwise=False, layout="RANGES",
+                       range_bytes=4096)
 
 
 def test_solve_arrow_ranges():
-    with _range_bytes(8192):
-        _solve_and_compare(_arrow_problem(), bitwise=False, layout="RANGES")
+    _solve_and_compare(_arrow_problem(), bitwise=False, layout="RANGES", range_bytes=8192)
 
 
 @pytest.mark.parametrize("kind", ["jacobi", "power"])
@@ -580,19 +575,90 @@ def test_step_api_matches_solve():
                              _arrow_problem(T=12)))
 
 
+@pytest.mark.parametrize("N,P,tile", [(24, 7, 256), (24, 1, 512), (30, 5, 768), (17, 33, 256)])
+def test_solve_jacobi_3d_plane_tiles(N, P, tile):
+    """3-D stencils swept in plane tiles (items ordered tile by tile, plane by
+    plane; the entries copied in that order): iterates bitwise equal to the
+    oracle.  A plane of N^2 rows cut into tiles of `tile` rows, with a ragged
+    last tile (24^2 = 576 = 2 x 256 + 64; 30^2 = 900 = 768 + 132; 17^2 = 289),
+    ranks cut across tiles
+    and planes, and one rank."""
+    prob = W.jacobi_3d(N=N, T=30, P=P)
+    run = _iterative(prob, tile_rows=tile)
+    E = _capi()
+    assert E.ecc_matrix_tiling(run.mat) == (N * N, tile)
+    run.close()
+    _solve_and_compare(prob, bitwise=True, layout="SHORT", tile_rows=tile)
+
+
+def test_plane_tiles_not_taken():
+    """Row order where tiling does not apply: no option (the plane is small),
+    a negative tile size, tiles as wide as the plane (3-D and 2-D stencils),
+    and a banded matrix whose columns spread over the whole band."""
+    E = _capi()
+    for prob, tile in [(W.jacobi_3d(N=16, T=2, P=3), 0), (W.jacobi_3d(N=16, T=2, P=3), -1),
+                       (W.jacobi_3d(N=16, T=2, P=3), 256), (W.jacobi_2d(N=64, T=2), 256),
+                       (_banded_problem("jacobi", 6000, 4, 4, T=2), 256)]:
+        run = _iterative(prob, tile_rows=tile)
+        assert E.ecc_matrix_tiling(run.mat) == (0, 0), (prob.name, tile)
+        run.close()
+
+
+def test_step_api_matches_solve_plane_tiles():
+    _step_api_matches_solve((W.jacobi_3d(N=20, T=15, P=6),), tile_rows=256)
+
+
+def _queue_cases():
+    return [("jacobi-1d", lambda: W.jacobi_1d(), 0),
+            ("jacobi-2d-48", lambda: W.jacobi_2d(N=48, T=40), 0),
+            ("jacobi-3d-24-tiled", lambda: W.jacobi_3d(N=24, T=30, P=7), 256),
+            ("jacobi-3d-20", lambda: W.jacobi_3d(N=20, T=30, P=40), 0),
+            ("banded-power-0-3", lambda: _banded_problem("power", 3000, 0, 3), 0),
+            ("banded-jacobi-8", lambda: _banded_problem("jacobi", 3000, 8, 8), 0)]
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_solve_queue_schedule(case):
+    """Items claimed from the run-time queue (forced on small problems): every
+    item swept exactly once, iterates bitwise equal to the oracle, the
+    per-item norm partials within tolerance; three solves of one handle (the
+    ticket counters start from zero at every launch)."""
+    name, make, tile = _queue_cases()[case]
+    E = _capi()
+    _solve_and_compare(make(), bitwise=True, layout="SHORT", tile_rows=tile,
+                       schedule=E.ECC_SCHEDULE_QUEUE, expect_schedule=E.ECC_SCHEDULE_QUEUE,
+                       solves=3)
+
+
+def test_step_api_matches_solve_queue():
+    E = _capi()
+    _step_api_matches_solve((W.jacobi_2d(N=40, T=25), W.jacobi_3d(N=20, T=15, P=6)),
+                            tile_rows=256, schedule=E.ECC_SCHEDULE_QUEUE)
+
+
+def test_schedule_choice():
+    """Static walk for few items per workgroup, unless forced."""
+    E = _capi()
+    prob = W.jacobi_2d(N=64, T=2)
+    for sch, want in [(0, E.ECC_SCHEDULE_STATIC), (E.ECC_SCHEDULE_STATIC, E.ECC_SCHEDULE_STATIC),
+                      (E.ECC_SCHEDULE_QUEUE, E.ECC_SCHEDULE_QUEUE)]:
+        run = _iterative(prob, schedule=sch)
+        assert E.ecc_matrix_schedule(run.mat) == want
+        run.close()
+    with pytest.raises(E.EccError):
+        _iterative(prob, schedule=7)
+
+
 def test_step_api_matches_solve_ranges():
     """The same for the range layout (sub-row sums, then rows)."""
-    with _range_bytes(2048):
-        _step_api_matches_solve((W.pagerank_rmat(scale=11, T=25), _arrow_problem(T=12)))
+    _step_api_matches_solve((W.pagerank_rmat(scale=11, T=25), _arrow_problem(T=12)),
+                            range_bytes=2048)
 
 
-def _step_api_matches_solve(problems):
-    R = _runner()
+def _step_api_matches_solve(problems, range_bytes=0, tile_rows=0, schedule=0):
     for prob in problems:
         announce("step api", prob.name)
-        run = R.Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts, prob.S,
-                          prob.mask, prob.kind, b=prob.b, alpha=prob.alpha, beta=prob.beta,
-                          x0=prob.x0)
+        run = _iterative(prob, range_bytes, tile_rows, schedule)
         run.solve()
         x_solve = run.d_x.cpu().numpy()
         rho_solve = run.d_rho.cpu().numpy()
@@ -622,15 +688,13 @@ def test_layout_choice():
              (W.pagerank_rmat(scale=10, T=2), E.ECC_LAYOUT_SORTED, 0)]
     for prob, layout, slots in cases:
         _check_layout(R, E, prob, layout, slots)
-    with _range_bytes(4096):          # 8 KB of vector: two column ranges
-        _check_layout(R, E, W.pagerank_rmat(scale=10, T=2), E.ECC_LAYOUT_RANGES, 2)
+    # 8 KB of vector per range: two column ranges
+    _check_layout(R, E, W.pagerank_rmat(scale=10, T=2), E.ECC_LAYOUT_RANGES, 2, range_bytes=4096)
 
 
-def _check_layout(R, E, prob, layout, slots):
+def _check_layout(R, E, prob, layout, slots, range_bytes=0):
     announce("layout", prob.name)
-    run = R.Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts, prob.S,
-                      prob.mask, prob.kind, b=prob.b, alpha=prob.alpha, beta=prob.beta,
-                      x0=prob.x0)
+    run = _iterative(prob, range_bytes)
     assert E.ecc_matrix_layout(run.mat) == (layout, slots), prob.name
     run.close()
 
