@@ -1,24 +1,26 @@
 #!/usr/bin/env python3
 """Benchmark of the eventually consistent collective data path on one MI355X.
 
-Default workload: 2-D 5-point Laplacian 1024x1024 (diagonal 8), 16 uneven
-block-row ranks, Bernoulli(0.9) arrivals, maximum staleness 3, 200 Jacobi
-iterations.  One step = one complete solve (plan reset, then 200 x
-[staleness decision + allgatherv assembly -> block-row sweep -> residual
-norm]) on inputs already resident in HBM.
+Default workload: 3-D 7-point Laplacian 400^3 (n = 64,000,000, diagonal 12),
+512 uneven block-row ranks, per-rank arrival probability q_p ~ U[0.6, 0.95],
+maximum staleness 5, 100 Jacobi iterations -- the largest configuration that
+fits one GPU.  One step = one complete solve (plan reset, x0 loaded, then
+100 x [staleness decision + allgatherv assembly -> block-row sweep ->
+residual norm]) on inputs already resident in HBM.
 
 Metric: assembled+iterated GB/s (algorithmic bytes of assembly + sweep + norm,
 each distinct element counted once) and iterations/s, with the dominant
-kernel's achieved bandwidth against the HBM roofline.  Prints one JSON line.
+kernel's achieved bandwidth against the HBM roofline and against the
+measured copy ceiling.  Prints one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--config NAME]
 
-NAME: jacobi-2d (the default above), jacobi-1d (tridiagonal, n = 4096, 4
-ranks, synchronous), pagerank-rmat (R-MAT scale 22, 64 ranks), jacobi-3d (7-point
-400^3, 512 ranks), allgatherv (256 lognormal blocks, 16.5M elements),
-allreduce (partial allreduce of 256 x 4M), hypercube (allreduce_SSP, 32 x
-16 MB), threshold (Broadcast + Reduce, 32 x 8M), mf (matrix factorisation,
-25M ratings, 32 workers).
+NAME: jacobi-3d (the default above), jacobi-1d (tridiagonal, n = 4096, 4
+ranks, synchronous), jacobi-2d (5-point 1024^2, 16 ranks), pagerank-rmat
+(R-MAT scale 22, 64 ranks), allgatherv (256 lognormal blocks, 16.5M
+elements), allreduce (partial allreduce of 256 x 4M), hypercube
+(allreduce_SSP, 32 x 16 MB), threshold (Broadcast + Reduce, 32 x 8M), mf
+(matrix factorisation, 25M ratings, 32 workers).
 """
 from __future__ import annotations
 
@@ -39,13 +41,11 @@ METRIC = "assembled+iterated GB/s and iterations/s at 1 GPU; % of HBM peak"
 PROFILES = os.path.join(ROOT, "profiles")
 
 
-def sweep_bytes(n, nnz, slots=0):
-    """Algorithmic bytes of one sweep: col + val per nonzero, row_ptr, the x view,
-    b (or x_own for the update norm), the written iterate.  With the short-row
-    layout (slots = entries held per row) the entries are read from the
-    column-major copy, padding included, and row_ptr is not read."""
-    if slots:
-        return 12 * slots * n + 24 * n
+def sweep_bytes(n, nnz):
+    """Algorithmic bytes of one sweep: col + val per nonzero, row_ptr, the x
+    view, b (or x_own for the update norm), the written iterate.  This is the
+    model of the method's data, whatever layout the library sweeps (the
+    short-row copy reads no row_ptr but its padding)."""
     return 12 * nnz + 28 * n + 4
 
 
@@ -58,8 +58,10 @@ def kernel_source_digest(names):
 
 
 def read_traffic(kernel_tag, digest):
-    """HBM traffic per launch from the committed rocprofv3 counter summary, or
-    None when absent or taken on other kernel sources."""
+    """Fabric bytes per launch (calibrated FETCH_SIZE + WRITE_SIZE: L2 to
+    Infinity Fabric requests, Infinity Cache hits included) from the
+    committed rocprofv3 counter summary, or None when absent or taken on other
+    kernel sources."""
     path = os.path.join(PROFILES, "%s.counters.txt" % kernel_tag)
     if not os.path.exists(path):
         return None
@@ -71,7 +73,7 @@ def read_traffic(kernel_tag, digest):
     if kv.get("source_digest") != digest:
         return None
     try:
-        return float(kv["hbm_bytes_per_launch"])
+        return float(kv["fabric_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
 
@@ -168,16 +170,31 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
     eff_hist = run.eff_hist.cpu().numpy()[:iters]
     for _ in range(warmup):
         run.solve(tol=prob.tol)
-    # timed region: K solves, bracketed by device synchronisation
+    # timed region: K solves, bracketed by device synchronisation and by two
+    # HIP events on the plan's stream (torch's current stream)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    ev0.record()
     for _ in range(steps):
         it = run.solve(tol=prob.tol)
         assert it == iters
+    ev1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    # the same K solves again with HIP events around every kernel launch on
-    # the plan's stream: per-kernel durations (the events add a little time)
+    region_ms = ev0.elapsed_time(ev1)
+    # the per-step work that is not a sweep: the solve's set-up (plan reset,
+    # x0 copy, loop-control reset and read-back: a solve of 0 iterations) ...
+    ev2, ev3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev2.record()
+    for _ in range(steps):
+        run.solve(T=0)
+    ev3.record()
+    torch.cuda.synchronize()
+    setup_ms = ev2.elapsed_time(ev3) / steps
+    # ... and the separate assembly / norm launches, timed by HIP events
+    # around every launch over a second region of the same K steps (the
+    # events add a little time per launch)
     E.ecc_plan_set_timing(run.plan.handle, True)
     for k in (E.ECC_TIMING_ASSEMBLE, E.ECC_TIMING_SWEEP, E.ECC_TIMING_NORM):
         E.ecc_plan_timing(run.plan.handle, k, reset=True)
@@ -193,25 +210,40 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
     rho = run.d_rho.cpu().numpy()[:iters]
     n_part = int(run.d_partials.numel())
     layout, slots = E.ecc_matrix_layout(run.mat)
+    schedule = E.ecc_matrix_schedule(run.mat)
+    tiling = E.ecc_matrix_tiling(run.mat)
     run.close()
 
     counts = prob.counts
     eff_elems = np.array([int(counts[eff_hist[t] == 1].sum()) for t in range(iters)])
-    # algorithmic bytes of the data path: assembly (read + write of every
-    # arrived element), sweep, norm partials
-    b_assemble = float(np.sum(16 * eff_elems + 14 * prob.P))
-    b_sweep = float(sweep_bytes(prob.n, prob.A.nnz, slots if layout == E.ECC_LAYOUT_SHORT else 0))
-    b_norm = 8.0 * n_part
-    bytes_per_step = b_assemble + iters * (b_sweep + b_norm)
     # one fused launch per iteration: the sweep plus the write of the arrived
-    # blocks into the assembled vector (their read is the sweep's own x read)
+    # blocks into the assembled vector (their read is the sweep's own x read);
+    # otherwise a separate assembly reads and writes every arrived element
     fused = times["SWEEP"][1] > 0 and times["ASSEMBLE"][1] == 0
-    dom = b_sweep + b_norm + (8.0 * float(eff_elems.mean()) + 14 * prob.P if fused else 0.0)
+    per_elem = 8.0 if fused else 16.0
+    b_assemble = per_elem * eff_elems + 14.0 * prob.P
+    b_sweep = float(sweep_bytes(prob.n, prob.A.nnz))
+    b_norm = 16.0 * n_part                 # partials written, then read by the second pass
+    bytes_per_step = float(np.sum(b_assemble)) + iters * (b_sweep + b_norm)
+    dom = b_sweep + b_norm + (float(np.mean(b_assemble)) if fused else 0.0)
+    # the sweep's average duration from the uninstrumented region: its time
+    # minus the set-up and the other launches, per sweep launch
+    other_ms = setup_ms + (times["ASSEMBLE"][0] + times["NORM"][0]) / steps
+    sweeps = times["SWEEP"][1] / steps
+    dom_ms = (region_ms / steps - other_ms) / sweeps
     return {
         "iters": iters, "wall": wall, "wall_events": wall_events, "times": times,
         "bytes_per_step": bytes_per_step, "dominant": "sweep",
         "dominant_bytes": dom, "footprint": footprint, "rho_last": float(rho[-1]),
-        "unit_per_step": iters, "fused": fused,
+        "unit_per_step": iters, "fused": fused, "dom_ms": dom_ms,
+        "dom_timing": "HIP events on the plan's stream around the timed region; the sweep's "
+                      "share is that time minus a 0-iteration solve's (set-up) and the other "
+                      "launches' (events around each), divided by the sweep launches",
+        "dom_events_avg_us": round(times["SWEEP"][0] / max(times["SWEEP"][1], 1) * 1e3, 3),
+        "extra": {"layout": {0: "stream", 1: "sorted", 2: "short", 3: "ranges"}[layout],
+                  "schedule": "queue" if schedule == E.ECC_SCHEDULE_QUEUE else "static",
+                  "plane_tiling": {"plane_rows": tiling[0], "tile_rows": tiling[1]},
+                  "assembly_bytes_per_arrived_element": per_elem},
     }
 
 
@@ -252,11 +284,41 @@ def run_allgatherv_gpu(prob, steps, warmup):
     times = {"ASSEMBLE": E.ecc_plan_timing(plan.handle, E.ECC_TIMING_ASSEMBLE)}
     E.ecc_plan_set_timing(plan.handle, False)
     assert torch.equal(recv, send)
-    plan.close()
     per_rep = 16.0 * float(prob.counts.sum()) + 14 * prob.P
+    # the same repetitions over four send/receive buffer sets used in turn:
+    # a working set of about 1 GB, four times the 256 MB Infinity Cache, so
+    # that every repetition streams from HBM
+    sets = [(send.clone(), torch.empty_like(send)) for _ in range(4)]
+    del recv
+
+    def step_rot():
+        plan.reset()
+        for r in range(prob.reps):
+            sd, rv = sets[r & 3]
+            E.ecc_allgatherv_assemble_packed(plan.handle, sd, rv, d_mask[r].data_ptr())
+
+    step_rot()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(steps):
+        step_rot()
+    ev1.record()
+    torch.cuda.synchronize()
+    rot_ms = ev0.elapsed_time(ev1) / steps
+    for sd, rv in sets:
+        assert torch.equal(rv, sd)
+    plan.close()
+    rot = {"value": round(per_rep * prob.reps / rot_ms / 1e6, 3), "unit": "GB/s",
+           "ms_per_step": round(rot_ms, 4),
+           "avg_rep_us": round(rot_ms / prob.reps * 1e3, 3),
+           "hbm_peak_frac": round(per_rep * prob.reps / rot_ms / 1e6 / HBM_PEAK_GBS, 4),
+           "note": "repetition r reads and writes buffer set r mod 4 (4 x 264 MB); HIP "
+                   "events around the K steps on the plan's stream"}
     return {"iters": prob.reps, "wall": wall, "wall_events": wall_events, "times": times,
             "bytes_per_step": per_rep * prob.reps, "dominant": "assemble",
-            "dominant_bytes": per_rep, "footprint": footprint, "unit_per_step": prob.reps}
+            "dominant_bytes": per_rep, "footprint": footprint, "unit_per_step": prob.reps,
+            "extra": {"rotated_4_buffer_sets": rot}}
 
 
 def run_allreduce_gpu(prob, steps, warmup):
@@ -504,28 +566,54 @@ def run_mf_gpu(prob, steps, warmup):
 # CPU baseline: the oracle as it stands, on a bounded sample
 # ----------------------------------------------------------------------------
 
+def host_cpu():
+    """Cores this process may run on, and the CPU model."""
+    cores = len(os.sched_getaffinity(0))
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return cores, model
+
+
 def cpu_baseline(cfg, prob, res, budget_s=12.0):
     import oracle
     cores = 1
+    n_cores, model = host_cpu()
     if cfg in ("jacobi-1d", "jacobi-2d", "pagerank-rmat", "jacobi-3d"):
-        # whole iterations of the oracle; sample = first k iterations
+        # whole iterations of the oracle (sample = the first k iterations), on
+        # one thread and on every core of this host: its row loops run on
+        # OpenMP threads, one row per thread in the same order, so both give
+        # the same bits
         per_iter_bytes = res["bytes_per_step"] / res["iters"]
-        t0 = time.perf_counter()
-        k = 0
         sample_iters = res["iters"] if cfg in ("jacobi-1d", "jacobi-2d") else min(res["iters"], 8)
-        done_iters = 0
-        while True:
-            oracle.run_iterative(prob, T=sample_iters, threads=cores)
-            done_iters += sample_iters
-            k += 1
-            if time.perf_counter() - t0 >= budget_s or k >= 50:
-                break
-        dt = time.perf_counter() - t0
-        gbs = per_iter_bytes * done_iters / dt / 1e9
-        return {"value": round(gbs, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
-                "sample": "%d oracle iterations (%d run(s) of %d) of this workload, 1 thread, "
-                          "%.1f s; %.3g iterations/s" % (done_iters, k, sample_iters, dt,
-                                                         done_iters / dt)}
+
+        def timed(threads, budget):
+            t0 = time.perf_counter()
+            k = done_iters = 0
+            while True:
+                oracle.run_iterative(prob, T=sample_iters, threads=threads)
+                done_iters += sample_iters
+                k += 1
+                if time.perf_counter() - t0 >= budget or k >= 50:
+                    break
+            dt = time.perf_counter() - t0
+            return per_iter_bytes * done_iters / dt / 1e9, done_iters, k, dt
+
+        g1, i1, k1, d1 = timed(1, budget_s / 2)
+        gn, i_n, kn, dn = timed(n_cores, budget_s / 2)
+        return {"value": round(gn, 4), "unit": "GB/s", "cores": n_cores, "kind": "oracle",
+                "value_1_thread": round(g1, 4), "cpu_model": model,
+                "iterations_per_s": round(i_n / dn, 4),
+                "iterations_per_s_1_thread": round(i1 / d1, 4),
+                "sample": "runs of the first %d oracle iterations of this workload: %d run(s) "
+                          "on %d threads in %.1f s, %d run(s) on 1 thread in %.1f s"
+                          % (sample_iters, kn, n_cores, dn, k1, d1)}
     if cfg == "allgatherv":
         version = np.full(prob.P, -1, dtype=np.int32)
         recv = np.empty_like(prob.send)
@@ -539,7 +627,8 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
         dt = time.perf_counter() - t0
         per_rep = res["bytes_per_step"] / res["iters"]
         return {"value": round(per_rep * reps / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
-                "kind": "oracle", "sample": "%d of %d repetitions, 1 thread, %.1f s"
+                "kind": "oracle", "cpu_model": model,
+                "sample": "%d of %d repetitions, 1 thread (the oracle has no threaded loop here), %.1f s"
                                             % (reps, prob.reps, dt)}
     if cfg == "mf":
         # worker 0's share of iteration 0: the errors and gradient of its shard
@@ -554,7 +643,8 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
         rows = prob.n_users + prob.n_items
         sample_bytes = (24.0 * prob.N + 12.0 * prob.P * rows) / prob.P + 16.0 * prob.m
         return {"value": round(sample_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
-                "kind": "oracle", "sample": "worker 0's errors and gradient at iteration 0 "
+                "kind": "oracle", "cpu_model": model,
+                "sample": "worker 0's errors and gradient at iteration 0 "
                                             "(1/%d of the ratings), 1 thread, %.1f s" % (prob.P, dt)}
     if cfg == "threshold":
         from oracle import threshold as THO
@@ -571,7 +661,8 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
         dt = time.perf_counter() - t0
         per_rep = res["bytes_per_step"] / res["iters"]
         return {"value": round(per_rep * reps / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
-                "kind": "oracle", "sample": "%d of %d repetitions, 1 thread, %.1f s"
+                "kind": "oracle", "cpu_model": model,
+                "sample": "%d of %d repetitions, 1 thread (the oracle has no threaded loop here), %.1f s"
                                             % (reps, prob.reps, dt)}
     if cfg == "hypercube":
         # whole calls of the oracle over the full vectors, from a reset
@@ -587,7 +678,8 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
         dt = time.perf_counter() - t0
         per_call = res["bytes_per_step"] / res["iters"]
         return {"value": round(per_call * calls / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
-                "kind": "oracle", "sample": "the first %d of %d calls, 1 thread, %.1f s"
+                "kind": "oracle", "cpu_model": model,
+                "sample": "the first %d of %d calls, 1 thread, %.1f s"
                                             % (calls, prob.calls, dt)}
     # 4b: a few repetitions over stored vectors
     P, m = prob.P, prob.m
@@ -604,7 +696,8 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
         reps += 1
     dt = time.perf_counter() - t0
     return {"value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
-            "kind": "oracle", "sample": "%d of %d repetitions over stored vectors, 1 thread, "
+            "kind": "oracle", "cpu_model": model,
+            "sample": "%d of %d repetitions over stored vectors, 1 thread, "
                                         "%.1f s" % (reps, prob.reps, dt)}
 
 
@@ -646,10 +739,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="jacobi-2d",
+    ap.add_argument("--config", default="jacobi-3d",
                     choices=["jacobi-1d", "jacobi-2d", "pagerank-rmat", "jacobi-3d", "allgatherv",
                              "allreduce", "hypercube", "threshold", "mf"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-copy-ceiling", action="store_true",
+                    help="skip the 4 GiB copy that measures the copy ceiling")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only measure a plain 4 GiB device copy (copy ceiling)")
     args = ap.parse_args()
@@ -710,9 +805,19 @@ def main():
     ms_per_step = wall / steps * 1e3
     gbs = res["bytes_per_step"] * steps / wall / 1e9
     iters_per_s = res["unit_per_step"] * steps / wall
-    avg_dom_s = dom_ms / max(dom_n, 1) / 1e3
+    if "dom_ms" in res:
+        avg_dom_s = res["dom_ms"] / 1e3
+        timing = res["dom_timing"]
+    else:
+        avg_dom_s = dom_ms / max(dom_n, 1) / 1e3
+        timing = "HIP events on the launching stream around every launch, over a second " \
+                 "region of the same K steps"
     achieved = res["dominant_bytes"] / avg_dom_s / 1e9 if avg_dom_s > 0 else None
     traffic = read_traffic(tag, digest)
+    ceiling = None
+    if not args.no_copy_ceiling:
+        print("[bench] copy ceiling", file=sys.stderr, flush=True)
+        ceiling = copy_probe(n_doubles=1 << 29, reps=5)["copy_probe"]["ecc_stream_copy"]["gbs"]
     line = {
         "metric": METRIC,
         "value": round(gbs, 3),
@@ -729,6 +834,8 @@ def main():
         "config": describe(cfg, prob),
         "iterations_per_s": round(iters_per_s, 2),
         "hbm_peak_frac": round(gbs / HBM_PEAK_GBS, 4),
+        "copy_ceiling_gbs": ceiling,
+        "copy_ceiling_frac": round(gbs / ceiling, 4) if ceiling else None,
         "ms_per_step_with_kernel_events": round(res["wall_events"] / steps * 1e3, 4),
         "peak_hbm_footprint_gb": round(res["footprint"] / 1e9, 3),
         "kernel_avg_us": {k.lower(): round(v[0] / max(v[1], 1) * 1e3, 3)
@@ -740,14 +847,19 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4) if achieved else None,
+            "frac_of_copy_ceiling": round(achieved / ceiling, 4) if (achieved and ceiling)
+            else None,
             "traffic": traffic,
+            "traffic_kind": "fabric bytes per launch: calibrated FETCH_SIZE + WRITE_SIZE (L2 to "
+                            "Infinity Fabric requests, Infinity Cache hits included)",
             "algorithmic_bytes_per_launch": res["dominant_bytes"],
             "avg_launch_us": round(avg_dom_s * 1e6, 3),
             "launches_timed": dom_n,
-            "timing": "HIP events on the plan's stream around every launch, over a second "
-                      "region of the same K steps",
+            "timing": timing,
         },
     }
+    if "dom_events_avg_us" in res:
+        line["roofline"]["avg_launch_us_with_events"] = res["dom_events_avg_us"]
     if "extra" in res:
         line.update(res["extra"])
     if not args.no_cpu_baseline:

@@ -25,3 +25,15 @@ def test_help_lists_every_workload():
     for cfg in ("jacobi-1d", "jacobi-2d", "pagerank-rmat", "jacobi-3d", "allgatherv", "allreduce",
                 "hypercube", "threshold", "mf"):
         assert cfg in r.stdout
+
+
+def test_byte_model_and_host_fields():
+    """The sweep's algorithmic bytes follow the model 12 nnz + 28 n + 4 (col
+    and val per nonzero, row_ptr, the x view, b, the written iterate); the
+    CPU baseline names the cores this process may use."""
+    sys.path.insert(0, ROOT)
+    import bench
+    assert bench.sweep_bytes(64_000_000, 447_040_000) == 12 * 447_040_000 + 28 * 64_000_000 + 4
+    cores, model = bench.host_cpu()
+    assert cores == len(os.sched_getaffinity(0)) and cores >= 1
+    assert model is None or isinstance(model, str)
