@@ -318,6 +318,23 @@ ecc_status_t ecc_iterate_spmv(ecc_plan_t plan, ecc_matrix_t W, double alpha, dou
                               const double *d_x_own, const double *d_x_hat, double *d_x_next,
                               double *d_partials);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): one
+ * ecc_iterate_jacobi sweep followed by its ecc_residual(..., ECC_NORM_L2,
+ * ...), without the caller's d_partials workspace.  The partial sums are
+ * kept in a static device array of the library, ECC_SCRATCH_DOUBLES doubles
+ * (8 MiB) on each GPU it runs on, held until the process ends; *d_rho
+ * (device, asynchronous) receives ||r||_2.  Results are bitwise those of
+ * ecc_iterate_jacobi + ecc_residual (the same kernels and order).  Calls no
+ * allocation routine.  ECC_ERR_RANGE when ecc_partials_size(A) exceeds
+ * ECC_SCRATCH_DOUBLES; other errors as ecc_iterate_jacobi.  Every call on a
+ * GPU uses that GPU's one array: calls that overlap on one GPU (from other
+ * streams or threads) race. */
+#define ECC_SCRATCH_DOUBLES (1 << 20)
+ecc_status_t ecc_iterate_jacobi_noalloc(ecc_plan_t plan, ecc_matrix_t A, const double *d_b,
+                                        const double *d_x_own, const double *d_x_hat,
+                                        double *d_x_next, double *d_rho);
+
 /* Second pass of the norm: reduces n_partials values in a fixed order
  * (deterministic) to sqrt(sum) (ECC_NORM_L2) or sum (ECC_NORM_L1).  Writes
  * *d_out (device, asynchronous) and/or *h_out (host: synchronises); at least

@@ -25,6 +25,7 @@ ECC_TIMING_MF_GRAD, ECC_TIMING_MF_STEP, ECC_TIMING_KINDS = 4, 5, 6
 ECC_THRESHOLD_DATA, ECC_THRESHOLD_PROCS = 0, 1
 ECC_LAYOUT_STREAM, ECC_LAYOUT_SORTED, ECC_LAYOUT_SHORT, ECC_LAYOUT_RANGES = 0, 1, 2, 3
 ECC_SCHEDULE_AUTO, ECC_SCHEDULE_STATIC, ECC_SCHEDULE_QUEUE = 0, 1, 2
+ECC_SCRATCH_DOUBLES = 1 << 20
 
 STATUS_NAMES = {0: "ECC_OK", 1: "ECC_ERR_ARG", 2: "ECC_ERR_OVERLAP", 3: "ECC_ERR_RANGE",
                 4: "ECC_ERR_ALLOC", 5: "ECC_ERR_DEVICE", 6: "ECC_ERR_STATE"}
@@ -78,6 +79,7 @@ _SIGS = [
     ("ecc_iterate_jacobi", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     ("ecc_iterate_spmv", ctypes.c_int, [_VP, _VP, _D, _D, _VP, _VP, _VP, _VP]),
     ("ecc_residual", ctypes.c_int, [_VP, _VP, _I64, _I32, _VP, _VP]),
+    ("ecc_iterate_jacobi_noalloc", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     ("ecc_stream_copy", ctypes.c_int, [_VP, _VP, _I64, _VP]),
     ("ecc_hypercube_create", ctypes.c_int, [_I32, _I64, _I32, _VP, ctypes.POINTER(_VP)]),
     ("ecc_hypercube_destroy", ctypes.c_int, [_VP]),
@@ -266,6 +268,11 @@ def ecc_matrix_layout(mat):
 def ecc_iterate_jacobi(plan, mat, d_b, d_x_own, d_x_hat, d_x_next, d_partials):
     _check(lib().ecc_iterate_jacobi(plan, mat, _ptr(d_b), _ptr(d_x_own), _ptr(d_x_hat),
                                     _ptr(d_x_next), _ptr(d_partials)))
+
+
+def ecc_iterate_jacobi_noalloc(plan, mat, d_b, d_x_own, d_x_hat, d_x_next, d_rho):
+    _check(lib().ecc_iterate_jacobi_noalloc(plan, mat, _ptr(d_b), _ptr(d_x_own), _ptr(d_x_hat),
+                                            _ptr(d_x_next), _ptr(d_rho)))
 
 
 def ecc_iterate_spmv(plan, mat, alpha, beta, d_x_own, d_x_hat, d_x_next, d_partials):

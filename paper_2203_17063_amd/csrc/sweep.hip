@@ -49,6 +49,7 @@
 // rank arrives.  No entry of x_hat that is written is read in the same
 // launch, so the fused step equals assemble-then-sweep bit for bit.
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include <new>
@@ -1958,6 +1959,83 @@ ecc_status_t ecc_iterate_spmv(ecc_plan_t plan, ecc_matrix_t W, double alpha, dou
                               double *d_partials) {
     return iterate(plan, W, ECC_KIND_POWER, nullptr, alpha, beta, d_x_own, d_x_hat, d_x_next,
                    d_partials);
+}
+
+// ---------------------------------------------------------------------------
+// The sweep's partial sums without a caller workspace: a static device array
+// of ECC_SCRATCH_DOUBLES doubles, one copy on every GPU the library runs on.
+// Host code never passes the array's name to a kernel (in host code it is a
+// stand-in, not a device address): its device address is looked up once per
+// device with hipGetSymbolAddress, with that device current, and kept here.
+// ---------------------------------------------------------------------------
+namespace {
+
+static __device__ __align__(256) double scratch[ECC_SCRATCH_DOUBLES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+double *g_scratch_ptr[kMaxDevices] = {};
+
+// The address of the array on the device that runs `stream`.
+ecc_status_t scratch_on(hipStream_t stream, double **out) {
+    int dev = 0;
+    if (stream) {
+        hipDevice_t d = 0;
+        ECC_HIP(hipStreamGetDevice(stream, &d));
+        dev = (int)d;
+    } else {
+        ECC_HIP(hipGetDevice(&dev));
+    }
+    if (dev < 0 || dev >= kMaxDevices) {
+        set_error("device %d beyond the %d devices the scratch table holds", dev, kMaxDevices);
+        return ECC_ERR_RANGE;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        int cur = 0;
+        ECC_HIP(hipGetDevice(&cur));
+        if (cur != dev) ECC_HIP(hipSetDevice(dev));
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur != dev) ECC_HIP(hipSetDevice(cur));
+        if (e != hipSuccess || !p) {
+            set_error("hipGetSymbolAddress of the scratch array failed: %s", hipGetErrorString(e));
+            return ECC_ERR_DEVICE;
+        }
+        g_scratch_ptr[dev] = static_cast<double *>(p);
+    }
+    *out = g_scratch_ptr[dev];
+    return ECC_OK;
+}
+
+}  // namespace
+
+ecc_status_t ecc_iterate_jacobi_noalloc(ecc_plan_t plan, ecc_matrix_t A, const double *d_b,
+                                        const double *d_x_own, const double *d_x_hat,
+                                        double *d_x_next, double *d_rho) {
+    clear_error();
+    ecc_status_t st = check_plan(plan);
+    if (st != ECC_OK) return st;
+    ECC_ARG(A != nullptr, "matrix is NULL");
+    ECC_ARG(d_rho != nullptr, "d_rho is NULL");
+    if (A->n_part > ECC_SCRATCH_DOUBLES) {
+        set_error("the sweep writes %lld partial sums; the scratch array holds %d",
+                  (long long)A->n_part, ECC_SCRATCH_DOUBLES);
+        return ECC_ERR_RANGE;
+    }
+    double *part = nullptr;
+    st = scratch_on(plan->stream, &part);
+    if (st != ECC_OK) return st;
+    // the same kernels as ecc_iterate_jacobi + ecc_residual: every partial
+    // is written by the sweep (and its split-row pass), so nothing in the
+    // array needs clearing
+    st = iterate(plan, A, ECC_KIND_JACOBI, d_b, 0.0, 0.0, d_x_own, d_x_hat, d_x_next, part);
+    if (st != ECC_OK) return st;
+    TimedLaunch timed(plan, ECC_TIMING_NORM);
+    hipLaunchKernelGGL(k_residual, dim3(1), dim3(kNormThreads), 0, plan->stream, part,
+                       A->n_part, ECC_NORM_L2, d_rho);
+    ECC_LAUNCH_CHECK();
+    return ECC_OK;
 }
 
 ecc_status_t ecc_residual(ecc_plan_t plan, const double *d_partials, int64_t n_partials,
