@@ -146,7 +146,7 @@ ecc_status_t ecc_plan_timing(ecc_plan_t plan, int32_t kernel, double *total_ms,
  * increments the clock on entry; t is that value minus one) and advances the
  * clock by one.  The staleness decision for every rank p is
  *     eff[p] = version[p] < 0  ||  arrived[p]  ||  t - version[p] > S
- * ("wait only if the data received is too stale": a block older than S
+ * (the caller waits only for data older than the slack: a block older than S
  * clocks is delivered now, a *forced* arrival); then version[p] := t where
  * eff[p] and age[p] := t - version[p], so 0 <= age <= S.
  * ------------------------------------------------------------------------- */
@@ -174,7 +174,11 @@ ecc_status_t ecc_allgatherv_assemble_packed(ecc_plan_t plan, const double *d_sen
                                             uint8_t *d_eff_out, int32_t *d_age_out);
 
 /* Partial allreduce (sum) with stale substitution: the reduction of
- * Algorithm 1 over the newest contribution held for each rank.
+ * Algorithm 1 over the newest contribution held for each rank.  This is the
+ * stale mode of the partial allreduce; the mode that drops contributions
+ * that did not arrive is the separate call ecc_allreduce_drop (it keeps no
+ * slots, versions or clock, so it takes no plan) instead of a mode argument
+ * here.
  *   for every p with eff[p]:  d_slots[p][i] = d_fresh[p][i]
  *   d_result[i] = ((slot_0[i] + slot_1[i]) + slot_2[i]) + ...   (rank order,
  *                 so the result is bitwise reproducible)

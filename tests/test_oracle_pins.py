@@ -6,6 +6,7 @@ closed forms of the staleness rule, brute force over every arrival schedule
 on tiny inputs, library solvers (LAPACK through numpy/scipy) for fixed
 points, and convergence bounds for bounded-delay iterations.
 """
+import dataclasses
 import itertools
 import math
 
@@ -288,6 +289,46 @@ def test_jacobi_2x2_hand_example(golden):
     assert h["x"].tolist() == g["expect"][-1]["x_next"]
     sync = iterative(A, np.array(g["b"]), g["counts"], g["S"], np.ones((3, 2)))
     assert oracle.run_iterative(sync)["x"].tolist() == g["synchronous_x3"]
+
+
+@pytest.mark.parametrize("tol,iters", [(1.5, 1), (math.sqrt(2.0), 2), (0.3, 2), (0.3125, 2),
+                                       (0.25, 3), (0.2, 3), (0.0, 3)])
+def test_stop_rule_on_the_2x2_hand_example(golden, tol, iters):
+    """Loop control (stop after the first iteration t whose norm is below the
+    tolerance) on the hand-computed norms sqrt(2), 1/4, 5/16: the run length is
+    that t + 1, a tolerance equal to a norm does not stop there (the test is
+    strict), the norm of the stopping iteration is kept, and the state is the
+    one after that iteration.  tol = 0 means no tolerance."""
+    g = golden("hand_examples.json")["jacobi_2x2"]
+    A = dense_csr(np.array(g["A"]))
+    prob = iterative(A, np.array(g["b"]), g["counts"], g["S"], g["mask"], tol=tol)
+    h = oracle.run_iterative(prob)
+    assert h["iters"] == iters
+    assert h["rho"].tolist() == [e["rho"] for e in g["expect"][:iters]]
+    assert h["x"].tolist() == g["expect"][iters - 1]["x_next"]
+    assert h["eff"].shape[0] == iters and h["forced"].sum() == (1 if iters == 3 else 0)
+
+
+@pytest.mark.parametrize("pick", [0, 1, 2])
+def test_stop_rule_first_iteration_below_tolerance(pick):
+    """PageRank on a scale-8 R-MAT graph under staleness: with a tolerance set
+    between two norms of the run without one, the run stops after the first
+    iteration whose norm is below it; with the tolerance equal to a norm, not
+    at that iteration."""
+    prob = W.pagerank_rmat(scale=8, T=120, P=4)
+    full = oracle.run_iterative(dataclasses.replace(prob, tol=0.0))
+    rho = full["rho"]
+    assert full["iters"] == prob.T
+    k = [10, 35, 60][pick]
+    for tol, strict in [((rho[k] + rho[k + 1]) / 2, False), (rho[k], True)]:
+        below = np.nonzero(rho < tol)[0]
+        want = int(below[0]) + 1 if below.size else prob.T
+        h = oracle.run_iterative(dataclasses.replace(prob, tol=tol))
+        assert h["iters"] == want
+        assert np.array_equal(h["rho"], rho[:want])
+        assert np.array_equal(h["eff"], full["eff"][:want])
+        if strict:
+            assert rho[want - 1] < tol and np.all(rho[:want - 1] >= tol)
 
 
 def test_jacobi_1d_fixed_point_thomas():
