@@ -241,7 +241,8 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
                       "launches' (events around each), divided by the sweep launches",
         "dom_events_avg_us": round(times["SWEEP"][0] / max(times["SWEEP"][1], 1) * 1e3, 3),
         "extra": {"layout": {0: "stream", 1: "sorted", 2: "short", 3: "ranges"}[layout],
-                  "schedule": "queue" if schedule == E.ECC_SCHEDULE_QUEUE else "static",
+                  "schedule": {E.ECC_SCHEDULE_STATIC: "static", E.ECC_SCHEDULE_QUEUE: "queue",
+                               E.ECC_SCHEDULE_SINGLE: "single launch"}[schedule],
                   "plane_tiling": {"plane_rows": tiling[0], "tile_rows": tiling[1]},
                   "assembly_bytes_per_arrived_element": per_elem},
     }

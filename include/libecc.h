@@ -272,13 +272,21 @@ ecc_status_t ecc_matrix_destroy(ecc_matrix_t A);
  *                the next item of its XCD's range with an atomic ticket (and
  *                of the other ranges once its own is exhausted); each item
  *                then writes its own partial norm, so ecc_partials_size is
- *                the item count + 1.  ECC_SCHEDULE_AUTO (0): the queue when
- *                a workgroup would walk at least 16 items.
+ *                the item count + 1.  ECC_SCHEDULE_SINGLE: ecc_solve runs
+ *                the whole loop as one launch of one 1,024-thread workgroup
+ *                holding the vectors in LDS, for at most 2,048 rows (4,096
+ *                rows of at most 3 entries), 64 items and 1,024 ranks (else
+ *                as ECC_SCHEDULE_AUTO); the other calls use the queue's
+ *                per-item partials.
+ *                ECC_SCHEDULE_AUTO (0): the single launch when the problem
+ *                fits it, else the queue when a workgroup would walk at
+ *                least 16 items, else the static walk.
  * opts may be NULL (the defaults).  ECC_ERR_ARG for a negative range_bytes
  * or an unknown schedule. */
 #define ECC_SCHEDULE_AUTO 0
 #define ECC_SCHEDULE_STATIC 1
 #define ECC_SCHEDULE_QUEUE 2
+#define ECC_SCHEDULE_SINGLE 3
 typedef struct {
     int64_t range_bytes;
     int64_t tile_rows;
@@ -292,8 +300,8 @@ ecc_status_t ecc_matrix_create_ex(ecc_plan_t plan, const ecc_csr_t *A, int32_t k
  * the items are swept in row order. */
 ecc_status_t ecc_matrix_tiling(ecc_matrix_t A, int64_t *plane_rows, int64_t *tile_rows);
 
-/* Schedule chosen at set-up (host only): ECC_SCHEDULE_STATIC or
- * ECC_SCHEDULE_QUEUE. */
+/* Schedule chosen at set-up (host only): ECC_SCHEDULE_STATIC,
+ * ECC_SCHEDULE_QUEUE or ECC_SCHEDULE_SINGLE. */
 ecc_status_t ecc_matrix_schedule(ecc_matrix_t A, int32_t *schedule);
 
 /* The layout ecc_matrix_create chose (ECC_LAYOUT_*) and, for

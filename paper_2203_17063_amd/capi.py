@@ -24,7 +24,7 @@ ECC_TIMING_ASSEMBLE, ECC_TIMING_ALLREDUCE, ECC_TIMING_SWEEP, ECC_TIMING_NORM = 0
 ECC_TIMING_MF_GRAD, ECC_TIMING_MF_STEP, ECC_TIMING_KINDS = 4, 5, 6
 ECC_THRESHOLD_DATA, ECC_THRESHOLD_PROCS = 0, 1
 ECC_LAYOUT_STREAM, ECC_LAYOUT_SORTED, ECC_LAYOUT_SHORT, ECC_LAYOUT_RANGES = 0, 1, 2, 3
-ECC_SCHEDULE_AUTO, ECC_SCHEDULE_STATIC, ECC_SCHEDULE_QUEUE = 0, 1, 2
+ECC_SCHEDULE_AUTO, ECC_SCHEDULE_STATIC, ECC_SCHEDULE_QUEUE, ECC_SCHEDULE_SINGLE = 0, 1, 2, 3
 ECC_SCRATCH_DOUBLES = 1 << 20
 
 STATUS_NAMES = {0: "ECC_OK", 1: "ECC_ERR_ARG", 2: "ECC_ERR_OVERLAP", 3: "ECC_ERR_RANGE",

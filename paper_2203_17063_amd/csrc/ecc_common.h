@@ -101,6 +101,19 @@ constexpr int64_t kTileMinRows = 4096;
 constexpr int kQueueRanges = 8;
 constexpr int kQueueStride = 64;
 constexpr int64_t kQueueMinItems = 16;
+// Single-launch solve of a small short-row problem (tiny.hip): one workgroup
+// of kTinyThreads holds x, the next iterate and the assembled vector in LDS.
+constexpr int kTinyThreads = 1024;
+constexpr int kTinyMaxRows = 4096;
+constexpr int kTinyMaxItems = 64;
+constexpr int kTinyMaxP = 1024;
+// Does a short-row problem fit the single launch: up to 2,048 rows with up to
+// 8 entries each, or up to 4,096 rows with up to 3 (the rows' entries are
+// held in registers), at most kTinyMaxItems items and kTinyMaxP ranks?
+inline bool tiny_fits(int64_t n, int32_t max_row, int64_t n_items, int32_t P) {
+    const bool rows = n <= 2 * kTinyThreads || (n <= kTinyMaxRows && max_row <= 3);
+    return n > 0 && rows && n_items <= kTinyMaxItems && P <= kTinyMaxP;
+}
 constexpr int kShortRow = 8;
 static_assert(kShortRow <= 8, "a short row is summed from eight registers");
 static_assert(kStreamRows <= 256 && kStreamRows <= kSweepThreads, "one lane per short row");
@@ -149,6 +162,8 @@ constexpr int kDppQuadXor1 = 0xB1;     // quad_perm [1,0,3,2]
 constexpr int kDppQuadXor2 = 0x4E;     // quad_perm [2,3,0,1]
 constexpr int kDppRowHalfMirror = 0x141;
 constexpr int kDppRowMirror = 0x140;
+constexpr int kDppRowBcast15 = 0x142;  // lane 15 of each row to the next row
+constexpr int kDppRowBcast31 = 0x143;  // lane 31 to rows 2 and 3
 
 // Sum over aligned groups of G lanes (G a power of two <= 64); every lane of
 // the group receives the group's sum.  The pairing is fixed, so the result is
@@ -161,6 +176,22 @@ __device__ __forceinline__ double group_sum(double v) {
     if constexpr (G >= 16) v += dpp_f64<kDppRowMirror>(v);
     if constexpr (G >= 32) v += __shfl_xor(v, 16, 64);
     if constexpr (G >= 64) v += __shfl_xor(v, 32, 64);
+    return v;
+}
+
+// The sum of a wave's 64 values, in lane 63 (other lanes hold partial sums):
+// group_sum<64>'s pairing -- quads, eights, rows of 16, then the four rows
+// pairwise -- with the last two steps done by the DPP row broadcasts 15 and
+// 31 instead of two shuffles through LDS.  Lane 63 adds (R3 + R2) + (R1 + R0)
+// where group_sum adds (R0 + R1) + (R2 + R3); IEEE addition is commutative,
+// so the two are bitwise equal.  All lanes must be active.
+__device__ __forceinline__ double wave_sum_lane63(double v) {
+    v += dpp_f64<kDppQuadXor1>(v);
+    v += dpp_f64<kDppQuadXor2>(v);
+    v += dpp_f64<kDppRowHalfMirror>(v);
+    v += dpp_f64<kDppRowMirror>(v);
+    v += dpp_f64<kDppRowBcast15>(v);
+    v += dpp_f64<kDppRowBcast31>(v);
     return v;
 }
 
@@ -248,11 +279,41 @@ __device__ __forceinline__ void record_step(int32_t P, int32_t S, int64_t t,
     __syncthreads();
 }
 
+// Row epilogue of the block-row iterations; returns the row's contribution
+// to the norm (r_i^2 for Jacobi, |x_next_j - x_own_j| for the power step).
+template <int KIND>
+__device__ __forceinline__ double row_finish(int32_t i, double s, double dg, double bi,
+                                             double xo, double alpha, double beta,
+                                             double *__restrict__ x_next) {
+    if constexpr (KIND == ECC_KIND_JACOBI) {
+        const double bs = bi - s;
+        const double xn = bs / dg;
+        x_next[i] = xn;
+        const double r = bs - dg * xo;
+        return r * r;
+    } else {
+        const double xn = alpha * s + beta;
+        x_next[i] = xn;
+        return fabs(xn - xo);
+    }
+}
+
+// Rows of a short-layout item padded to a multiple of 32 in the item-major
+// copy of its entries.
+__device__ __forceinline__ int32_t sell_pad(int32_t nrows) { return (nrows + 31) & ~31; }
+
+// The sum of 8 values as a pairwise tree: ((0+1)+(2+3))+((4+5)+(6+7)).
+__device__ __forceinline__ double tree8(const double *t) {
+    return ((t[0] + t[1]) + (t[2] + t[3])) + ((t[4] + t[5]) + (t[6] + t[7]));
+}
+
 // Deterministic reduction of n values to their sum by kNormThreads threads:
-// thread j adds values j, j + kNormThreads, ... in order, then a fixed tree.
-// The value at index `n - 1` may be supplied in a register (`last`, used when
-// `use_last`) instead of being read, with the same order of operations.
-// Loads are issued eight at a time, the additions stay in that order.
+// thread j takes values j, j + kNormThreads, ... eight at a time, adds each
+// full group of eight as a pairwise tree (tree8) to its running sum, then the
+// remaining values one by one, in index order; then a fixed tree over the
+// threads (block_sum).  The value at index `n - 1` may be supplied in a
+// register (`last`, used when `use_last`) instead of being read, with the
+// same order of operations.
 __device__ __forceinline__ double reduce_values(const double *__restrict__ v, int64_t n,
                                                 bool use_last, double last, double *scratch) {
     double acc = 0.0;
@@ -264,8 +325,7 @@ __device__ __forceinline__ double reduce_values(const double *__restrict__ v, in
             const int64_t q = k + (int64_t)j * kNormThreads;
             t[j] = (use_last && q == n - 1) ? last : v[q];
         }
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc += t[j];
+        acc += tree8(t);
     }
     for (; k < n; k += kNormThreads) acc += (use_last && k == n - 1) ? last : v[k];
     return block_sum<kNormThreads>(acc, scratch);
@@ -343,6 +403,8 @@ struct ecc_matrix_s {
     double *d_partials = nullptr;   // internal partials of ecc_solve: 2 x n_part
     int64_t n_part = 1;             // partial sums a sweep writes: grid + 1, or n_items + 1 (queue)
     bool queue = false;             // short layout: items claimed from a run-time queue
+    bool tiny = false;              // short layout: ecc_solve runs as one single-workgroup launch;
+                                    // sweeps write one partial per row (n_part = n + 1)
     unsigned *d_queue = nullptr;    // its ticket counters, (kQueueRanges + 1) x kQueueStride
 };
 
@@ -390,6 +452,11 @@ struct Pass2Launch {
     const int32_t *done = nullptr;
 };
 ecc_status_t launch_pass2(ecc_matrix_t M, const Pass2Launch &L);
+// The whole loop of ecc_solve as one single-workgroup launch (M->tiny).
+ecc_status_t launch_solve_tiny(ecc_matrix_t M, const double *d_b, double alpha, double beta,
+                               double *d_x, double *d_x_hat, const uint8_t *d_mask, int32_t T,
+                               double tol, double *d_rho, uint8_t *d_eff_hist,
+                               int32_t *d_age_hist);
 ecc_status_t check_plan(ecc_plan_t plan);
 
 // Event timing around one launch (no-ops unless the plan's timing is on).

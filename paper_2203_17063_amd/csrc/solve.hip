@@ -51,6 +51,19 @@ extern "C" ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double 
 
     hipLaunchKernelGGL(k_ctrl_reset, dim3(1), dim3(64), 0, plan->stream, plan->d_ctrl);
     ECC_LAUNCH_CHECK();
+    if (A->tiny && T > 0 && n > 0) {
+        // the whole loop in one launch; the last iterate lands in d_x
+        st = launch_solve_tiny(A, d_b, alpha, beta, d_x, d_x_hat, d_mask, T, tol, d_rho,
+                               d_eff_hist, d_age_hist);
+        if (st != ECC_OK) return st;
+        int32_t ctrl[2] = {0, 0};
+        ECC_HIP(hipMemcpyAsync(ctrl, plan->d_ctrl, sizeof(ctrl), hipMemcpyDeviceToHost,
+                               plan->stream));
+        ECC_HIP(hipStreamSynchronize(plan->stream));
+        plan->clock = clock0 + ctrl[1];
+        *h_iters = ctrl[1];
+        return ECC_OK;
+    }
     const int32_t *done = plan->d_ctrl;
     const int64_t G1 = A->n_part;
     // Without a tolerance and without split rows, every iteration is a single

@@ -107,6 +107,7 @@ struct SweepArgs {
     // queue-scheduled matrix, its ticket counters
     int64_t n_part;
     unsigned *queue;
+    int32_t row_part;  // short layout: one partial per row (partials[i] = row i's share)
 };
 
 // Rank state staged in LDS by a fused step.
@@ -163,24 +164,6 @@ __device__ __forceinline__ double view_load(int32_t c, int32_t lo, int32_t hi,
     return (own ? x_own : x_hat)[c];
 }
 
-// Row epilogue; returns the row's contribution to the norm (r_i^2 for Jacobi,
-// |x_next_j - x_own_j| for the power step).
-template <int KIND>
-__device__ __forceinline__ double row_finish(int32_t i, double s, double dg, double bi,
-                                             double xo, double alpha, double beta,
-                                             double *__restrict__ x_next) {
-    if constexpr (KIND == ECC_KIND_JACOBI) {
-        const double bs = bi - s;
-        const double xn = bs / dg;
-        x_next[i] = xn;
-        const double r = bs - dg * xo;
-        return r * r;
-    } else {
-        const double xn = alpha * s + beta;
-        x_next[i] = xn;
-        return fabs(xn - xo);
-    }
-}
 
 // Lanes per row of a stream item: rows of at most 16 nonzeros on average are
 // summed by one lane in CSR order; longer ones by up to 64 lanes, keeping at
@@ -637,7 +620,6 @@ struct EllEntries {
     double v[R];
 };
 
-__device__ __forceinline__ int32_t sell_pad(int32_t nrows) { return (nrows + 31) & ~31; }
 
 template <int R>
 __device__ __forceinline__ void ell_entries(const SweepArgs &a, bool live, const WorkItem &w,
@@ -707,7 +689,9 @@ __device__ __forceinline__ void short_body(const SweepArgs &a) {
                 }
             }
             if (STEP && s_eff[cur.rank] != 0) a.x_hat[i] = xo;
-            contrib += row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+            const double c = row_finish<KIND>(i, s, dg, bi, xo, a.alpha, a.beta, a.x_next);
+            if (a.row_part) a.partials[i] = c;
+            else contrib += c;
         }
         w += w_step;
         have = have_next;
@@ -716,6 +700,7 @@ __device__ __forceinline__ void short_body(const SweepArgs &a) {
         nxt = nn;
         E = En;
     }
+    if (a.row_part) return;  // (uniform across the grid)
     const double total = block_sum<kSweepThreads>(contrib, s_red);
     if (tid == 0) a.partials[blockIdx.x] = total;
 }
@@ -1449,6 +1434,7 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     a.reserve0 = (M->grid >= kReserveMinGrid && !M->queue) ? 1 : 0;
     a.n_part = M->n_part;
     a.queue = M->queue ? M->d_queue : nullptr;
+    a.row_part = M->tiny ? 1 : 0;
     a.zero_extra = M->n_fixups == 0 ? 1 : 0;
     a.prev_partials = L.prev_partials;
     a.prev_rho = L.prev_rho;
@@ -1566,7 +1552,7 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
     const ecc_matrix_opts_t opts = opts_in ? *opts_in : ecc_matrix_opts_t{0, 0, 0};
     ECC_ARG(opts.range_bytes >= 0, "range_bytes is negative");
     ECC_ARG(opts.schedule == ECC_SCHEDULE_AUTO || opts.schedule == ECC_SCHEDULE_STATIC ||
-                opts.schedule == ECC_SCHEDULE_QUEUE,
+                opts.schedule == ECC_SCHEDULE_QUEUE || opts.schedule == ECC_SCHEDULE_SINGLE,
             "unknown schedule %d", opts.schedule);
     const int64_t range_bytes = opts.range_bytes > 0 ? opts.range_bytes : kRangeBytes;
     ECC_ARG(kind == ECC_KIND_JACOBI || kind == ECC_KIND_POWER, "unknown kind %d", kind);
@@ -1742,7 +1728,13 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
     M->queue = layout == kLayShort && (opts.schedule == ECC_SCHEDULE_QUEUE ||
                                        (opts.schedule == ECC_SCHEDULE_AUTO &&
                                         M->n_items >= kQueueMinItems * (int64_t)M->grid));
-    M->n_part = M->queue ? M->n_items + 1 : (int64_t)M->grid + 1;
+    // A small short-row problem is solved by one launch (tiny.hip), whose
+    // norm reduces one partial per row: its sweeps write per-row partials
+    // too, so that every entry point gives the same norm.
+    M->tiny = layout == kLayShort && tiny_fits(n, M->short_r, M->n_items, plan->P) &&
+              (opts.schedule == ECC_SCHEDULE_AUTO || opts.schedule == ECC_SCHEDULE_SINGLE);
+    if (M->tiny) M->queue = false;
+    M->n_part = M->tiny ? n + 1 : M->queue ? M->n_items + 1 : (int64_t)M->grid + 1;
     auto fail = [&](const char *what) {
         set_error("%s", what);
         ecc_matrix_destroy(M);
@@ -1899,7 +1891,7 @@ ecc_status_t ecc_matrix_schedule(ecc_matrix_t M, int32_t *schedule) {
     clear_error();
     ECC_ARG(M != nullptr, "matrix is NULL");
     ECC_ARG(schedule != nullptr, "NULL output");
-    *schedule = M->queue ? ECC_SCHEDULE_QUEUE : ECC_SCHEDULE_STATIC;
+    *schedule = M->tiny ? ECC_SCHEDULE_SINGLE : M->queue ? ECC_SCHEDULE_QUEUE : ECC_SCHEDULE_STATIC;
     return ECC_OK;
 }
 

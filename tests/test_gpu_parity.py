@@ -7,6 +7,8 @@ problem's scale; stencil sweeps sum every row on one lane in CSR order, so
 their iterates are also checked bit for bit.
 """
 
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -637,16 +639,81 @@ def test_step_api_matches_solve_queue():
 
 
 def test_schedule_choice():
-    """Static walk for few items per workgroup, unless forced."""
+    """A problem of at most 2,048 rows (4,096 rows of at most 3 entries) is
+    solved by one launch; a larger one with few items per workgroup walks them
+    statically; either can be forced."""
     E = _capi()
-    prob = W.jacobi_2d(N=64, T=2)
-    for sch, want in [(0, E.ECC_SCHEDULE_STATIC), (E.ECC_SCHEDULE_STATIC, E.ECC_SCHEDULE_STATIC),
-                      (E.ECC_SCHEDULE_QUEUE, E.ECC_SCHEDULE_QUEUE)]:
+    small, big = W.jacobi_2d(N=40, T=2), W.jacobi_2d(N=64, T=2)
+    for prob, sch, want in [(small, 0, E.ECC_SCHEDULE_SINGLE),
+                            (small, E.ECC_SCHEDULE_STATIC, E.ECC_SCHEDULE_STATIC),
+                            (small, E.ECC_SCHEDULE_QUEUE, E.ECC_SCHEDULE_QUEUE),
+                            (small, E.ECC_SCHEDULE_SINGLE, E.ECC_SCHEDULE_SINGLE),
+                            (big, 0, E.ECC_SCHEDULE_STATIC),
+                            (big, E.ECC_SCHEDULE_SINGLE, E.ECC_SCHEDULE_STATIC)]:
         run = _iterative(prob, schedule=sch)
-        assert E.ecc_matrix_schedule(run.mat) == want
+        assert E.ecc_matrix_schedule(run.mat) == want, (prob.n, sch)
         run.close()
     with pytest.raises(E.EccError):
-        _iterative(prob, schedule=7)
+        _iterative(small, schedule=7)
+
+
+def _single_cases():
+    def power_tol():
+        prob = _banded_problem("power", 3000, 0, 3, T=80)
+        rho = oracle.run_iterative(prob)["rho"]
+        return dataclasses.replace(prob, tol=float(rho[37]) * (1 + 1e-9))
+    return [("jacobi-1d", lambda: W.jacobi_1d()),
+            ("jacobi-2d-33", lambda: W.jacobi_2d(N=33, T=40)),
+            ("jacobi-2d-45", lambda: W.jacobi_2d(N=45, T=30)),
+            ("jacobi-3d-12", lambda: W.jacobi_3d(N=12, T=30, P=40)),
+            ("banded-jacobi-8", lambda: _banded_problem("jacobi", 2000, 8, 8)),
+            ("power-tol", power_tol)]
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_single_launch_matches_launch_loop(case):
+    """The whole loop as one single-workgroup launch (vectors in LDS) against
+    the launch-per-iteration loop (queue schedule) on the same problem:
+    iterates, assembled vector, eff/age histories, versions, forced arrivals
+    and clock bit for bit, norms within tolerance (the queue path adds them
+    per work item); against the separate calls on the same matrix, norms bit
+    for bit too (both reduce one partial per row); a tolerance that stops the
+    run midway; and the oracle."""
+    E = _capi()
+    name, make = _single_cases()[case]
+    prob = make()
+    announce("single", name, prob.n, prob.P, prob.T)
+    out = []
+    for sch in (E.ECC_SCHEDULE_SINGLE, E.ECC_SCHEDULE_QUEUE):
+        run = _iterative(prob, schedule=sch)
+        assert E.ecc_matrix_schedule(run.mat) == sch
+        iters = run.solve(tol=prob.tol, histories=True)
+        torch.cuda.synchronize()
+        out.append((iters, run.d_x.cpu().numpy(), run.d_x_hat.cpu().numpy(),
+                    run.d_rho.cpu().numpy()[:iters], run.eff_hist.cpu().numpy()[:iters],
+                    run.age_hist.cpu().numpy()[:iters], run.plan.stats()))
+        if sch == E.ECC_SCHEDULE_SINGLE:
+            # the separate calls over the same matrix: assemble, sweep, norm
+            run.plan.reset()
+            xa = torch.from_numpy(prob.x0.copy()).cuda()
+            xb = torch.empty_like(xa)
+            rhos = []
+            for t in range(iters):
+                rhos.append(run.step(t, xa, xb))
+                xa, xb = xb, xa
+            assert np.array_equal(np.array(rhos), out[0][3])
+            assert np.array_equal(xa.cpu().numpy(), out[0][1])
+        run.close()
+    (i1, x1, h1, r1, e1, a1, s1), (i2, x2, h2, r2, e2, a2, s2) = out
+    assert i1 == i2
+    assert np.array_equal(x1, x2) and np.array_equal(h1, h2)
+    assert np.all(np.abs(r1 - r2) <= 1e-12 * np.abs(r2) + 1e-300)
+    assert np.array_equal(e1, e2) and np.array_equal(a1, a2)
+    assert s1[0] == s2[0] and s1[1] == s2[1]
+    assert np.array_equal(s1[2], s2[2]) and np.array_equal(s1[3], s2[3])
+    if prob.tol > 0:
+        assert i1 < prob.T
+    _solve_and_compare(prob, bitwise=True, expect_schedule=E.ECC_SCHEDULE_SINGLE, solves=2)
 
 
 def test_step_api_matches_solve_ranges():
