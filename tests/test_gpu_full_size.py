@@ -139,3 +139,114 @@ def test_mf_full():
     within 1e-12."""
     from test_gpu_mf import _compare
     _compare(W.mf_problem(T=2))
+
+
+def test_partial_allreduce_full_every_repetition():
+    """The partial allreduce at the benchmark's shape: 256 ranks x 2^22
+    elements, Bernoulli(0.7) arrivals, no staleness bound, 1,000 repetitions,
+    each rank's contribution at repetition r regenerated on the device from
+    its counters.  Every repetition: eff, result clock and the result at 4,096
+    sampled indices (first and last included) bit for bit against the oracle's
+    rank-ordered sum of each rank's last arrival; repetitions 0-9 and 999:
+    the whole result vector, by chunks of the index range; at the end, every
+    slot at the sampled indices."""
+    from paper_2203_17063_amd import capi as E
+    from paper_2203_17063_amd import runner as R
+    prob = W.partial_allreduce()
+    P, m = prob.P, prob.m
+    announce("4b full, every repetition", P, m, prob.reps)
+    fresh = torch.empty((P, m), dtype=torch.float64, device="cuda")
+    slots = torch.empty((P, m), dtype=torch.float64, device="cuda")
+    result = torch.empty(m, dtype=torch.float64, device="cuda")
+    d_fresh = R.ptr_array([fresh[p] for p in range(P)])
+    d_slots = R.ptr_array([slots[p] for p in range(P)])
+    d_mask = torch.from_numpy(prob.mask).cuda()
+    eff_d = torch.empty((prob.reps, P), dtype=torch.uint8, device="cuda")
+    clk_d = torch.empty(prob.reps, dtype=torch.int32, device="cuda")
+    plan = R.Plan(P, None, None, prob.S)
+    stream = torch.cuda.current_stream().cuda_stream
+    rng = np.random.default_rng(44)
+    idx = np.sort(rng.choice(m, 4096, replace=False))
+    idx[0], idx[-1] = 0, m - 1
+    d_idx = torch.from_numpy(idx).cuda()
+    version = np.full(P, -1, dtype=np.int32)
+    full = set(range(10)) | {prob.reps - 1}
+    chunk = 1 << 18
+    for r in range(prob.reps):
+        # rank p's contribution of repetition r: counters (r P + p) m + i
+        W.uniform_device(prob.seed, W.STREAM_PAYLOAD_REDUCE, P * m, fresh.data_ptr(),
+                         ctr0=prob.fresh_ctr0(0, r), lo=-1.0, hi=1.0, hip_stream=stream)
+        E.ecc_allreduce_partial(plan.handle, m, d_fresh, d_slots, result, d_mask[r].data_ptr(),
+                                eff_d[r], clk_d[r:r + 1])
+        eff, _, _ = oracle.select(prob.S, r, prob.mask[r], version)
+        got = result[d_idx].cpu().numpy()
+        cols = [prob.fresh_at(p, int(version[p]), idx) for p in range(P)]
+        ref = oracle.allreduce(np.zeros(P, dtype=np.uint8), [np.zeros(idx.size)] * P, cols)
+        assert np.array_equal(got, ref), r
+        assert np.array_equal(eff_d[r].cpu().numpy(), eff), r
+        assert int(clk_d[r].item()) == oracle.result_clock(version), r
+        if r in full:
+            res = result.cpu().numpy()
+            for a in range(0, m, chunk):
+                parts = [W.uniform(prob.seed, W.STREAM_PAYLOAD_REDUCE, chunk,
+                                   ctr0=prob.fresh_ctr0(p, int(version[p])) + a, lo=-1.0, hi=1.0)
+                         for p in range(P)]
+                ref = oracle.allreduce(np.zeros(P, dtype=np.uint8), [np.zeros(chunk)] * P, parts)
+                assert np.array_equal(res[a:a + chunk], ref), (r, a)
+    for p in range(P):
+        assert np.array_equal(slots[p][d_idx].cpu().numpy(),
+                              prob.fresh_at(p, int(version[p]), idx)), p
+    plan.close()
+
+
+def test_allgatherv_full_stale():
+    """allgatherv of the 256 lognormal blocks (16.5M elements) with Bernoulli(0.7)
+    arrivals and maximum staleness 3, 1,000 repetitions, the send arena of
+    repetition r regenerated on the device (counters r E + i): eff and ages
+    bit for bit at every repetition, and the receive vector bit for bit
+    against the oracle's assembly (oracle.select then oracle.allgatherv over
+    the same arena) every 25 repetitions, at 4,096 sampled indices at every
+    other one."""
+    from paper_2203_17063_amd import capi as E
+    from paper_2203_17063_amd import runner as R
+    base = W.allgatherv_lognormal()
+    P, reps, S = base.P, base.reps, 3
+    seed = W.seed_of(4)
+    mask = W.arrival_mask(seed + 100, reps, np.full(P, 0.7))
+    counts, displs = base.counts, base.displs
+    Etot = int(counts.sum())
+    announce("4a full, stale", P, Etot, reps, S)
+    send = torch.empty(Etot, dtype=torch.float64, device="cuda")
+    recv = torch.full((Etot,), float("nan"), dtype=torch.float64, device="cuda")
+    d_mask = torch.from_numpy(mask).cuda()
+    eff_d = torch.empty(P, dtype=torch.uint8, device="cuda")
+    age_d = torch.empty(P, dtype=torch.int32, device="cuda")
+    plan = R.Plan(P, counts, displs, S)
+    stream = torch.cuda.current_stream().cuda_stream
+    version = np.full(P, -1, dtype=np.int32)
+    h_recv = np.full(Etot, np.nan)
+    rng = np.random.default_rng(45)
+    idx = np.sort(rng.choice(Etot, 4096, replace=False))
+    d_idx = torch.from_numpy(idx).cuda()
+    sends = None
+    forced_total = 0
+    for r in range(reps):
+        W.uniform_device(seed, W.STREAM_PAYLOAD, Etot, send.data_ptr(), ctr0=r * Etot,
+                         lo=-1.0, hi=1.0, hip_stream=stream)
+        E.ecc_allgatherv_assemble_packed(plan.handle, send, recv, d_mask[r].data_ptr(), eff_d,
+                                         age_d)
+        eff, age, forced = oracle.select(S, r, mask[r], version)
+        forced_total += forced
+        assert np.array_equal(eff_d.cpu().numpy(), eff), r
+        assert np.array_equal(age_d.cpu().numpy(), age), r
+        # the oracle's receive vector: every repetition's arena, arrived blocks copied
+        arena = W.uniform(seed, W.STREAM_PAYLOAD, Etot, ctr0=r * Etot, lo=-1.0, hi=1.0)
+        sends = [arena[d:d + c] for d, c in zip(displs, counts)]
+        oracle.allgatherv(counts, displs, eff, sends, h_recv)
+        if r % 25 == 0 or r == reps - 1:
+            assert np.array_equal(recv.cpu().numpy(), h_recv), r
+        else:
+            assert np.array_equal(recv[d_idx].cpu().numpy(), h_recv[idx]), r
+    clock, forced, ver, _ = plan.stats()
+    assert clock == reps and forced == forced_total > 0 and np.array_equal(ver, version)
+    plan.close()

@@ -23,6 +23,8 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "gen.c")
 _LIB = os.path.join(_HERE, "libgen.so")
+_GPU_SRC = os.path.join(_HERE, "gen_gpu.hip")
+_GPU_LIB = os.path.join(_HERE, "libgen_gpu.so")
 
 # Named random streams (one per kind of draw).
 STREAM_PARTITION = 0
@@ -57,13 +59,50 @@ def seed_of(config: int) -> int:
 
 
 def build(force: bool = False) -> str:
-    """Compile gen.c into libgen.so with gcc (no floating-point contraction)."""
+    """Compile gen.c into libgen.so with gcc, and gen_gpu.hip into
+    libgen_gpu.so with hipcc for gfx950 (both without floating-point
+    contraction)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
         subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fopenmp", "-fPIC",
                                "-shared", "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
+    if force or not os.path.exists(_GPU_LIB) or \
+            os.path.getmtime(_GPU_LIB) < os.path.getmtime(_GPU_SRC):
+        tmp = _GPU_LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call([os.environ.get("HIPCC", "/opt/rocm/bin/hipcc"), "-O3",
+                               "--offload-arch=gfx950", "-ffp-contract=off", "-fPIC", "-shared",
+                               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                               "-o", tmp, _GPU_SRC])
+        os.replace(tmp, _GPU_LIB)
     return _LIB
+
+
+_gpu_lib = None
+
+
+def gpu_lib():
+    """The device-side uniform generator (gen_gpu.hip); raises if not built."""
+    global _gpu_lib
+    if _gpu_lib is None:
+        if not os.path.exists(_GPU_LIB):
+            raise RuntimeError("libgen_gpu.so is not built; run workloads.build()")
+        L = ctypes.CDLL(_GPU_LIB)
+        L.gen_uniform_range_device.restype = ctypes.c_int
+        L.gen_uniform_range_device.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
+                                               ctypes.c_int64, ctypes.c_double, ctypes.c_double,
+                                               ctypes.c_void_p, ctypes.c_void_p]
+        _gpu_lib = L
+    return _gpu_lib
+
+
+def uniform_device(seed: int, stream: int, n: int, d_out: int, ctr0: int = 0,
+                   lo: float = 0.0, hi: float = 1.0, hip_stream: int = 0) -> None:
+    """Writes uniform(seed, stream, n, ctr0, lo, hi) into device memory at
+    d_out (asynchronous on hip_stream)."""
+    e = gpu_lib().gen_uniform_range_device(seed, stream, ctr0, n, lo, hi, d_out, hip_stream)
+    if e != 0:
+        raise RuntimeError("gen_uniform_range_device failed: HIP error %d" % e)
 
 
 _lib = None
