@@ -126,13 +126,15 @@ def describe(cfg, prob):
                 "P": prob.P, "elements": int(prob.counts.sum()), "reps": prob.reps,
                 "name": cfg}
     if cfg == "mf":
-        return {"workload": "data-parallel matrix factorisation over the partial allreduce: %d "
-                            "synthetic ratings (%d users x %d items), rank %d, P=%d workers, slack "
-                            "%d, Bernoulli(%.1f) arrivals, %d iterations"
-                            % (prob.N, prob.n_users, prob.n_items, prob.rank, prob.P, prob.S,
-                               prob.meta["q"], prob.T),
+        return {"workload": "data-parallel matrix factorisation by minibatch SGD over the partial "
+                            "allreduce: %d synthetic ratings (%d users x %d items), rank %d, P=%d "
+                            "workers of %d minibatches, slack %d, Bernoulli(%.1f) arrivals, %d "
+                            "iterations"
+                            % (prob.N, prob.n_users, prob.n_items, prob.rank, prob.P, prob.K,
+                               prob.S, prob.meta["q"], prob.T),
                 "N": prob.N, "n_users": prob.n_users, "n_items": prob.n_items, "rank": prob.rank,
-                "P": prob.P, "slack": prob.S, "iterations": prob.T, "name": cfg}
+                "P": prob.P, "minibatches": prob.K, "slack": prob.S, "iterations": prob.T,
+                "name": cfg}
     if cfg == "threshold":
         return {"workload": "threshold broadcast + reduce over a binomial tree, P=%d processes x "
                             "%d elements, data fraction %.2f, %d repetitions"
@@ -487,17 +489,18 @@ def mf_bytes(prob, arrivals):
     """Algorithmic bytes of one factorisation iteration, per kernel."""
     N, m, P = prob.N, prob.m, prob.P
     rows = prob.n_users + prob.n_items
-    return {"MF_GRAD": 24.0 * N + 12.0 * P * rows + 8.0 * m + 8.0 * m * P,
-            # 2 x (other row, rating) per rating, (row, start, length) per
-            # (worker, row), the model, P gradients written
+    return {"MF_GRAD": 24.0 * N / prob.K + 12.0 * P * rows + 8.0 * m + 8.0 * m * P,
+            # 2 x (other row, rating) per rating of the minibatches, (row,
+            # start, length) per (worker, row), the model, P gradients written
             "ALLREDUCE": 8.0 * m * (P + arrivals + 1),
             "MF_STEP": 24.0 * m + 8.0 * rows}
 
 
 def run_mf_gpu(prob, steps, warmup):
     """One step = a reset and prob.T iterations.  Afterwards, a slack study:
-    the iterations needed at slack 0 / 2 / 32 / 64 to reach the error that
-    slack 0 reaches after prob.T iterations (same arrival probability)."""
+    the iterations needed at slack 0 / 2 / 32 / 64 to reach the full training
+    error that slack 0 reaches after prob.T iterations (same arrival
+    probability and minibatch schedule)."""
     import dataclasses
     import torch
     import workloads as W
@@ -536,29 +539,33 @@ def run_mf_gpu(prob, steps, warmup):
     E.ecc_plan_set_timing(ph, False)
     run.close()
     per = mf_bytes(prob, float(arrivals.mean()))
-    # slack study, 3 x T iterations each, arrivals Bernoulli(q) per (iteration, worker)
+    # slack study, 3 x T iterations each, arrivals Bernoulli(q) per (iteration,
+    # worker), the same minibatch schedule; the full training error before
+    # every iteration (err[t] = error of W^t) and after the last
     T3 = 3 * prob.T
     study = {}
     target = None
     for S in (0, 2, 32, 64):
         pS = dataclasses.replace(prob, S=S, T=T3,
-                                 mask=W.arrival_mask(W.seed_of(8), T3, np.full(prob.P, prob.meta["q"])))
+                                 mask=W.arrival_mask(W.seed_of(8), T3, np.full(prob.P, prob.meta["q"])),
+                                 batch=W.batch_schedule(W.seed_of(8), T3, prob.P, prob.K))
         rs = R.MatrixFactorization(pS)
-        rs.run()
+        rs.run(errors=True)
         torch.cuda.synchronize()
-        rm = rs.d_rmse.cpu().numpy()
+        err = rs.d_err.cpu().numpy()[:T3 + 1]
         _, forced, _, _ = rs.plan.stats()
         rs.close()
         if target is None:
-            target = float(rm[prob.T - 1])
-        hit = np.nonzero(rm <= target)[0]
+            target = float(err[prob.T])
+        hit = np.nonzero(err[1:] <= target)[0]
         study[str(S)] = {"iterations_to_target": int(hit[0]) + 1 if hit.size else None,
                          "forced_arrivals_in_%d" % T3: int(forced),
-                         "rmse_at_%d" % prob.T: round(float(rm[prob.T - 1]), 6)}
+                         "error_after_%d" % prob.T: round(float(err[prob.T]), 6)}
     return {"iters": prob.T, "wall": wall, "wall_events": wall_events, "times": times,
             "bytes_per_step": sum(per.values()) * prob.T, "dominant": "mf_grad",
             "dominant_bytes": per["MF_GRAD"], "footprint": footprint, "unit_per_step": prob.T,
-            "extra": {"rmse_after_T": round(rmse_T, 6), "target_rmse": round(target, 6),
+            "extra": {"minibatch_rmse_at_T": round(rmse_T, 6), "target_error": round(target, 6),
+                      "minibatches_per_worker": prob.K, "eta": prob.eta,
                       "slack_study": study,
                       "kernel_bytes": {k: round(v) for k, v in per.items()}}}
 
@@ -632,21 +639,27 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
                 "sample": "%d of %d repetitions, 1 thread (the oracle has no threaded loop here), %.1f s"
                                             % (reps, prob.reps, dt)}
     if cfg == "mf":
-        # worker 0's share of iteration 0: the errors and gradient of its shard
+        # workers' shares of iteration 0, one after another: the errors and
+        # gradient of each worker's minibatch, until the time is used
         from oracle import mf as MFO
-        a, b = prob.shard(0)
-        t0 = time.perf_counter()
         e = np.zeros(prob.N)
-        e[a:b] = MFO.errors(prob, prob.W0, a, b)
-        MFO.worker_gradient(prob, prob.W0, e, 0)
+        t0 = time.perf_counter()
+        done = 0
+        while done < prob.P and (done == 0 or time.perf_counter() - t0 < budget_s):
+            lo, hi = prob.batch_range(done, int(prob.batch[0][done]))
+            e[lo:hi] = MFO.errors(prob, prob.W0, lo, hi)
+            MFO.worker_gradient(prob, prob.W0, e, done, lo, hi)
+            done += 1
         dt = time.perf_counter() - t0
-        # worker 0's share of the index and ratings, the model read, its gradient written
+        # per worker: its share of the index and ratings, the model read,
+        # its gradient written
         rows = prob.n_users + prob.n_items
-        sample_bytes = (24.0 * prob.N + 12.0 * prob.P * rows) / prob.P + 16.0 * prob.m
-        return {"value": round(sample_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
+        per_worker = (24.0 * prob.N / prob.K + 12.0 * prob.P * rows) / prob.P + 16.0 * prob.m
+        return {"value": round(per_worker * done / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
                 "kind": "oracle", "cpu_model": model,
-                "sample": "worker 0's errors and gradient at iteration 0 "
-                                            "(1/%d of the ratings), 1 thread, %.1f s" % (prob.P, dt)}
+                "sample": "the errors and gradients of %d of the %d workers' minibatches at "
+                          "iteration 0 (1/%d of the ratings each), 1 thread, %.1f s"
+                          % (done, prob.P, prob.P * prob.K, dt)}
     if cfg == "threshold":
         from oracle import threshold as THO
         P, m = prob.P, prob.m

@@ -490,45 +490,59 @@ ecc_status_t ecc_allreduce_drop(int32_t P, int64_t m, const double *const *d_fre
                                 void *hip_stream);
 
 /* ---------------------------------------------------------------------------
- * Data-parallel matrix factorisation over the partial allreduce: the
- * workload of the paper's allreduce_SSP experiment (Section IV), P workers,
- * each holding a shard of the ratings and a replica of the model
- * W = [U; V] ((n_users + n_items) rows of `rank` doubles, row-major, U
- * first).  Ratings k < N are (d_users[k], d_items[k], d_ratings[k]); worker
- * p's shard is k in [N p / P, N (p + 1) / P).
+ * Data-parallel matrix factorisation by minibatch stochastic gradient
+ * descent over the partial allreduce: the workload of the paper's
+ * allreduce_SSP experiment (Section IV), P workers, each holding a shard of
+ * the ratings and a replica of the model W = [U; V] ((n_users + n_items)
+ * rows of `rank` doubles, row-major, U first).  Ratings k < N are
+ * (d_users[k], d_items[k], d_ratings[k]); worker p's shard is k in
+ * [N p / P, N (p + 1) / P), of L ratings, and its minibatch b (0 <= b < K)
+ * the shard's ratings [L b / K, L (b + 1) / K).
  * --------------------------------------------------------------------------- */
 
-/* Build the per-worker gradient index on the host, by counting sorts: the
- * ratings of every (worker, row) in shard order, stored as the other
- * factor's row index and the rating value (12 bytes per rating and side),
- * and the rows sorted by their number of ratings (12 bytes per row).  The
- * rating arrays are read once, here; the state keeps its own copy, so the
- * caller may free or change them afterwards.
- * rank: a power of two in [1, 64]; N in [1, 2^30).  ECC_ERR_ARG for bad
- * sizes or an out-of-range user/item index; ECC_ERR_RANGE when
- * P * (n_users + n_items) reaches 2^31; ECC_ERR_ALLOC on allocation
- * failure.  Synchronous. */
-ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32_t P, int64_t N,
-                           const int32_t *d_users, const int32_t *d_items,
+/* Build the gradient index on the host, by counting sorts: for every
+ * (worker, minibatch), the ratings of every row in storage order, stored as
+ * the other factor's row index and the rating value (12 bytes per rating
+ * and side), and the rows of all n_users + n_items entities sorted by their
+ * number of ratings (12 bytes per row: 12 P K (n_users + n_items) bytes in
+ * all).  The state also keeps a copy of the ratings (16 bytes each) for
+ * ecc_mf_error; the caller may free or change its arrays afterwards.
+ * rank: a power of two in [1, 64]; K >= 1 minibatches per shard (1: full
+ * batches); N in [1, 2^30).  ECC_ERR_ARG for bad sizes or an out-of-range
+ * user/item index; ECC_ERR_RANGE when P exceeds 65535 or P K (n_users +
+ * n_items) reaches 2^40; ECC_ERR_ALLOC on allocation failure.  Synchronous. */
+ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32_t P, int32_t K,
+                           int64_t N, const int32_t *d_users, const int32_t *d_items,
                            const double *d_ratings, ecc_mf_t *out);
 ecc_status_t ecc_mf_destroy(ecc_mf_t h);
 
 /* One iteration, enqueued on the plan's stream (the plan has P ranks and
- * carries the slack and the clock):
- *   e_k = r_k - U[u_k] . V[i_k]        (products added for j = 0 .. rank-1);
- *   *d_rmse = sqrt(sum_k e_k^2 / N)    (the error at the model on entry);
- *   d_grads[p] := worker p's gradient of sum over its shard of e_k^2: row
- *     U[u] accumulates (-2 e_k) V[i_k] and row V[i] accumulates (-2 e_k)
- *     U[u_k] over the worker's ratings in shard order (0 for rows without);
+ * carries the slack and the clock); worker p uses minibatch d_batch[p]
+ * (device array of P int32 in [0, K), read on the device; a value outside
+ * is clamped into it):
+ *   e_k = r_k - U[u_k] . V[i_k]        (products added for j = 0 .. rank-1)
+ *     for the ratings of every worker's minibatch;
+ *   *d_rmse = sqrt(sum e_k^2 / (ratings of those minibatches))  (the error
+ *     at the model on entry);
+ *   d_grads[p] := worker p's gradient of the sum over its minibatch of e_k^2:
+ *     row U[u] accumulates (-2 e_k) V[i_k] and row V[i] accumulates
+ *     (-2 e_k) U[u_k] over the minibatch's ratings in storage order (0 for
+ *     rows without);
  *   d_G := ecc_allreduce_partial(plan, m, d_grads, d_slots, ..., d_arrived,
  *     d_eff_out) with m = (n_users + n_items) * rank (stale gradients
  *     substituted from the slots; the plan's clock advances);
- *   W := W - eta * (G * c_row + 2 lam W), c_row = 1 / max(1, ratings of
+ *   W := W - eta * (G * c_row + 2 lam W), c_row = K / max(1, ratings of
  *     the row).
  * d_grads, d_slots: device arrays of P device pointers to m doubles each. */
 ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam, double *d_W,
                             double *const *d_grads, double *const *d_slots, double *d_G,
-                            const uint8_t *d_arrived, double *d_rmse, uint8_t *d_eff_out);
+                            const uint8_t *d_arrived, const int32_t *d_batch, double *d_rmse,
+                            uint8_t *d_eff_out);
+
+/* The training error at model d_W over every rating: *d_rmse = sqrt(sum_k
+ * e_k^2 / N), enqueued on hip_stream.  It shares the state's partial sums
+ * with ecc_mf_iterate: the two must not overlap on different streams. */
+ecc_status_t ecc_mf_error(ecc_mf_t h, const double *d_W, double *d_rmse, void *hip_stream);
 
 /* ---------------------------------------------------------------------------
  * Plain streaming copy d_dst[i] = d_src[i], 0 <= i < n, enqueued on

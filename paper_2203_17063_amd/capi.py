@@ -90,10 +90,12 @@ _SIGS = [
     ("ecc_reduce_threshold", ctypes.c_int, [_I32, _I32, _I64, _D, _I32, _VP, _VP, _VP, _VP,
                                             _VP]),
     ("ecc_allreduce_drop", ctypes.c_int, [_I32, _I64, _VP, _VP, _VP, _VP, _VP]),
-    ("ecc_mf_create", ctypes.c_int, [_I32, _I32, _I32, _I32, _I64, _VP, _VP, _VP,
+    ("ecc_mf_create", ctypes.c_int, [_I32, _I32, _I32, _I32, _I32, _I64, _VP, _VP, _VP,
                                      ctypes.POINTER(_VP)]),
     ("ecc_mf_destroy", ctypes.c_int, [_VP]),
-    ("ecc_mf_iterate", ctypes.c_int, [_VP, _VP, _D, _D, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
+    ("ecc_mf_iterate", ctypes.c_int, [_VP, _VP, _D, _D, _VP, _VP, _VP, _VP, _VP, _VP, _VP,
+                                      _VP]),
+    ("ecc_mf_error", ctypes.c_int, [_VP, _VP, _VP, _VP]),
     ("ecc_solve", ctypes.c_int, [_VP, _VP, _VP, _D, _D, _VP, _VP, _VP, _VP, _I32, _D, _VP, _VP,
                                  _VP, _VP]),
 ]
@@ -354,9 +356,9 @@ def ecc_allreduce_drop(P, m, d_fresh, d_arrived, d_result, d_count=None, stream=
                                     _ptr(d_count), stream))
 
 
-def ecc_mf_create(n_users, n_items, rank, P, N, d_users, d_items, d_ratings) -> int:
+def ecc_mf_create(n_users, n_items, rank, P, K, N, d_users, d_items, d_ratings) -> int:
     out = _VP()
-    _check(lib().ecc_mf_create(n_users, n_items, rank, P, N, _ptr(d_users), _ptr(d_items),
+    _check(lib().ecc_mf_create(n_users, n_items, rank, P, K, N, _ptr(d_users), _ptr(d_items),
                                _ptr(d_ratings), ctypes.byref(out)))
     return out.value
 
@@ -365,7 +367,12 @@ def ecc_mf_destroy(h):
     _check(lib().ecc_mf_destroy(h))
 
 
-def ecc_mf_iterate(h, plan, eta, lam, d_W, d_grads, d_slots, d_G, d_arrived, d_rmse,
+def ecc_mf_iterate(h, plan, eta, lam, d_W, d_grads, d_slots, d_G, d_arrived, d_batch, d_rmse,
                    d_eff_out=None):
     _check(lib().ecc_mf_iterate(h, plan, eta, lam, _ptr(d_W), _ptr(d_grads), _ptr(d_slots),
-                                _ptr(d_G), _ptr(d_arrived), _ptr(d_rmse), _ptr(d_eff_out)))
+                                _ptr(d_G), _ptr(d_arrived), _ptr(d_batch), _ptr(d_rmse),
+                                _ptr(d_eff_out)))
+
+
+def ecc_mf_error(h, d_W, d_rmse, hip_stream=None):
+    _check(lib().ecc_mf_error(h, _ptr(d_W), _ptr(d_rmse), hip_stream))

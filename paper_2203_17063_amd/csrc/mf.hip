@@ -1,29 +1,36 @@
-// Data-parallel matrix factorisation by gradient steps over the eventually
-// consistent partial allreduce: the workload of the paper's allreduce_SSP
-// experiment (Section IV), P workers each holding a shard of the ratings
-// and a replica of the model W = [U; V] (rows of `rank` doubles).
+// Data-parallel matrix factorisation by minibatch stochastic gradient
+// descent over the eventually consistent partial allreduce: the workload of
+// the paper's allreduce_SSP experiment (Section IV), P workers each holding
+// a shard of the ratings, cut into K minibatches of consecutive ratings, and
+// a replica of the model W = [U; V] (rows of `rank` doubles).
 //
-// One iteration, enqueued on the plan's stream:
+// One iteration, enqueued on the plan's stream, worker p using minibatch
+// batch[p] (a device array, so that a schedule can be replayed without the
+// host):
 //  (1) k_mf_grad: every row (p, entity) of every worker's gradient of its
-//      shard's squared error.  For the worker's ratings of that entity, in
-//      shard order, the rating's error e_k = r_k - U[u_k] . V[i_k] (products
-//      added for j = 0 .. rank-1 in order) and then row += (-2 e_k) times the
-//      other factor's row; rows without ratings are 0.  The errors met in
-//      user rows (every rating lies in exactly one) also feed per-workgroup
-//      sums of e_k^2.
+//      minibatch's squared error.  For the minibatch's ratings of that
+//      entity, in storage order, the rating's error e_k = r_k - U[u_k] .
+//      V[i_k] (products added for j = 0 .. rank-1 in order) and then
+//      row += (-2 e_k) times the other factor's row; rows without ratings in
+//      the minibatch are 0.  The errors met in user rows (every rating lies in
+//      exactly one) also feed per-workgroup sums of e_k^2.
 //  (2) the partial allreduce of the workers' gradients (ecc_allreduce_partial:
 //      staleness decision, stale gradients substituted from the slots);
-//  (3) k_mf_rmse: sqrt(sum e_k^2 / N) from the workgroup sums in a fixed
-//      order; k_mf_step: W := W - eta * (G * c_row + 2 lam W), c_row = 1 /
-//      (number of ratings of the row, at least 1).
+//  (3) k_mf_rmse: sqrt(sum e_k^2 / ratings used) from the workgroup sums in a
+//      fixed order; k_mf_step: W := W - eta * (G * c_row + 2 lam W), c_row =
+//      K / (number of ratings of the row, at least 1).
+// ecc_mf_error evaluates sqrt(sum e_k^2 / N) over all ratings at a model.
 //
-// The gradient index is built once, on the host: the ratings of each row in
-// shard order (other factor's row index and rating value, stored in that
-// order), and the rows sorted by their number of ratings, longest first.
+// The gradient index is built once, on the host, for every (worker,
+// minibatch): the ratings of each row in storage order (other factor's row
+// index and rating value, stored in that order), and every entity's row in
+// order of its number of ratings, longest first.  The gradient kernel's
+// grid is two-dimensional: blockIdx.y is the worker, whose workgroups walk
+// the rows of its minibatch's list.
 //  - A row of more than kMfHeavy ratings takes a whole workgroup: chunks of
 //    its ratings are spread over the workgroup, whose lane groups compute
 //    the errors and products into LDS, and then `rank` lanes add the
-//    products in shard order.  The longest rows (thousands of ratings for
+//    products in storage order.  The longest rows (hundreds of ratings for
 //    the most popular items) thus wait on a few memory latencies per chunk
 //    instead of a serial chain of loads per rating.
 //  - Other rows take a group of rank / 4 lanes (4 columns each; one lane
@@ -61,17 +68,18 @@ struct MfShape {
 struct MfGradArgs {
     int32_t n_users;
     int64_t E;                    // n_users + n_items
+    int32_t K;                    // minibatches per worker
     const double *W;              // [U; V]
-    const int32_t *oidx;          // [2N] other factor's row, ratings of each row in shard order
+    const int32_t *oidx;          // [2N] other factor's row, ratings of each row in storage order
     const double *rv;             // [2N] rating values, same order
-    const int32_t *row_of;        // [n_rows] rows (p * E + entity), longest first
-    const int32_t *start_of;      // [n_rows] first rating of that row in oidx / rv
-    const int32_t *len_of;        // [n_rows] its number of ratings
-    int64_t n_rows;
-    int64_t n_heavy;              // the first n_heavy rows take a workgroup each
-    int64_t n_work;               // n_heavy + light items of GROUPS rows
+    const int32_t *row_of;        // [P K E] entity of each row of each (worker, minibatch)
+                                  // list, longest first
+    const int32_t *start_of;      // same order: first rating of that row in oidx / rv
+    const int32_t *len_of;        // same order: its number of ratings
+    const int32_t *n_heavy;       // [P K] rows of more than kMfHeavy ratings, per list
+    const int32_t *batch;         // [P] this iteration's minibatch of each worker
     double *const *grads;         // [P] -> m doubles
-    double *partials;             // [gridDim.x] sums of e^2 over user rows
+    double *partials;             // [gridDim.y][gridDim.x] sums of e^2 over user rows
 };
 
 // own . other over a lane group: lane l holds columns l*C .. l*C + C-1 of
@@ -95,11 +103,10 @@ __device__ __forceinline__ double mf_dot(const double (&ow)[MfShape<R>::C],
 // One light row on the lane group (lane = column block); returns the lane's
 // sum of e^2 (user rows, lane 0 only).
 template <int R>
-__device__ __forceinline__ double mf_light_row(const MfGradArgs &a, int32_t row, int32_t x0,
-                                               int32_t len, int lane) {
+__device__ __forceinline__ double mf_light_row(const MfGradArgs &a, int32_t p, int32_t ent,
+                                               int32_t x0, int32_t len, int lane) {
     constexpr int C = MfShape<R>::C, K = kMfBatch;
-    const int32_t p = (int32_t)(row / a.E);
-    const int64_t e = row - (int64_t)p * a.E;
+    const int64_t e = ent;
     const bool user = e < a.n_users;
     const double *own = a.W + e * R + lane * C;
     const double *other = (user ? a.W + (int64_t)a.n_users * R : a.W) + lane * C;
@@ -152,13 +159,12 @@ __device__ __forceinline__ double mf_light_row(const MfGradArgs &a, int32_t row,
 
 // One heavy row on the whole workgroup; returns the thread's sum of e^2.
 template <int R>
-__device__ __forceinline__ double mf_heavy_row(const MfGradArgs &a, int32_t row, int32_t x0,
-                                               int32_t len, double *s_prod) {
+__device__ __forceinline__ double mf_heavy_row(const MfGradArgs &a, int32_t p, int32_t ent,
+                                               int32_t x0, int32_t len, double *s_prod) {
     constexpr int LPR = MfShape<R>::LPR, C = MfShape<R>::C, NG = MfShape<R>::GROUPS;
     constexpr int CH = MfShape<R>::CHUNK, J = MfShape<R>::J;
     const int tid = threadIdx.x, lane = tid % LPR, grp = tid / LPR;
-    const int32_t p = (int32_t)(row / a.E);
-    const int64_t e = row - (int64_t)p * a.E;
+    const int64_t e = ent;
     const bool user = e < a.n_users;
     const double *own = a.W + e * R + lane * C;
     const double *other = (user ? a.W + (int64_t)a.n_users * R : a.W) + lane * C;
@@ -211,43 +217,52 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfGradArgs a) {
     constexpr int LPR = MfShape<R>::LPR, G = MfShape<R>::GROUPS;
     static_assert(MfShape<R>::CHUNK * R == kMfStage, "a heavy chunk fills the stage");
     const int lane = threadIdx.x % LPR, grp = threadIdx.x / LPR;
+    // worker p's list for its minibatch of this iteration
+    const int32_t p = blockIdx.y;
+    const int32_t bp = min(max(a.batch[p], 0), a.K - 1);  // (values outside [0, K) clamped)
+    const int64_t list = (int64_t)p * a.K + bp;
+    const int32_t *row_of = a.row_of + list * a.E;
+    const int32_t *start_of = a.start_of + list * a.E;
+    const int32_t *len_of = a.len_of + list * a.E;
+    const int64_t n_rows = a.E, n_heavy = a.n_heavy[list];
+    const int64_t n_work = n_heavy + (n_rows - n_heavy + G - 1) / G;
     double sq = 0.0;
     // this lane group's row in a light item w (descriptors one item ahead)
-    auto light_q = [&](int64_t w) { return a.n_heavy + (w - a.n_heavy) * G + grp; };
+    auto light_q = [&](int64_t w) { return n_heavy + (w - n_heavy) * G + grp; };
     int32_t nrow = 0, nx0 = 0, nlen = -1;
     int64_t w = blockIdx.x;
-    if (w < a.n_work && w >= a.n_heavy && light_q(w) < a.n_rows) {
+    if (w < n_work && w >= n_heavy && light_q(w) < n_rows) {
         const int64_t q = light_q(w);
-        nrow = a.row_of[q];
-        nx0 = a.start_of[q];
-        nlen = a.len_of[q];
+        nrow = row_of[q];
+        nx0 = start_of[q];
+        nlen = len_of[q];
     }
-    for (; w < a.n_work; w += gridDim.x) {
-        if (w < a.n_heavy) {
-            sq += mf_heavy_row<R>(a, a.row_of[w], a.start_of[w], a.len_of[w], s_prod);
+    for (; w < n_work; w += gridDim.x) {
+        if (w < n_heavy) {
+            sq += mf_heavy_row<R>(a, p, row_of[w], start_of[w], len_of[w], s_prod);
             const int64_t wn = w + gridDim.x;
             nlen = -1;
-            if (wn < a.n_work && wn >= a.n_heavy && light_q(wn) < a.n_rows) {
+            if (wn < n_work && wn >= n_heavy && light_q(wn) < n_rows) {
                 const int64_t q = light_q(wn);
-                nrow = a.row_of[q];
-                nx0 = a.start_of[q];
-                nlen = a.len_of[q];
+                nrow = row_of[q];
+                nx0 = start_of[q];
+                nlen = len_of[q];
             }
             continue;
         }
         const int32_t row = nrow, x0 = nx0, len = nlen;
         const int64_t wn = w + gridDim.x;
         nlen = -1;
-        if (wn < a.n_work && light_q(wn) < a.n_rows) {
+        if (wn < n_work && light_q(wn) < n_rows) {
             const int64_t q = light_q(wn);
-            nrow = a.row_of[q];
-            nx0 = a.start_of[q];
-            nlen = a.len_of[q];
+            nrow = row_of[q];
+            nx0 = start_of[q];
+            nlen = len_of[q];
         }
-        if (len >= 0) sq += mf_light_row<R>(a, row, x0, len, lane);
+        if (len >= 0) sq += mf_light_row<R>(a, p, row, x0, len, lane);
     }
     const double tot = block_sum<kMfThreads>(sq, s_red);
-    if (threadIdx.x == 0) a.partials[blockIdx.x] = tot;
+    if (threadIdx.x == 0) a.partials[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = tot;
 }
 
 __global__ __launch_bounds__(kMfThreads) void k_mf_step(int64_t m, int log2r, double eta,
@@ -262,12 +277,58 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_step(int64_t m, int log2r, do
     }
 }
 
+// sqrt(sum / count): the n partial sums of e^2 reduced in a fixed order,
+// over the ratings of the minibatches used (sizes[p K + batch[p]] for each
+// worker), or over N ratings when batch is NULL.
 __global__ __launch_bounds__(kNormThreads) void k_mf_rmse(const double *__restrict__ partials,
-                                                          int64_t n, int64_t N,
+                                                          int64_t n, int64_t N, int32_t P,
+                                                          int32_t K,
+                                                          const int32_t *__restrict__ batch,
+                                                          const int64_t *__restrict__ sizes,
                                                           double *__restrict__ out) {
     __shared__ double s_red[kNormThreads / 64];
     const double sum = reduce_values(partials, n, false, 0.0, s_red);
-    if (threadIdx.x == 0) *out = sqrt(sum / (double)N);
+    if (threadIdx.x == 0) {
+        int64_t cnt = N;
+        if (batch) {
+            cnt = 0;
+            for (int32_t p = 0; p < P; ++p) cnt += sizes[(int64_t)p * K + min(max(batch[p], 0), K - 1)];
+        }
+        *out = cnt > 0 ? sqrt(sum / (double)cnt) : 0.0;
+    }
+}
+
+// Errors of every rating at W, one lane group per rating (products in
+// column order as in the gradient kernel): per-workgroup sums of e^2.
+template <int R>
+__global__ __launch_bounds__(kMfThreads) void k_mf_error(int64_t N, int32_t n_users,
+                                                         const int32_t *__restrict__ users,
+                                                         const int32_t *__restrict__ items,
+                                                         const double *__restrict__ ratings,
+                                                         const double *__restrict__ W,
+                                                         double *__restrict__ partials) {
+    __shared__ double s_red[kMfThreads / 64];
+    constexpr int LPR = MfShape<R>::LPR, C = MfShape<R>::C, G = MfShape<R>::GROUPS;
+    const int lane = threadIdx.x % LPR, grp = threadIdx.x / LPR;
+    double sq = 0.0;
+    for (int64_t k0 = (int64_t)blockIdx.x * G; k0 < N; k0 += (int64_t)gridDim.x * G) {
+        const int64_t k = k0 + grp;
+        const bool live = k < N;
+        double ow[C], o[C];
+        const int64_t u = live ? users[k] : 0, i = live ? items[k] : 0;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            ow[c] = live ? W[u * R + lane * C + c] : 0.0;
+            o[c] = live ? W[((int64_t)n_users + i) * R + lane * C + c] : 0.0;
+        }
+        const double d = mf_dot<R>(ow, o);
+        if (live && lane == 0) {
+            const double err = ratings[k] - d;
+            sq = sq + err * err;
+        }
+    }
+    const double tot = block_sum<kMfThreads>(sq, s_red);
+    if (threadIdx.x == 0) partials[blockIdx.x] = tot;
 }
 
 int32_t mf_grid(int64_t work, int per_cu) {
@@ -283,17 +344,21 @@ int32_t mf_grid(int64_t work, int per_cu) {
 using namespace ecc;
 
 struct ecc_mf_s {
-    int32_t n_users = 0, n_items = 0, rank = 0, P = 0;
+    int32_t n_users = 0, n_items = 0, rank = 0, P = 0, K = 1;
     int64_t N = 0;
-    int32_t *d_oidx = nullptr;      // [2N] other factor's row, ratings of each row in shard order
+    int32_t *d_oidx = nullptr;      // [2N] other factor's row, ratings of each row in storage order
     double *d_rv = nullptr;         // [2N] rating values, same order
-    int32_t *d_row_of = nullptr;    // [P * (n_users + n_items)] rows, longest first
+    int32_t *d_row_of = nullptr;    // [P K E] entity of each row of each list, longest first
     int32_t *d_start_of = nullptr;  // same order: first rating in d_oidx / d_rv
     int32_t *d_len_of = nullptr;    // same order: number of ratings
-    int64_t n_heavy = 0;            // rows of more than kMfHeavy ratings
-    double *d_scale = nullptr;      // [n_users + n_items]
-    double *d_partials = nullptr;   // [grad_grid]
-    int32_t grad_grid = 1, step_grid = 1;
+    int32_t *d_n_heavy = nullptr;   // [P K] rows of more than kMfHeavy ratings, per list
+    int64_t *d_sizes = nullptr;     // [P K] ratings of each minibatch
+    int32_t *d_users = nullptr;     // [N] copies of the ratings, for ecc_mf_error
+    int32_t *d_items = nullptr;
+    double *d_ratings = nullptr;
+    double *d_scale = nullptr;      // [n_users + n_items]: K / ratings of the row
+    double *d_partials = nullptr;   // [max(grad_grid * P, err_grid)]
+    int32_t grad_grid = 1, step_grid = 1, err_grid = 1;
 };
 
 extern "C" {
@@ -306,15 +371,21 @@ ecc_status_t ecc_mf_destroy(ecc_mf_t h) {
     (void)hipFree(h->d_row_of);
     (void)hipFree(h->d_start_of);
     (void)hipFree(h->d_len_of);
+    (void)hipFree(h->d_n_heavy);
+    (void)hipFree(h->d_sizes);
+    (void)hipFree(h->d_users);
+    (void)hipFree(h->d_items);
+    (void)hipFree(h->d_ratings);
     (void)hipFree(h->d_scale);
     (void)hipFree(h->d_partials);
     delete h;
     return ECC_OK;
 }
 
-static ecc_status_t ecc_mf_create_impl(int32_t n_users, int32_t n_items, int32_t rank, int32_t P, int64_t N,
-                           const int32_t *d_users, const int32_t *d_items,
-                           const double *d_ratings, ecc_mf_t *out) {
+static ecc_status_t ecc_mf_create_impl(int32_t n_users, int32_t n_items, int32_t rank, int32_t P,
+                                       int32_t K, int64_t N, const int32_t *d_users,
+                                       const int32_t *d_items, const double *d_ratings,
+                                       ecc_mf_t *out) {
     clear_error();
     ECC_ARG(out != nullptr, "out is NULL");
     *out = nullptr;
@@ -322,12 +393,13 @@ static ecc_status_t ecc_mf_create_impl(int32_t n_users, int32_t n_items, int32_t
     ECC_ARG(rank >= 1 && rank <= kMfMaxRank && (rank & (rank - 1)) == 0,
             "rank = %d must be a power of two in [1, 64]", rank);
     ECC_ARG(P >= 1, "P must be >= 1");
+    ECC_ARG(K >= 1, "K must be >= 1");
     ECC_ARG(N >= 1 && 2 * N < (int64_t(1) << 31), "N must lie in [1, 2^30)");
     ECC_ARG(d_users && d_items && d_ratings, "NULL rating arrays");
     const int64_t E = (int64_t)n_users + n_items;
-    const int64_t n_rows = (int64_t)P * E;
-    if (n_rows + 1 >= (int64_t(1) << 31)) {
-        set_error("P * (n_users + n_items) too large");
+    const int64_t n_lists = (int64_t)P * K;
+    if (n_lists * E >= (int64_t(1) << 40) || P > 65535) {
+        set_error("P * K * (n_users + n_items) too large");
         return ECC_ERR_RANGE;
     }
     std::vector<int32_t> users(N), items(N);
@@ -342,64 +414,73 @@ static ecc_status_t ecc_mf_create_impl(int32_t n_users, int32_t n_items, int32_t
         ++cnt[users[k]];
         ++cnt[(int64_t)n_users + items[k]];
     }
-    // rows (p, entity): users then items of worker p; their ratings in shard
-    // order (counting sort), stored as the other factor's row and the value
-    std::vector<int32_t> rp(n_rows + 1, 0), oidx(2 * N);
+    // For every (worker p, minibatch b): the rows of all E entities, their
+    // ratings of the minibatch in storage order (counting sort), stored as
+    // the other factor's row and the value; then the rows by number of
+    // ratings, longest first (rows of equal length in entity order): heavy
+    // rows by a sort, the rest by a counting sort.
+    std::vector<int32_t> oidx(2 * N), row_of(n_lists * E), start_of(n_lists * E),
+        len_of(n_lists * E), n_heavy(n_lists);
+    std::vector<int64_t> sizes(n_lists);
     std::vector<double> rv(2 * N);
-    std::vector<int32_t> fill(E);
+    std::vector<int32_t> rp(E + 1), fill(E), heavy, by_len(kMfHeavy + 2);
+    std::vector<int64_t> slot(kMfHeavy + 1);
     int64_t pos = 0;
     for (int32_t p = 0; p < P; ++p) {
-        const int64_t a = N * p / P, b = N * (p + 1) / P;
-        std::fill(fill.begin(), fill.end(), 0);
-        for (int64_t k = a; k < b; ++k) {
-            ++fill[users[k]];
-            ++fill[(int64_t)n_users + items[k]];
+        const int64_t a = N * p / P, c = N * (p + 1) / P, L = c - a;
+        for (int32_t b = 0; b < K; ++b) {
+            const int64_t lo = a + L * b / K, hi = a + L * (b + 1) / K;
+            const int64_t list = (int64_t)p * K + b;
+            sizes[list] = hi - lo;
+            std::fill(fill.begin(), fill.end(), 0);
+            for (int64_t k = lo; k < hi; ++k) {
+                ++fill[users[k]];
+                ++fill[(int64_t)n_users + items[k]];
+            }
+            for (int64_t e = 0; e < E; ++e) {
+                rp[e] = (int32_t)pos;
+                pos += fill[e];
+                fill[e] = rp[e];
+            }
+            rp[E] = (int32_t)pos;
+            for (int64_t k = lo; k < hi; ++k) {
+                const int32_t xu = fill[users[k]]++;
+                const int32_t xi = fill[(int64_t)n_users + items[k]]++;
+                oidx[xu] = items[k];
+                rv[xu] = ratings[k];
+                oidx[xi] = users[k];
+                rv[xi] = ratings[k];
+            }
+            heavy.clear();
+            std::fill(by_len.begin(), by_len.end(), 0);
+            for (int64_t e = 0; e < E; ++e) {
+                const int32_t len = rp[e + 1] - rp[e];
+                if (len > kMfHeavy) heavy.push_back((int32_t)e);
+                else ++by_len[len];
+            }
+            std::stable_sort(heavy.begin(), heavy.end(), [&](int32_t x, int32_t y) {
+                return rp[x + 1] - rp[x] > rp[y + 1] - rp[y];
+            });
+            int32_t *ro = row_of.data() + list * E;
+            int64_t next = (int64_t)heavy.size();
+            for (int32_t len = kMfHeavy; len >= 0; --len) {
+                slot[len] = next;
+                next += by_len[len];
+            }
+            for (size_t j = 0; j < heavy.size(); ++j) ro[j] = heavy[j];
+            for (int64_t e = 0; e < E; ++e) {
+                const int32_t len = rp[e + 1] - rp[e];
+                if (len <= kMfHeavy) ro[slot[len]++] = (int32_t)e;
+            }
+            for (int64_t q = 0; q < E; ++q) {
+                start_of[list * E + q] = rp[ro[q]];
+                len_of[list * E + q] = rp[ro[q] + 1] - rp[ro[q]];
+            }
+            n_heavy[list] = (int32_t)heavy.size();
         }
-        const int64_t base = (int64_t)p * E;
-        for (int64_t e = 0; e < E; ++e) {
-            rp[base + e] = (int32_t)pos;
-            pos += fill[e];
-            fill[e] = rp[base + e];
-        }
-        for (int64_t k = a; k < b; ++k) {
-            const int32_t xu = fill[users[k]]++;
-            const int32_t xi = fill[(int64_t)n_users + items[k]]++;
-            oidx[xu] = items[k];
-            rv[xu] = ratings[k];
-            oidx[xi] = users[k];
-            rv[xi] = ratings[k];
-        }
-    }
-    rp[n_rows] = (int32_t)pos;
-    // rows by number of ratings, longest first (rows of equal length in row
-    // order): heavy rows by a sort, the rest by a counting sort
-    std::vector<int32_t> heavy, by_len(kMfHeavy + 2, 0);
-    for (int64_t r = 0; r < n_rows; ++r) {
-        const int32_t len = rp[r + 1] - rp[r];
-        if (len > kMfHeavy) heavy.push_back((int32_t)r);
-        else ++by_len[len];
-    }
-    std::stable_sort(heavy.begin(), heavy.end(), [&](int32_t x, int32_t y) {
-        return rp[x + 1] - rp[x] > rp[y + 1] - rp[y];
-    });
-    std::vector<int32_t> row_of(n_rows), start_of(n_rows), len_of(n_rows);
-    int64_t next = (int64_t)heavy.size();
-    std::vector<int64_t> slot(kMfHeavy + 1);
-    for (int32_t len = kMfHeavy; len >= 0; --len) {
-        slot[len] = next;
-        next += by_len[len];
-    }
-    for (size_t j = 0; j < heavy.size(); ++j) row_of[j] = heavy[j];
-    for (int64_t r = 0; r < n_rows; ++r) {
-        const int32_t len = rp[r + 1] - rp[r];
-        if (len <= kMfHeavy) row_of[slot[len]++] = (int32_t)r;
-    }
-    for (int64_t q = 0; q < n_rows; ++q) {
-        start_of[q] = rp[row_of[q]];
-        len_of[q] = rp[row_of[q] + 1] - rp[row_of[q]];
     }
     std::vector<double> scale(E);
-    for (int64_t e = 0; e < E; ++e) scale[e] = 1.0 / (double)std::max<int64_t>(1, cnt[e]);
+    for (int64_t e = 0; e < E; ++e) scale[e] = (double)K / (double)std::max<int64_t>(1, cnt[e]);
 
     ecc_mf_s *h = new (std::nothrow) ecc_mf_s();
     if (!h) {
@@ -410,58 +491,72 @@ static ecc_status_t ecc_mf_create_impl(int32_t n_users, int32_t n_items, int32_t
     h->n_items = n_items;
     h->rank = rank;
     h->P = P;
+    h->K = K;
     h->N = N;
-    h->n_heavy = (int64_t)heavy.size();
+    // a worker's workgroups: its share of what the device holds at once
+    // (8 per CU), at least 1
     const int64_t groups = kMfThreads / (rank < 4 ? 1 : rank / 4);
-    const int64_t n_work = h->n_heavy + (n_rows - h->n_heavy + groups - 1) / groups;
-    h->grad_grid = mf_grid(n_work, 8);
+    h->grad_grid = std::max<int32_t>(1, mf_grid((E + groups - 1) / groups, 8) / P);
     h->step_grid = mf_grid((E * rank + kMfThreads - 1) / kMfThreads, 8);
+    h->err_grid = mf_grid((N + groups - 1) / groups, 8);
+    const int64_t n_part = std::max<int64_t>((int64_t)h->grad_grid * P, h->err_grid);
     auto fail = [&](const char *what) {
         set_error("%s", what);
         ecc_mf_destroy(h);
         return ECC_ERR_ALLOC;
     };
-    if (hipMalloc((void **)&h->d_oidx, sizeof(int32_t) * 2 * N) != hipSuccess ||
-        hipMalloc((void **)&h->d_rv, sizeof(double) * 2 * N) != hipSuccess ||
-        hipMalloc((void **)&h->d_row_of, sizeof(int32_t) * n_rows) != hipSuccess ||
-        hipMalloc((void **)&h->d_start_of, sizeof(int32_t) * n_rows) != hipSuccess ||
-        hipMalloc((void **)&h->d_len_of, sizeof(int32_t) * n_rows) != hipSuccess ||
-        hipMalloc((void **)&h->d_scale, sizeof(double) * E) != hipSuccess ||
-        hipMalloc((void **)&h->d_partials, sizeof(double) * h->grad_grid) != hipSuccess)
-        return fail("hipMalloc of the factorisation state failed");
-    if (hipMemcpy(h->d_oidx, oidx.data(), sizeof(int32_t) * 2 * N, hipMemcpyHostToDevice) !=
-            hipSuccess ||
-        hipMemcpy(h->d_rv, rv.data(), sizeof(double) * 2 * N, hipMemcpyHostToDevice) !=
-            hipSuccess ||
-        hipMemcpy(h->d_row_of, row_of.data(), sizeof(int32_t) * n_rows, hipMemcpyHostToDevice) !=
-            hipSuccess ||
-        hipMemcpy(h->d_start_of, start_of.data(), sizeof(int32_t) * n_rows,
-                  hipMemcpyHostToDevice) != hipSuccess ||
-        hipMemcpy(h->d_len_of, len_of.data(), sizeof(int32_t) * n_rows, hipMemcpyHostToDevice) !=
-            hipSuccess ||
-        hipMemcpy(h->d_scale, scale.data(), sizeof(double) * E, hipMemcpyHostToDevice) !=
-            hipSuccess)
-        return fail("upload of the factorisation state failed");
+    auto up = [&](void **dst, const void *src, size_t bytes) {
+        if (hipMalloc(dst, std::max<size_t>(bytes, 8)) != hipSuccess) return false;
+        return hipMemcpy(*dst, src, bytes, hipMemcpyHostToDevice) == hipSuccess;
+    };
+    if (!up((void **)&h->d_oidx, oidx.data(), sizeof(int32_t) * 2 * N) ||
+        !up((void **)&h->d_rv, rv.data(), sizeof(double) * 2 * N) ||
+        !up((void **)&h->d_row_of, row_of.data(), sizeof(int32_t) * n_lists * E) ||
+        !up((void **)&h->d_start_of, start_of.data(), sizeof(int32_t) * n_lists * E) ||
+        !up((void **)&h->d_len_of, len_of.data(), sizeof(int32_t) * n_lists * E) ||
+        !up((void **)&h->d_n_heavy, n_heavy.data(), sizeof(int32_t) * n_lists) ||
+        !up((void **)&h->d_sizes, sizes.data(), sizeof(int64_t) * n_lists) ||
+        !up((void **)&h->d_users, users.data(), sizeof(int32_t) * N) ||
+        !up((void **)&h->d_items, items.data(), sizeof(int32_t) * N) ||
+        !up((void **)&h->d_ratings, ratings.data(), sizeof(double) * N) ||
+        !up((void **)&h->d_scale, scale.data(), sizeof(double) * E))
+        return fail("allocating or uploading the factorisation state failed");
+    if (hipMalloc((void **)&h->d_partials, sizeof(double) * n_part) != hipSuccess)
+        return fail("hipMalloc of the partial sums failed");
     *out = h;
     return ECC_OK;
 }
 
 // Host allocations of the set-up throw std::bad_alloc when memory runs
 // out: the C ABI reports ECC_ERR_ALLOC instead of letting it escape.
-ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32_t P, int64_t N,
-                           const int32_t *d_users, const int32_t *d_items,
+ecc_status_t ecc_mf_create(int32_t n_users, int32_t n_items, int32_t rank, int32_t P, int32_t K,
+                           int64_t N, const int32_t *d_users, const int32_t *d_items,
                            const double *d_ratings, ecc_mf_t *out) {
     try {
-        return ecc_mf_create_impl(n_users, n_items, rank, P, N, d_users, d_items, d_ratings, out);
+        return ecc_mf_create_impl(n_users, n_items, rank, P, K, N, d_users, d_items, d_ratings,
+                                  out);
     } catch (const std::bad_alloc &) {
         set_error("host allocation failed");
         return ECC_ERR_ALLOC;
     }
 }
 
+#define ECC_MF_RANKS(KERNEL, GRID, ...)                                              \
+    switch (h->rank) {                                                               \
+        case 1: hipLaunchKernelGGL(KERNEL<1>, GRID, dim3(kMfThreads), 0, s, __VA_ARGS__); break;   \
+        case 2: hipLaunchKernelGGL(KERNEL<2>, GRID, dim3(kMfThreads), 0, s, __VA_ARGS__); break;   \
+        case 4: hipLaunchKernelGGL(KERNEL<4>, GRID, dim3(kMfThreads), 0, s, __VA_ARGS__); break;   \
+        case 8: hipLaunchKernelGGL(KERNEL<8>, GRID, dim3(kMfThreads), 0, s, __VA_ARGS__); break;   \
+        case 16: hipLaunchKernelGGL(KERNEL<16>, GRID, dim3(kMfThreads), 0, s, __VA_ARGS__); break; \
+        case 32: hipLaunchKernelGGL(KERNEL<32>, GRID, dim3(kMfThreads), 0, s, __VA_ARGS__); break; \
+        case 64: hipLaunchKernelGGL(KERNEL<64>, GRID, dim3(kMfThreads), 0, s, __VA_ARGS__); break; \
+        default: set_error("internal: rank %d", h->rank); return ECC_ERR_STATE;      \
+    }
+
 ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam, double *d_W,
                             double *const *d_grads, double *const *d_slots, double *d_G,
-                            const uint8_t *d_arrived, double *d_rmse, uint8_t *d_eff_out) {
+                            const uint8_t *d_arrived, const int32_t *d_batch, double *d_rmse,
+                            uint8_t *d_eff_out) {
     clear_error();
     ECC_ARG(h != nullptr, "factorisation state is NULL");
     ecc_status_t st = check_plan(plan);
@@ -470,43 +565,30 @@ ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam,
         set_error("plan has %d ranks, the factorisation %d workers", plan->P, h->P);
         return ECC_ERR_STATE;
     }
-    ECC_ARG(d_W && d_grads && d_slots && d_G && d_arrived && d_rmse, "NULL argument");
+    ECC_ARG(d_W && d_grads && d_slots && d_G && d_arrived && d_batch && d_rmse, "NULL argument");
     hipStream_t s = plan->stream;
     const int64_t E = (int64_t)h->n_users + h->n_items;
-    const int64_t n_rows = (int64_t)h->P * E;
     const int64_t m = E * h->rank;
     int log2r = 0;
     while ((1 << log2r) < h->rank) ++log2r;
-    const int64_t groups = kMfThreads / (h->rank < 4 ? 1 : h->rank / 4);
     MfGradArgs ga{};
     ga.n_users = h->n_users;
     ga.E = E;
+    ga.K = h->K;
     ga.W = d_W;
     ga.oidx = h->d_oidx;
     ga.rv = h->d_rv;
     ga.row_of = h->d_row_of;
     ga.start_of = h->d_start_of;
     ga.len_of = h->d_len_of;
-    ga.n_rows = n_rows;
-    ga.n_heavy = h->n_heavy;
-    ga.n_work = h->n_heavy + (n_rows - h->n_heavy + groups - 1) / groups;
+    ga.n_heavy = h->d_n_heavy;
+    ga.batch = d_batch;
     ga.grads = d_grads;
     ga.partials = h->d_partials;
     {
         TimedLaunch timed(plan, ECC_TIMING_MF_GRAD);
-        const dim3 grid(h->grad_grid), block(kMfThreads);
-        switch (h->rank) {
-            case 1: hipLaunchKernelGGL(k_mf_grad<1>, grid, block, 0, s, ga); break;
-            case 2: hipLaunchKernelGGL(k_mf_grad<2>, grid, block, 0, s, ga); break;
-            case 4: hipLaunchKernelGGL(k_mf_grad<4>, grid, block, 0, s, ga); break;
-            case 8: hipLaunchKernelGGL(k_mf_grad<8>, grid, block, 0, s, ga); break;
-            case 16: hipLaunchKernelGGL(k_mf_grad<16>, grid, block, 0, s, ga); break;
-            case 32: hipLaunchKernelGGL(k_mf_grad<32>, grid, block, 0, s, ga); break;
-            case 64: hipLaunchKernelGGL(k_mf_grad<64>, grid, block, 0, s, ga); break;
-            default:
-                set_error("internal: rank %d", h->rank);
-                return ECC_ERR_STATE;
-        }
+        const dim3 grid(h->grad_grid, h->P);
+        ECC_MF_RANKS(k_mf_grad, grid, ga)
         ECC_LAUNCH_CHECK();
     }
     st = ecc_allreduce_partial(plan, m, d_grads, d_slots, d_G, d_arrived, d_eff_out, nullptr);
@@ -514,10 +596,25 @@ ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam,
     {
         TimedLaunch timed(plan, ECC_TIMING_MF_STEP);
         hipLaunchKernelGGL(k_mf_rmse, dim3(1), dim3(kNormThreads), 0, s, h->d_partials,
-                           (int64_t)h->grad_grid, h->N, d_rmse);
+                           (int64_t)h->grad_grid * h->P, h->N, h->P, h->K, d_batch, h->d_sizes,
+                           d_rmse);
         hipLaunchKernelGGL(k_mf_step, dim3(h->step_grid), dim3(kMfThreads), 0, s, m, log2r, eta,
                            2.0 * lam, d_G, h->d_scale, d_W);
     }
+    ECC_LAUNCH_CHECK();
+    return ECC_OK;
+}
+
+ecc_status_t ecc_mf_error(ecc_mf_t h, const double *d_W, double *d_rmse, void *hip_stream) {
+    clear_error();
+    ECC_ARG(h != nullptr, "factorisation state is NULL");
+    ECC_ARG(d_W && d_rmse, "NULL argument");
+    hipStream_t s = (hipStream_t)hip_stream;
+    ECC_MF_RANKS(k_mf_error, dim3(h->err_grid), h->N, h->n_users, h->d_users, h->d_items,
+                 h->d_ratings, d_W, h->d_partials)
+    ECC_LAUNCH_CHECK();
+    hipLaunchKernelGGL(k_mf_rmse, dim3(1), dim3(kNormThreads), 0, s, h->d_partials,
+                       (int64_t)h->err_grid, h->N, h->P, h->K, nullptr, nullptr, d_rmse);
     ECC_LAUNCH_CHECK();
     return ECC_OK;
 }

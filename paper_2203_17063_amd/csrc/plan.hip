@@ -104,7 +104,7 @@ using namespace ecc;
 
 extern "C" {
 
-int32_t ecc_abi_version(void) { return 1; }
+int32_t ecc_abi_version(void) { return 2; }
 
 const char *ecc_last_error(void) { return g_err; }
 

@@ -153,26 +153,37 @@ class MatrixFactorization:
         self.d_slots = ptr_array(self.slots, device)
         self.d_G = torch.empty(m, dtype=torch.float64, device=device)
         self.d_mask = _dev(np.asarray(prob.mask, dtype=np.uint8), device=device)
+        self.d_batch = _dev(np.asarray(prob.batch, dtype=np.int32), device=device)
         self.d_rmse = torch.zeros(max(prob.T, 1), dtype=torch.float64, device=device)
+        self.d_err = torch.zeros(max(prob.T, 1) + 1, dtype=torch.float64, device=device)
         self.d_eff = torch.zeros((max(prob.T, 1), P), dtype=torch.uint8, device=device)
         self.plan = Plan(P, None, None, prob.S)
-        self.handle = E.ecc_mf_create(prob.n_users, prob.n_items, prob.rank, P, prob.N,
+        self.handle = E.ecc_mf_create(prob.n_users, prob.n_items, prob.rank, P, prob.K, prob.N,
                                       self.d_users, self.d_items, self.d_ratings)
 
     def reset(self):
         self.plan.reset()
         self.d_W.copy_(self.d_W0)
 
-    def iterate(self, t, record=True):
+    def iterate(self, t, record=True, error=False):
+        """Iteration t; with error, also the full training error at the model
+        on entry into d_err[t]."""
+        if error:
+            E.ecc_mf_error(self.handle, self.d_W, self.d_err[t].data_ptr(), current_stream())
         E.ecc_mf_iterate(self.handle, self.plan.handle, self.prob.eta, self.prob.lam, self.d_W,
                          self.d_grads, self.d_slots, self.d_G, self.d_mask[t].data_ptr(),
-                         self.d_rmse[t].data_ptr(), self.d_eff[t] if record else None)
+                         self.d_batch[t].data_ptr(), self.d_rmse[t].data_ptr(),
+                         self.d_eff[t] if record else None)
 
-    def run(self, T=None, record=True):
+    def run(self, T=None, record=True, errors=False):
+        """T iterations from W0; with errors, the full training error before
+        every iteration and after the last (d_err[0 .. T])."""
         T = self.prob.T if T is None else T
         self.reset()
         for t in range(T):
-            self.iterate(t, record)
+            self.iterate(t, record, errors)
+        if errors:
+            E.ecc_mf_error(self.handle, self.d_W, self.d_err[T].data_ptr(), current_stream())
 
     def close(self):
         if getattr(self, "handle", None):

@@ -134,9 +134,9 @@ def test_threshold_full():
 
 def test_mf_full():
     """The factorisation at the benchmark's shape (25M ratings, 160,000 users,
-    60,000 items, rank 16, 32 workers, slack 2, Bernoulli(0.8) arrivals), two
-    iterations: the model bit for bit, the decisions exactly, the error
-    within 1e-12."""
+    60,000 items, rank 16, 32 workers of 8 minibatches, slack 2,
+    Bernoulli(0.8) arrivals), two iterations: the model bit for bit, the
+    decisions exactly, the errors within 1e-12."""
     from test_gpu_mf import _compare
     _compare(W.mf_problem(T=2))
 

@@ -1,7 +1,8 @@
-"""GPU parity of the data-parallel matrix factorisation over the partial
-allreduce (Section IV's workload) through the C ABI against the oracle: the
-model after every iteration and the staleness decisions bit for bit, the
-error within 1e-12 (its sum is reduced in another order)."""
+"""GPU parity of the data-parallel matrix factorisation by minibatch SGD over
+the partial allreduce (Section IV's workload) through the C ABI against the
+oracle: the model after every iteration and the staleness decisions bit for
+bit, the minibatch error and the full training error within 1e-12 (their
+sums are reduced in another order)."""
 import numpy as np
 import pytest
 
@@ -37,11 +38,13 @@ def _compare(prob, clobber_inputs=False):
     try:
         run.reset()
         for t in range(prob.T):
-            run.iterate(t)
+            run.iterate(t, error=True)
             torch.cuda.synchronize()
             got = run.d_W.cpu().numpy()
             assert np.array_equal(got, ref["kept"][t + 1]), \
                 (t, np.abs(got - ref["kept"][t + 1]).max())
+            err = float(run.d_err[t].item())
+            assert abs(err - M.full_rmse(prob, ref["kept"][t])) <= 1e-12 * err, t
         rmse = run.d_rmse.cpu().numpy()[:prob.T]
         assert np.allclose(rmse, ref["rmse"], rtol=1e-12, atol=0)
         assert np.array_equal(run.d_eff.cpu().numpy()[:prob.T], ref["eff"])
@@ -51,25 +54,28 @@ def _compare(prob, clobber_inputs=False):
         run.close()
 
 
-@pytest.mark.parametrize("rank", [1, 4, 16, 32])
-def test_mf_synchronous(rank):
+@pytest.mark.parametrize("rank,K", [(1, 1), (4, 4), (16, 8), (32, 3)])
+def test_mf_synchronous(rank, K):
+    """Every worker fresh; full batches (K = 1) and minibatches."""
     _compare(W.mf_problem(n_users=300, n_items=120, n_ratings=20011, rank=rank, P=8, S=0, q=1.0,
-                          T=6, eta=1.0, seed=rank))
+                          T=6, eta=0.5, seed=rank, K=K))
 
 
-@pytest.mark.parametrize("S,q", [(0, 0.5), (2, 0.6), (5, 0.3)])
-def test_mf_stale(S, q):
+@pytest.mark.parametrize("S,q,K", [(0, 0.5, 8), (2, 0.6, 8), (5, 0.3, 2)])
+def test_mf_stale(S, q, K):
+    """32 workers, stale gradients substituted; more iterations than
+    minibatches (several epochs of the schedule)."""
     _compare(W.mf_problem(n_users=700, n_items=250, n_ratings=40009, rank=16, P=32, S=S, q=q,
-                          T=10, eta=1.0, seed=7 + S))
+                          T=20, eta=0.5, seed=7 + S, K=K))
 
 
 @pytest.mark.parametrize("rank", [1, 16, 64])
 def test_mf_long_rows(rank):
-    """Few users and items: every (worker, row) holds hundreds to thousands
-    of ratings, so each row is summed by a whole workgroup over several
-    chunks of its ratings."""
+    """Few users and items: every (worker, minibatch, row) holds hundreds to
+    thousands of ratings, so each row is summed by a whole workgroup over
+    several chunks of its ratings."""
     _compare(W.mf_problem(n_users=60, n_items=25, n_ratings=50021, rank=rank, P=2, S=1, q=0.7,
-                          T=4, eta=1.0, seed=11 + rank))
+                          T=4, eta=0.5, seed=11 + rank, K=2))
 
 
 @pytest.mark.parametrize("rank", [2, 8, 16])
@@ -77,18 +83,19 @@ def test_mf_long_and_short_rows(rank):
     """Item rows of hundreds of ratings next to user rows of a few: both
     row paths in one launch."""
     _compare(W.mf_problem(n_users=2000, n_items=40, n_ratings=60013, rank=rank, P=4, S=2, q=0.6,
-                          T=5, eta=1.0, seed=23 + rank))
+                          T=5, eta=0.5, seed=23 + rank, K=2))
 
 
 def test_mf_inputs_copied_at_create():
     _compare(W.mf_problem(n_users=400, n_items=90, n_ratings=30011, rank=8, P=4, S=1, q=0.7,
-                          T=4, eta=1.0, seed=31), clobber_inputs=True)
+                          T=4, eta=0.5, seed=31, K=4), clobber_inputs=True)
 
 
 def test_mf_one_worker_and_idle_rows():
-    """P = 1; many users and items without ratings (their rows only decay)."""
+    """P = 1; many users and items without ratings, in the minibatch or at
+    all (their rows only decay)."""
     _compare(W.mf_problem(n_users=5000, n_items=3000, n_ratings=3001, rank=8, P=1, S=0, q=1.0,
-                          T=4, eta=1.0, seed=2))
+                          T=4, eta=0.5, seed=2, K=5))
 
 
 def test_mf_errors():
@@ -97,12 +104,13 @@ def test_mf_errors():
     u = torch.zeros(10, dtype=torch.int32, device="cuda")
     i = torch.zeros(10, dtype=torch.int32, device="cuda")
     r = torch.zeros(10, dtype=torch.float64, device="cuda")
-    for args in [(4, 4, 3, 2, 10), (4, 4, 128, 2, 10), (0, 4, 4, 2, 10), (4, 4, 4, 0, 10)]:
+    for args in [(4, 4, 3, 2, 1, 10), (4, 4, 128, 2, 1, 10), (0, 4, 4, 2, 1, 10),
+                 (4, 4, 4, 0, 1, 10), (4, 4, 4, 2, 0, 10)]:
         with pytest.raises(E.EccError) as ei:
             E.ecc_mf_create(*args, u, i, r)
         assert ei.value.status == E.ECC_ERR_ARG
     bad = u.clone()
     bad[7] = 4
     with pytest.raises(E.EccError) as ei:
-        E.ecc_mf_create(4, 4, 4, 2, 10, bad, i, r)
+        E.ecc_mf_create(4, 4, 4, 2, 1, 10, bad, i, r)
     assert ei.value.status == E.ECC_ERR_ARG

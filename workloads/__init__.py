@@ -44,6 +44,7 @@ STREAM_MF_NOISE = 13
 STREAM_MF_TRUTH = 14
 STREAM_MF_INIT = 15
 STREAM_MF_PERM = 16
+STREAM_MF_BATCH = 17
 
 SEED_BASE = 2203170630
 
@@ -525,17 +526,21 @@ def threshold_collectives(P: int = 32, m: int = 1 << 23, theta: float = 0.5,
 
 @dataclass
 class MFProblem:
-    """Matrix factorisation by gradient steps, data parallel over P workers
-    (the paper's allreduce_SSP experiment, Section IV, on synthetic ratings).
+    """Matrix factorisation by minibatch stochastic gradient descent, data
+    parallel over P workers (the paper's allreduce_SSP experiment, Section
+    IV, on synthetic ratings).
 
     Ratings (users[k], items[k], ratings[k]), k < N, are stored in shard order:
-    worker p holds k in [p*N/P, (p+1)*N/P).  The model W = [U; V] is
-    (n_users + n_items) x rank doubles, row-major, U first.  One iteration at
-    model W: every worker p computes the gradient of its shard's squared error
+    worker p holds k in [p*N/P, (p+1)*N/P), cut into K minibatches of
+    consecutive ratings (batch b: offsets [L b / K, L (b+1) / K) of the
+    shard's L ratings).  The model W = [U; V] is (n_users + n_items) x rank
+    doubles, row-major, U first.  One iteration t at model W: worker p takes
+    minibatch batch[t][p] and computes the gradient of its squared error
     sum_k (r_k - U[u_k].V[i_k])^2; the partial allreduce combines the workers'
     gradients (stale ones substituted, slack S, arrivals `mask`); the step is
-    W := W - eta * (G_row / n_row + 2 lam W), n_row = the row's number of
-    ratings (1 if none)."""
+    W := W - eta * (G_row K / n_row + 2 lam W), n_row = the row's number of
+    ratings (1 if none).  batch[t][p] runs through a seeded permutation of
+    the K minibatches in every epoch of K iterations."""
     n_users: int
     n_items: int
     rank: int
@@ -549,11 +554,19 @@ class MFProblem:
     S: int
     mask: np.ndarray         # uint8 [T][P]
     T: int
+    K: int = 1               # minibatches per shard
+    batch: np.ndarray = None  # int32 [T][P]: the minibatch of worker p at iteration t
     meta: dict = field(default_factory=dict)
 
     @property
     def N(self) -> int:
         return int(self.ratings.shape[0])
+
+    def batch_range(self, p: int, b: int):
+        """Ratings [lo, hi) of minibatch b of worker p's shard."""
+        a, c = self.shard(p)
+        L = c - a
+        return a + L * b // self.K, a + L * (b + 1) // self.K
 
     @property
     def m(self) -> int:
@@ -575,15 +588,30 @@ def _zipf_pick(seed: int, stream: int, n_draws: int, n: int, s: float) -> np.nda
     return perm[k].astype(np.int32)
 
 
+def batch_schedule(seed: int, T: int, P: int, K: int) -> np.ndarray:
+    """[T][P] minibatch indices: for worker p and epoch e (iterations e K ..
+    e K + K - 1) a seeded permutation of 0 .. K-1 (the order of K uniforms
+    at counters (p * 2^32 + e) * K + j, ties to the lower j)."""
+    out = np.empty((T, P), dtype=np.int32)
+    for p in range(P):
+        for e in range((T + K - 1) // K):
+            u = uniform(seed, STREAM_MF_BATCH, K, ctr0=((p << 32) + e) * K)
+            perm = np.argsort(u, kind="stable").astype(np.int32)
+            n = min(K, T - e * K)
+            out[e * K:e * K + n, p] = perm[:n]
+    return out
+
+
 def mf_problem(n_users: int = 160_000, n_items: int = 60_000, n_ratings: int = 25_000_000,
                rank: int = 16, P: int = 32, S: int = 2, q: float = 0.8, T: int = 100,
-               eta: float = 1.0, lam: float = 1e-4, true_rank: int = 8, seed: int = None
-               ) -> MFProblem:
+               eta: float = 0.5, lam: float = 1e-4, true_rank: int = 8, seed: int = None,
+               K: int = 8) -> MFProblem:
     """Synthetic ratings shaped like a large movie-rating set (25M ratings;
     Zipf user activity, exponent 0.5, and item popularity, exponent 0.6):
     half-star ratings in [0.5, 5] from a planted rank-`true_rank` model plus
-    noise, centred; uniformly shuffled into P equal shards, each stored by
-    user then item; the model starts at N(0, 0.1^2)."""
+    noise, centred; drawn independently, so consecutive ratings form uniform
+    shards and minibatches; P equal shards of K minibatches, each minibatch
+    stored by user then item; the model starts at N(0, 0.1^2)."""
     seed = seed_of(8) if seed is None else seed
     users = _zipf_pick(seed, STREAM_MF_USERS, n_ratings, n_users, 0.5)
     items = _zipf_pick(seed, STREAM_MF_ITEMS, n_ratings, n_items, 0.6)
@@ -594,12 +622,17 @@ def mf_problem(n_users: int = 160_000, n_items: int = 60_000, n_ratings: int = 2
                                                                          n_ratings)
     r = np.clip(np.round(raw * 2.0) / 2.0, 0.5, 5.0)
     ratings = r - r.mean()
-    # within each worker's shard, ratings are stored by user, then item
+    # within each minibatch of each worker's shard, ratings are stored by
+    # user, then item
     for p in range(P):
         a, b = n_ratings * p // P, n_ratings * (p + 1) // P
-        o = np.lexsort((items[a:b], users[a:b]))
-        users[a:b], items[a:b], ratings[a:b] = users[a:b][o], items[a:b][o], ratings[a:b][o]
+        for j in range(K):
+            lo, hi = a + (b - a) * j // K, a + (b - a) * (j + 1) // K
+            o = np.lexsort((items[lo:hi], users[lo:hi]))
+            users[lo:hi], items[lo:hi], ratings[lo:hi] = (users[lo:hi][o], items[lo:hi][o],
+                                                          ratings[lo:hi][o])
     W0 = 0.1 * normal(seed, STREAM_MF_INIT, (n_users + n_items) * rank)
     mask = arrival_mask(seed, T, np.full(P, q))
     return MFProblem(n_users, n_items, rank, P, users, items, ratings, W0, eta, lam, S, mask, T,
+                     K=K, batch=batch_schedule(seed, T, P, K),
                      meta={"q": q, "true_rank": true_rank, "rating_mean": float(r.mean())})
