@@ -41,11 +41,15 @@ METRIC = "assembled+iterated GB/s and iterations/s at 1 GPU; % of HBM peak"
 PROFILES = os.path.join(ROOT, "profiles")
 
 
-def sweep_bytes(n, nnz):
+def sweep_bytes(n, nnz, column_values=False):
     """Algorithmic bytes of one sweep: col + val per nonzero, row_ptr, the x
     view, b (or x_own for the update norm), the written iterate.  This is the
     model of the method's data, whatever layout the library sweeps (the
-    short-row copy reads no row_ptr but its padding)."""
+    short-row copy reads no row_ptr but its padding).  A matrix whose columns
+    each hold one value (PageRank's A^T D^-1) is that value per column in
+    place of a value per nonzero."""
+    if column_values:
+        return 4 * nnz + 36 * n + 4
     return 12 * nnz + 28 * n + 4
 
 
@@ -214,6 +218,7 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
     layout, slots = E.ecc_matrix_layout(run.mat)
     schedule = E.ecc_matrix_schedule(run.mat)
     tiling = E.ecc_matrix_tiling(run.mat)
+    column_values = bool(E.ecc_matrix_columns(run.mat))
     run.close()
 
     counts = prob.counts
@@ -224,7 +229,7 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
     fused = times["SWEEP"][1] > 0 and times["ASSEMBLE"][1] == 0
     per_elem = 8.0 if fused else 16.0
     b_assemble = per_elem * eff_elems + 14.0 * prob.P
-    b_sweep = float(sweep_bytes(prob.n, prob.A.nnz))
+    b_sweep = float(sweep_bytes(prob.n, prob.A.nnz, column_values))
     b_norm = 16.0 * n_part                 # partials written, then read by the second pass
     bytes_per_step = float(np.sum(b_assemble)) + iters * (b_sweep + b_norm)
     dom = b_sweep + b_norm + (float(np.mean(b_assemble)) if fused else 0.0)
@@ -246,6 +251,7 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
                   "schedule": {E.ECC_SCHEDULE_STATIC: "static", E.ECC_SCHEDULE_QUEUE: "queue",
                                E.ECC_SCHEDULE_SINGLE: "single launch"}[schedule],
                   "plane_tiling": {"plane_rows": tiling[0], "tile_rows": tiling[1]},
+                  "column_values": column_values,
                   "assembly_bytes_per_arrived_element": per_elem},
     }
 

@@ -234,7 +234,8 @@ ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *con
  *                      of device memory) and swept in runs staged in LDS;
  *   ECC_LAYOUT_RANGES  very uneven rows over a longer vector: the columns are
  *                      cut into R = ceil(8 x n_rows / 8 MiB) ranges of equal
- *                      width (2 <= R <= 16; ecc_matrix_opts_t.range_bytes
+ *                      width (16 MiB in the column-value form below;
+ *                      2 <= R <= 16; ecc_matrix_opts_t.range_bytes
  *                      replaces the 8 MiB), every row into its entries of
  *                      each range, and these
  *                      sub-rows are copied range by range in order of
@@ -247,7 +248,19 @@ ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *con
  *   ECC_LAYOUT_STREAM  otherwise: runs of rows staged in LDS.
  * ECC_LAYOUT_STREAM reads the matrix arrays at every sweep: they must then
  * outlive the handle and stay unchanged.  The other layouts sweep the copy
- * made here. */
+ * made here.
+ * Column values (ECC_KIND_POWER in ECC_LAYOUT_SORTED or ECC_LAYOUT_RANGES):
+ * when all entries of every column j hold one value c_j, bit for bit -- the
+ * PageRank matrix W = A^T D^-1 of Section IV holds 1 / outdeg(j) throughout
+ * column j -- the copy keeps c (8 bytes x n_rows) in place of the entries'
+ * values (8 bytes x nnz).  Every sweep then first forms z_own = c * x_own
+ * and z_hat = c * x_hat elementwise (in 16 bytes x n_rows the handle owns)
+ * and adds z_j where the general form adds w_ij * y_j: the same IEEE
+ * product of the same two operands, so the iterates are bit for bit those
+ * of the general form (the residual norm agrees to rounding: the kernel
+ * stages no values, more of its workgroups fit on the device, and the
+ * per-workgroup partial sums group the rows differently).
+ * ecc_matrix_columns reports the choice. */
 #define ECC_LAYOUT_STREAM 0
 #define ECC_LAYOUT_SORTED 1
 #define ECC_LAYOUT_SHORT 2
@@ -261,7 +274,7 @@ ecc_status_t ecc_matrix_destroy(ecc_matrix_t A);
  * computes, except that range_bytes changes the ECC_LAYOUT_RANGES rounding
  * (the number of sub-row sums added per row).
  *   range_bytes  ECC_LAYOUT_RANGES: bytes of the vector per column range
- *                (0: 8 MiB).
+ *                (0: 8 MiB, 16 MiB in the column-value form).
  *   tile_rows    ECC_LAYOUT_SHORT plane tiles: 0 chosen from the matrix, > 0
  *                that many rows per tile (rounded up to a multiple of 256;
  *                applied only to a matrix that qualifies for tiling), < 0
@@ -281,16 +294,22 @@ ecc_status_t ecc_matrix_destroy(ecc_matrix_t A);
  *                ECC_SCHEDULE_AUTO (0): the single launch when the problem
  *                fits it, else the queue when a workgroup would walk at
  *                least 16 items, else the static walk.
- * opts may be NULL (the defaults).  ECC_ERR_ARG for a negative range_bytes
- * or an unknown schedule. */
+ *   columns      ECC_COLUMNS_AUTO (0): the column-value form (above)
+ *                whenever the matrix qualifies; ECC_COLUMNS_GENERAL: the
+ *                entries' own values always.
+ * opts may be NULL (the defaults).  ECC_ERR_ARG for a negative range_bytes,
+ * an unknown schedule or an unknown columns choice. */
 #define ECC_SCHEDULE_AUTO 0
 #define ECC_SCHEDULE_STATIC 1
 #define ECC_SCHEDULE_QUEUE 2
 #define ECC_SCHEDULE_SINGLE 3
+#define ECC_COLUMNS_AUTO 0
+#define ECC_COLUMNS_GENERAL 1
 typedef struct {
     int64_t range_bytes;
     int64_t tile_rows;
     int32_t schedule;
+    int32_t columns;
 } ecc_matrix_opts_t;
 ecc_status_t ecc_matrix_create_ex(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
                                   const ecc_matrix_opts_t *opts, ecc_matrix_t *out);
@@ -299,6 +318,10 @@ ecc_status_t ecc_matrix_create_ex(ecc_plan_t plan, const ecc_csr_t *A, int32_t k
  * the bandwidth B taken as the plane size and *tile_rows = W, both 0 when
  * the items are swept in row order. */
 ecc_status_t ecc_matrix_tiling(ecc_matrix_t A, int64_t *plane_rows, int64_t *tile_rows);
+
+/* Host only: *one_value = 1 when the sweeps use the column-value form
+ * (one value per column, see ecc_matrix_create), else 0. */
+ecc_status_t ecc_matrix_columns(ecc_matrix_t A, int32_t *one_value);
 
 /* Schedule chosen at set-up (host only): ECC_SCHEDULE_STATIC,
  * ECC_SCHEDULE_QUEUE or ECC_SCHEDULE_SINGLE. */

@@ -88,6 +88,7 @@ enum { kItemStream = 0, kItemVector = 1, kItemPiece = 2 };
 enum { kLayStream = 0, kLaySorted = 1, kLayShort = 2, kLayRanges = 3 };
 constexpr int kMaxRanges = 16;              // column ranges of the range layout at most
 constexpr int64_t kRangeBytes = 8 << 20;    // bytes of the vector per column range
+constexpr int64_t kRangeBytesColumns = 16 << 20;  // the same for a column-value matrix
 // Plane tiling of the short-row layout: applied when one plane of rows
 // streams more than kTileMinBytes (the rows one plane apart no longer meet
 // in an XCD's 4 MB L2); tiles of kTileNearFactor times the largest in-plane
@@ -406,6 +407,12 @@ struct ecc_matrix_s {
     bool tiny = false;              // short layout: ecc_solve runs as one single-workgroup launch;
                                     // sweeps write one partial per row (n_part = n + 1)
     unsigned *d_queue = nullptr;    // its ticket counters, (kQueueRanges + 1) x kQueueStride
+    // power kind, sorted or range layout: every column's entries hold one
+    // value; the copy keeps no values, and sweeps gather z = c * x instead
+    bool colscale = false;
+    double *d_cscale = nullptr;     // [n] the value of each column (0 for empty ones)
+    double *d_zown = nullptr;       // [n] c * x_own of the current sweep
+    double *d_zhat = nullptr;       // [n] c * x_hat of the current sweep
 };
 
 namespace ecc {
@@ -432,8 +439,17 @@ struct SweepLaunch {
     double *prev_rho = nullptr;
     int32_t norm = 0;
     const int32_t *done = nullptr;
+    // column-value matrix: the scaled views are already formed (by the
+    // assembly of the same loop iteration)
+    bool scaled = false;
 };
 ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L);
+// Column-value matrix: the staleness decision and assembly of one loop
+// iteration (as launch_assemble, from x_own into x_hat) that also forms the
+// scaled views M->d_zown and M->d_zhat for the sweep that follows.
+ecc_status_t launch_assemble_scaled(ecc_matrix_t M, const double *x_own, double *x_hat,
+                                    const uint8_t *d_arrived, uint8_t *d_eff_out,
+                                    int32_t *d_age_out, const int32_t *d_done);
 // Second pass: split rows (their contribution -> partial G) and, with
 // norm != 0, the norm into *rho_out and the loop control block.
 struct Pass2Launch {

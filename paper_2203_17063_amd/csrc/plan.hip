@@ -104,7 +104,7 @@ using namespace ecc;
 
 extern "C" {
 
-int32_t ecc_abi_version(void) { return 2; }
+int32_t ecc_abi_version(void) { return 3; }
 
 const char *ecc_last_error(void) { return g_err; }
 

@@ -87,7 +87,10 @@ extern "C" ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double 
         int32_t *age_t = d_age_hist ? d_age_hist + (int64_t)t * P : nullptr;
         double *part = A->d_partials + (deferred ? (t & 1) * G1 : 0);
         if (!fused) {
-            st = launch_assemble(plan, nullptr, cur, d_x_hat, mask_t, eff_t, age_t, done);
+            // a column-value matrix's assembly also forms the scaled views
+            st = A->colscale
+                     ? launch_assemble_scaled(A, cur, d_x_hat, mask_t, eff_t, age_t, done)
+                     : launch_assemble(plan, nullptr, cur, d_x_hat, mask_t, eff_t, age_t, done);
             if (st != ECC_OK) return st;
         }
         SweepLaunch L;
@@ -100,6 +103,7 @@ extern "C" ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double 
         L.partials = part;
         L.norm = norm;
         L.done = done;
+        L.scaled = !fused && A->colscale;
         if (fused) {
             L.arrived = mask_t;
             L.eff_user = eff_t;

@@ -73,6 +73,10 @@ struct SweepArgs {
     const double *x_own;
     double *x_hat;
     double *x_next;
+    // what the stream layouts gather: x_own and x_hat, or for a column-value
+    // matrix the scaled views c * x_own and c * x_hat
+    const double *g_own;
+    const double *g_hat;
     double *partials;
     double2 *pieces;
     const int32_t *order;    // sorted layout: the row at each sorted position
@@ -178,8 +182,10 @@ __device__ __forceinline__ int lanes_per_row(int32_t nnz, int32_t nr) {
 // Accumulates a lane's entries k0, k0 + stride, ... (< k1) of row i, in that
 // order, W at a time: the next W (col, val) loads are in flight while the
 // current W gathers of y complete.  With stride 1 this is the row's CSR
-// order.  Jacobi skips (and records) the diagonal entry.
-template <int KIND, bool STEP, int W>
+// order.  Jacobi skips (and records) the diagonal entry.  CS: the gathers
+// come from the scaled views and the entries' values are all 1 (the product
+// v * y is then y itself).
+template <int KIND, bool STEP, int W, bool CS>
 __device__ __forceinline__ void seg_accumulate(int32_t i, int32_t k0, int32_t k1, int32_t stride,
                                                const SweepArgs &a, int32_t lo, int32_t hi,
                                                const StepView &sv, RankCache &rc, double &s,
@@ -191,13 +197,13 @@ __device__ __forceinline__ void seg_accumulate(int32_t i, int32_t k0, int32_t k1
     for (int u = 0; u < W; ++u) {
         const int32_t k = k0 + u * stride;
         c[u] = (k < k1) ? a.col[k] : 0;
-        v[u] = (k < k1) ? a.val[k] : 0.0;
+        v[u] = CS ? 1.0 : (k < k1) ? a.val[k] : 0.0;
     }
     for (int32_t k = k0; k < k1; k += W * stride) {
         double y[W];
 #pragma unroll
         for (int u = 0; u < W; ++u)
-            y[u] = (k + u * stride < k1) ? view_load<STEP>(c[u], lo, hi, a.x_own, a.x_hat, sv, rc)
+            y[u] = (k + u * stride < k1) ? view_load<STEP>(c[u], lo, hi, a.g_own, a.g_hat, sv, rc)
                                           : 0.0;
         const int32_t kn = k + W * stride;
         int32_t cn[W];
@@ -206,7 +212,7 @@ __device__ __forceinline__ void seg_accumulate(int32_t i, int32_t k0, int32_t k1
         for (int u = 0; u < W; ++u) {
             const int32_t kk = kn + u * stride;
             cn[u] = (kk < k1) ? a.col[kk] : 0;
-            vn[u] = (kk < k1) ? a.val[kk] : 0.0;
+            vn[u] = CS ? 1.0 : (kk < k1) ? a.val[kk] : 0.0;
         }
 #pragma unroll
         for (int u = 0; u < W; ++u) {
@@ -235,7 +241,7 @@ struct StreamPrefetch {
     double bi, xo;
 };
 
-template <int KIND, int LAY>
+template <int KIND, int LAY, bool CS>
 __device__ __forceinline__ void stream_load(const WorkItem &it, const SweepArgs &a,
                                             StreamPrefetch &pf) {
     const int tid = threadIdx.x;
@@ -250,10 +256,10 @@ __device__ __forceinline__ void stream_load(const WorkItem &it, const SweepArgs 
                 // gathered vector from L2 (measured on MI355X, PageRank on a
                 // scale-22 R-MAT graph: 573 against 600 us per sweep)
                 pf.cv[u] = __builtin_nontemporal_load(a.col + kc);
-                pf.vv[u] = __builtin_nontemporal_load(a.val + kc);
+                if constexpr (!CS) pf.vv[u] = __builtin_nontemporal_load(a.val + kc);
             } else {
                 pf.cv[u] = a.col[kc];
-                pf.vv[u] = a.val[kc];
+                if constexpr (!CS) pf.vv[u] = a.val[kc];
             }
         }
     }
@@ -281,6 +287,7 @@ __device__ __forceinline__ void stream_load(const WorkItem &it, const SweepArgs 
     }
 }
 
+template <bool CS>
 __device__ __forceinline__ void stream_stage(const WorkItem &it, const StreamPrefetch &pf,
                                              int32_t *s_col, double *s_val) {
     const int32_t nnz = it.k1 - it.k0;
@@ -289,7 +296,7 @@ __device__ __forceinline__ void stream_stage(const WorkItem &it, const StreamPre
         const int32_t k = threadIdx.x + u * kSweepThreads;
         if (k < nnz) {
             s_col[k] = pf.cv[u];
-            s_val[k] = pf.vv[u];
+            if constexpr (!CS) s_val[k] = pf.vv[u];
         }
     }
 }
@@ -298,7 +305,7 @@ __device__ __forceinline__ void stream_stage(const WorkItem &it, const StreamPre
 // norm contribution.  i: the index of the row this thread finishes; [lo, hi):
 // its rank block.  The range layout stores the sum of a sub-row instead
 // (item rank = column range), for the finishing pass.
-template <int KIND, bool STEP, int LAY>
+template <int KIND, bool STEP, int LAY, bool CS>
 __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0, int32_t rp1,
                                                  int32_t i, int32_t lo, int32_t hi, double bi,
                                                  double xo, const SweepArgs &a,
@@ -322,11 +329,11 @@ __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0
         for (int j = 0; j < 8; ++j) {
             // entries past the row's end are read but unused (LDS is padded)
             c8[j] = s_col[rs + j];
-            v8[j] = s_val[rs + j];
+            v8[j] = CS ? 1.0 : s_val[rs + j];
         }
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-            y8[j] = (j < len) ? view_load<STEP>(c8[j], lo, hi, a.x_own, a.x_hat, sv, rc)
+            y8[j] = (j < len) ? view_load<STEP>(c8[j], lo, hi, a.g_own, a.g_hat, sv, rc)
                               : 0.0;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -337,22 +344,22 @@ __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0
         }
         for (int32_t k = rs + 8; k < re; ++k) {
             const int32_t c = s_col[k];
-            const double v = s_val[k];
+            const double v = CS ? 1.0 : s_val[k];
             if (KIND == ECC_KIND_JACOBI && c == i) {
                 dg = v;
                 continue;
             }
-            s = s + v * view_load<STEP>(c, lo, hi, a.x_own, a.x_hat, sv, rc);
+            s = s + v * view_load<STEP>(c, lo, hi, a.g_own, a.g_hat, sv, rc);
         }
     } else {
         for (int32_t k = rs + lane; k < re; k += tpr) {
             const int32_t c = s_col[k];
-            const double v = s_val[k];
+            const double v = CS ? 1.0 : s_val[k];
             if (KIND == ECC_KIND_JACOBI && c == i) {
                 dg = v;
                 continue;
             }
-            s = s + v * view_load<STEP>(c, lo, hi, a.x_own, a.x_hat, sv, rc);
+            s = s + v * view_load<STEP>(c, lo, hi, a.g_own, a.g_hat, sv, rc);
         }
         s = group_sum_dyn(s, tpr);
         if (KIND == ECC_KIND_JACOBI) dg = group_sum_dyn(dg, tpr);
@@ -369,14 +376,14 @@ __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0
 
 // One long row (or a slice of it) by the whole workgroup; returns the norm
 // contribution (in thread 0).
-template <int KIND, bool STEP, int LAY>
+template <int KIND, bool STEP, int LAY, bool CS>
 __device__ __forceinline__ double long_compute(const WorkItem &it, const SweepArgs &a,
                                                const StepView &sv, RankCache &rc,
                                                bool own_arrives, double *s_red) {
     const int tid = threadIdx.x;
     const int32_t i = it.row0, lo = it.lo, hi = it.hi;
     double s = 0.0, dg = 0.0;
-    seg_accumulate<KIND, STEP, 4>(i, it.k0 + tid, it.k1, kSweepThreads, a, lo, hi, sv, rc, s, dg);
+    seg_accumulate<KIND, STEP, 4, CS>(i, it.k0 + tid, it.k1, kSweepThreads, a, lo, hi, sv, rc, s, dg);
     s = block_sum<kSweepThreads>(s, s_red);
     if (KIND == ECC_KIND_JACOBI) dg = block_sum<kSweepThreads>(dg, s_red);
     if (tid != 0) return 0.0;
@@ -457,13 +464,13 @@ __device__ __forceinline__ void sweep_prologue(const SweepArgs &a, uint8_t *s_ef
 // its sorted copy (kLaySorted) or over its sub-rows cut by column range
 // (kLayRanges); all may contain vector items and pieces.
 // The short-row layout has its own body.
-template <int KIND, bool STEP, int LAY>
+template <int KIND, bool STEP, int LAY, bool CS>
 __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
     static_assert(LAY == kLayStream || LAY == kLaySorted || LAY == kLayRanges,
                   "stream layouts only");
     // padded by 8 so that a row's first eight entries can be read unclamped
     __shared__ int32_t s_col[kStreamCap + 8];
-    __shared__ double s_val[kStreamCap + 8];
+    __shared__ double s_val[CS ? 1 : kStreamCap + 8];
     __shared__ double s_red[kSweepThreads / 64];
     __shared__ uint8_t s_eff[STEP ? kFusedMaxP : 1];
     __shared__ int32_t s_bs[STEP ? kFusedMaxP + 1 : 1];
@@ -479,7 +486,7 @@ __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
     const bool have0 = w < i_end;
     if (have0) {
         cur = a.items[w];
-        if (cur.kind == kItemStream) stream_load<KIND, LAY>(cur, a, pf);
+        if (cur.kind == kItemStream) stream_load<KIND, LAY, CS>(cur, a, pf);
     }
     bool have_next = (int64_t)w + w_step < i_end;
     if (have_next) nxt = a.items[w + w_step];
@@ -499,21 +506,21 @@ __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
         WorkItem nn{};
         const bool have_nn = (int64_t)w + 2 * (int64_t)w_step < i_end;
         if (cur.kind == kItemStream) {
-            stream_stage(cur, pf, s_col, s_val);
+            stream_stage<CS>(cur, pf, s_col, s_val);
             const int32_t rp0 = pf.rp0, rp1 = pf.rp1, ri = pf.ri;
             const int32_t lo = LAY == kLayRanges ? pf.lo : cur.lo;
             const int32_t hi = LAY == kLayRanges ? pf.hi : cur.hi;
             const double bi = pf.bi, xo = pf.xo;
             __syncthreads();
-            if (next_stream) stream_load<KIND, LAY>(nxt, a, pf);
+            if (next_stream) stream_load<KIND, LAY, CS>(nxt, a, pf);
             if (have_nn) nn = a.items[w + 2 * w_step];
-            contrib += stream_compute<KIND, STEP, LAY>(cur, rp0, rp1, ri, lo, hi, bi, xo, a, s_col,
+            contrib += stream_compute<KIND, STEP, LAY, CS>(cur, rp0, rp1, ri, lo, hi, bi, xo, a, s_col,
                                                        s_val, sv, rc, own_arrives);
             __syncthreads();  // LDS is reused by the next item
         } else {
             if (have_nn) nn = a.items[w + 2 * w_step];
-            contrib += long_compute<KIND, STEP, LAY>(cur, a, sv, rc, own_arrives, s_red);
-            if (next_stream) stream_load<KIND, LAY>(nxt, a, pf);
+            contrib += long_compute<KIND, STEP, LAY, CS>(cur, a, sv, rc, own_arrives, s_red);
+            if (next_stream) stream_load<KIND, LAY, CS>(nxt, a, pf);
         }
         w += w_step;
         have = have_next;
@@ -526,9 +533,120 @@ __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
     if (tid == 0) a.partials[blockIdx.x] = total;
 }
 
-template <int KIND, bool STEP, int LAY>
+template <int KIND, bool STEP, int LAY, bool CS = false>
 __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
-    sweep_body<KIND, STEP, LAY>(a);
+    sweep_body<KIND, STEP, LAY, CS>(a);
+}
+
+// ---------------------------------------------------------------------------
+// Column-value matrices (every entry of column j holds c_j): the sweep adds
+// z_j = c_j * y_j, formed here once per element of each view, in place of
+// the product w_ij * y_j of each entry.
+// ---------------------------------------------------------------------------
+
+// c[col[k]] = val[k] for every entry (any one of a column's values wins).
+__global__ void k_col_values(int64_t nnz, const int32_t *__restrict__ col,
+                             const double *__restrict__ val, double *__restrict__ c) {
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < nnz;
+         k += (int64_t)gridDim.x * blockDim.x)
+        c[col[k]] = val[k];
+}
+
+// Entries whose value differs, bit for bit, from the value kept for their
+// column; *bad = their count.
+__global__ void k_col_check(int64_t nnz, const int32_t *__restrict__ col,
+                            const double *__restrict__ val, const double *__restrict__ c,
+                            unsigned long long *__restrict__ bad) {
+    unsigned long long nb = 0;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < nnz;
+         k += (int64_t)gridDim.x * blockDim.x)
+        nb += __double_as_longlong(val[k]) != __double_as_longlong(c[col[k]]) ? 1 : 0;
+    if (nb) atomicAdd(bad, nb);
+}
+
+constexpr int kScaleThreads = 256;
+constexpr int kScaleElems = 4;  // elements per thread, all loads in flight together
+
+// The scaled views of a plain sweep: z_own = c * x_own, z_hat = c * x_hat.
+__global__ __launch_bounds__(kScaleThreads) void k_col_scale(
+    int64_t n, const double *__restrict__ c, const double *__restrict__ x_own,
+    const double *__restrict__ x_hat, double *__restrict__ z_own, double *__restrict__ z_hat,
+    const int32_t *__restrict__ done) {
+    if (done && *done) return;
+    const int64_t stride = (int64_t)gridDim.x * kScaleThreads;
+    for (int64_t j0 = (int64_t)blockIdx.x * kScaleThreads + threadIdx.x; j0 < n;
+         j0 += stride * kScaleElems) {
+        double cj[kScaleElems], xo[kScaleElems], xh[kScaleElems];
+#pragma unroll
+        for (int u = 0; u < kScaleElems; ++u) {
+            const int64_t j = min(j0 + u * stride, n - 1);
+            cj[u] = c[j];
+            xo[u] = x_own[j];
+            xh[u] = x_hat[j];
+        }
+#pragma unroll
+        for (int u = 0; u < kScaleElems; ++u) {
+            const int64_t j = j0 + u * stride;
+            if (j < n) {
+                z_own[j] = cj[u] * xo[u];
+                z_hat[j] = cj[u] * xh[u];
+            }
+        }
+    }
+}
+
+// One loop iteration's staleness decision and assembly (as k_assemble, over
+// the same tiles) fused with the scaled views: for every element j of a tile
+// of rank p, z_own[j] = c_j * x_own[j]; if p's block is taken at this step,
+// x_hat[j] = x_own[j] and z_hat[j] = z_own[j] (= c_j * x_hat[j] after the
+// copy), else z_hat[j] = c_j * x_hat[j].  Workgroup 0 records the step.
+__global__ __launch_bounds__(kAssembleThreads) void k_assemble_scaled(
+    int32_t P, int32_t S, int64_t t, const uint8_t *__restrict__ arrived,
+    const int32_t *__restrict__ ver_in, int32_t *__restrict__ ver_out,
+    int32_t *__restrict__ age_state, uint8_t *__restrict__ eff_state,
+    unsigned long long *__restrict__ forced, uint8_t *__restrict__ eff_user,
+    int32_t *__restrict__ age_user, const Tile *__restrict__ tiles,
+    const int64_t *__restrict__ displs, const double *__restrict__ c,
+    const double *__restrict__ x_own, double *__restrict__ x_hat, double *__restrict__ z_own,
+    double *__restrict__ z_hat, const int32_t *__restrict__ done) {
+    if (done && *done) return;
+    if (blockIdx.x == 0) {
+        record_step(P, S, t, arrived, ver_in, ver_out, age_state, eff_state, forced, eff_user,
+                    age_user, nullptr);
+        return;
+    }
+    const Tile tile = tiles[blockIdx.x - 1];
+    const int32_t p = tile.rank;
+    const bool take = stale_select(ver_in[p], arrived[p], t, S);
+    const int64_t j0 = displs[p] + tile.off;
+    const int32_t len = tile.len;
+    static_assert(kAssembleTile / kAssembleThreads == 8, "eight elements per thread");
+    if (len <= 0) return;
+    const int32_t last = len - 1;
+    double cj[8], xo[8], xh[8];
+    // clamped reads, all in flight together
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int64_t j = j0 + min((int32_t)threadIdx.x + u * kAssembleThreads, last);
+        cj[u] = c[j];
+        xo[u] = x_own[j];
+        xh[u] = take ? 0.0 : x_hat[j];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int32_t k = threadIdx.x + u * kAssembleThreads;
+        if (k < len) {
+            const int64_t j = j0 + k;
+            const double zo = cj[u] * xo[u];
+            z_own[j] = zo;
+            if (take) {
+                x_hat[j] = xo[u];
+                z_hat[j] = zo;
+            } else {
+                z_hat[j] = cj[u] * xh[u];
+            }
+        }
+    }
 }
 
 // Range layout: the sum of a sub-row cut into pieces, its pieces added in
@@ -1311,7 +1429,7 @@ __global__ void k_sort_rows(int32_t n, const int32_t *__restrict__ order,
         const int32_t src = row_ptr[i], len = row_ptr[i + 1] - src, dst = srow_ptr[r];
         for (int32_t k = lane; k < len; k += 64) {
             scol[dst + k] = col[src + k];
-            sval[dst + k] = val[src + k];
+            if (sval) sval[dst + k] = val[src + k];
         }
     }
 }
@@ -1322,8 +1440,13 @@ __global__ void k_sort_rows(int32_t n, const int32_t *__restrict__ order,
 // Occupancy of the kernel a loop iteration launches: the fused one, except
 // for the sorted and range layouts, which are never fused.
 template <int LAY>
-static hipError_t sweep_occupancy(int *per_cu, int kind) {
+static hipError_t sweep_occupancy(int *per_cu, int kind, bool colscale) {
     constexpr bool S = LAY != kLaySorted && LAY != kLayRanges;
+    if constexpr (!S) {
+        if (colscale)
+            return hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                per_cu, k_sweep<ECC_KIND_POWER, false, LAY, true>, kSweepThreads, 0);
+    }
     return kind == ECC_KIND_JACOBI
                ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
                      per_cu, k_sweep<ECC_KIND_JACOBI, S, LAY>, kSweepThreads, 0)
@@ -1356,15 +1479,17 @@ static hipError_t short_occupancy(int *per_cu, int kind, int32_t short_r) {
     }
 }
 
-static int32_t sweep_grid(int64_t n_items, int kind, int layout, int32_t short_r) {
+static int32_t sweep_grid(int64_t n_items, int kind, int layout, int32_t short_r,
+                          bool colscale) {
     int dev = 0, cus = 0, per_cu = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         cus = 256;
-    const hipError_t e = layout == kLaySorted  ? sweep_occupancy<kLaySorted>(&per_cu, kind)
-                         : layout == kLayRanges ? sweep_occupancy<kLayRanges>(&per_cu, kind)
-                         : layout == kLayShort ? short_occupancy(&per_cu, kind, short_r)
-                                               : sweep_occupancy<kLayStream>(&per_cu, kind);
+    const hipError_t e =
+        layout == kLaySorted   ? sweep_occupancy<kLaySorted>(&per_cu, kind, colscale)
+        : layout == kLayRanges ? sweep_occupancy<kLayRanges>(&per_cu, kind, colscale)
+        : layout == kLayShort  ? short_occupancy(&per_cu, kind, short_r)
+                               : sweep_occupancy<kLayStream>(&per_cu, kind, false);
     if (e != hipSuccess || per_cu < 1) per_cu = 4;
     const int64_t resident = (int64_t)std::max(cus, 1) * per_cu;
     int64_t g = std::max<int64_t>(1, std::min<int64_t>({n_items, resident, (int64_t)kMaxSweepBlocks}));
@@ -1378,7 +1503,14 @@ static int32_t sweep_grid(int64_t n_items, int kind, int layout, int32_t short_r
 template <int K, bool S>
 static void launch_layout(ecc_matrix_t M, dim3 grid, dim3 block, hipStream_t st,
                           const SweepArgs &a) {
-    if (M->layout == kLaySorted) {
+    if (K == ECC_KIND_POWER && !S && M->colscale) {
+        if (M->layout == kLaySorted)
+            hipLaunchKernelGGL((k_sweep<ECC_KIND_POWER, false, kLaySorted, true>), grid, block, 0,
+                               st, a);
+        else
+            hipLaunchKernelGGL((k_sweep<ECC_KIND_POWER, false, kLayRanges, true>), grid, block, 0,
+                               st, a);
+    } else if (M->layout == kLaySorted) {
         if constexpr (!S) hipLaunchKernelGGL((k_sweep<K, S, kLaySorted>), grid, block, 0, st, a);
     } else if (M->layout == kLayRanges) {
         if constexpr (!S) hipLaunchKernelGGL((k_sweep<K, S, kLayRanges>), grid, block, 0, st, a);
@@ -1418,6 +1550,8 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     a.x_own = L.x_own;
     a.x_hat = L.x_hat;
     a.x_next = L.x_next;
+    a.g_own = M->colscale ? M->d_zown : L.x_own;
+    a.g_hat = M->colscale ? M->d_zhat : L.x_hat;
     a.partials = L.partials;
     a.pieces = M->d_pieces;
     a.order = M->d_order;
@@ -1465,6 +1599,15 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     TimedLaunch timed(pl, ECC_TIMING_SWEEP);
     const dim3 grid(M->grid), block(kSweepThreads);
     hipStream_t st = pl->stream;
+    if (M->colscale && !L.scaled && M->A.n_rows > 0) {
+        // the views this sweep gathers, scaled by the column values
+        const int64_t n = M->A.n_rows;
+        const int64_t per = (int64_t)kScaleThreads * kScaleElems;
+        const int sg = (int)std::min<int64_t>(8192, (n + per - 1) / per);
+        hipLaunchKernelGGL(k_col_scale, dim3(sg), dim3(kScaleThreads), 0, st, n, M->d_cscale,
+                           L.x_own, L.x_hat, M->d_zown, M->d_zhat, L.done);
+        ECC_LAUNCH_CHECK();
+    }
     if (M->kind == ECC_KIND_JACOBI) {
         if (step) launch_layout<ECC_KIND_JACOBI, true>(M, grid, block, st, a);
         else launch_layout<ECC_KIND_JACOBI, false>(M, grid, block, st, a);
@@ -1502,6 +1645,32 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
         ECC_LAUNCH_CHECK();
     }
     if (step) pl->clock += 1;
+    return ECC_OK;
+}
+
+ecc_status_t launch_assemble_scaled(ecc_matrix_t M, const double *x_own, double *x_hat,
+                                    const uint8_t *d_arrived, uint8_t *d_eff_out,
+                                    int32_t *d_age_out, const int32_t *d_done) {
+    ecc_plan_t plan = M->plan;
+    if (!M->colscale) {
+        set_error("internal: scaled assembly for a matrix without column values");
+        return ECC_ERR_STATE;
+    }
+    const int64_t t = plan->clock;
+    const int32_t *ver_in = plan->d_version + (t & 1) * plan->P;
+    int32_t *ver_out = plan->d_version + ((t + 1) & 1) * plan->P;
+    const int64_t grid = 1 + plan->n_tiles;
+    if (grid > 0x7fffffff) {
+        set_error("too many assembly tiles");
+        return ECC_ERR_RANGE;
+    }
+    TimedLaunch timed(plan, ECC_TIMING_ASSEMBLE);
+    hipLaunchKernelGGL(k_assemble_scaled, dim3((unsigned)grid), dim3(kAssembleThreads), 0,
+                       plan->stream, plan->P, plan->S, t, d_arrived, ver_in, ver_out, plan->d_age,
+                       plan->d_eff, plan->d_forced, d_eff_out, d_age_out, plan->d_tiles,
+                       plan->d_displs, M->d_cscale, x_own, x_hat, M->d_zown, M->d_zhat, d_done);
+    ECC_LAUNCH_CHECK();
+    plan->clock = t + 1;
     return ECC_OK;
 }
 
@@ -1549,12 +1718,13 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
     ecc_status_t st = check_plan(plan);
     if (st != ECC_OK) return st;
     ECC_ARG(A != nullptr, "A is NULL");
-    const ecc_matrix_opts_t opts = opts_in ? *opts_in : ecc_matrix_opts_t{0, 0, 0};
+    const ecc_matrix_opts_t opts = opts_in ? *opts_in : ecc_matrix_opts_t{0, 0, 0, 0};
     ECC_ARG(opts.range_bytes >= 0, "range_bytes is negative");
     ECC_ARG(opts.schedule == ECC_SCHEDULE_AUTO || opts.schedule == ECC_SCHEDULE_STATIC ||
                 opts.schedule == ECC_SCHEDULE_QUEUE || opts.schedule == ECC_SCHEDULE_SINGLE,
             "unknown schedule %d", opts.schedule);
-    const int64_t range_bytes = opts.range_bytes > 0 ? opts.range_bytes : kRangeBytes;
+    ECC_ARG(opts.columns == ECC_COLUMNS_AUTO || opts.columns == ECC_COLUMNS_GENERAL,
+            "unknown columns choice %d", opts.columns);
     ECC_ARG(kind == ECC_KIND_JACOBI || kind == ECC_KIND_POWER, "unknown kind %d", kind);
     ECC_ARG(A->n_rows >= 0 && A->n_cols >= 0 && A->nnz >= 0, "negative matrix size");
     if (A->nnz >= (int64_t(1) << 31) || A->n_rows >= (int64_t(1) << 31) ||
@@ -1628,9 +1798,62 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
     int32_t max_row = 0;
     for (int64_t i = 0; i < n; ++i) max_row = std::max(max_row, rp[i + 1] - rp[i]);
     const bool short_rows = max_row <= kShortRow;
+    // Column values: a power matrix with very uneven rows whose every column
+    // holds one value (the PageRank matrix) is swept from c and the scaled
+    // views, without the entries' values.  Measured on MI355X (PageRank on a
+    // scale-22 R-MAT graph, 64 ranks, ecc_solve): 472 against 533 us per
+    // iteration at 8 MiB ranges.
+    double *d_cscale = nullptr;
+    bool colscale = false;
+    if (kind == ECC_KIND_POWER && irregular && opts.columns == ECC_COLUMNS_AUTO && n > 0 &&
+        A->nnz > 0) {
+        unsigned long long *d_bad = nullptr;
+        unsigned long long h_bad = 1;
+        hipError_t e = hipMalloc((void **)&d_cscale, sizeof(double) * n);
+        if (e == hipSuccess) e = hipMalloc((void **)&d_bad, sizeof(unsigned long long));
+        if (e == hipSuccess) e = hipMemsetAsync(d_cscale, 0, sizeof(double) * n, plan->stream);
+        if (e == hipSuccess) e = hipMemsetAsync(d_bad, 0, sizeof(unsigned long long), plan->stream);
+        if (e == hipSuccess) {
+            const int blocks = (int)std::min<int64_t>(8192, (A->nnz + 255) / 256);
+            hipLaunchKernelGGL(k_col_values, dim3(blocks), dim3(256), 0, plan->stream, A->nnz,
+                               A->d_col, A->d_val, d_cscale);
+            hipLaunchKernelGGL(k_col_check, dim3(blocks), dim3(256), 0, plan->stream, A->nnz,
+                               A->d_col, A->d_val, d_cscale, d_bad);
+            e = hipGetLastError();
+            if (e == hipSuccess) e = hipStreamSynchronize(plan->stream);
+            if (e == hipSuccess)
+                e = hipMemcpy(&h_bad, d_bad, sizeof(h_bad), hipMemcpyDeviceToHost);
+        }
+        (void)hipFree(d_bad);
+        if (e != hipSuccess) {
+            (void)hipFree(d_cscale);
+            set_error("column value check failed: %s", hipGetErrorString(e));
+            return e == hipErrorOutOfMemory ? ECC_ERR_ALLOC : ECC_ERR_DEVICE;
+        }
+        colscale = h_bad == 0;
+        if (!colscale) {
+            (void)hipFree(d_cscale);
+            d_cscale = nullptr;
+        }
+    }
+    // owned by the handle from here on (freed by fail() below or by destroy)
+    struct CscaleGuard {
+        double **p;
+        ~CscaleGuard() {
+            if (*p) (void)hipFree(*p);
+        }
+    } cscale_guard{&d_cscale};
     // Very uneven rows over a vector of more than one range: the range layout
     // (each range of the vector, about kRangeBytes, is gathered by all
-    // workgroups at once and stays in the XCDs' L2).
+    // workgroups at once, so that the gathers of a time hit one window of
+    // the vector).  Without a value stream
+    // the sub-rows' own costs weigh more, and wider ranges pay: measured on
+    // MI355X (the same PageRank), 452 us per iteration at 16 MiB against 472
+    // at 8 MiB and 512 unsplit; the general form takes 533 at 8 MiB and 539
+    // at 16 MiB.
+    const int64_t range_bytes = opts.range_bytes > 0 ? opts.range_bytes
+                                : colscale            ? kRangeBytesColumns
+                                                      : kRangeBytes;
     const int32_t n_ranges = irregular ? range_count(n, range_bytes) : 1;
     const int layout = irregular ? (n_ranges >= 2 ? kLayRanges : kLaySorted)
                                  : (short_rows ? kLayShort : kLayStream);
@@ -1720,7 +1943,10 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
     M->bandwidth = bandwidth;
     M->tile_plane = tile_plane;
     M->tile_rows = tile_rows;
-    M->grid = sweep_grid(M->n_items, kind, layout, M->short_r);
+    M->grid = sweep_grid(M->n_items, kind, layout, M->short_r, colscale);
+    M->colscale = colscale;
+    M->d_cscale = d_cscale;
+    d_cscale = nullptr;
     // Queue-claimed items for a short-layout matrix that gives each workgroup
     // many items (the static walk's drift grows with them): measured on
     // MI355X, Jacobi on the 400^3 7-point stencil, 1.55 against 1.66 ms per
@@ -1761,8 +1987,9 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
             hipMalloc((void **)&M->d_srow_ptr, sizeof(int32_t) * (n + 1)) != hipSuccess ||
             hipMalloc((void **)&M->d_scol, sizeof(int32_t) * std::max<int64_t>(1, A->nnz)) !=
                 hipSuccess ||
-            hipMalloc((void **)&M->d_sval, sizeof(double) * std::max<int64_t>(1, A->nnz)) !=
-                hipSuccess)
+            (!colscale &&
+             hipMalloc((void **)&M->d_sval, sizeof(double) * std::max<int64_t>(1, A->nnz)) !=
+                 hipSuccess))
             return fail("hipMalloc of the sorted copy failed");
         if (hipMemcpy(M->d_order, order.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice) !=
                 hipSuccess ||
@@ -1787,7 +2014,8 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
         if (!up((void **)&M->d_srow_ptr, RB.srp.data(), sizeof(int32_t) * RB.srp.size()) ||
             !up((void **)&M->d_sinfo, RB.sinfo.data(), sizeof(int2) * RB.sinfo.size()) ||
             !up((void **)&M->d_scol, RB.scol.data(), sizeof(int32_t) * RB.scol.size()) ||
-            !up((void **)&M->d_sval, RB.sval.data(), sizeof(double) * RB.sval.size()) ||
+            (!colscale &&
+             !up((void **)&M->d_sval, RB.sval.data(), sizeof(double) * RB.sval.size())) ||
             !up((void **)&M->d_rmask, RB.rmask.data(), sizeof(uint16_t) * RB.rmask.size()) ||
             !up((void **)&M->d_diag, RB.diag.data(), sizeof(double) * RB.diag.size()) ||
             !up((void **)&M->d_rfix, RB.rfix.data(), sizeof(Fixup) * RB.rfix.size()))
@@ -1809,6 +2037,9 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
         if (hipGetLastError() != hipSuccess || hipStreamSynchronize(plan->stream) != hipSuccess)
             return fail("building the item-major entries failed");
     }
+    if (colscale && (hipMalloc((void **)&M->d_zown, sizeof(double) * n) != hipSuccess ||
+                     hipMalloc((void **)&M->d_zhat, sizeof(double) * n) != hipSuccess))
+        return fail("hipMalloc of the scaled views failed");
     // two buffers of G + 1 partials: a loop iteration writes one while the
     // next launch reduces the other
     if (hipMalloc((void **)&M->d_partials, sizeof(double) * 2 * M->n_part) != hipSuccess)
@@ -1860,6 +2091,9 @@ ecc_status_t ecc_matrix_destroy(ecc_matrix_t M) {
     (void)hipFree(M->d_ell_col);
     (void)hipFree(M->d_ell_val);
     (void)hipFree(M->d_queue);
+    (void)hipFree(M->d_cscale);
+    (void)hipFree(M->d_zown);
+    (void)hipFree(M->d_zhat);
     delete M;
     return ECC_OK;
 }
@@ -1884,6 +2118,14 @@ ecc_status_t ecc_matrix_tiling(ecc_matrix_t M, int64_t *plane_rows, int64_t *til
     ECC_ARG(plane_rows != nullptr && tile_rows != nullptr, "NULL output");
     *plane_rows = M->tile_plane;
     *tile_rows = M->tile_rows;
+    return ECC_OK;
+}
+
+ecc_status_t ecc_matrix_columns(ecc_matrix_t M, int32_t *one_value) {
+    clear_error();
+    ECC_ARG(M != nullptr, "matrix is NULL");
+    ECC_ARG(one_value != nullptr, "NULL output");
+    *one_value = M->colscale ? 1 : 0;
     return ECC_OK;
 }
 

@@ -33,7 +33,7 @@ def test_library_loads_and_exports_header():
     exp = exported_symbols()
     assert decl == exp
     assert sorted(E.EXPORTED) == decl          # the binding covers every entry point
-    assert E.ecc_abi_version() == 2
+    assert E.ecc_abi_version() == 3
 
 
 def header_constants():

@@ -34,6 +34,9 @@ def test_byte_model_and_host_fields():
     sys.path.insert(0, ROOT)
     import bench
     assert bench.sweep_bytes(64_000_000, 447_040_000) == 12 * 447_040_000 + 28 * 64_000_000 + 4
+    # one value per column: 8 bytes per column in place of 8 per nonzero
+    assert (bench.sweep_bytes(4_194_304, 67_108_864, True)
+            == bench.sweep_bytes(4_194_304, 67_108_864) - 8 * 67_108_864 + 8 * 4_194_304)
     cores, model = bench.host_cpu()
     assert cores == len(os.sched_getaffinity(0)) and cores >= 1
     assert model is None or isinstance(model, str)

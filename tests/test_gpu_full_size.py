@@ -28,8 +28,24 @@ def _gpu():
 
 
 def test_pagerank_rmat_full():
-    """PageRank on R-MAT scale 22 (2^26 edges), 64 ranks, S = 4."""
-    _solve_and_compare(W.pagerank_rmat(), bitwise=False, threads=THREADS)
+    """PageRank on R-MAT scale 22 (2^26 edges), 64 ranks, S = 4: the range
+    layout in 2 column ranges, in the column-value form, against the oracle
+    (normwise); then, both over 4 ranges of 8 MiB, the column-value form and
+    the general form give bitwise equal iterates."""
+    from paper_2203_17063_amd import capi as E
+    from test_gpu_parity import _iterative, _solve_x_rho
+    prob = W.pagerank_rmat()
+    run = _iterative(prob)
+    assert E.ecc_matrix_layout(run.mat) == (E.ECC_LAYOUT_RANGES, 2)
+    assert E.ecc_matrix_columns(run.mat) == 1
+    run.close()
+    _solve_and_compare(prob, bitwise=False, threads=THREADS)
+    rb = 8 << 20
+    a = _solve_x_rho(prob, rb, columns=E.ECC_COLUMNS_AUTO)
+    g = _solve_x_rho(prob, rb, columns=E.ECC_COLUMNS_GENERAL)
+    assert a[4] == 1 and g[4] == 0 and a[0] == g[0]
+    assert np.array_equal(a[1], g[1]) and np.array_equal(a[2], g[2])
+    assert np.allclose(a[3], g[3], rtol=1e-12, atol=0.0)
 
 
 def test_jacobi_3d_full():

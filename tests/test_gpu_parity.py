@@ -258,19 +258,22 @@ def _floor(prob, x):
     return float(np.sum(prob.alpha * wx + prob.beta + np.abs(x)))
 
 
-def _iterative(prob, range_bytes=0, tile_rows=0, schedule=0):
-    """The problem resident on the GPU; range_bytes / tile_rows / schedule are
-    the matrix set-up options (0: the library's choice)."""
+def _iterative(prob, range_bytes=0, tile_rows=0, schedule=0, columns=0):
+    """The problem resident on the GPU; range_bytes / tile_rows / schedule /
+    columns are the matrix set-up options (0: the library's choice)."""
     return _runner().Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts,
                                prob.S, prob.mask, prob.kind, b=prob.b, alpha=prob.alpha,
                                beta=prob.beta, x0=prob.x0, range_bytes=range_bytes,
-                               tile_rows=tile_rows, schedule=schedule)
+                               tile_rows=tile_rows, schedule=schedule, columns=columns)
 
 
 def _solve_and_compare(prob, bitwise, threads=8, layout=None, range_bytes=0, tile_rows=0,
-                       tiling=None, schedule=0, expect_schedule=None, solves=1):
+                       tiling=None, schedule=0, expect_schedule=None, solves=1, columns=0,
+                       one_value=None):
     announce("solve", prob.name, prob.n, prob.A.nnz, prob.P, prob.T)
-    run = _iterative(prob, range_bytes, tile_rows, schedule)
+    run = _iterative(prob, range_bytes, tile_rows, schedule, columns)
+    if one_value is not None:  # the column-value form the set-up must choose
+        assert _capi().ecc_matrix_columns(run.mat) == one_value
     if tiling is not None:  # (plane rows, tile rows) the set-up must choose
         assert _capi().ecc_matrix_tiling(run.mat) == tiling
     if expect_schedule is not None:
@@ -494,11 +497,13 @@ def test_solve_arrow_split_rows():
     _solve_and_compare(_arrow_problem(), bitwise=False, layout="SORTED")
 
 
-def _powerlaw_problem(kind, n, counts, seed, T=25, S=2):
+def _powerlaw_problem(kind, n, counts, seed, T=25, S=2, column_values=False):
     """Rows whose lengths follow a heavy tail (most hold a few entries, a few
     hold thousands, one is split into pieces) at random columns: very uneven
-    rows, swept in the sorted layout.  PageRank rows may be empty."""
+    rows, swept in the sorted layout.  PageRank rows may be empty.  With
+    column_values every entry of column j holds the same value."""
     rng = np.random.default_rng(seed)
+    col_value = rng.uniform(0.05, 1.0, n) / 64.0
     lens = np.minimum((rng.pareto(1.1, n) * 2.0).astype(np.int64), n - 1)
     lens[rng.integers(0, n)] = n - 1                       # longer than one vector item
     lens[rng.choice(n, 6, replace=False)] = rng.integers(2049, 9000, 6)  # whole-workgroup rows
@@ -508,6 +513,8 @@ def _powerlaw_problem(kind, n, counts, seed, T=25, S=2):
         if kind == "jacobi" and i not in c:
             c = np.sort(np.concatenate([c[1:], [i]])) if c.size else np.array([i])
         v = rng.uniform(0.05, 1.0, c.size) / max(c.size, 1)
+        if column_values:
+            v = col_value[c]
         if kind == "jacobi":
             v = -v
             v[c == i] = 2.0 * np.abs(v).sum() + 1.0
@@ -550,6 +557,72 @@ def test_solve_pagerank_rmat_ranges(scale):
 
 def test_solve_arrow_ranges():
     _solve_and_compare(_arrow_problem(), bitwise=False, layout="RANGES", range_bytes=8192)
+
+
+def _solve_x_rho(prob, range_bytes=0, columns=0):
+    run = _iterative(prob, range_bytes, columns=columns)
+    iters = run.solve(tol=prob.tol, histories=True)
+    torch.cuda.synchronize()
+    out = (iters, run.d_x.cpu().numpy(), run.d_x_hat.cpu().numpy(),
+           run.d_rho.cpu().numpy()[:iters], _capi().ecc_matrix_columns(run.mat))
+    run.close()
+    return out
+
+
+@pytest.mark.parametrize("which", ["rmat12", "rmat15", "rmat17", "powerlaw"])
+@pytest.mark.parametrize("range_bytes", [0, 4096])
+def test_column_values_match_general_form(which, range_bytes):
+    """A matrix whose every column holds one value (the PageRank matrix, and
+    heavy-tailed rows with whole-workgroup rows and split rows) is swept from
+    the column values and the scaled views: iterate and assembled vector equal
+    the general form's bit for bit at every iteration count, in the sorted
+    and the range layout, and match the oracle (checked by
+    _solve_and_compare).  The residuals agree to rounding: the column-value
+    kernel holds no values in LDS, so more of its workgroups fit on a CU and
+    the sweep's per-workgroup partial sums group the rows differently."""
+    prob = (W.pagerank_rmat(scale=int(which[4:]), T=40) if which.startswith("rmat")
+            else _powerlaw_problem("power", 20000, 9, seed=77, column_values=True))
+    layout = "RANGES" if range_bytes else "SORTED"
+    _solve_and_compare(prob, bitwise=False, layout=layout, range_bytes=range_bytes, one_value=1)
+    a = _solve_x_rho(prob, range_bytes, columns=0)
+    g = _solve_x_rho(prob, range_bytes, columns=_capi().ECC_COLUMNS_GENERAL)
+    assert a[4] == 1 and g[4] == 0
+    assert a[0] == g[0]
+    assert np.array_equal(a[1], g[1]) and np.array_equal(a[2], g[2])
+    assert np.allclose(a[3], g[3], rtol=1e-12, atol=0.0)
+
+
+def test_column_values_choice():
+    """Only power matrices in the sorted or range layout whose columns each
+    hold one value, bit for bit, take the column-value form: one entry off by
+    one unit in the last place, a general heavy-tailed matrix, a Jacobi
+    matrix, a short-row matrix and the caller's ECC_COLUMNS_GENERAL keep the
+    general form."""
+    E = _capi()
+    announce("column values choice")
+    prob = W.pagerank_rmat(scale=10, T=2)
+
+    def one(p, **kw):
+        run = _iterative(p, **kw)
+        v = E.ecc_matrix_columns(run.mat)
+        run.close()
+        return v
+
+    assert one(prob) == 1
+    assert one(prob, range_bytes=4096) == 1
+    assert one(prob, columns=E.ECC_COLUMNS_GENERAL) == 0
+    val = prob.A.val.copy()
+    k = int(np.argmax(np.bincount(prob.A.col, minlength=prob.n)[prob.A.col]))  # busiest column
+    val[k] = np.nextafter(val[k], 1.0)
+    bent = dataclasses.replace(prob, A=W.CSR(prob.n, prob.n, prob.A.row_ptr, prob.A.col, val))
+    assert one(bent) == 0
+    assert one(_powerlaw_problem("power", 12000, 3, seed=5, T=2)) == 0
+    assert one(_powerlaw_problem("power", 12000, 3, seed=5, T=2, column_values=True)) == 1
+    assert one(_powerlaw_problem("jacobi", 12000, 3, seed=5, T=2)) == 0
+    assert one(_banded_problem("power", 3000, 6, 6, T=2)) == 0
+    with pytest.raises(E.EccError) as ei:
+        _iterative(prob, columns=7)
+    assert ei.value.status == E.ECC_ERR_ARG
 
 
 @pytest.mark.parametrize("kind", ["jacobi", "power"])
