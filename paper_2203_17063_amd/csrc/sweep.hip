@@ -1066,12 +1066,16 @@ __global__ __launch_bounds__(kNormThreads) void k_residual(const double *__restr
 // missing, duplicated or zero (Jacobi only) and entries whose column is out of
 // range, and finds the bandwidth max |col - row|.  bad[0] = bad rows,
 // bad[1] = bad columns, bad[2] = bandwidth.
+// Rows longer than kCheckLong entries are left to k_check_long.
+constexpr int32_t kCheckLong = 256;
+
 __global__ void k_check(int32_t n_rows, int32_t n_cols, const int32_t *__restrict__ row_ptr,
                         const int32_t *__restrict__ col, const double *__restrict__ val,
                         int32_t check_diag, unsigned long long *__restrict__ bad) {
     unsigned long long bad_rows = 0, bad_cols = 0, band = 0;
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n_rows;
          i += gridDim.x * blockDim.x) {
+        if (row_ptr[i + 1] - row_ptr[i] > kCheckLong) continue;
         int ndiag = 0;
         bool zero = false;
         for (int32_t k = row_ptr[i]; k < row_ptr[i + 1]; ++k) {
@@ -1087,6 +1091,44 @@ __global__ void k_check(int32_t n_rows, int32_t n_cols, const int32_t *__restric
         if (check_diag && (ndiag != 1 || zero)) ++bad_rows;
     }
     if (bad_rows) atomicAdd(&bad[0], bad_rows);
+    if (bad_cols) atomicAdd(&bad[1], bad_cols);
+    if (band) atomicMax(&bad[2], band);
+}
+
+// The same checks for the rows listed in `rows` (those longer than
+// kCheckLong), one workgroup per row.
+__global__ void k_check_long(int32_t n_long, const int32_t *__restrict__ rows, int32_t n_cols,
+                             const int32_t *__restrict__ row_ptr,
+                             const int32_t *__restrict__ col, const double *__restrict__ val,
+                             int32_t check_diag, unsigned long long *__restrict__ bad) {
+    __shared__ int s_ndiag, s_zero;
+    unsigned long long bad_cols = 0, band = 0;
+    for (int32_t r = blockIdx.x; r < n_long; r += gridDim.x) {
+        const int32_t i = rows[r];
+        if (threadIdx.x == 0) {
+            s_ndiag = 0;
+            s_zero = 0;
+        }
+        __syncthreads();
+        int ndiag = 0;
+        bool zero = false;
+        for (int32_t k = row_ptr[i] + threadIdx.x; k < row_ptr[i + 1]; k += blockDim.x) {
+            const int32_t c = col[k];
+            if (c < 0 || c >= n_cols) ++bad_cols;
+            const int64_t d = (int64_t)c - i;
+            band = max(band, (unsigned long long)(d < 0 ? -d : d));
+            if (c == i) {
+                ++ndiag;
+                zero = zero || (val[k] == 0.0);
+            }
+        }
+        if (ndiag) atomicAdd(&s_ndiag, ndiag);
+        if (zero) atomicOr(&s_zero, 1);
+        __syncthreads();
+        if (threadIdx.x == 0 && check_diag && (s_ndiag != 1 || s_zero))
+            atomicAdd(&bad[0], 1ull);
+        __syncthreads();
+    }
     if (bad_cols) atomicAdd(&bad[1], bad_cols);
     if (band) atomicMax(&bad[2], band);
 }
@@ -1753,23 +1795,41 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
         ECC_ARG(rp[i + 1] >= rp[i], "row_ptr must be non-decreasing (row %lld)", (long long)i);
     ECC_ARG(rp[n] == A->nnz, "row_ptr[n] = %d differs from nnz = %lld", rp[n], (long long)A->nnz);
 
-    // structural check on the device
+    // structural check on the device: short rows one per lane, long rows
+    // (listed here) one per workgroup
     int64_t bandwidth = 0;
     if (n > 0) {
+        std::vector<int32_t> long_rows;
+        for (int64_t i = 0; i < n; ++i)
+            if (rp[i + 1] - rp[i] > kCheckLong) long_rows.push_back((int32_t)i);
         unsigned long long *d_bad = nullptr;
-        ECC_HIP(hipMalloc((void **)&d_bad, 3 * sizeof(unsigned long long)));
+        int32_t *d_long = nullptr;
         unsigned long long h_bad[3] = {0, 0, 0};
-        hipError_t e = hipMemcpy(d_bad, h_bad, sizeof(h_bad), hipMemcpyHostToDevice);
+        hipError_t e = hipMalloc((void **)&d_bad, 3 * sizeof(unsigned long long));
+        if (e == hipSuccess && !long_rows.empty())
+            e = hipMalloc((void **)&d_long, sizeof(int32_t) * long_rows.size());
+        if (e == hipSuccess && d_long)
+            e = hipMemcpy(d_long, long_rows.data(), sizeof(int32_t) * long_rows.size(),
+                          hipMemcpyHostToDevice);
+        if (e == hipSuccess) e = hipMemcpy(d_bad, h_bad, sizeof(h_bad), hipMemcpyHostToDevice);
         if (e == hipSuccess) {
             const int blocks = (int)std::min<int64_t>(4096, (n + 255) / 256);
             hipLaunchKernelGGL(k_check, dim3(blocks), dim3(256), 0, plan->stream, (int32_t)n,
                                (int32_t)A->n_cols, A->d_row_ptr, A->d_col, A->d_val,
                                kind == ECC_KIND_JACOBI ? 1 : 0, d_bad);
+            if (d_long) {
+                const int lb = (int)std::min<size_t>(4096, long_rows.size());
+                hipLaunchKernelGGL(k_check_long, dim3(lb), dim3(256), 0, plan->stream,
+                                   (int32_t)long_rows.size(), d_long, (int32_t)A->n_cols,
+                                   A->d_row_ptr, A->d_col, A->d_val,
+                                   kind == ECC_KIND_JACOBI ? 1 : 0, d_bad);
+            }
             e = hipGetLastError();
             if (e == hipSuccess) e = hipStreamSynchronize(plan->stream);
             if (e == hipSuccess) e = hipMemcpy(h_bad, d_bad, sizeof(h_bad), hipMemcpyDeviceToHost);
         }
         (void)hipFree(d_bad);
+        (void)hipFree(d_long);
         if (e != hipSuccess) {
             set_error("matrix check failed: %s", hipGetErrorString(e));
             return ECC_ERR_DEVICE;

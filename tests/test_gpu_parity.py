@@ -870,6 +870,37 @@ def test_matrix_checks():
     run.close()
 
 
+def test_matrix_checks_long_rows():
+    """Rows longer than 256 entries are checked by a workgroup each: a zero
+    or doubled diagonal entry and an out-of-range column in such a row are
+    refused, as in short rows; the unchanged arrow matrix is accepted."""
+    E, R = _capi(), _runner()
+    prob = _arrow_problem(n=5000, T=2)
+    announce("matrix checks, long rows")
+    rp, col, val = prob.A.row_ptr, prob.A.col, prob.A.val
+    run = _iterative(prob)
+    row0 = np.arange(rp[0], rp[1])
+    assert row0.size > 256 and (col[row0] == 0).sum() == 1
+
+    def refused(c, v, kind):
+        d_c, d_v = torch.from_numpy(c).cuda(), torch.from_numpy(v).cuda()
+        csr = E.make_csr(prob.n, prob.n, prob.A.nnz, run.d_row_ptr, d_c, d_v)
+        with pytest.raises(E.EccError) as ei:
+            E.ecc_matrix_create(run.plan.handle, csr, kind)
+        return ei.value.status
+
+    v = val.copy()
+    v[row0[col[row0] == 0]] = 0.0
+    assert refused(col, v, E.ECC_KIND_JACOBI) == E.ECC_ERR_ARG
+    c = col.copy()
+    c[row0[-1]] = 0                        # a second diagonal entry in row 0
+    assert refused(c, val, E.ECC_KIND_JACOBI) == E.ECC_ERR_ARG
+    c = col.copy()
+    c[row0[-1]] = prob.n                   # a column one past the end
+    assert refused(c, val, E.ECC_KIND_POWER) == E.ECC_ERR_ARG
+    run.close()
+
+
 @pytest.mark.parametrize("n,off", [(0, 0), (1, 0), (3, 0), (1001, 0), (1001, 1), (65536 * 3 + 5, 0),
                                    (65536 * 3 + 5, 1)])
 def test_stream_copy(n, off):
