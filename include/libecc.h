@@ -385,8 +385,10 @@ ecc_status_t ecc_residual(ecc_plan_t plan, const double *d_partials, int64_t n_p
  * on the device: no host round trip per iteration).
  *   d_x       in: x^0; out: the last iterate.  n_rows doubles.
  *   d_x_tmp   workspace, n_rows doubles.
- *   d_x_hat   the assembled vector, n_rows doubles (contents on entry unused:
- *             at the plan's first clock every block arrives).
+ *   d_x_hat   the assembled vector, n_rows doubles.  in: as the plan's last
+ *             clock left it (blocks that do not arrive at the first iteration
+ *             keep these values; unused at the plan's first clock, when every
+ *             block arrives); out: as the last iteration leaves it.
  *   d_mask    device [T][P] bytes; row t is the arrival mask of iteration t.
  *   d_rho     device [T] doubles: the norm of every iteration run.
  *   d_eff_hist, d_age_hist  optional device [T][P] histories.

@@ -359,6 +359,8 @@ struct ecc_plan_s {
     ecc::Tile *d_tiles = nullptr;   // assembly tiles (packed layout)
     int64_t n_tiles = 0;
     int32_t *d_ctrl = nullptr;      // [0] done flag, [1] iterations run (loop control)
+    int32_t *h_ctrl = nullptr;      // pinned host copy of d_ctrl[0..1], written by the
+                                    // single-launch solve (no copy back to the host)
     double *d_scalar = nullptr;     // scratch result of ecc_residual
 
     // optional event timing per kernel kind

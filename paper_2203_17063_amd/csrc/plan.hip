@@ -214,6 +214,12 @@ static ecc_status_t ecc_plan_create_impl(int32_t P, const int64_t *h_counts, con
     ALLOC(pl->d_eff, sizeof(uint8_t) * P);
     ALLOC(pl->d_forced, sizeof(unsigned long long));
     ALLOC(pl->d_ctrl, sizeof(int32_t) * 4);
+    if (hipHostMalloc((void **)&pl->h_ctrl, sizeof(int32_t) * 2, hipHostMallocDefault) !=
+        hipSuccess) {
+        pl->h_ctrl = nullptr;
+        set_error("hipHostMalloc of the loop control failed");
+        return fail(ECC_ERR_ALLOC);
+    }
     ALLOC(pl->d_scalar, sizeof(double) * 2);
     if (pl->has_layout) {
         ALLOC(pl->d_displs, sizeof(int64_t) * P);
@@ -275,6 +281,7 @@ ecc_status_t ecc_plan_destroy(ecc_plan_t plan) {
     (void)hipFree(plan->d_eff);
     (void)hipFree(plan->d_forced);
     (void)hipFree(plan->d_ctrl);
+    if (plan->h_ctrl) (void)hipHostFree(plan->h_ctrl);
     (void)hipFree(plan->d_scalar);
     (void)hipFree(plan->d_displs);
     (void)hipFree(plan->d_tiles);

@@ -49,21 +49,28 @@ extern "C" ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double 
     const int64_t clock0 = plan->clock;
     const int32_t P = plan->P;
 
-    hipLaunchKernelGGL(k_ctrl_reset, dim3(1), dim3(64), 0, plan->stream, plan->d_ctrl);
-    ECC_LAUNCH_CHECK();
     if (A->tiny && T > 0 && n > 0) {
-        // the whole loop in one launch; the last iterate lands in d_x
+        // the whole loop in one launch; the last iterate lands in d_x, and the
+        // kernel writes the loop control (which it sets whole) to the device
+        // and to pinned host memory (every earlier solve of the plan has
+        // synchronised, so no kernel still writes it)
+        plan->h_ctrl[0] = 0;
+        plan->h_ctrl[1] = -1;
         st = launch_solve_tiny(A, d_b, alpha, beta, d_x, d_x_hat, d_mask, T, tol, d_rho,
                                d_eff_hist, d_age_hist);
         if (st != ECC_OK) return st;
-        int32_t ctrl[2] = {0, 0};
-        ECC_HIP(hipMemcpyAsync(ctrl, plan->d_ctrl, sizeof(ctrl), hipMemcpyDeviceToHost,
-                               plan->stream));
         ECC_HIP(hipStreamSynchronize(plan->stream));
-        plan->clock = clock0 + ctrl[1];
-        *h_iters = ctrl[1];
+        const int32_t iters = plan->h_ctrl[1];
+        if (iters < 0 || iters > T) {
+            set_error("the single-launch solve reported %d iterations", iters);
+            return ECC_ERR_DEVICE;
+        }
+        plan->clock = clock0 + iters;
+        *h_iters = iters;
         return ECC_OK;
     }
+    hipLaunchKernelGGL(k_ctrl_reset, dim3(1), dim3(64), 0, plan->stream, plan->d_ctrl);
+    ECC_LAUNCH_CHECK();
     const int32_t *done = plan->d_ctrl;
     const int64_t G1 = A->n_part;
     // Without a tolerance and without split rows, every iteration is a single

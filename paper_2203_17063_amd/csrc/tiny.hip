@@ -38,7 +38,7 @@ struct TinyArgs {
     const double *b;
     double alpha, beta;
     double *x;      // in: x^0; out: the last iterate
-    double *x_hat;  // out: the assembled vector after the last iteration
+    double *x_hat;  // in: the assembled vector of the plan's last clock; out: after the last iteration
     const uint8_t *mask;
     int32_t T;
     double tol;
@@ -52,51 +52,86 @@ struct TinyArgs {
     uint8_t *eff_state;
     unsigned long long *forced;
     int32_t *ctrl;     // ctrl[0] := 1 when stopped by the tolerance, ctrl[1] := iterations
+    int32_t *ctrl_host;  // the same two values in pinned host memory
     int32_t norm;
 };
 
-// RPT rows per thread: thread tid sweeps rows tid, tid + kTinyThreads, ...,
-// with their entries in registers (4 rows of 3 entries, or 2 of up to 8,
-// fit the 128 VGPRs of a 1,024-thread workgroup without spilling).
+// Rows of a thread: with j = tid mod 256 and q = tid / 256, rows
+// j + 256 (RPT q + m), m = 0 .. RPT-1.  The norm adds the rows' shares as
+// reduce_values does with 256 threads: thread j adds rows j, j + 256, ...
+// eight at a time as a pairwise tree; the RPT rows of one thread here are
+// one subtree of such a group of eight (a pair, or a half), which the thread
+// sums in registers, so only those subtree sums pass through LDS.  Rows in a
+// group of eight that is not complete (the last rows before n) are added one
+// by one, through LDS, as reduce_values adds them.
+// The entries of a thread's rows (the diagonal entry held apart for Jacobi;
+// padding turned into a zero value that gathers a zero), the LDS offsets
+// their gathers read, its right-hand sides and its rows' current iterate
+// stay in registers.  The iterate has one copy in LDS: the sweep keeps the
+// new values in registers, and each thread writes its rows' values over
+// the old ones only once every gather of the sweep is done (a barrier).
+// The staleness decisions depend only on the arrival flags and the versions
+// (Algorithm 1's acceptance test), not on the iterate: thread p decides rank
+// p's steps for a chunk of iterations at once, into LDS, and the
+// iterations then only read them.  The loop thus issues no global load: no
+// wait on the memory counter (which also counts the history stores) stalls
+// an iteration.
+constexpr int kTinyMaskBytes = 1024;  // arrival flags staged per chunk
+constexpr int kTinyChunkMax = 256;    // iterations per chunk at most
 
 template <int KIND, int R, int RPT>
 __global__ __launch_bounds__(kTinyThreads) void k_solve_tiny(TinyArgs a) {
+    static_assert(RPT == 2 || RPT == 4, "a thread's rows form a subtree of a group of eight");
     static_assert(RPT * kTinyThreads <= kTinyMaxRows, "rows of a thread beyond the LDS arrays");
-    // [0], [1]: the iterate and the next one (in turn); [2]: the assembled vector
-    __shared__ double s_v[3][kTinyMaxRows];
-    __shared__ double s_c[kTinyMaxRows];        // each row's norm contribution
-    __shared__ uint8_t s_item[kTinyMaxRows];    // the work item of each row
-    __shared__ int32_t s_ver[2][kTinyMaxP];     // versions before / after a step
+    static_assert(kTinyThreads == 4 * kNormThreads, "four row sets per norm thread");
+    constexpr int N = kTinyMaxRows;
+    constexpr int RO = KIND == ECC_KIND_JACOBI ? R - 1 : R;  // entries summed per row
+    static_assert(RPT * RO <= 32, "one bit per entry in a 32-bit mask");
+    // [0, N): the iterate; [N, 2N): the assembled vector; [2N]: zero,
+    // gathered by padding entries
+    __shared__ double s_v[2 * N + 2];
+    __shared__ double s_c[N];                    // shares of rows outside complete groups
+    __shared__ double s_h[4][kNormThreads];      // subtree sums of complete groups, [q][j]
+    __shared__ uint8_t s_item[N];                // the work item of each row
+    __shared__ uint8_t s_mask[kTinyMaskBytes];   // arrival flags of a chunk, [u][p]
+    __shared__ uint8_t s_eff[kTinyMaskBytes];    // its decisions: bit 0 taken, bit 1 forced
+    __shared__ int32_t s_nv[kTinyMaskBytes];     // the versions after each of its steps
     __shared__ double s_red[kNormThreads / 64];
-    __shared__ unsigned s_forced;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
+    const int jn = tid & (kNormThreads - 1), qn = tid / kNormThreads;
     const int32_t n = a.n, P = a.P, NI = a.n_items;
-    for (int32_t i = tid; i < n; i += kTinyThreads) s_v[0][i] = a.x[i];
-    const int32_t *ver_in = a.version + (a.t0 & 1) * P;
-    for (int32_t p = tid; p < P; p += kTinyThreads) s_ver[0][p] = ver_in[p];
+    for (int32_t i = tid; i < n; i += kTinyThreads) {
+        s_v[i] = a.x[i];
+        s_v[N + i] = a.x_hat[i];  // the assembled vector of the plan's last clock
+    }
+    if (tid == 0) s_v[2 * N] = 0.0;
     for (int32_t q = tid; q < NI * kSweepThreads; q += kTinyThreads) {
         const int32_t w = q / kSweepThreads, l = q % kSweepThreads;
         const WorkItem it = a.items[w];
         if (l < it.nrows) s_item[it.row0 + l] = (uint8_t)w;
     }
-    if (tid == 0) s_forced = 0;
+    // rank tid's version (its state between the decisions of two chunks)
+    int32_t ver = tid < P ? a.version[(a.t0 & 1) * P + tid] : 0;
     __syncthreads();
-    // this thread's rows: entries, right-hand side, rank block, held in
-    // registers for the whole solve (the item-major copy, read once)
-    int32_t col[RPT][R];
-    double val[RPT][R];
-    double bi[RPT];
-    int32_t blk[RPT], rk[RPT];  // rank block [lo, hi) packed as lo | hi << 16 (n <= 4096)
+    // row m of this thread is row0 + 256 m; rank of row m in bits 16 (m & 1)
+    // of rkp[m / 2] (ranks < 1024)
+    const int32_t row0 = jn + kNormThreads * RPT * qn;
+    uint32_t rkp[RPT / 2] = {};
+    int32_t ad[RPT][RO];  // byte offset in s_v of each gather
+    double val[RPT][RO];
+    double dg[RPT], bi[RPT], xr[RPT];
 #pragma unroll
-    for (int k = 0; k < RPT; ++k) {
-        const int32_t i = tid + k * kTinyThreads;
-        blk[k] = rk[k] = 0;
-        bi[k] = 0.0;
+    for (int m = 0; m < RPT; ++m) {
+        const int32_t i = row0 + kNormThreads * m;
+        dg[m] = bi[m] = xr[m] = 0.0;
+        int32_t c8[R];
+        double v8[R];
+        int32_t lo = 0, hi = 0;
 #pragma unroll
-        for (int j = 0; j < R; ++j) {
-            col[k][j] = -1;
-            val[k][j] = 0.0;
+        for (int e = 0; e < R; ++e) {
+            c8[e] = -1;
+            v8[e] = 0.0;
         }
         if (i < n) {
             const WorkItem it = a.items[s_item[i]];
@@ -104,144 +139,202 @@ __global__ __launch_bounds__(kTinyThreads) void k_solve_tiny(TinyArgs a) {
             const int64_t base = (int64_t)it.k0 * R + l;
             const int32_t pad = sell_pad(it.nrows);
 #pragma unroll
-            for (int j = 0; j < R; ++j) {
-                col[k][j] = a.ell_col[base + (int64_t)j * pad];
-                val[k][j] = a.ell_val[base + (int64_t)j * pad];
+            for (int e = 0; e < R; ++e) {
+                c8[e] = a.ell_col[base + (int64_t)e * pad];
+                v8[e] = a.ell_val[base + (int64_t)e * pad];
             }
-            blk[k] = it.lo | (it.hi << 16);
-            rk[k] = it.rank;
-            if (KIND == ECC_KIND_JACOBI) bi[k] = a.b[i];
+            lo = it.lo;
+            hi = it.hi;
+            rkp[m / 2] |= (uint32_t)it.rank << (16 * (m & 1));
+            if (KIND == ECC_KIND_JACOBI) bi[m] = a.b[i];
+            xr[m] = s_v[i];
+        }
+        int dpos = R;  // Jacobi: the diagonal entry, summed apart
+        if constexpr (KIND == ECC_KIND_JACOBI) {
+#pragma unroll
+            for (int e = R - 1; e >= 0; --e)
+                if (c8[e] == i) dpos = e;
+#pragma unroll
+            for (int e = 0; e < R; ++e)
+                if (e == dpos) dg[m] = v8[e];
+        }
+#pragma unroll
+        for (int o = 0; o < RO; ++o) {
+            // the others in CSR order (selects with fixed indices keep the
+            // arrays in registers)
+            const int32_t c = (KIND == ECC_KIND_JACOBI && o >= dpos) ? c8[o + 1] : c8[o];
+            const double v = (KIND == ECC_KIND_JACOBI && o >= dpos) ? v8[o + 1] : v8[o];
+            const bool in_own = c >= lo && c < hi;
+            // padding: value 0 times the zero slot adds +0 to a sum that
+            // is never -0 (it starts at +0, and only -0 + -0 gives -0), so
+            // it leaves the sum unchanged, as if the entry were skipped
+            val[m][o] = c >= 0 ? v : 0.0;
+            ad[m][o] = 8 * (c < 0 ? 2 * N : in_own ? c : N + c);
         }
     }
-    int cur = 0, iters = 0, stopped = 0;
+    // the group of eight of this thread's rows, and whether it is complete
+    // (its eight values, the zero partial at index n included, all exist)
+    const int32_t grp = (RPT * qn) / 8;
+    const bool complete = jn + 8 * kNormThreads * grp + 7 * kNormThreads <= n;
+    const char *sb = reinterpret_cast<const char *>(s_v);
+    int32_t iters = 0, stopped = 0;
     unsigned forced = 0;
-    // arrival flags, loaded one iteration ahead: of rank tid (its official
-    // decision) and of this thread's rows' ranks (their assembly)
-    uint8_t ar_p = (tid < P && a.T > 0) ? a.mask[tid] : 0;
-    uint8_t ar_r[RPT];
+    const int32_t chunk = min(kTinyChunkMax, max(1, kTinyMaskBytes / max(P, 1)));
+
+    // One iteration: the assembly of the taken ranks' rows, the sweep, the
+    // new iterate over the old one, the norm.  Returns whether the tolerance
+    // stops the loop.
+    auto iteration = [&](int32_t tc, int32_t u) -> bool {
+        const int32_t t = tc + u;
+        const uint8_t *ef = s_eff + u * P;
 #pragma unroll
-    for (int k = 0; k < RPT; ++k) ar_r[k] = a.T > 0 ? a.mask[rk[k]] : 0;
-    for (int32_t t = 0; t < a.T; ++t) {
-        const int64_t tt = a.t0 + t;
-        const int vb = t & 1;
-        const uint8_t arp = ar_p;
-        uint8_t arr[RPT];
-#pragma unroll
-        for (int k = 0; k < RPT; ++k) arr[k] = ar_r[k];
-        if (t + 1 < a.T) {
-            const uint8_t *mn = a.mask + (int64_t)(t + 1) * P;
-            if (tid < P) ar_p = mn[tid];
-#pragma unroll
-            for (int k = 0; k < RPT; ++k) ar_r[k] = mn[rk[k]];
-        }
-        // staleness decision of rank tid (P <= kTinyThreads): the plan's
-        // bookkeeping; every thread also decides its own rows' ranks from the
-        // same versions (the same result) and assembles those rows
-        if (tid < P) {
-            const int32_t v = s_ver[vb][tid];
-            const bool e = stale_select(v, arp, tt, a.S);
-            if (e && arp == 0 && v >= 0) ++forced;
-            const int32_t nv = e ? (int32_t)tt : v;
-            s_ver[vb ^ 1][tid] = nv;
-            if (a.eff_hist) a.eff_hist[(int64_t)t * P + tid] = e ? 1 : 0;
-            if (a.age_hist) a.age_hist[(int64_t)t * P + tid] = (int32_t)(tt - nv);
-        }
-        const double *xo = s_v[cur];
-        double *xn = s_v[cur ^ 1];
-        double *xh = s_v[2];
-#pragma unroll
-        for (int k = 0; k < RPT; ++k) {
-            const int32_t i = tid + k * kTinyThreads;
-            if (i < n && stale_select(s_ver[vb][rk[k]], arr[k], tt, a.S)) xh[i] = xo[i];
+        for (int m = 0; m < RPT; ++m) {
+            const int32_t i = row0 + kNormThreads * m;
+            const uint32_t r = (rkp[m / 2] >> (16 * (m & 1))) & 0xffffu;
+            if (i < n && (ef[r] & 1)) s_v[N + i] = xr[m];
         }
         lds_barrier();
-        // sweep: one thread per row, entries in CSR order, without branches
-        // (padding gathers entry 0 and is not added); every row's gathers
-        // first, so that the rows' arithmetic chains overlap
-        double y[RPT][R], xoi[RPT];
+        // every row's gathers first, so that the rows' arithmetic chains
+        // overlap
+        double y[RPT][RO];
 #pragma unroll
-        for (int k = 0; k < RPT; ++k) {
-            const int32_t i = tid + k * kTinyThreads;
+        for (int m = 0; m < RPT; ++m)
 #pragma unroll
-            for (int j = 0; j < R; ++j) {
-                const int32_t cj = col[k][j];
-                const int32_t c = cj >= 0 ? cj : 0;
-                const bool own = cj >= (blk[k] & 0xffff) && cj < (blk[k] >> 16);
-                y[k][j] = s_v[own ? cur : 2][c];  // one load: the view's source by index
+            for (int o = 0; o < RO; ++o)
+                y[m][o] = *reinterpret_cast<const double *>(sb + ad[m][o]);
+        double sh[RPT];
+#pragma unroll
+        for (int m = 0; m < RPT; ++m) {
+            double sum = 0.0;
+#pragma unroll
+            for (int o = 0; o < RO; ++o) sum = sum + val[m][o] * y[m][o];
+            double xnew, share;
+            if constexpr (KIND == ECC_KIND_JACOBI) {
+                const double bs = bi[m] - sum;
+                xnew = bs / dg[m];
+                const double r = bs - dg[m] * xr[m];
+                share = r * r;
+            } else {
+                xnew = a.alpha * sum + a.beta;
+                share = fabs(xnew - xr[m]);
             }
-            xoi[k] = xo[i];
+            xr[m] = xnew;
+            sh[m] = row0 + kNormThreads * m < n ? share : 0.0;  // index n: the zero partial
         }
+        if (complete) {
+            double h;
+            if constexpr (RPT == 4) h = (sh[0] + sh[1]) + (sh[2] + sh[3]);
+            else h = sh[0] + sh[1];
+            s_h[qn][jn] = h;
+        } else {
 #pragma unroll
-        for (int k = 0; k < RPT; ++k) {
-            const int32_t i = tid + k * kTinyThreads;
-            double s = 0.0, dg = 0.0;
-#pragma unroll
-            for (int j = 0; j < R; ++j) {
-                const int32_t cj = col[k][j];
-                const bool diag = KIND == ECC_KIND_JACOBI && cj == i;
-                if (diag) dg = val[k][j];
-                const double sn = s + val[k][j] * y[k][j];
-                s = (cj >= 0 && !diag) ? sn : s;
-            }
-            // rows past n (up to RPT x kTinyThreads <= kTinyMaxRows) compute
-            // into the unread tail of the LDS arrays: no branch per row
-            s_c[i] = row_finish<KIND>(i, s, dg, bi[k], xoi[k], a.alpha, a.beta, xn);
+            for (int m = 0; m < RPT; ++m)
+                if (row0 + kNormThreads * m < n) s_c[row0 + kNormThreads * m] = sh[m];
         }
         lds_barrier();
-        // the norm: the rows' shares and a last, zero, partial reduced in
-        // reduce_values' order (thread j takes rows j, j + 256, ..., groups of
-        // eight as pairwise trees, then the waves' sums in order)
+        // every gather of the sweep is done: the new iterate replaces the old
+        // (rows past n write into the unread tail of the array)
+#pragma unroll
+        for (int m = 0; m < RPT; ++m) s_v[row0 + kNormThreads * m] = xr[m];
+        // the norm in reduce_values' order: each complete group of eight as
+        // its tree, then the remaining values one by one
         if (tid < kNormThreads) {
             double acc = 0.0;
             int32_t k = tid;
-            for (; k + 7 * kNormThreads <= n; k += 8 * kNormThreads) {
-                double t8[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int32_t q = k + j * kNormThreads;
-                    t8[j] = q < n ? s_c[q] : 0.0;
-                }
-                acc += tree8(t8);
+            for (int g = 0; g < RPT / 2 && k + 7 * kNormThreads <= n;
+                 ++g, k += 8 * kNormThreads) {
+                if constexpr (RPT == 4) acc += s_h[2 * g][tid] + s_h[2 * g + 1][tid];
+                else acc += (s_h[0][tid] + s_h[1][tid]) + (s_h[2][tid] + s_h[3][tid]);
             }
             for (; k <= n; k += kNormThreads) acc += k < n ? s_c[k] : 0.0;
             acc = wave_sum_lane63(acc);
             if (lane == 63) s_red[wave] = acc;
         }
         lds_barrier();
-        double sum = s_red[0];
-        for (int w = 1; w < kNormThreads / 64; ++w) sum += s_red[w];
-        const double v = (a.norm == ECC_NORM_L2) ? sqrt(sum) : sum;
-        if (tid == 0) a.rho[t] = v;
-        cur ^= 1;
-        ++iters;
-        if (a.tol > 0.0 && v < a.tol) {
-            stopped = 1;
-            break;
+        bool stop = false;
+        if (tid == 0 || a.tol > 0.0) {  // uniform unless only thread 0's rho is needed
+            double sum = s_red[0];
+            for (int w = 1; w < kNormThreads / 64; ++w) sum += s_red[w];
+            const double v = (a.norm == ECC_NORM_L2) ? sqrt(sum) : sum;
+            if (tid == 0) a.rho[t] = v;
+            stop = a.tol > 0.0 && v < a.tol;
         }
+        return stop;
+    };
+
+    for (int32_t tc = 0; tc < a.T && !stopped; tc += chunk) {
+        const int32_t cn = min(chunk, a.T - tc);
+        __syncthreads();  // the previous chunk's decisions are no longer read
+        for (int32_t q = tid; q < cn * P; q += kTinyThreads)
+            s_mask[q] = a.mask[(int64_t)tc * P + q];
+        __syncthreads();
+        if (tid < P) {
+            // rank tid's decisions at the chunk's steps, in order: taken if
+            // fresh, never taken, or too stale (as record_step)
+            for (int32_t u0 = 0; u0 < cn; u0 += 8) {
+                uint8_t ar[8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) ar[k] = u0 + k < cn ? s_mask[(u0 + k) * P + tid] : 0;
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    if (u0 + k < cn) {
+                        const int64_t tt = a.t0 + tc + u0 + k;
+                        const bool e = stale_select(ver, ar[k], tt, a.S);
+                        const bool f = e && ar[k] == 0 && ver >= 0;
+                        ver = e ? (int32_t)tt : ver;
+                        s_eff[(u0 + k) * P + tid] = (uint8_t)((e ? 1 : 0) | (f ? 2 : 0));
+                        s_nv[(u0 + k) * P + tid] = ver;
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        int32_t u = 0;
+        bool stop = false;
+        while (!stop && u < cn) {
+            stop = iteration(tc, u);
+            ++u;
+        }
+        // the histories and forced arrivals of the iterations run
+        if (tid < P) {
+            for (int32_t k = 0; k < u; ++k) {
+                const uint8_t e = s_eff[k * P + tid];
+                const int64_t tt = a.t0 + tc + k;
+                if (a.eff_hist) a.eff_hist[(int64_t)(tc + k) * P + tid] = e & 1;
+                if (a.age_hist) a.age_hist[(int64_t)(tc + k) * P + tid] =
+                    (int32_t)(tt - s_nv[k * P + tid]);
+                forced += (e >> 1) & 1;
+            }
+            if (u < cn) ver = s_nv[(u - 1) * P + tid];  // stopped: the last step run
+        }
+        iters += u;
+        if (stop) stopped = 1;
     }
     // state after the last iteration: the iterate, the assembled vector, the
     // plan's versions (half (t0 + iters) & 1), ages, decisions, forced count
-    if (forced) atomicAdd(&s_forced, forced);
     __syncthreads();
-    for (int32_t i = tid; i < n; i += kTinyThreads) {
-        a.x[i] = s_v[cur][i];
-        a.x_hat[i] = s_v[2][i];
-    }
-    if (iters > 0) {
-        int32_t *ver_out = a.version + ((a.t0 + iters) & 1) * P;
+#pragma unroll
+    for (int m = 0; m < RPT; ++m)
+        if (row0 + kNormThreads * m < n) a.x[row0 + kNormThreads * m] = xr[m];
+    for (int32_t i = tid; i < n; i += kTinyThreads) a.x_hat[i] = s_v[N + i];
+    if (iters > 0 && tid < P) {
         const int64_t tl = a.t0 + iters - 1;
-        const int vb = iters & 1;
-        for (int32_t p = tid; p < P; p += kTinyThreads) {
-            const int32_t nv = s_ver[vb][p];
-            ver_out[p] = nv;
-            a.age_state[p] = (int32_t)(tl - nv);
-            a.eff_state[p] = nv == (int32_t)tl ? 1 : 0;
-        }
+        a.version[((a.t0 + iters) & 1) * P + tid] = ver;
+        a.age_state[tid] = (int32_t)(tl - ver);
+        a.eff_state[tid] = ver == (int32_t)tl ? 1 : 0;
     }
+    // the forced arrivals, added in rank order (one thread: P <= kTinyMaxP)
+    __shared__ unsigned s_forced[kTinyMaxP];
+    if (tid < P) s_forced[tid] = forced;
+    __syncthreads();
     if (tid == 0) {
-        *a.forced = *a.forced + s_forced;
+        unsigned long long total = 0;
+        for (int32_t p = 0; p < P; ++p) total += s_forced[p];
+        *a.forced = *a.forced + total;
         a.ctrl[0] = stopped;
         a.ctrl[1] = iters;
+        a.ctrl_host[0] = stopped;
+        a.ctrl_host[1] = iters;
     }
 }
 
@@ -275,6 +368,7 @@ ecc_status_t launch_solve_tiny(ecc_matrix_t M, const double *d_b, double alpha, 
     a.eff_state = pl->d_eff;
     a.forced = pl->d_forced;
     a.ctrl = pl->d_ctrl;
+    a.ctrl_host = pl->h_ctrl;
     a.norm = M->kind == ECC_KIND_JACOBI ? ECC_NORM_L2 : ECC_NORM_L1;
     if (!tiny_fits(a.n, M->short_r, M->n_items, a.P) || M->layout != kLayShort) {
         set_error("internal: the single-launch solve does not fit the matrix");

@@ -335,6 +335,66 @@ def test_solve_pagerank_rmat_small(scale):
     _solve_and_compare(W.pagerank_rmat(scale=scale, T=60), bitwise=False, layout="SORTED")
 
 
+def _plan_continuation(prob, split, **kw):
+    """One ecc_solve of T iterations against two calls of split and T - split
+    iterations without a reset in between (the second continues the plan's
+    clock from the iterate and assembled vector the first left).  Returns
+    both runs' (x, x_hat, rho, eff, age, clock)."""
+    E = _capi()
+    run = _iterative(prob, **kw)
+    P, T = prob.P, prob.T
+    out = []
+    for parts in ((0, T), (0, split, T)):
+        run.plan.reset()
+        run.load_x0()
+        rho = torch.zeros(T, dtype=torch.float64, device="cuda")
+        eff = torch.zeros((T, P), dtype=torch.uint8, device="cuda")
+        age = torch.zeros((T, P), dtype=torch.int32, device="cuda")
+        for t0, t1 in zip(parts[:-1], parts[1:]):
+            # the iterate of the first call is the second call's x^0
+            it = E.ecc_solve(run.plan.handle, run.mat, run.d_b, run.alpha, run.beta, run.d_x,
+                             run.d_x_tmp, run.d_x_hat, run.d_mask[t0:].data_ptr(), t1 - t0, 0.0,
+                             rho[t0:].data_ptr(), eff[t0:].data_ptr(), age[t0:].data_ptr())
+            assert it == t1 - t0
+        torch.cuda.synchronize()
+        out.append((run.d_x.cpu().numpy(), run.d_x_hat.cpu().numpy(), rho.cpu().numpy(),
+                    eff.cpu().numpy(), age.cpu().numpy(), run.plan.stats()[0]))
+    schedule = E.ecc_matrix_schedule(run.mat)
+    run.close()
+    return out, schedule
+
+
+@pytest.mark.parametrize("which", ["jacobi1d", "jacobi2d", "jacobi3d_unfused", "pagerank"])
+def test_solve_continues_plan(which):
+    """ecc_solve continues a plan: two calls (the second starting where the
+    first stopped, with blocks that do not arrive at its first iteration
+    keeping the assembled values the first call left) equal one call of both
+    lengths bit for bit -- iterate, assembled vector, norms, histories and
+    clock -- in the single-launch loop, the fused loop, the loop with
+    separate assembly launches and the column-value range loop."""
+    E = _capi()
+    if which == "jacobi1d":
+        prob, kw, sched = W.jacobi_1d(), {}, E.ECC_SCHEDULE_SINGLE
+        rng = np.random.default_rng(3)
+        mask = (rng.random(prob.mask.shape) < 0.5).astype(np.uint8)
+        mask[0] = 1
+        prob = dataclasses.replace(prob, S=2, mask=mask)
+    elif which == "jacobi2d":
+        prob, kw, sched = W.jacobi_2d(N=64, T=30), {}, None
+    elif which == "jacobi3d_unfused":
+        prob, kw, sched = W.jacobi_3d(N=16, T=24, P=2048), {}, None
+    else:
+        prob, kw, sched = W.pagerank_rmat(scale=12, T=30), {"range_bytes": 4096}, None
+    announce("solve continuation", which)
+    # a block does not arrive at the continuation's first iteration
+    split = next(t for t in range(prob.T // 3, prob.T) if not prob.mask[t].all())
+    (a, b), schedule = _plan_continuation(prob, split, **kw)
+    if sched is not None:
+        assert schedule == sched
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
+
+
 def test_solve_many_ranks_unfused():
     """More ranks than a workgroup stages in LDS: separate assembly launches."""
     _solve_and_compare(W.jacobi_3d(N=24, T=30, P=2048), bitwise=True)
