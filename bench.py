@@ -41,16 +41,24 @@ METRIC = "assembled+iterated GB/s and iterations/s at 1 GPU; % of HBM peak"
 PROFILES = os.path.join(ROOT, "profiles")
 
 
-def sweep_bytes(n, nnz, column_values=False):
+def sweep_bytes(n, nnz):
     """Algorithmic bytes of one sweep: col + val per nonzero, row_ptr, the x
     view, b (or x_own for the update norm), the written iterate.  This is the
-    model of the method's data, whatever layout the library sweeps (the
-    short-row copy reads no row_ptr but its padding).  A matrix whose columns
-    each hold one value (PageRank's A^T D^-1) is that value per column in
-    place of a value per nonzero."""
-    if column_values:
-        return 4 * nnz + 36 * n + 4
+    model of the method's data (CSR), whatever layout the library sweeps."""
     return 12 * nnz + 28 * n + 4
+
+
+def format_sweep_bytes(n, nnz, form, row_class):
+    """The same for the bytes the library's copy of the matrix holds: the
+    diagonal form reads values by diagonal (row_class per row, absent ones
+    included) and a mask byte per row, and no column indices or row
+    pointers; the column-value form one value per column in place of one
+    per nonzero.  The general form: the CSR model."""
+    if form == "diagonals":
+        return 8 * row_class * n + n + 24 * n
+    if form == "column values":
+        return 4 * nnz + 4 * (n + 1) + 8 * n + 24 * n
+    return sweep_bytes(n, nnz)
 
 
 def kernel_source_digest(names):
@@ -218,7 +226,9 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
     layout, slots = E.ecc_matrix_layout(run.mat)
     schedule = E.ecc_matrix_schedule(run.mat)
     tiling = E.ecc_matrix_tiling(run.mat)
-    column_values = bool(E.ecc_matrix_columns(run.mat))
+    form_id, offsets = E.ecc_matrix_form(run.mat)
+    form = {E.ECC_FORM_GENERAL: "general", E.ECC_FORM_COLUMN_VALUES: "column values",
+            E.ECC_FORM_DIAGONALS: "diagonals"}[form_id]
     run.close()
 
     counts = prob.counts
@@ -229,7 +239,9 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
     fused = times["SWEEP"][1] > 0 and times["ASSEMBLE"][1] == 0
     per_elem = 8.0 if fused else 16.0
     b_assemble = per_elem * eff_elems + 14.0 * prob.P
-    b_sweep = float(sweep_bytes(prob.n, prob.A.nnz, column_values))
+    b_sweep = float(sweep_bytes(prob.n, prob.A.nnz))
+    b_sweep_form = float(format_sweep_bytes(prob.n, prob.A.nnz, form,
+                                            slots if layout == E.ECC_LAYOUT_SHORT else 0))
     b_norm = 16.0 * n_part                 # partials written, then read by the second pass
     bytes_per_step = float(np.sum(b_assemble)) + iters * (b_sweep + b_norm)
     dom = b_sweep + b_norm + (float(np.mean(b_assemble)) if fused else 0.0)
@@ -242,6 +254,7 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
         "iters": iters, "wall": wall, "wall_events": wall_events, "times": times,
         "bytes_per_step": bytes_per_step, "dominant": "sweep",
         "dominant_bytes": dom, "footprint": footprint, "rho_last": float(rho[-1]),
+        "dominant_format_bytes": dom - b_sweep + b_sweep_form,
         "unit_per_step": iters, "fused": fused, "dom_ms": dom_ms,
         "dom_timing": "HIP events on the plan's stream around the timed region; the sweep's "
                       "share is that time minus a 0-iteration solve's (set-up) and the other "
@@ -251,7 +264,7 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
                   "schedule": {E.ECC_SCHEDULE_STATIC: "static", E.ECC_SCHEDULE_QUEUE: "queue",
                                E.ECC_SCHEDULE_SINGLE: "single launch"}[schedule],
                   "plane_tiling": {"plane_rows": tiling[0], "tile_rows": tiling[1]},
-                  "column_values": column_values,
+                  "matrix_form": form, "diagonal_offsets": offsets,
                   "assembly_bytes_per_arrived_element": per_elem},
     }
 
@@ -873,6 +886,8 @@ def main():
             "traffic_kind": "fabric bytes per launch: calibrated FETCH_SIZE + WRITE_SIZE (L2 to "
                             "Infinity Fabric requests, Infinity Cache hits included)",
             "algorithmic_bytes_per_launch": res["dominant_bytes"],
+            "algorithmic_model": "the method's data as its definition holds it (CSR for the "
+                                 "iterations), each element counted once",
             "avg_launch_us": round(avg_dom_s * 1e6, 3),
             "launches_timed": dom_n,
             "timing": timing,
@@ -880,6 +895,13 @@ def main():
     }
     if "dom_events_avg_us" in res:
         line["roofline"]["avg_launch_us_with_events"] = res["dom_events_avg_us"]
+    if "dominant_format_bytes" in res and achieved:
+        # the same launch against the bytes the library's copy of the matrix
+        # holds (compact forms drop column indices or per-entry values)
+        fb = res["dominant_format_bytes"]
+        line["roofline"]["format_bytes_per_launch"] = round(fb)
+        line["roofline"]["achieved_format"] = round(fb / avg_dom_s / 1e9, 2)
+        line["roofline"]["frac_format"] = round(fb / avg_dom_s / 1e9 / HBM_PEAK_GBS, 4)
     if "extra" in res:
         line.update(res["extra"])
     if not args.no_cpu_baseline:

@@ -248,7 +248,15 @@ ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *con
  *   ECC_LAYOUT_STREAM  otherwise: runs of rows staged in LDS.
  * ECC_LAYOUT_STREAM reads the matrix arrays at every sweep: they must then
  * outlive the handle and stay unchanged.  The other layouts sweep the copy
- * made here.
+ * made here.  Two compact forms of the copy, reported by ecc_matrix_form,
+ * leave the results bit for bit as the general form gives them:
+ * Diagonals (ECC_LAYOUT_SHORT): when every row's entries are in increasing
+ * column order and lie on at most as many offsets col - row as the row class
+ * R holds (a grid stencil: 3 offsets in 1-D, 5 in 2-D, 7 in 3-D), the copy
+ * keeps each row's values by diagonal and one byte per row naming the
+ * diagonals it holds, in place of the column indices (8 bytes x R per row
+ * instead of 12 bytes x R); diagonals are summed in increasing offset order,
+ * which is the rows' CSR order.
  * Column values (ECC_KIND_POWER in ECC_LAYOUT_SORTED or ECC_LAYOUT_RANGES):
  * when all entries of every column j hold one value c_j, bit for bit -- the
  * PageRank matrix W = A^T D^-1 of Section IV holds 1 / outdeg(j) throughout
@@ -259,8 +267,7 @@ ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *con
  * product of the same two operands, so the iterates are bit for bit those
  * of the general form (the residual norm agrees to rounding: the kernel
  * stages no values, more of its workgroups fit on the device, and the
- * per-workgroup partial sums group the rows differently).
- * ecc_matrix_columns reports the choice. */
+ * per-workgroup partial sums group the rows differently). */
 #define ECC_LAYOUT_STREAM 0
 #define ECC_LAYOUT_SORTED 1
 #define ECC_LAYOUT_SHORT 2
@@ -294,22 +301,22 @@ ecc_status_t ecc_matrix_destroy(ecc_matrix_t A);
  *                ECC_SCHEDULE_AUTO (0): the single launch when the problem
  *                fits it, else the queue when a workgroup would walk at
  *                least 16 items, else the static walk.
- *   columns      ECC_COLUMNS_AUTO (0): the column-value form (above)
- *                whenever the matrix qualifies; ECC_COLUMNS_GENERAL: the
- *                entries' own values always.
+ *   compact      ECC_COMPACT_AUTO (0): a compact form of the copy (above)
+ *                whenever the matrix qualifies; ECC_COMPACT_NONE: the
+ *                general form always.
  * opts may be NULL (the defaults).  ECC_ERR_ARG for a negative range_bytes,
- * an unknown schedule or an unknown columns choice. */
+ * an unknown schedule or an unknown compact choice. */
 #define ECC_SCHEDULE_AUTO 0
 #define ECC_SCHEDULE_STATIC 1
 #define ECC_SCHEDULE_QUEUE 2
 #define ECC_SCHEDULE_SINGLE 3
-#define ECC_COLUMNS_AUTO 0
-#define ECC_COLUMNS_GENERAL 1
+#define ECC_COMPACT_AUTO 0
+#define ECC_COMPACT_NONE 1
 typedef struct {
     int64_t range_bytes;
     int64_t tile_rows;
     int32_t schedule;
-    int32_t columns;
+    int32_t compact;
 } ecc_matrix_opts_t;
 ecc_status_t ecc_matrix_create_ex(ecc_plan_t plan, const ecc_csr_t *A, int32_t kind,
                                   const ecc_matrix_opts_t *opts, ecc_matrix_t *out);
@@ -319,9 +326,18 @@ ecc_status_t ecc_matrix_create_ex(ecc_plan_t plan, const ecc_csr_t *A, int32_t k
  * the items are swept in row order. */
 ecc_status_t ecc_matrix_tiling(ecc_matrix_t A, int64_t *plane_rows, int64_t *tile_rows);
 
-/* Host only: *one_value = 1 when the sweeps use the column-value form
- * (one value per column, see ecc_matrix_create), else 0. */
-ecc_status_t ecc_matrix_columns(ecc_matrix_t A, int32_t *one_value);
+/* The form of the copy ecc_matrix_create made (host only):
+ * ECC_FORM_GENERAL, ECC_FORM_DIAGONALS or ECC_FORM_COLUMN_VALUES.  For the
+ * diagonal form *n_diagonals = their number and offsets[0 ..
+ * ECC_MAX_DIAGONALS - 1] their offsets col - row in increasing order (0
+ * past the last); otherwise 0 and zeros.  n_diagonals and offsets may be
+ * NULL. */
+#define ECC_FORM_GENERAL 0
+#define ECC_FORM_COLUMN_VALUES 1
+#define ECC_FORM_DIAGONALS 2
+#define ECC_MAX_DIAGONALS 8
+ecc_status_t ecc_matrix_form(ecc_matrix_t A, int32_t *form, int32_t *n_diagonals,
+                             int32_t *offsets);
 
 /* Schedule chosen at set-up (host only): ECC_SCHEDULE_STATIC,
  * ECC_SCHEDULE_QUEUE or ECC_SCHEDULE_SINGLE. */

@@ -25,7 +25,9 @@ ECC_TIMING_MF_GRAD, ECC_TIMING_MF_STEP, ECC_TIMING_KINDS = 4, 5, 6
 ECC_THRESHOLD_DATA, ECC_THRESHOLD_PROCS = 0, 1
 ECC_LAYOUT_STREAM, ECC_LAYOUT_SORTED, ECC_LAYOUT_SHORT, ECC_LAYOUT_RANGES = 0, 1, 2, 3
 ECC_SCHEDULE_AUTO, ECC_SCHEDULE_STATIC, ECC_SCHEDULE_QUEUE, ECC_SCHEDULE_SINGLE = 0, 1, 2, 3
-ECC_COLUMNS_AUTO, ECC_COLUMNS_GENERAL = 0, 1
+ECC_COMPACT_AUTO, ECC_COMPACT_NONE = 0, 1
+ECC_FORM_GENERAL, ECC_FORM_COLUMN_VALUES, ECC_FORM_DIAGONALS = 0, 1, 2
+ECC_MAX_DIAGONALS = 8
 ECC_SCRATCH_DOUBLES = 1 << 20
 
 STATUS_NAMES = {0: "ECC_OK", 1: "ECC_ERR_ARG", 2: "ECC_ERR_OVERLAP", 3: "ECC_ERR_RANGE",
@@ -46,7 +48,7 @@ class ecc_csr_t(ctypes.Structure):
 
 class ecc_matrix_opts_t(ctypes.Structure):
     _fields_ = [("range_bytes", ctypes.c_int64), ("tile_rows", ctypes.c_int64),
-                ("schedule", ctypes.c_int32), ("columns", ctypes.c_int32)]
+                ("schedule", ctypes.c_int32), ("compact", ctypes.c_int32)]
 
 
 _lib = None
@@ -75,7 +77,7 @@ _SIGS = [
     ("ecc_matrix_destroy", ctypes.c_int, [_VP]),
     ("ecc_matrix_tiling", ctypes.c_int, [_VP, _VP, _VP]),
     ("ecc_matrix_schedule", ctypes.c_int, [_VP, _VP]),
-    ("ecc_matrix_columns", ctypes.c_int, [_VP, _VP]),
+    ("ecc_matrix_form", ctypes.c_int, [_VP, _VP, _VP, _VP]),
     ("ecc_partials_size", _I64, [_VP]),
     ("ecc_matrix_layout", ctypes.c_int, [_VP, _VP, _VP]),
     ("ecc_iterate_jacobi", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP]),
@@ -233,9 +235,9 @@ def ecc_matrix_create(plan, csr: ecc_csr_t, kind: int) -> int:
 
 
 def ecc_matrix_create_ex(plan, csr: ecc_csr_t, kind: int, range_bytes: int = 0,
-                         tile_rows: int = 0, schedule: int = 0, columns: int = 0) -> int:
+                         tile_rows: int = 0, schedule: int = 0, compact: int = 0) -> int:
     out = _VP()
-    opts = ecc_matrix_opts_t(range_bytes, tile_rows, schedule, columns)
+    opts = ecc_matrix_opts_t(range_bytes, tile_rows, schedule, compact)
     _check(lib().ecc_matrix_create_ex(plan, ctypes.byref(csr), kind, ctypes.byref(opts),
                                       ctypes.byref(out)))
     return out.value
@@ -254,11 +256,13 @@ def ecc_matrix_schedule(mat) -> int:
     return sch.value
 
 
-def ecc_matrix_columns(mat) -> int:
-    """1 when the matrix is swept in the column-value form, else 0."""
-    one = ctypes.c_int32(0)
-    _check(lib().ecc_matrix_columns(mat, ctypes.byref(one)))
-    return one.value
+def ecc_matrix_form(mat):
+    """(form, diagonal offsets): ECC_FORM_* and, for the diagonal form, the
+    offsets col - row in increasing order (else an empty list)."""
+    form, nd = ctypes.c_int32(0), ctypes.c_int32(0)
+    offs = (ctypes.c_int32 * ECC_MAX_DIAGONALS)()
+    _check(lib().ecc_matrix_form(mat, ctypes.byref(form), ctypes.byref(nd), offs))
+    return form.value, list(offs[:nd.value])
 
 
 def ecc_matrix_destroy(mat):

@@ -64,6 +64,13 @@ constexpr int kMaxSweepBlocks = 8192;    // workgroups of one sweep launch at mo
 constexpr int kFusedMaxP = 1024;         // ranks whose state a fused sweep stages in LDS
 constexpr int kNormThreads = 256;        // threads of every norm reduction
 
+// Diagonal form of a short-row matrix: the offsets col - row its entries
+// lie on (at most kDiagMax, ascending).
+constexpr int kDiagMax = ECC_MAX_DIAGONALS;
+struct DiagOffsets {
+    int32_t v[kDiagMax];
+};
+
 // One assembly tile: `len` elements of rank `rank` starting `off` elements
 // into its block.
 struct Tile {
@@ -400,6 +407,10 @@ struct ecc_matrix_s {
     ecc::Fixup *d_rfix = nullptr;   // split sub-rows: (row, first piece, pieces, range)
     int64_t n_rfix = 0;
     int32_t *d_ell_col = nullptr;   // short layout: entries item by item, entry-major (-1: padding)
+    uint8_t *d_ell_mask = nullptr;  // short layout, diagonal form: the diagonals each row holds
+    bool dia = false;               // short layout in diagonal form (d_ell_mask, no d_ell_col)
+    int32_t n_dia = 0;              // its diagonals
+    ecc::DiagOffsets dia_off{};     // their offsets, ascending
     double *d_ell_val = nullptr;    // short layout: their values
     int64_t tile_plane = 0;         // short layout: plane rows of the tiled item order (0: row order)
     int64_t tile_rows = 0;          // short layout: rows per tile

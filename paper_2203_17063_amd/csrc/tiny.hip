@@ -35,6 +35,8 @@ struct TinyArgs {
     int32_t n;
     const int32_t *ell_col;
     const double *ell_val;
+    const uint8_t *ell_mask;  // diagonal form: the diagonals of each row (no ell_col)
+    DiagOffsets dia;
     const double *b;
     double alpha, beta;
     double *x;      // in: x^0; out: the last iterate
@@ -138,9 +140,11 @@ __global__ __launch_bounds__(kTinyThreads) void k_solve_tiny(TinyArgs a) {
             const int32_t l = i - it.row0;
             const int64_t base = (int64_t)it.k0 * R + l;
             const int32_t pad = sell_pad(it.nrows);
+            const uint32_t mk = a.ell_mask ? a.ell_mask[(int64_t)it.k0 + l] : 0u;
 #pragma unroll
             for (int e = 0; e < R; ++e) {
-                c8[e] = a.ell_col[base + (int64_t)e * pad];
+                c8[e] = a.ell_mask ? (((mk >> e) & 1u) ? i + a.dia.v[e] : -1)
+                                   : a.ell_col[base + (int64_t)e * pad];
                 v8[e] = a.ell_val[base + (int64_t)e * pad];
             }
             lo = it.lo;
@@ -349,6 +353,8 @@ ecc_status_t launch_solve_tiny(ecc_matrix_t M, const double *d_b, double alpha, 
     a.n = (int32_t)M->A.n_rows;
     a.ell_col = M->d_ell_col;
     a.ell_val = M->d_ell_val;
+    a.ell_mask = M->dia ? M->d_ell_mask : nullptr;
+    a.dia = M->dia_off;
     a.b = d_b;
     a.alpha = alpha;
     a.beta = beta;

@@ -57,7 +57,7 @@ class Iterative:
 
     def __init__(self, n, row_ptr, col, val, counts, S, mask, kind, b=None, alpha=0.0,
                  beta=0.0, x0=None, device="cuda", range_bytes=0, tile_rows=0, schedule=0,
-                 columns=0):
+                 compact=0):
         self.n = int(n)
         self.kind = kind
         self.alpha, self.beta = float(alpha), float(beta)
@@ -83,7 +83,7 @@ class Iterative:
         self.csr = E.make_csr(self.n, self.n, self.nnz, self.d_row_ptr, self.d_col, self.d_val)
         ekind = E.ECC_KIND_JACOBI if kind == "jacobi" else E.ECC_KIND_POWER
         self.mat = E.ecc_matrix_create_ex(self.plan.handle, self.csr, ekind, range_bytes,
-                                          tile_rows, schedule, columns)
+                                          tile_rows, schedule, compact)
         self.d_partials = torch.empty(E.ecc_partials_size(self.mat), dtype=torch.float64,
                                       device=device)
 

@@ -34,9 +34,15 @@ def test_byte_model_and_host_fields():
     sys.path.insert(0, ROOT)
     import bench
     assert bench.sweep_bytes(64_000_000, 447_040_000) == 12 * 447_040_000 + 28 * 64_000_000 + 4
-    # one value per column: 8 bytes per column in place of 8 per nonzero
-    assert (bench.sweep_bytes(4_194_304, 67_108_864, True)
-            == bench.sweep_bytes(4_194_304, 67_108_864) - 8 * 67_108_864 + 8 * 4_194_304)
+    # compact forms: one value per column in place of one per nonzero; values
+    # by diagonal and a mask byte per row in place of columns and row pointers
+    n, nnz = 4_194_304, 67_108_864
+    assert (bench.format_sweep_bytes(n, nnz, "column values", 0)
+            == bench.sweep_bytes(n, nnz) - 8 * nnz + 8 * n)
+    n, nnz = 64_000_000, 447_040_000
+    assert (bench.format_sweep_bytes(n, nnz, "diagonals", 7)
+            == 56 * n + n + 24 * n)
+    assert bench.format_sweep_bytes(n, nnz, "general", 7) == bench.sweep_bytes(n, nnz)
     cores, model = bench.host_cpu()
     assert cores == len(os.sched_getaffinity(0)) and cores >= 1
     assert model is None or isinstance(model, str)

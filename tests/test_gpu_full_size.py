@@ -37,13 +37,13 @@ def test_pagerank_rmat_full():
     prob = W.pagerank_rmat()
     run = _iterative(prob)
     assert E.ecc_matrix_layout(run.mat) == (E.ECC_LAYOUT_RANGES, 2)
-    assert E.ecc_matrix_columns(run.mat) == 1
+    assert E.ecc_matrix_form(run.mat)[0] == E.ECC_FORM_COLUMN_VALUES
     run.close()
     _solve_and_compare(prob, bitwise=False, threads=THREADS)
     rb = 8 << 20
-    a = _solve_x_rho(prob, rb, columns=E.ECC_COLUMNS_AUTO)
-    g = _solve_x_rho(prob, rb, columns=E.ECC_COLUMNS_GENERAL)
-    assert a[4] == 1 and g[4] == 0 and a[0] == g[0]
+    a = _solve_x_rho(prob, rb, compact=E.ECC_COMPACT_AUTO)
+    g = _solve_x_rho(prob, rb, compact=E.ECC_COMPACT_NONE)
+    assert a[4] == E.ECC_FORM_COLUMN_VALUES and g[4] == E.ECC_FORM_GENERAL and a[0] == g[0]
     assert np.array_equal(a[1], g[1]) and np.array_equal(a[2], g[2])
     assert np.allclose(a[3], g[3], rtol=1e-12, atol=0.0)
 

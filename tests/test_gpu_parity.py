@@ -258,22 +258,22 @@ def _floor(prob, x):
     return float(np.sum(prob.alpha * wx + prob.beta + np.abs(x)))
 
 
-def _iterative(prob, range_bytes=0, tile_rows=0, schedule=0, columns=0):
+def _iterative(prob, range_bytes=0, tile_rows=0, schedule=0, compact=0):
     """The problem resident on the GPU; range_bytes / tile_rows / schedule /
-    columns are the matrix set-up options (0: the library's choice)."""
+    compact are the matrix set-up options (0: the library's choice)."""
     return _runner().Iterative(prob.n, prob.A.row_ptr, prob.A.col, prob.A.val, prob.counts,
                                prob.S, prob.mask, prob.kind, b=prob.b, alpha=prob.alpha,
                                beta=prob.beta, x0=prob.x0, range_bytes=range_bytes,
-                               tile_rows=tile_rows, schedule=schedule, columns=columns)
+                               tile_rows=tile_rows, schedule=schedule, compact=compact)
 
 
 def _solve_and_compare(prob, bitwise, threads=8, layout=None, range_bytes=0, tile_rows=0,
-                       tiling=None, schedule=0, expect_schedule=None, solves=1, columns=0,
-                       one_value=None):
+                       tiling=None, schedule=0, expect_schedule=None, solves=1, compact=0,
+                       form=None):
     announce("solve", prob.name, prob.n, prob.A.nnz, prob.P, prob.T)
-    run = _iterative(prob, range_bytes, tile_rows, schedule, columns)
-    if one_value is not None:  # the column-value form the set-up must choose
-        assert _capi().ecc_matrix_columns(run.mat) == one_value
+    run = _iterative(prob, range_bytes, tile_rows, schedule, compact)
+    if form is not None:  # the form of the copy the set-up must choose
+        assert _capi().ecc_matrix_form(run.mat)[0] == form
     if tiling is not None:  # (plane rows, tile rows) the set-up must choose
         assert _capi().ecc_matrix_tiling(run.mat) == tiling
     if expect_schedule is not None:
@@ -619,12 +619,12 @@ def test_solve_arrow_ranges():
     _solve_and_compare(_arrow_problem(), bitwise=False, layout="RANGES", range_bytes=8192)
 
 
-def _solve_x_rho(prob, range_bytes=0, columns=0):
-    run = _iterative(prob, range_bytes, columns=columns)
+def _solve_x_rho(prob, range_bytes=0, compact=0):
+    run = _iterative(prob, range_bytes, compact=compact)
     iters = run.solve(tol=prob.tol, histories=True)
     torch.cuda.synchronize()
     out = (iters, run.d_x.cpu().numpy(), run.d_x_hat.cpu().numpy(),
-           run.d_rho.cpu().numpy()[:iters], _capi().ecc_matrix_columns(run.mat))
+           run.d_rho.cpu().numpy()[:iters], _capi().ecc_matrix_form(run.mat)[0])
     run.close()
     return out
 
@@ -643,10 +643,12 @@ def test_column_values_match_general_form(which, range_bytes):
     prob = (W.pagerank_rmat(scale=int(which[4:]), T=40) if which.startswith("rmat")
             else _powerlaw_problem("power", 20000, 9, seed=77, column_values=True))
     layout = "RANGES" if range_bytes else "SORTED"
-    _solve_and_compare(prob, bitwise=False, layout=layout, range_bytes=range_bytes, one_value=1)
-    a = _solve_x_rho(prob, range_bytes, columns=0)
-    g = _solve_x_rho(prob, range_bytes, columns=_capi().ECC_COLUMNS_GENERAL)
-    assert a[4] == 1 and g[4] == 0
+    E = _capi()
+    _solve_and_compare(prob, bitwise=False, layout=layout, range_bytes=range_bytes,
+                       form=E.ECC_FORM_COLUMN_VALUES)
+    a = _solve_x_rho(prob, range_bytes, compact=E.ECC_COMPACT_AUTO)
+    g = _solve_x_rho(prob, range_bytes, compact=E.ECC_COMPACT_NONE)
+    assert a[4] == E.ECC_FORM_COLUMN_VALUES and g[4] == E.ECC_FORM_GENERAL
     assert a[0] == g[0]
     assert np.array_equal(a[1], g[1]) and np.array_equal(a[2], g[2])
     assert np.allclose(a[3], g[3], rtol=1e-12, atol=0.0)
@@ -656,7 +658,7 @@ def test_column_values_choice():
     """Only power matrices in the sorted or range layout whose columns each
     hold one value, bit for bit, take the column-value form: one entry off by
     one unit in the last place, a general heavy-tailed matrix, a Jacobi
-    matrix, a short-row matrix and the caller's ECC_COLUMNS_GENERAL keep the
+    matrix, a short-row matrix and the caller's ECC_COMPACT_NONE keep the
     general form."""
     E = _capi()
     announce("column values choice")
@@ -664,13 +666,13 @@ def test_column_values_choice():
 
     def one(p, **kw):
         run = _iterative(p, **kw)
-        v = E.ecc_matrix_columns(run.mat)
+        v = int(E.ecc_matrix_form(run.mat)[0] == E.ECC_FORM_COLUMN_VALUES)
         run.close()
         return v
 
     assert one(prob) == 1
     assert one(prob, range_bytes=4096) == 1
-    assert one(prob, columns=E.ECC_COLUMNS_GENERAL) == 0
+    assert one(prob, compact=E.ECC_COMPACT_NONE) == 0
     val = prob.A.val.copy()
     k = int(np.argmax(np.bincount(prob.A.col, minlength=prob.n)[prob.A.col]))  # busiest column
     val[k] = np.nextafter(val[k], 1.0)
@@ -681,8 +683,83 @@ def test_column_values_choice():
     assert one(_powerlaw_problem("jacobi", 12000, 3, seed=5, T=2)) == 0
     assert one(_banded_problem("power", 3000, 6, 6, T=2)) == 0
     with pytest.raises(E.EccError) as ei:
-        _iterative(prob, columns=7)
+        _iterative(prob, compact=7)
     assert ei.value.status == E.ECC_ERR_ARG
+
+
+def _form(prob, **kw):
+    run = _iterative(prob, **kw)
+    f = _capi().ecc_matrix_form(run.mat)
+    run.close()
+    return f
+
+
+def test_diagonal_form_choice():
+    """Short-row matrices whose sorted rows lie on at most R offsets col - row
+    (R: the row class) take the diagonal form, with those offsets ascending;
+    random columns within a band, a row out of column order, a
+    caller's ECC_COMPACT_NONE and the longer rows of other layouts do not."""
+    E = _capi()
+    announce("diagonal form choice")
+    D, G = E.ECC_FORM_DIAGONALS, E.ECC_FORM_GENERAL
+    assert _form(W.jacobi_1d()) == (D, [-1, 0, 1])
+    assert _form(W.jacobi_2d(N=33, T=2)) == (D, [-33, -1, 0, 1, 33])
+    assert _form(W.jacobi_3d(N=12, T=2, P=8)) == (D, [-144, -12, -1, 0, 1, 12, 144])
+    assert _form(W.jacobi_2d(N=33, T=2), compact=E.ECC_COMPACT_NONE) == (G, [])
+    assert _form(_banded_problem("jacobi", 3000, 4, 4, T=2))[0] == G
+    assert _form(_banded_problem("jacobi", 3000, 9, 16, T=2))[0] == G   # stream layout
+    # one row with its entries out of column order
+    prob = W.jacobi_2d(N=33, T=2)
+    rp, col, val = prob.A.row_ptr, prob.A.col.copy(), prob.A.val.copy()
+    k0 = int(rp[40])
+    col[k0], col[k0 + 1] = col[k0 + 1], col[k0]
+    val[k0], val[k0 + 1] = val[k0 + 1], val[k0]
+    bent = dataclasses.replace(prob, A=W.CSR(prob.n, prob.n, rp, col, val))
+    assert _form(bent)[0] == G
+
+
+@pytest.mark.parametrize("which", ["jacobi1d", "jacobi2d", "jacobi3d", "jacobi3d_tiled",
+                                   "power_stencil"])
+def test_diagonal_form_matches_general_form(which):
+    """The diagonal form (values by diagonal, one mask byte per row) gives
+    the iterate, assembled vector and every residual of the general form bit
+    for bit, and the oracle's (checked by _solve_and_compare): the
+    single-launch loop, the fused loop (static and queue schedules), plane
+    tiles, and the power step on a stencil."""
+    E = _capi()
+    kw = {}
+    if which == "jacobi1d":
+        prob = W.jacobi_1d()
+    elif which == "jacobi2d":
+        prob = W.jacobi_2d(N=64, T=30)
+    elif which == "jacobi3d":
+        prob = W.jacobi_3d(N=24, T=20, P=512)
+        kw = {"schedule": E.ECC_SCHEDULE_QUEUE}
+    elif which == "jacobi3d_tiled":
+        prob = W.jacobi_3d(N=40, T=12, P=64)
+        kw = {"tile_rows": 256}
+    else:
+        base = W.jacobi_2d(N=48, T=20)
+        A = base.A
+        val = np.abs(A.val) / 8.0
+        rng = np.random.default_rng(5)
+        x0 = rng.random(base.n)
+        prob = W.Iterative("power-stencil", "power", W.CSR(base.n, base.n, A.row_ptr, A.col, val),
+                           base.counts, base.displs, base.S, base.mask, base.T, x0,
+                           alpha=0.85, beta=0.15 / base.n, norm=1)
+    _solve_and_compare(prob, bitwise=True, form=E.ECC_FORM_DIAGONALS, **kw)
+    run_a = _iterative(prob, compact=E.ECC_COMPACT_AUTO, **kw)
+    run_g = _iterative(prob, compact=E.ECC_COMPACT_NONE, **kw)
+    outs = []
+    for run in (run_a, run_g):
+        iters = run.solve(tol=prob.tol, histories=True)
+        torch.cuda.synchronize()
+        outs.append((iters, run.d_x.cpu().numpy(), run.d_x_hat.cpu().numpy(),
+                     run.d_rho.cpu().numpy()[:iters]))
+        run.close()
+    assert outs[0][0] == outs[1][0]
+    for u, v in zip(outs[0][1:], outs[1][1:]):
+        assert np.array_equal(u, v)
 
 
 @pytest.mark.parametrize("kind", ["jacobi", "power"])
