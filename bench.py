@@ -804,7 +804,7 @@ def main():
     print("[bench] running on GPU", file=sys.stderr, flush=True)
     if cfg in ("jacobi-1d", "jacobi-2d", "pagerank-rmat", "jacobi-3d"):
         res = run_iterative_gpu(cfg, prob, args.steps, args.warmup)
-        digest = kernel_source_digest(["sweep.hip", "ecc_common.h"])
+        digest = kernel_source_digest(["sweep.hip", "tiny.hip", "ecc_common.h"])
         tag = "sweep_" + cfg.replace("-", "_")
         dom_ms, dom_n = res["times"]["SWEEP"]
     elif cfg == "allgatherv":
