@@ -250,15 +250,21 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
     other_ms = setup_ms + (times["ASSEMBLE"][0] + times["NORM"][0]) / steps
     sweeps = times["SWEEP"][1] / steps
     dom_ms = (region_ms / steps - other_ms) / sweeps
+    dom_timing = ("HIP events on the plan's stream around the timed region; the sweep's share "
+                  "is that time minus a 0-iteration solve's (set-up) and the other launches' "
+                  "(events around each), divided by the sweep launches")
+    if schedule == E.ECC_SCHEDULE_SINGLE:
+        # one launch per solve, bracketed by the solve's own synchronisation:
+        # the events around that launch
+        dom_ms = times["SWEEP"][0] / max(times["SWEEP"][1], 1)
+        dom_timing = "HIP events on the plan's stream around the single launch of each solve"
     return {
         "iters": iters, "wall": wall, "wall_events": wall_events, "times": times,
         "bytes_per_step": bytes_per_step, "dominant": "sweep",
         "dominant_bytes": dom, "footprint": footprint, "rho_last": float(rho[-1]),
         "dominant_format_bytes": dom - b_sweep + b_sweep_form,
         "unit_per_step": iters, "fused": fused, "dom_ms": dom_ms,
-        "dom_timing": "HIP events on the plan's stream around the timed region; the sweep's "
-                      "share is that time minus a 0-iteration solve's (set-up) and the other "
-                      "launches' (events around each), divided by the sweep launches",
+        "dom_timing": dom_timing,
         "dom_events_avg_us": round(times["SWEEP"][0] / max(times["SWEEP"][1], 1) * 1e3, 3),
         "extra": {"layout": {0: "stream", 1: "sorted", 2: "short", 3: "ranges"}[layout],
                   "schedule": {E.ECC_SCHEDULE_STATIC: "static", E.ECC_SCHEDULE_QUEUE: "queue",

@@ -687,6 +687,46 @@ def test_column_values_choice():
     assert ei.value.status == E.ECC_ERR_ARG
 
 
+@pytest.mark.parametrize("which", ["sorted", "ranges", "ranges_general", "powerlaw_sorted",
+                                   "powerlaw_ranges"])
+def test_reordered_layouts_every_iterate(which):
+    """Layouts that add a row's entries in another order than CSR (the
+    sorted copy with rows on several lanes, the range layout's per-range
+    sub-row sums): through the separate calls, the assembled vector and the
+    new iterate of every iteration against the oracle's, normwise within
+    1e-12, and every norm within its bound."""
+    E = _capi()
+    if which == "sorted":
+        prob, kw = W.pagerank_rmat(scale=13, T=30), {}
+    elif which == "ranges":
+        prob, kw = W.pagerank_rmat(scale=13, T=30), {"range_bytes": 4096}
+    elif which == "ranges_general":
+        prob, kw = W.pagerank_rmat(scale=13, T=30), {"range_bytes": 4096,
+                                                     "compact": E.ECC_COMPACT_NONE}
+    elif which == "powerlaw_sorted":
+        prob, kw = _powerlaw_problem("jacobi", 20000, 9, seed=40, T=20), {}
+    else:
+        prob, kw = _powerlaw_problem("jacobi", 20000, 9, seed=40, T=20), {"range_bytes": 8192}
+    announce("every iterate", which)
+    ref = oracle.run_iterative(prob, threads=8, keep_x=tuple(range(prob.T)))
+    assert ref["iters"] == prob.T
+    run = _iterative(prob, **kw)
+    layout = E.ecc_matrix_layout(run.mat)[0]
+    assert layout == (E.ECC_LAYOUT_SORTED if "sorted" in which else E.ECC_LAYOUT_RANGES)
+    run.plan.reset()
+    a = torch.from_numpy(prob.x0.copy()).cuda()
+    b = torch.empty_like(a)
+    rhos = []
+    for t in range(prob.T):
+        rhos.append(run.step(t, a, b))
+        assert_iterates_close(run.d_x_hat.cpu().numpy(), ref["kept"][t][1])
+        expect = ref["kept"][t + 1][0] if t + 1 < prob.T else ref["x"]
+        assert_iterates_close(b.cpu().numpy(), expect)
+        a, b = b, a
+    assert_rho_close(np.array(rhos), ref["rho"], _floor(prob, ref["x"]))
+    run.close()
+
+
 def _form(prob, **kw):
     run = _iterative(prob, **kw)
     f = _capi().ecc_matrix_form(run.mat)
