@@ -579,11 +579,27 @@ def run_mf_gpu(prob, steps, warmup):
         torch.cuda.synchronize()
         err = rs.d_err.cpu().numpy()[:T3 + 1]
         _, forced, _, _ = rs.plan.stats()
-        rs.close()
         if target is None:
             target = float(err[prob.T])
         hit = np.nonzero(err[1:] <= target)[0]
+        # time to the target: the iterations it takes, run again without the
+        # error evaluations (a fresh slot costs a write where a reused one
+        # costs a read, so the time per iteration depends on the slack)
+        ms_to_target = None
+        if hit.size:
+            n_it = int(hit[0]) + 1
+            rs.run(T=n_it, record=False)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            rs.run(T=n_it, record=False)
+            e1.record()
+            torch.cuda.synchronize()
+            ms_to_target = round(e0.elapsed_time(e1), 3)
+        rs.close()
         study[str(S)] = {"iterations_to_target": int(hit[0]) + 1 if hit.size else None,
+                         "gpu_ms_to_target": ms_to_target,
                          "forced_arrivals_in_%d" % T3: int(forced),
                          "error_after_%d" % prob.T: round(float(err[prob.T]), 6)}
     return {"iters": prob.T, "wall": wall, "wall_events": wall_events, "times": times,
