@@ -604,14 +604,16 @@ def batch_schedule(seed: int, T: int, P: int, K: int) -> np.ndarray:
 
 def mf_problem(n_users: int = 160_000, n_items: int = 60_000, n_ratings: int = 25_000_000,
                rank: int = 16, P: int = 32, S: int = 2, q: float = 0.8, T: int = 100,
-               eta: float = 0.5, lam: float = 1e-4, true_rank: int = 8, seed: int = None,
+               eta: float = 0.3, lam: float = 1e-4, true_rank: int = 8, seed: int = None,
                K: int = 8) -> MFProblem:
     """Synthetic ratings shaped like a large movie-rating set (25M ratings;
     Zipf user activity, exponent 0.5, and item popularity, exponent 0.6):
     half-star ratings in [0.5, 5] from a planted rank-`true_rank` model plus
     noise, centred; drawn independently, so consecutive ratings form uniform
     shards and minibatches; P equal shards of K minibatches, each minibatch
-    stored by user then item; the model starts at N(0, 0.1^2)."""
+    stored by user then item; the model starts at N(0, 0.1^2).  The step size
+    0.3 keeps the training error falling through the first 100 iterations
+    (from 0.5 on, it reaches the minibatches' noise floor before then)."""
     seed = seed_of(8) if seed is None else seed
     users = _zipf_pick(seed, STREAM_MF_USERS, n_ratings, n_users, 0.5)
     items = _zipf_pick(seed, STREAM_MF_ITEMS, n_ratings, n_items, 0.6)
