@@ -798,8 +798,10 @@ __device__ __forceinline__ void short_body(const SweepArgs &a) {
         double y[R];
 #pragma unroll
         for (int j = 0; j < R; ++j)
-            y[j] = (E.c[j] >= 0) ? view_load<STEP>(E.c[j], cur.lo, cur.hi, a.x_own, a.x_hat, sv, rc)
-                                 : 0.0;
+            // Jacobi sums the diagonal entry apart: no gather for it
+            y[j] = (E.c[j] >= 0 && !(KIND == ECC_KIND_JACOBI && E.c[j] == i))
+                       ? view_load<STEP>(E.c[j], cur.lo, cur.hi, a.x_own, a.x_hat, sv, rc)
+                       : 0.0;
         double xo = 0.0, bi = 0.0;
         if (live) {
             xo = a.x_own[i];
@@ -904,8 +906,10 @@ __device__ __forceinline__ void short_body_queue(const SweepArgs &a) {
         double y[R];
 #pragma unroll
         for (int j = 0; j < R; ++j)
-            y[j] = (E.c[j] >= 0) ? view_load<STEP>(E.c[j], cur.lo, cur.hi, a.x_own, a.x_hat, sv, rc)
-                                 : 0.0;
+            // Jacobi sums the diagonal entry apart: no gather for it
+            y[j] = (E.c[j] >= 0 && !(KIND == ECC_KIND_JACOBI && E.c[j] == i))
+                       ? view_load<STEP>(E.c[j], cur.lo, cur.hi, a.x_own, a.x_hat, sv, rc)
+                       : 0.0;
         double xo = 0.0, bi = 0.0;
         if (live) {
             xo = a.x_own[i];
