@@ -758,6 +758,66 @@ def test_diagonal_form_choice():
     assert _form(bent)[0] == G
 
 
+def _offset_subset_problem(kind, n, offsets, P, seed, T=30, S=2):
+    """Rows holding a random subset of a fixed set of offsets col - row (the
+    diagonal always, for Jacobi; possibly none at all, for the power step),
+    in increasing column order: the diagonal form with gaps in every row's
+    mask."""
+    rng = np.random.default_rng(seed)
+    rows_c, rows_v = [], []
+    for i in range(n):
+        keep = rng.random(len(offsets)) < 0.6
+        c = np.array([i + d for d, k in zip(offsets, keep) if k and 0 <= i + d < n], dtype=np.int64)
+        if kind == "jacobi" and i not in c:
+            c = np.sort(np.append(c, i))
+        v = -rng.uniform(0.05, 1.0, c.size)
+        if kind == "jacobi":
+            v[c == i] = 2.0 * np.abs(v).sum() + 1.0
+        else:
+            v = np.abs(v) / len(offsets)
+        rows_c.append(c)
+        rows_v.append(v)
+    rp = np.zeros(n + 1, dtype=np.int32)
+    rp[1:] = np.cumsum([c.size for c in rows_c])
+    A = W.CSR(n, n, rp, np.concatenate(rows_c).astype(np.int32), np.concatenate(rows_v))
+    counts = W.dirichlet_partition(n, P, seed)
+    mask = (rng.random((T, P)) < 0.7).astype(np.uint8)
+    mask[0] = 1
+    if kind == "jacobi":
+        return W.Iterative("offsets-jacobi", "jacobi", A, counts, W.exclusive_scan(counts), S,
+                           mask, T, np.zeros(n), b=rng.standard_normal(n), norm=2)
+    return W.Iterative("offsets-power", "power", A, counts, W.exclusive_scan(counts), S, mask, T,
+                       rng.random(n), alpha=0.85, beta=0.15 / n, norm=1)
+
+
+@pytest.mark.parametrize("kind,offsets,n,P", [
+    ("jacobi", [-700, -3, -1, 0, 2, 650, 1800], 20000, 9),
+    ("power", [-1500, -40, -1, 0, 1, 40, 1500], 20000, 5),
+    ("power", [-5, 0, 7], 3001, 3),        # the single-launch solve
+    ("jacobi", [-64, -1, 0, 1, 64], 700, 2),
+])
+def test_diagonal_form_with_gaps(kind, offsets, n, P):
+    """Every row a random subset of the offsets (the power step's rows may be
+    empty): the diagonal form, bitwise against the oracle and the general
+    form, through the loop and the separate calls."""
+    E = _capi()
+    prob = _offset_subset_problem(kind, n, offsets, P, seed=n + P)
+    announce("diagonal form with gaps", kind, offsets, n, P)
+    assert _form(prob) == (E.ECC_FORM_DIAGONALS, sorted(offsets))
+    _solve_and_compare(prob, bitwise=True, form=E.ECC_FORM_DIAGONALS)
+    outs = []
+    for compact in (E.ECC_COMPACT_AUTO, E.ECC_COMPACT_NONE):
+        run = _iterative(prob, compact=compact)
+        run.solve(histories=True)
+        torch.cuda.synchronize()
+        outs.append((run.d_x.cpu().numpy(), run.d_x_hat.cpu().numpy(),
+                     run.d_rho.cpu().numpy()[:prob.T]))
+        run.close()
+    for u, v in zip(*outs):
+        assert np.array_equal(u, v)
+    _step_api_matches_solve((prob,))
+
+
 @pytest.mark.parametrize("which", ["jacobi1d", "jacobi2d", "jacobi3d", "jacobi3d_tiled",
                                    "power_stencil"])
 def test_diagonal_form_matches_general_form(which):
