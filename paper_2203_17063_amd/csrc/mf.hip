@@ -16,9 +16,10 @@
 //      exactly one) also feed per-workgroup sums of e_k^2.
 //  (2) the partial allreduce of the workers' gradients (ecc_allreduce_partial:
 //      staleness decision, stale gradients substituted from the slots);
-//  (3) k_mf_rmse: sqrt(sum e_k^2 / ratings used) from the workgroup sums in a
-//      fixed order; k_mf_step: W := W - eta * (G * c_row + 2 lam W), c_row =
-//      K / (number of ratings of the row, at least 1).
+//  (3) k_mf_step: W := W - eta * (G * c_row + 2 lam W), c_row = K / (number
+//      of ratings of the row, at least 1); its workgroup 0 also reduces the
+//      minibatch error sqrt(sum e_k^2 / ratings used) from the gradient
+//      kernel's workgroup sums, in a fixed order.
 // ecc_mf_error evaluates sqrt(sum e_k^2 / N) over all ratings at a model.
 //
 // The gradient index is built once, on the host, for every (worker,
@@ -265,13 +266,46 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfGradArgs a) {
     if (threadIdx.x == 0) a.partials[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = tot;
 }
 
+// The minibatch error of an iteration: sqrt(sum / count) of the gradient
+// kernel's per-workgroup sums of e^2, reduced in a fixed order (see
+// k_mf_rmse).
+struct MfRmseArgs {
+    const double *partials;
+    int64_t n, N;
+    int32_t P, K;
+    const int32_t *batch;
+    const int64_t *sizes;
+    double *out;
+};
+
+__device__ __forceinline__ void mf_rmse_body(const MfRmseArgs &r, double *s_red) {
+    static_assert(kMfThreads == kNormThreads, "the reduction's thread count");
+    const double sum = reduce_values(r.partials, r.n, false, 0.0, s_red);
+    if (threadIdx.x == 0) {
+        int64_t cnt = r.N;
+        if (r.batch) {
+            cnt = 0;
+            for (int32_t p = 0; p < r.P; ++p)
+                cnt += r.sizes[(int64_t)p * r.K + min(max(r.batch[p], 0), r.K - 1)];
+        }
+        *r.out = cnt > 0 ? sqrt(sum / (double)cnt) : 0.0;
+    }
+}
+
+// The step, one element per thread and one workgroup per kMfThreads
+// elements; workgroup 0 first reduces the iteration's minibatch error, which
+// then overlaps the other workgroups' elements (measured on MI355X, 25M
+// ratings, rank 16, 32 workers: 21 us for both against 17 + 18 us as a
+// grid-stride step over the resident workgroups and a separate reduction).
 __global__ __launch_bounds__(kMfThreads) void k_mf_step(int64_t m, int log2r, double eta,
                                                         double lam2,
                                                         const double *__restrict__ G,
                                                         const double *__restrict__ row_scale,
-                                                        double *__restrict__ W) {
-    const int64_t stride = (int64_t)gridDim.x * kMfThreads;
-    for (int64_t x = (int64_t)blockIdx.x * kMfThreads + threadIdx.x; x < m; x += stride) {
+                                                        double *__restrict__ W, MfRmseArgs r) {
+    __shared__ double s_red[kNormThreads / 64];
+    if (blockIdx.x == 0) mf_rmse_body(r, s_red);
+    const int64_t x = (int64_t)blockIdx.x * kMfThreads + threadIdx.x;
+    if (x < m) {
         const double w = W[x];
         W[x] = w - eta * (G[x] * row_scale[x >> log2r] + lam2 * w);
     }
@@ -287,15 +321,7 @@ __global__ __launch_bounds__(kNormThreads) void k_mf_rmse(const double *__restri
                                                           const int64_t *__restrict__ sizes,
                                                           double *__restrict__ out) {
     __shared__ double s_red[kNormThreads / 64];
-    const double sum = reduce_values(partials, n, false, 0.0, s_red);
-    if (threadIdx.x == 0) {
-        int64_t cnt = N;
-        if (batch) {
-            cnt = 0;
-            for (int32_t p = 0; p < P; ++p) cnt += sizes[(int64_t)p * K + min(max(batch[p], 0), K - 1)];
-        }
-        *out = cnt > 0 ? sqrt(sum / (double)cnt) : 0.0;
-    }
+    mf_rmse_body(MfRmseArgs{partials, n, N, P, K, batch, sizes, out}, s_red);
 }
 
 // Errors of every rating at W, one lane group per rating (products in
@@ -358,7 +384,7 @@ struct ecc_mf_s {
     double *d_ratings = nullptr;
     double *d_scale = nullptr;      // [n_users + n_items]: K / ratings of the row
     double *d_partials = nullptr;   // [max(grad_grid * P, err_grid)]
-    int32_t grad_grid = 1, step_grid = 1, err_grid = 1;
+    int32_t grad_grid = 1, err_grid = 1;
 };
 
 extern "C" {
@@ -497,7 +523,6 @@ static ecc_status_t ecc_mf_create_impl(int32_t n_users, int32_t n_items, int32_t
     // (8 per CU), at least 1
     const int64_t groups = kMfThreads / (rank < 4 ? 1 : rank / 4);
     h->grad_grid = std::max<int32_t>(1, mf_grid((E + groups - 1) / groups, 8) / P);
-    h->step_grid = mf_grid((E * rank + kMfThreads - 1) / kMfThreads, 8);
     h->err_grid = mf_grid((N + groups - 1) / groups, 8);
     const int64_t n_part = std::max<int64_t>((int64_t)h->grad_grid * P, h->err_grid);
     auto fail = [&](const char *what) {
@@ -595,11 +620,15 @@ ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam,
     if (st != ECC_OK) return st;
     {
         TimedLaunch timed(plan, ECC_TIMING_MF_STEP);
-        hipLaunchKernelGGL(k_mf_rmse, dim3(1), dim3(kNormThreads), 0, s, h->d_partials,
-                           (int64_t)h->grad_grid * h->P, h->N, h->P, h->K, d_batch, h->d_sizes,
-                           d_rmse);
-        hipLaunchKernelGGL(k_mf_step, dim3(h->step_grid), dim3(kMfThreads), 0, s, m, log2r, eta,
-                           2.0 * lam, d_G, h->d_scale, d_W);
+        const MfRmseArgs r{h->d_partials, (int64_t)h->grad_grid * h->P, h->N, h->P, h->K,
+                           d_batch, h->d_sizes, d_rmse};
+        const int64_t sg = std::max<int64_t>(1, (m + kMfThreads - 1) / kMfThreads);
+        if (sg > 0x7fffffff) {
+            set_error("model too large for one step launch");
+            return ECC_ERR_RANGE;
+        }
+        hipLaunchKernelGGL(k_mf_step, dim3((unsigned)sg), dim3(kMfThreads), 0, s, m, log2r, eta,
+                           2.0 * lam, d_G, h->d_scale, d_W, r);
     }
     ECC_LAUNCH_CHECK();
     return ECC_OK;
