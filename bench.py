@@ -229,6 +229,9 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
     form_id, offsets = E.ecc_matrix_form(run.mat)
     form = {E.ECC_FORM_GENERAL: "general", E.ECC_FORM_COLUMN_VALUES: "column values",
             E.ECC_FORM_DIAGONALS: "diagonals"}[form_id]
+    probe = None
+    if layout in (E.ECC_LAYOUT_SORTED, E.ECC_LAYOUT_RANGES):
+        probe = gather_probe(prob, run, slots if layout == E.ECC_LAYOUT_RANGES else 1)
     run.close()
 
     counts = prob.counts
@@ -258,6 +261,10 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
         # the events around that launch
         dom_ms = times["SWEEP"][0] / max(times["SWEEP"][1], 1)
         dom_timing = "HIP events on the plan's stream around the single launch of each solve"
+    if probe:
+        best = max(v["gathers_per_s"] for v in probe.values())
+        probe["sweep_gathers_per_s"] = round(prob.A.nnz / (dom_ms / 1e3), 0)
+        probe["sweep_over_probe"] = round(prob.A.nnz / (dom_ms / 1e3) / best, 4)
     return {
         "iters": iters, "wall": wall, "wall_events": wall_events, "times": times,
         "bytes_per_step": bytes_per_step, "dominant": "sweep",
@@ -271,8 +278,43 @@ def run_iterative_gpu(cfg, prob, steps, warmup):
                                E.ECC_SCHEDULE_SINGLE: "single launch"}[schedule],
                   "plane_tiling": {"plane_rows": tiling[0], "tile_rows": tiling[1]},
                   "matrix_form": form, "diagonal_offsets": offsets,
+                  "gather_probe": probe,
                   "assembly_bytes_per_arrived_element": per_elem},
     }
+
+
+def gather_probe(prob, run, n_ranges, reps=20):
+    """The gather-rate ceiling of the matrix's columns (ecc_gather_probe: the
+    index stream read, one vector gathered, nothing else), over the CSR
+    order and over the order of its column ranges (entries grouped by range,
+    CSR order within a range, as the range layout sweeps them), with HIP
+    events around `reps` probes of each."""
+    import torch
+    from paper_2203_17063_amd import capi as E
+    n, nnz = prob.n, prob.A.nnz
+    col = prob.A.col
+    orders = {"csr": None}
+    if n_ranges > 1:
+        rng_of = (col.astype(np.int64) * n_ranges) // n
+        orders["ranges"] = np.argsort(rng_of, kind="stable")
+    out = torch.empty((nnz + E.ECC_GATHER_CHUNK - 1) // E.ECC_GATHER_CHUNK, dtype=torch.float64,
+                      device="cuda")
+    x = run.d_x
+    res = {}
+    for name, order in orders.items():
+        d_idx = run.d_col if order is None else torch.from_numpy(col[order]).cuda()
+        E.ecc_gather_probe(d_idx, nnz, x, n, out, out.numel())
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            E.ecc_gather_probe(d_idx, nnz, x, n, out, out.numel())
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / reps * 1e3
+        res[name] = {"us": round(us, 2), "gathers_per_s": round(nnz / us * 1e6, 0)}
+        del d_idx
+    return res
 
 
 def run_allgatherv_gpu(prob, steps, warmup):

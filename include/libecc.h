@@ -594,6 +594,18 @@ ecc_status_t ecc_mf_error(ecc_mf_t h, const double *d_W, double *d_rmse, void *h
  * ------------------------------------------------------------------------- */
 ecc_status_t ecc_stream_copy(double *d_dst, const double *d_src, int64_t n, void *hip_stream);
 
+/* Gather-rate ceiling of an index stream (measurement): the sum of
+ * d_x[d_idx[k]] over 0 <= k < n, eight consecutive indices per thread and
+ * one workgroup per ECC_GATHER_CHUNK indices, added per workgroup in a fixed
+ * order into d_out[0 .. ceil(n / ECC_GATHER_CHUNK) - 1] (n_out doubles
+ * available, ECC_ERR_ARG if fewer), enqueued on hip_stream.  Indices outside
+ * [0, n_x) are skipped.  It does what a sweep's gathers do -- read an index
+ * stream and gather one vector -- without values, rows or results, so its
+ * rate bounds a sweep over the same columns. */
+#define ECC_GATHER_CHUNK 2048
+ecc_status_t ecc_gather_probe(const int32_t *d_idx, int64_t n, const double *d_x, int64_t n_x,
+                              double *d_out, int64_t n_out, void *hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -29,6 +29,7 @@ ECC_COMPACT_AUTO, ECC_COMPACT_NONE = 0, 1
 ECC_FORM_GENERAL, ECC_FORM_COLUMN_VALUES, ECC_FORM_DIAGONALS = 0, 1, 2
 ECC_MAX_DIAGONALS = 8
 ECC_SCRATCH_DOUBLES = 1 << 20
+ECC_GATHER_CHUNK = 2048
 
 STATUS_NAMES = {0: "ECC_OK", 1: "ECC_ERR_ARG", 2: "ECC_ERR_OVERLAP", 3: "ECC_ERR_RANGE",
                 4: "ECC_ERR_ALLOC", 5: "ECC_ERR_DEVICE", 6: "ECC_ERR_STATE"}
@@ -85,6 +86,7 @@ _SIGS = [
     ("ecc_residual", ctypes.c_int, [_VP, _VP, _I64, _I32, _VP, _VP]),
     ("ecc_iterate_jacobi_noalloc", ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     ("ecc_stream_copy", ctypes.c_int, [_VP, _VP, _I64, _VP]),
+    ("ecc_gather_probe", ctypes.c_int, [_VP, _I64, _VP, _I64, _VP, _I64, _VP]),
     ("ecc_hypercube_create", ctypes.c_int, [_I32, _I64, _I32, _VP, ctypes.POINTER(_VP)]),
     ("ecc_hypercube_destroy", ctypes.c_int, [_VP]),
     ("ecc_hypercube_reset", ctypes.c_int, [_VP]),
@@ -314,6 +316,10 @@ def ecc_solve(plan, mat, d_b, alpha, beta, d_x, d_x_tmp, d_x_hat, d_mask, T, tol
 
 def ecc_stream_copy(d_dst, d_src, n, stream=None):
     _check(lib().ecc_stream_copy(_ptr(d_dst), _ptr(d_src), n, stream))
+
+
+def ecc_gather_probe(d_idx, n, d_x, n_x, d_out, n_out, stream=None):
+    _check(lib().ecc_gather_probe(_ptr(d_idx), n, _ptr(d_x), n_x, _ptr(d_out), n_out, stream))
 
 
 def ecc_hypercube_create(P, m, slack, stream=None) -> int:

@@ -1,6 +1,7 @@
 // Plain streaming copy (16-byte accesses, one per thread): the
 // reference kernel for the measured copy ceiling and for calibrating the
-// HBM byte counters against a kernel of known traffic.
+// HBM byte counters against a kernel of known traffic.  And a gather probe:
+// the rate of gathers of one vector over an index stream.
 #include <algorithm>
 
 #include "ecc_common.h"
@@ -44,9 +45,57 @@ __global__ __launch_bounds__(kCopyThreads) void k_copy_f64(double *__restrict__ 
     if (k < n) dst[k] = src[k];
 }
 
+// Gather probe: workgroup w sums d_x at indices [w C, (w + 1) C) (C =
+// kGatherChunk), eight per thread with every load in flight, and writes the
+// workgroup's sum.
+constexpr int kGatherThreads = 256;
+constexpr int kGatherPer = ECC_GATHER_CHUNK / kGatherThreads;
+static_assert(kGatherPer == 8, "eight indices per thread");
+
+__global__ __launch_bounds__(kGatherThreads) void k_gather_probe(const int32_t *__restrict__ idx,
+                                                                 int64_t n,
+                                                                 const double *__restrict__ x,
+                                                                 int64_t n_x,
+                                                                 double *__restrict__ out) {
+    __shared__ double s_red[kGatherThreads / 64];
+    const int64_t base = (int64_t)blockIdx.x * ECC_GATHER_CHUNK + threadIdx.x;
+    int32_t c[kGatherPer];
+#pragma unroll
+    for (int u = 0; u < kGatherPer; ++u) {
+        const int64_t k = base + (int64_t)u * kGatherThreads;
+        c[u] = k < n ? __builtin_nontemporal_load(idx + k) : -1;
+    }
+    double y[kGatherPer];
+#pragma unroll
+    for (int u = 0; u < kGatherPer; ++u)
+        y[u] = (c[u] >= 0 && (int64_t)c[u] < n_x) ? x[c[u]] : 0.0;
+    double s = 0.0;
+#pragma unroll
+    for (int u = 0; u < kGatherPer; ++u) s = s + y[u];
+    const double total = block_sum<kGatherThreads>(s, s_red);
+    if (threadIdx.x == 0) out[blockIdx.x] = total;
+}
+
 }  // namespace ecc
 
 using namespace ecc;
+
+extern "C" ecc_status_t ecc_gather_probe(const int32_t *d_idx, int64_t n, const double *d_x,
+                                         int64_t n_x, double *d_out, int64_t n_out,
+                                         void *hip_stream) {
+    clear_error();
+    ECC_ARG(n >= 0 && n_x >= 0, "negative size");
+    if (n == 0) return ECC_OK;
+    ECC_ARG(d_idx && d_x && d_out, "NULL pointer");
+    const int64_t grid = (n + ECC_GATHER_CHUNK - 1) / ECC_GATHER_CHUNK;
+    ECC_ARG(n_out >= grid, "d_out holds %lld doubles; %lld needed", (long long)n_out,
+            (long long)grid);
+    ECC_ARG(grid < 0x7fffffff, "n too large");
+    hipLaunchKernelGGL(k_gather_probe, dim3((unsigned)grid), dim3(kGatherThreads), 0,
+                       (hipStream_t)hip_stream, d_idx, n, d_x, n_x, d_out);
+    ECC_LAUNCH_CHECK();
+    return ECC_OK;
+}
 
 extern "C" ecc_status_t ecc_stream_copy(double *d_dst, const double *d_src, int64_t n,
                                         void *hip_stream) {

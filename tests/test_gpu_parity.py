@@ -8,6 +8,7 @@ their iterates are also checked bit for bit.
 """
 
 import dataclasses
+import math
 
 import numpy as np
 import pytest
@@ -1136,6 +1137,38 @@ def test_matrix_checks_long_rows():
     c[row0[-1]] = prob.n                   # a column one past the end
     assert refused(c, val, E.ECC_KIND_POWER) == E.ECC_ERR_ARG
     run.close()
+
+
+@pytest.mark.parametrize("n", [0, 1, 2047, 2048, 2049, 100003])
+def test_gather_probe(n):
+    """ecc_gather_probe: per-workgroup sums of x[idx[k]] over chunks of 2,048
+    indices (compared with exact sums of the same chunks within rounding),
+    indices outside [0, n_x) skipped, and a too-small output refused."""
+    E = _capi()
+    announce("gather probe", n)
+    rng = np.random.default_rng(n + 3)
+    n_x = 5000
+    idx = rng.integers(-3, n_x + 3, n).astype(np.int32)   # a few out of range
+    x = rng.standard_normal(n_x)
+    chunks = max(1, (n + E.ECC_GATHER_CHUNK - 1) // E.ECC_GATHER_CHUNK)
+    out = torch.full((chunks + 1,), np.nan, dtype=torch.float64, device="cuda")
+    d_idx, d_x = torch.from_numpy(idx).cuda(), torch.from_numpy(x).cuda()
+    E.ecc_gather_probe(d_idx, n, d_x, n_x, out, out.numel())
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    ok = (idx >= 0) & (idx < n_x)
+    vals = np.where(ok, x[np.clip(idx, 0, n_x - 1)], 0.0)
+    for c in range((n + E.ECC_GATHER_CHUNK - 1) // E.ECC_GATHER_CHUNK):
+        part = vals[c * E.ECC_GATHER_CHUNK:(c + 1) * E.ECC_GATHER_CHUNK]
+        ref = math.fsum(part)
+        assert abs(got[c] - ref) <= 1e-13 * np.abs(part).sum(), (c, got[c], ref)
+    if n == 0:
+        assert np.isnan(got).all()                      # nothing written
+    else:
+        assert np.isnan(got[(n + E.ECC_GATHER_CHUNK - 1) // E.ECC_GATHER_CHUNK:]).all()
+        with pytest.raises(E.EccError) as ei:
+            E.ecc_gather_probe(d_idx, n, d_x, n_x, out, 0)
+        assert ei.value.status == E.ECC_ERR_ARG
 
 
 @pytest.mark.parametrize("n,off", [(0, 0), (1, 0), (3, 0), (1001, 0), (1001, 1), (65536 * 3 + 5, 0),
