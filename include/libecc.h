@@ -436,11 +436,14 @@ ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double *d_b, doubl
  * k of call t is the sender's partial reduction at step k of call t.
  * --------------------------------------------------------------------------- */
 
-/* Create the hypercube state for P processes (a power of two, 1..64) with
+/* Create the hypercube state for P processes (a power of two, 1..4096) with
  * vectors of m doubles and the given slack (ECC_UNBOUNDED: never wait for a
  * slot that holds a message).  Allocates P * d * m doubles of receive slots
  * (d = log2 P) and their clocks on the current device; work is enqueued on
- * hip_stream.  ECC_ERR_ARG for a bad P, m or slack; ECC_ERR_RANGE when the
+ * hip_stream.  Up to 64 processes a call is one kernel launch; beyond, it is
+ * d - 3 launches (the decisions, the first five steps in sub-cubes of 32
+ * processes, then one launch per further step, partials kept in the result),
+ * with the same results bit for bit.  ECC_ERR_ARG for a bad P, m or slack; ECC_ERR_RANGE when the
  * slots would exceed 2^40 elements; ECC_ERR_ALLOC when allocation fails. */
 ecc_status_t ecc_hypercube_create(int32_t P, int64_t m, int32_t slack, void *hip_stream,
                                   ecc_hypercube_t *out);

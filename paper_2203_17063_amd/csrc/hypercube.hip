@@ -32,7 +32,10 @@ __device__ __forceinline__ void hc_st(double *p, double v) { __builtin_nontempor
 __device__ __forceinline__ double hc_ld(const double *p) { return __builtin_nontemporal_load(p); }
 
 constexpr int kHcThreads = 256;
-constexpr int kHcMaxDims = 6;  // P <= 64: one lane per process in the scalar phase
+constexpr int kHcMaxDims = 6;  // P <= 64: one launch, one lane per process in the scalar phase
+constexpr int kHcMaxDimsBig = 12;  // P <= 4096: decisions, sub-cubes, then step by step
+constexpr int kHcCubeDims = 5;     // sub-cubes of 32 processes in the P > 64 path
+constexpr int kHcDecideThreads = 1024;
 constexpr int32_t kHcNever = INT32_MIN;  // clock of a slot that was never written
 
 struct HcArgs {
@@ -139,6 +142,125 @@ __global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp(HcArgs a) {
     }
 }
 
+// More than 64 processes.  One call is then three kinds of launch:
+//  (1) k_hc_decide_big, one workgroup: process r's thread replays its d
+//      steps in order (its partner's partial clock read from LDS after every
+//      step), writes the (process, step) fresh flags for the data kernels
+//      and the same bookkeeping as hc_decide;
+//  (2) k_hc_cube: the first five steps inside every sub-cube of 32
+//      processes (partners r XOR 2^k, k < 5, share the sub-cube), a thread
+//      carrying element j of the sub-cube's 32 partials in registers as
+//      k_allreduce_ssp<5> does, the partials then stored in the result;
+//  (3) k_hc_pair_step for every further step k: a thread takes element j of
+//      one pair (r, r XOR 2^k) of partials from the result, receives for
+//      each from the partner's partial or its slot, and stores both
+//      partial + received.
+// The additions are those of the one-launch kernel, in the same order.
+__global__ __launch_bounds__(kHcDecideThreads) void k_hc_decide_big(HcArgs a,
+                                                                    uint8_t *__restrict__ fresh) {
+    __shared__ int32_t s_pc[2][1 << kHcMaxDimsBig];
+    const int64_t min_accepted =
+        a.slack == ECC_UNBOUNDED ? INT64_MIN : (int64_t)a.t - (int64_t)a.slack;
+    for (int32_t r = threadIdx.x; r < a.P; r += kHcDecideThreads) s_pc[0][r] = a.t;
+    __syncthreads();
+    for (int k = 0; k < a.D; ++k) {
+        const int cur = k & 1;
+        for (int32_t r = threadIdx.x; r < a.P; r += kHcDecideThreads) {
+            const int32_t sent_clock = s_pc[cur][r ^ (1 << k)];
+            const int64_t sk = (int64_t)r * a.D + k;
+            int32_t sc = a.clk_in[sk];
+            const bool arrived = a.delivered[sk] != 0;
+            uint8_t how;
+            if (arrived) how = 1;                              // delivered
+            else if (sc == kHcNever) how = 3;                  // first receipt: wait
+            else if ((int64_t)sc < min_accepted) how = 2;      // too old: wait
+            else how = 0;                                      // reuse the slot
+            if (how != 0) sc = sent_clock;
+            fresh[sk] = how != 0 ? 1 : 0;
+            s_pc[cur ^ 1][r] = min(s_pc[cur][r], sc);
+            a.clk_out[sk] = sc;
+            if (how == 2) a.waits[sk] += 1;
+            if (a.outcome) a.outcome[sk] = how;
+        }
+        __syncthreads();
+    }
+    if (a.result_clock)
+        for (int32_t r = threadIdx.x; r < a.P; r += kHcDecideThreads)
+            a.result_clock[r] = s_pc[a.D & 1][r];
+}
+
+// Steps 0 .. kHcCubeDims-1 of sub-cube blockIdx.y (processes 32 y .. 32 y +
+// 31); element blockIdx.x * kHcThreads + threadIdx.x.
+__global__ __launch_bounds__(kHcThreads) void k_hc_cube(HcArgs a,
+                                                        const uint8_t *__restrict__ fresh_in) {
+    constexpr int DL = kHcCubeDims, Pt = 1 << DL;
+    __shared__ unsigned long long s_fresh[DL];
+    const int32_t p0 = (int32_t)blockIdx.y * Pt;
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x;
+        for (int k = 0; k < DL; ++k) {
+            const bool f = lane < Pt && fresh_in[(int64_t)(p0 + lane) * a.D + k] != 0;
+            const unsigned long long mask = __ballot(f);
+            if (lane == 0) s_fresh[k] = mask;
+        }
+    }
+    __syncthreads();
+    unsigned long long fresh[DL];
+#pragma unroll
+    for (int k = 0; k < DL; ++k) fresh[k] = uniform64(s_fresh[k]);
+    const int64_t m = a.m;
+    const int64_t j = (int64_t)blockIdx.x * kHcThreads + threadIdx.x;
+    if (j >= m) return;
+    double part[Pt];
+#pragma unroll
+    for (int i = 0; i < Pt; ++i) part[i] = hc_ld(a.contrib + (int64_t)(p0 + i) * m + j);
+#pragma unroll
+    for (int k = 0; k < DL; ++k) {
+        double *srow = a.slots + ((int64_t)p0 * a.D + k) * m + j;  // + i * D * m
+        const int bit = 1 << k;
+#pragma unroll
+        for (int i = 0; i < Pt; ++i) {
+            if (i & bit) continue;
+            const int q = i | bit;
+            const bool fr = (fresh[k] >> i) & 1ull, fq = (fresh[k] >> q) & 1ull;
+            double *sr = srow + (int64_t)i * a.D * m, *sq = srow + (int64_t)q * a.D * m;
+            const double gr = fr ? part[q] : hc_ld(sr);
+            const double gq = fq ? part[i] : hc_ld(sq);
+            if (fr) hc_st(sr, gr);
+            if (fq) hc_st(sq, gq);
+            part[i] = part[i] + gr;
+            part[q] = part[q] + gq;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = 0; i < Pt; ++i) hc_st(a.result + (int64_t)(p0 + i) * m + j, part[i]);
+}
+
+// Step k >= kHcCubeDims for pair blockIdx.y of the partials in the result.
+__global__ __launch_bounds__(kHcThreads) void k_hc_pair_step(HcArgs a,
+                                                             const uint8_t *__restrict__ fresh_in,
+                                                             int32_t k) {
+    const int64_t pi = blockIdx.y;
+    const int32_t bit = 1 << k;
+    const int32_t r = (int32_t)(((pi >> k) << (k + 1)) | (pi & (bit - 1)));
+    const int32_t q = r | bit;
+    const bool fr = fresh_in[(int64_t)r * a.D + k] != 0, fq = fresh_in[(int64_t)q * a.D + k] != 0;
+    const int64_t m = a.m;
+    const int64_t j = (int64_t)blockIdx.x * kHcThreads + threadIdx.x;
+    if (j >= m) return;
+    double *pr = a.result + (int64_t)r * m + j, *pq = a.result + (int64_t)q * m + j;
+    double *sr = a.slots + ((int64_t)r * a.D + k) * m + j;
+    double *sq = a.slots + ((int64_t)q * a.D + k) * m + j;
+    const double xr = hc_ld(pr), xq = hc_ld(pq);
+    const double gr = fr ? xq : hc_ld(sr);
+    const double gq = fq ? xr : hc_ld(sq);
+    if (fr) hc_st(sr, gr);
+    if (fq) hc_st(sq, gq);
+    hc_st(pr, xr + gr);
+    hc_st(pq, xq + gq);
+}
+
 }  // namespace ecc
 
 using namespace ecc;
@@ -152,6 +274,7 @@ struct ecc_hypercube_s {
     double *d_slots = nullptr;               // [P][D][m]
     int32_t *d_clk = nullptr;                // [2][P][D]
     unsigned long long *d_waits = nullptr;   // [P][D]
+    uint8_t *d_fresh = nullptr;              // P > 64: [P][D] this call's fresh slots
 };
 
 namespace {
@@ -188,8 +311,8 @@ ecc_status_t ecc_hypercube_create(int32_t P, int64_t m, int32_t slack, void *hip
     clear_error();
     ECC_ARG(out != nullptr, "out is NULL");
     *out = nullptr;
-    ECC_ARG(P >= 1 && P <= (1 << kHcMaxDims) && (P & (P - 1)) == 0,
-            "P = %d must be a power of two in [1, 64]", P);
+    ECC_ARG(P >= 1 && P <= (1 << kHcMaxDimsBig) && (P & (P - 1)) == 0,
+            "P = %d must be a power of two in [1, %d]", P, 1 << kHcMaxDimsBig);
     ECC_ARG(m >= 0, "m must be >= 0");
     ECC_ARG(slack >= 0, "slack must be >= 0 (ECC_UNBOUNDED for no limit)");
     int D = 0;
@@ -222,6 +345,8 @@ ecc_status_t ecc_hypercube_create(int32_t P, int64_t m, int32_t slack, void *hip
             return fail("hipMalloc of the slot clocks failed");
         if (hipMalloc((void **)&h->d_waits, sizeof(unsigned long long) * n) != hipSuccess)
             return fail("hipMalloc of the wait counters failed");
+        if (D > kHcMaxDims && hipMalloc((void **)&h->d_fresh, n) != hipSuccess)
+            return fail("hipMalloc of the fresh flags failed");
     }
     // grid: one workgroup per pass over its elements (measured on MI355X,
     // 32 processes x 16 MB: 945 us, against 974 us with the resident
@@ -244,6 +369,7 @@ ecc_status_t ecc_hypercube_destroy(ecc_hypercube_t h) {
     (void)hipFree(h->d_slots);
     (void)hipFree(h->d_clk);
     (void)hipFree(h->d_waits);
+    (void)hipFree(h->d_fresh);
     delete h;
     return ECC_OK;
 }
@@ -287,6 +413,22 @@ ecc_status_t ecc_allreduce_ssp(ecc_hypercube_t h, const double *d_contrib,
     a.result_clock = d_result_clock;
     a.outcome = d_outcome;
     const dim3 grid(h->grid);
+    if (h->D > kHcMaxDims) {
+        // decisions, the sub-cubes' steps, then one launch per further step
+        hipLaunchKernelGGL(k_hc_decide_big, dim3(1), dim3(kHcDecideThreads), 0, h->stream, a,
+                           h->d_fresh);
+        ECC_LAUNCH_CHECK();
+        hipLaunchKernelGGL(k_hc_cube, dim3(h->grid, h->P >> kHcCubeDims), dim3(kHcThreads), 0,
+                           h->stream, a, h->d_fresh);
+        ECC_LAUNCH_CHECK();
+        for (int32_t k = kHcCubeDims; k < h->D; ++k) {
+            hipLaunchKernelGGL(k_hc_pair_step, dim3(h->grid, h->P / 2), dim3(kHcThreads), 0,
+                               h->stream, a, h->d_fresh, k);
+            ECC_LAUNCH_CHECK();
+        }
+        h->clock += 1;
+        return ECC_OK;
+    }
     switch (h->D) {
         case 0: hc_launch<0>(grid, h->stream, a); break;
         case 1: hc_launch<1>(grid, h->stream, a); break;

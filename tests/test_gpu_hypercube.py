@@ -79,6 +79,30 @@ def test_parity_ragged_lengths(m):
     _run_and_compare(32, m, 1, 0.6, T=8, seed=m)
 
 
+@pytest.mark.parametrize("P,m,slack,q,in_place", [
+    (128, 700, 1, 0.6, False),
+    (256, 257, 2, 0.5, True),
+    (512, 3, 0, 0.7, False),
+    (1024, 1000, H.UNBOUNDED, 0.3, False),
+    (4096, 40, 3, 0.8, True),
+    (128, 0, 1, 0.5, False),
+])
+def test_parity_many_processes(P, m, slack, q, in_place):
+    """More than 64 processes: the decisions in one workgroup, the first
+    five steps in sub-cubes of 32, then one launch per further step -- the
+    same results, clocks, slot outcomes and waits as the oracle, bit for
+    bit, up to the 4,096-process maximum, in place too."""
+    _run_and_compare(P, m, slack, q, T=6, seed=P + m, in_place=in_place)
+
+
+def test_too_many_processes_refused():
+    E = _E()
+    for P in (8192, 96):
+        with pytest.raises(E.EccError) as ei:
+            E.ecc_hypercube_create(P, 10, 1, _stream())
+        assert ei.value.status == E.ECC_ERR_ARG
+
+
 def test_parity_larger_vector_in_place():
     _run_and_compare(16, 200003, 3, 0.8, T=6, seed=3, in_place=True)
 
@@ -86,7 +110,7 @@ def test_parity_larger_vector_in_place():
 def test_reset_and_errors():
     E = _E()
     announce("hypercube errors")
-    for bad in (0, 3, 12, 128):
+    for bad in (0, 3, 12, 8192):
         with pytest.raises(E.EccError) as ei:
             E.ecc_hypercube_create(bad, 10, 1, _stream())
         assert ei.value.status == E.ECC_ERR_ARG
