@@ -99,10 +99,12 @@ __device__ __forceinline__ unsigned long long uniform64(unsigned long long v) {
 // pair (r, r XOR 2^k) sit in the same thread and are updated together from
 // their old partials.  A scheduling barrier between steps keeps the loads of
 // a step from being hoisted above the stores of the previous one (register
-// pressure).  Measured on MI355X (slack 2, 80 % delivery): P = 32 x 16 MB,
-// 168 VGPRs, 3.98 TB/s; P = 64 x 8 MB, 256 VGPRs, 2.63 TB/s (2.23 TB/s with
-// two lanes per element, whose per-lane delivery bits make every slot
-// access divergent).
+// pressure).  The grid has one thread per element and no loop: a loop over
+// elements kept every row address live across it, and the 224 addresses of
+// P = 32 then spilled 620 SGPRs (942 against 933 us per call).  Measured on
+// MI355X (slack 2, 80 % delivery): P = 32 x 16 MB, 166 VGPRs, 4.03 TB/s;
+// P = 64 x 8 MB, 255 VGPRs, 2.63 TB/s (2.23 TB/s with two lanes per element,
+// whose per-lane delivery bits make every slot access divergent).
 template <int D>
 __global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp(HcArgs a) {
     constexpr int Pt = 1 << D;
@@ -113,8 +115,8 @@ __global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp(HcArgs a) {
 #pragma unroll
     for (int k = 0; k < D; ++k) fresh[k] = uniform64(s_fresh[k]);
     const int64_t m = a.m;
-    const int64_t stride = (int64_t)gridDim.x * kHcThreads;
-    for (int64_t j = (int64_t)blockIdx.x * kHcThreads + threadIdx.x; j < m; j += stride) {
+    const int64_t j = (int64_t)blockIdx.x * kHcThreads + threadIdx.x;
+    if (j < m) {
         double part[Pt];
 #pragma unroll
         for (int i = 0; i < Pt; ++i) part[i] = hc_ld(a.contrib + i * m + j);
@@ -322,6 +324,11 @@ ecc_status_t ecc_hypercube_create(int32_t P, int64_t m, int32_t slack, void *hip
         set_error("P * d * m too large");
         return ECC_ERR_RANGE;
     }
+    // one thread per element: the grid's x extent holds at most 2^31 - 1 workgroups
+    if (m > (int64_t)0x7fffffff * kHcThreads) {
+        set_error("m too large");
+        return ECC_ERR_RANGE;
+    }
     ecc_hypercube_s *h = new (std::nothrow) ecc_hypercube_s();
     if (!h) {
         set_error("host allocation failed");
@@ -352,8 +359,7 @@ ecc_status_t ecc_hypercube_create(int32_t P, int64_t m, int32_t slack, void *hip
     // 32 processes x 16 MB: 945 us, against 974 us with the resident
     // workgroups walking the vector)
     const int64_t per_wg = kHcThreads;  // elements of one workgroup
-    const int64_t need = std::max<int64_t>(1, (m + per_wg - 1) / per_wg);
-    h->grid = (int32_t)std::min<int64_t>(need, 0x7fffffff);
+    h->grid = (int32_t)std::max<int64_t>(1, (m + per_wg - 1) / per_wg);
     ecc_status_t st = hc_reset(h);
     if (st != ECC_OK) {
         ecc_hypercube_destroy(h);

@@ -100,3 +100,19 @@ def test_product_path_does_not_touch_oracle():
                 text = open(os.path.join(dirpath, f)).read()
                 for bad in ("import oracle", "from oracle", "liboracle", "orc_"):
                     assert bad not in text, (f, bad)
+
+
+@pytest.mark.parametrize("P,m,slack,expect", [
+    (0, 16, 0, E.ECC_ERR_ARG),                        # P < 1
+    (3, 16, 0, E.ECC_ERR_ARG),                        # not a power of two
+    (8192, 16, 0, E.ECC_ERR_ARG),                     # beyond 4096 processes
+    (4, -1, 0, E.ECC_ERR_ARG),                        # negative length
+    (4, 16, -1, E.ECC_ERR_ARG),                       # negative slack
+    (4, (1 << 40) // 8 + 1, 0, E.ECC_ERR_RANGE),      # slots beyond 2^40 elements
+    (1, 0x7fffffff * 256 + 1, 0, E.ECC_ERR_RANGE),    # beyond one thread per element
+])
+def test_hypercube_create_checks_without_device(P, m, slack, expect):
+    """Argument and range checks return before any device call."""
+    with pytest.raises(E.EccError) as err:
+        E.ecc_hypercube_create(P, m, slack)
+    assert err.value.status == expect
