@@ -39,6 +39,10 @@
 //    length (rows sorted by length); kMfBatch ratings' loads
 //    are in flight and the next batch's indices are loaded while one is
 //    summed; the next item's row descriptors are loaded one item ahead.
+//  - Rows without ratings in the minibatch (about half of each list at the
+//    benchmark's shape) end the list; every workgroup of the worker first
+//    writes zeros over a contiguous share of them, with the entity indices
+//    of several passes loaded together.
 // A rating's dot product is the running sum of the group's lanes in column
 // order, handed from lane to lane by shuffles, so errors and gradients are
 // the sequential definition's, bit for bit.
@@ -56,6 +60,15 @@ constexpr int kMfMaxRank = 64;
 constexpr int kMfHeavy = 128;   // rows with more ratings take a whole workgroup
 constexpr int kMfStage = 2048;  // doubles of LDS for one chunk of a heavy row
 constexpr int kMfBatch = 4;     // ratings of a light row in flight together
+constexpr int kMfZeroPasses = 8;  // passes of rows without ratings with loads in flight together
+
+// Rows without ratings: R / V lanes per row, V doubles per lane.
+template <int R>
+struct MfZero {
+    static constexpr int V = R >= 2 ? 2 : 1;
+    static constexpr int LPR = R / V;
+    static constexpr int ROWS = kMfThreads / LPR;  // rows of one pass of the workgroup
+};
 
 template <int R>
 struct MfShape {
@@ -78,6 +91,7 @@ struct MfGradArgs {
     const int32_t *start_of;      // same order: first rating of that row in oidx / rv
     const int32_t *len_of;        // same order: its number of ratings
     const int32_t *n_heavy;       // [P K] rows of more than kMfHeavy ratings, per list
+    const int32_t *n_rated;       // [P K] rows with ratings, per list (the rows without follow)
     const int32_t *batch;         // [P] this iteration's minibatch of each worker
     double *const *grads;         // [P] -> m doubles
     double *partials;             // [gridDim.y][gridDim.x] sums of e^2 over user rows
@@ -216,6 +230,7 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfGradArgs a) {
     __shared__ double s_prod[kMfStage];
     __shared__ double s_red[kMfThreads / 64];
     constexpr int LPR = MfShape<R>::LPR, G = MfShape<R>::GROUPS;
+    using Z = MfZero<R>;
     static_assert(MfShape<R>::CHUNK * R == kMfStage, "a heavy chunk fills the stage");
     const int lane = threadIdx.x % LPR, grp = threadIdx.x / LPR;
     // worker p's list for its minibatch of this iteration
@@ -225,25 +240,56 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfGradArgs a) {
     const int32_t *row_of = a.row_of + list * a.E;
     const int32_t *start_of = a.start_of + list * a.E;
     const int32_t *len_of = a.len_of + list * a.E;
-    const int64_t n_rows = a.E, n_heavy = a.n_heavy[list];
-    const int64_t n_work = n_heavy + (n_rows - n_heavy + G - 1) / G;
+    const int64_t n_rows = a.E, n_heavy = a.n_heavy[list], n_rated = a.n_rated[list];
+    const int64_t n_work = n_heavy + (n_rated - n_heavy + G - 1) / G;
+    const int64_t g = gridDim.x;
     double sq = 0.0;
+    // Rows without ratings (list positions n_rated .. E-1, in entity order):
+    // this workgroup's contiguous share is written as zeros first,
+    // kMfZeroPasses passes at a time with all their entity loads in flight
+    // (measured on MI355X, 25M ratings, rank 16, 32 workers: 806 against
+    // 863 us per iteration when they were light rows of length 0 at the end
+    // of the list; writing them last, or first in every other workgroup,
+    // 815 and 810 us).
+    const int64_t n_zero = n_rows - n_rated;
+    const int64_t z_lo = n_rated + n_zero * (int64_t)blockIdx.x / g;
+    const int64_t z_hi = n_rated + n_zero * ((int64_t)blockIdx.x + 1) / g;
+    {
+        double *const grad = a.grads[p];
+        const int zl = threadIdx.x % Z::LPR, zr = threadIdx.x / Z::LPR;
+        for (int64_t zq = z_lo; zq < z_hi; zq += (int64_t)kMfZeroPasses * Z::ROWS) {
+            int32_t ent[kMfZeroPasses];
+#pragma unroll
+            for (int s = 0; s < kMfZeroPasses; ++s) {
+                const int64_t q = zq + (int64_t)s * Z::ROWS + zr;
+                ent[s] = q < z_hi ? row_of[q] : -1;
+            }
+#pragma unroll
+            for (int s = 0; s < kMfZeroPasses; ++s) {
+                if (ent[s] >= 0) {
+                    double *gz = grad + (int64_t)ent[s] * R + zl * Z::V;
+#pragma unroll
+                    for (int c = 0; c < Z::V; ++c) gz[c] = 0.0;
+                }
+            }
+        }
+    }
     // this lane group's row in a light item w (descriptors one item ahead)
     auto light_q = [&](int64_t w) { return n_heavy + (w - n_heavy) * G + grp; };
     int32_t nrow = 0, nx0 = 0, nlen = -1;
     int64_t w = blockIdx.x;
-    if (w < n_work && w >= n_heavy && light_q(w) < n_rows) {
+    if (w < n_work && w >= n_heavy && light_q(w) < n_rated) {
         const int64_t q = light_q(w);
         nrow = row_of[q];
         nx0 = start_of[q];
         nlen = len_of[q];
     }
-    for (; w < n_work; w += gridDim.x) {
+    for (; w < n_work; w += g) {
         if (w < n_heavy) {
             sq += mf_heavy_row<R>(a, p, row_of[w], start_of[w], len_of[w], s_prod);
-            const int64_t wn = w + gridDim.x;
+            const int64_t wn = w + g;
             nlen = -1;
-            if (wn < n_work && wn >= n_heavy && light_q(wn) < n_rows) {
+            if (wn < n_work && wn >= n_heavy && light_q(wn) < n_rated) {
                 const int64_t q = light_q(wn);
                 nrow = row_of[q];
                 nx0 = start_of[q];
@@ -252,9 +298,9 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfGradArgs a) {
             continue;
         }
         const int32_t row = nrow, x0 = nx0, len = nlen;
-        const int64_t wn = w + gridDim.x;
+        const int64_t wn = w + g;
         nlen = -1;
-        if (wn < n_work && light_q(wn) < n_rows) {
+        if (wn < n_work && light_q(wn) < n_rated) {
             const int64_t q = light_q(wn);
             nrow = row_of[q];
             nx0 = start_of[q];
@@ -378,6 +424,7 @@ struct ecc_mf_s {
     int32_t *d_start_of = nullptr;  // same order: first rating in d_oidx / d_rv
     int32_t *d_len_of = nullptr;    // same order: number of ratings
     int32_t *d_n_heavy = nullptr;   // [P K] rows of more than kMfHeavy ratings, per list
+    int32_t *d_n_rated = nullptr;   // [P K] rows with ratings, per list
     int64_t *d_sizes = nullptr;     // [P K] ratings of each minibatch
     int32_t *d_users = nullptr;     // [N] copies of the ratings, for ecc_mf_error
     int32_t *d_items = nullptr;
@@ -398,6 +445,7 @@ ecc_status_t ecc_mf_destroy(ecc_mf_t h) {
     (void)hipFree(h->d_start_of);
     (void)hipFree(h->d_len_of);
     (void)hipFree(h->d_n_heavy);
+    (void)hipFree(h->d_n_rated);
     (void)hipFree(h->d_sizes);
     (void)hipFree(h->d_users);
     (void)hipFree(h->d_items);
@@ -446,7 +494,7 @@ static ecc_status_t ecc_mf_create_impl(int32_t n_users, int32_t n_items, int32_t
     // ratings, longest first (rows of equal length in entity order): heavy
     // rows by a sort, the rest by a counting sort.
     std::vector<int32_t> oidx(2 * N), row_of(n_lists * E), start_of(n_lists * E),
-        len_of(n_lists * E), n_heavy(n_lists);
+        len_of(n_lists * E), n_heavy(n_lists), n_rated(n_lists);
     std::vector<int64_t> sizes(n_lists);
     std::vector<double> rv(2 * N);
     std::vector<int32_t> rp(E + 1), fill(E), heavy, by_len(kMfHeavy + 2);
@@ -503,6 +551,7 @@ static ecc_status_t ecc_mf_create_impl(int32_t n_users, int32_t n_items, int32_t
                 len_of[list * E + q] = rp[ro[q] + 1] - rp[ro[q]];
             }
             n_heavy[list] = (int32_t)heavy.size();
+            n_rated[list] = (int32_t)(E - by_len[0]);
         }
     }
     std::vector<double> scale(E);
@@ -519,10 +568,13 @@ static ecc_status_t ecc_mf_create_impl(int32_t n_users, int32_t n_items, int32_t
     h->P = P;
     h->K = K;
     h->N = N;
-    // a worker's workgroups: its share of what the device holds at once
-    // (8 per CU), at least 1
+    // a worker's workgroups: its share of 16 per CU (four times what the
+    // device holds at once), at most one per light item of a whole list, at
+    // least 1.  Measured on MI355X (25M ratings, rank 16, 32 workers: 107
+    // workgroups per worker): 763 us per iteration, against 798 us with 8
+    // per CU and 783-785 us with 160-512 per worker.
     const int64_t groups = kMfThreads / (rank < 4 ? 1 : rank / 4);
-    h->grad_grid = std::max<int32_t>(1, mf_grid((E + groups - 1) / groups, 8) / P);
+    h->grad_grid = std::max<int32_t>(1, mf_grid((E + groups - 1) / groups, 16) / P);
     h->err_grid = mf_grid((N + groups - 1) / groups, 8);
     const int64_t n_part = std::max<int64_t>((int64_t)h->grad_grid * P, h->err_grid);
     auto fail = [&](const char *what) {
@@ -540,6 +592,7 @@ static ecc_status_t ecc_mf_create_impl(int32_t n_users, int32_t n_items, int32_t
         !up((void **)&h->d_start_of, start_of.data(), sizeof(int32_t) * n_lists * E) ||
         !up((void **)&h->d_len_of, len_of.data(), sizeof(int32_t) * n_lists * E) ||
         !up((void **)&h->d_n_heavy, n_heavy.data(), sizeof(int32_t) * n_lists) ||
+        !up((void **)&h->d_n_rated, n_rated.data(), sizeof(int32_t) * n_lists) ||
         !up((void **)&h->d_sizes, sizes.data(), sizeof(int64_t) * n_lists) ||
         !up((void **)&h->d_users, users.data(), sizeof(int32_t) * N) ||
         !up((void **)&h->d_items, items.data(), sizeof(int32_t) * N) ||
@@ -607,6 +660,7 @@ ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam,
     ga.start_of = h->d_start_of;
     ga.len_of = h->d_len_of;
     ga.n_heavy = h->d_n_heavy;
+    ga.n_rated = h->d_n_rated;
     ga.batch = d_batch;
     ga.grads = d_grads;
     ga.partials = h->d_partials;
