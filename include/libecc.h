@@ -440,7 +440,7 @@ ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double *d_b, doubl
  * vectors of m doubles and the given slack (ECC_UNBOUNDED: never wait for a
  * slot that holds a message).  Allocates P * d * m doubles of receive slots
  * (d = log2 P) and their clocks on the current device; work is enqueued on
- * hip_stream.  Up to 64 processes a call is one kernel launch; beyond, it is
+ * hip_stream.  Up to 32 processes a call is one kernel launch; beyond, it is
  * d - 3 launches (the decisions, the first five steps in sub-cubes of 32
  * processes, then one launch per further step, partials kept in the result),
  * with the same results bit for bit.  ECC_ERR_ARG for a bad P, m or slack; ECC_ERR_RANGE when the

@@ -32,9 +32,9 @@ __device__ __forceinline__ void hc_st(double *p, double v) { __builtin_nontempor
 __device__ __forceinline__ double hc_ld(const double *p) { return __builtin_nontemporal_load(p); }
 
 constexpr int kHcThreads = 256;
-constexpr int kHcMaxDims = 6;  // P <= 64: one launch, one lane per process in the scalar phase
+constexpr int kHcMaxDims = 5;  // P <= 32: one launch, one lane per process in the scalar phase
 constexpr int kHcMaxDimsBig = 12;  // P <= 4096: decisions, sub-cubes, then step by step
-constexpr int kHcCubeDims = 5;     // sub-cubes of 32 processes in the P > 64 path
+constexpr int kHcCubeDims = 5;     // sub-cubes of 32 processes in the P > 32 path
 constexpr int kHcDecideThreads = 1024;
 constexpr int32_t kHcNever = INT32_MIN;  // clock of a slot that was never written
 
@@ -94,7 +94,7 @@ __device__ __forceinline__ unsigned long long uniform64(unsigned long long v) {
 }
 
 // Column layout: a thread carries element j of all P = 2^D partial
-// reductions in registers (P <= 64), so every load and store of a wave
+// reductions in registers (P <= 32), so every load and store of a wave
 // covers contiguous bytes of one row.  At step k the two processes of each
 // pair (r, r XOR 2^k) sit in the same thread and are updated together from
 // their old partials.  A scheduling barrier between steps keeps the loads of
@@ -102,9 +102,11 @@ __device__ __forceinline__ unsigned long long uniform64(unsigned long long v) {
 // pressure).  The grid has one thread per element and no loop: a loop over
 // elements kept every row address live across it, and the 224 addresses of
 // P = 32 then spilled 620 SGPRs (942 against 933 us per call).  Measured on
-// MI355X (slack 2, 80 % delivery): P = 32 x 16 MB, 166 VGPRs, 4.03 TB/s;
-// P = 64 x 8 MB, 255 VGPRs, 2.63 TB/s (2.23 TB/s with two lanes per element,
-// whose per-lane delivery bits make every slot access divergent).
+// MI355X (slack 2, 80 % delivery): P = 32 x 16 MB, 166 VGPRs, 4.03 TB/s.
+// Sixty-four processes take the multi-launch path below: 1,202 us per call
+// of 8 MB vectors, against 1,530 us with all 64 partials of an element in
+// one thread (255 VGPRs, one wave per SIMD), and slower still with two lanes
+// per element, whose per-lane delivery bits make every slot access divergent.
 template <int D>
 __global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp(HcArgs a) {
     constexpr int Pt = 1 << D;
@@ -144,7 +146,7 @@ __global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp(HcArgs a) {
     }
 }
 
-// More than 64 processes.  One call is then three kinds of launch:
+// More than 32 processes.  One call is then three kinds of launch:
 //  (1) k_hc_decide_big, one workgroup: process r's thread replays its d
 //      steps in order (its partner's partial clock read from LDS after every
 //      step), writes the (process, step) fresh flags for the data kernels
@@ -441,8 +443,7 @@ ecc_status_t ecc_allreduce_ssp(ecc_hypercube_t h, const double *d_contrib,
         case 2: hc_launch<2>(grid, h->stream, a); break;
         case 3: hc_launch<3>(grid, h->stream, a); break;
         case 4: hc_launch<4>(grid, h->stream, a); break;
-        case 5: hc_launch<5>(grid, h->stream, a); break;
-        default: hc_launch<6>(grid, h->stream, a); break;
+        default: hc_launch<5>(grid, h->stream, a); break;
     }
     ECC_LAUNCH_CHECK();
     h->clock += 1;

@@ -98,6 +98,23 @@ def test_mf_one_worker_and_idle_rows():
                           T=4, eta=0.5, seed=2, K=5))
 
 
+def test_mf_empty_minibatches():
+    """Fewer ratings per shard than minibatches: some workers' minibatches
+    are empty (their lists hold only rows without ratings), though never
+    all of one iteration's."""
+    prob = W.mf_problem(n_users=40, n_items=25, n_ratings=20, rank=4, P=4, S=1, q=0.7, T=8,
+                        eta=0.5, seed=1, K=8)
+    N, P, K = prob.N, prob.P, prob.K
+    used = np.zeros((prob.T, P), dtype=np.int64)
+    for t in range(prob.T):
+        for p in range(P):
+            L = N * (p + 1) // P - N * p // P
+            b = prob.batch[t][p]
+            used[t, p] = L * (b + 1) // K - L * b // K
+    assert (used == 0).sum() > 3 and (used.sum(axis=1) > 0).all()
+    _compare(prob)
+
+
 def test_mf_errors():
     from paper_2203_17063_amd import capi as E
     announce("mf errors")
