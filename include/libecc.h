@@ -506,7 +506,7 @@ ecc_status_t ecc_bcast_threshold(int32_t P, int32_t root, int64_t m, double thet
                                  const double *d_src, double *const *d_dst, int64_t *h_count,
                                  void *hip_stream);
 
-/* Reduce (sum) to the root over the binomial spanning tree, 1 <= P <= 64.
+/* Reduce (sum) to the root over the binomial spanning tree, 1 <= P <= 4096.
  *   mode ECC_THRESHOLD_DATA:  theta in [0, 1]; the first k = ceil(theta * m)
  *     elements of all P processes are reduced; d_result[k, m) untouched.
  *   mode ECC_THRESHOLD_PROCS: theta in (0, 1]; the full vectors (k = m) of

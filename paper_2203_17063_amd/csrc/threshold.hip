@@ -14,7 +14,8 @@
 //    (at least ceil(theta * P) of them).  The order is the tree's: a parent
 //    adds its children's partial sums leaves first, which is, stage by stage
 //    from the last one, q += partial(q + 2^s) for every q < 2^s.  A thread
-//    carries one element of every involved process in registers.
+//    carries one element of every involved process in registers; beyond 64
+//    processes it sums them in the same tree as a pairwise sum (below).
 //  - The dropping allreduce sums, in rank order from +0.0, the contributions
 //    of the ranks that arrived in this step.
 // All sums are fp64 without contraction, in the order stated, so results
@@ -28,6 +29,7 @@ namespace ecc {
 
 constexpr int kThrThreads = 256;
 constexpr int kThrMaxStages = 6;  // Reduce: at most 64 processes in registers
+constexpr int kThrMaxStagesBig = 12;  // Reduce beyond 64 processes: up to 4096
 constexpr int kBcastTile = 4096;  // elements one workgroup copies
 
 // One workgroup per tile of kBcastTile elements of the prefix: the tile is
@@ -100,6 +102,82 @@ __global__ __launch_bounds__(kThrThreads) void k_reduce_bst(int32_t P, int32_t r
                 if (q + (1 << s) < n) part[q] = part[q] + part[q + (1 << s)];
         }
         result[j] = part[0];
+    }
+}
+
+// More than 64 processes.  Stage by stage from the last, q += partial(q +
+// 2^s) builds a binary tree whose leaves, read left to right, are the
+// relative ranks in the bit-reversed order of D = ceil(log2 n) bits: the
+// two children of a node combined at stage s are its halves, the lower
+// rank on the left and added first.  A rank at or beyond n is absent; as
+// absence grows with the rank, a node whose left child is absent has an
+// absent right child too, and a node with an absent right child is its
+// left child.  So the reduction is a pairwise sum over that order, and a
+// thread computes it for its element with a stack of one node per level:
+// the 8 leaves of each group of 8 consecutive positions are loaded
+// together and added into one node, which is merged into the stack as a
+// binary counter over the group index.
+constexpr int kBrev3[8] = {0, 4, 2, 6, 1, 5, 3, 7};
+
+template <int D>
+__global__ __launch_bounds__(kThrThreads) void k_reduce_bst_big(
+    int32_t P, int32_t root, int32_t n, int64_t k, const double *const *__restrict__ src,
+    double *__restrict__ result) {
+    constexpr int H = D - 3;  // levels above a group of 8 leaves
+    static_assert(H >= 1 && D <= kThrMaxStagesBig, "more than 64 processes");
+    const int64_t stride = (int64_t)gridDim.x * kThrThreads;
+    for (int64_t j = (int64_t)blockIdx.x * kThrThreads + threadIdx.x; j < k; j += stride) {
+        double st[H];
+        bool sv[H];
+#pragma unroll
+        for (int l = 0; l < H; ++l) {
+            st[l] = 0.0;
+            sv[l] = false;
+        }
+        double node = 0.0;
+        for (int32_t b = 0; b < (1 << H); ++b) {
+            // leaf u of group b sits at position 8 b + u: relative rank
+            // bitrev3(u) 2^H + bitrev_H(b)
+            const int32_t hb = (int32_t)(__brev((uint32_t)b) >> (32 - H));
+            double v[8];
+            bool e[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int32_t q = (kBrev3[u] << H) | hb;
+                e[u] = q < n;
+                int32_t p = (e[u] ? q : 0) + root;  // (an absent leaf names no process)
+                if (p >= P) p -= P;
+                v[u] = e[u] ? __builtin_nontemporal_load(src[p] + j) : 0.0;
+            }
+            // the group's node: pairs, then quads, then the eight
+#pragma unroll
+            for (int w = 1; w < 8; w *= 2) {
+#pragma unroll
+                for (int u = 0; u < 8; u += 2 * w)
+                    if (e[u + w]) v[u] = v[u] + v[u + w];
+            }
+            node = v[0];
+            bool nv = e[0];
+            // merge as a binary counter: level l holds the left sibling while
+            // bit l of b is 1
+            bool carry = true;
+#pragma unroll
+            for (int l = 0; l < H; ++l) {
+                if (carry) {
+                    if ((b >> l) & 1) {
+                        if (sv[l] && nv) node = st[l] + node;
+                        else if (sv[l]) node = st[l];
+                        nv = sv[l];
+                    } else {
+                        st[l] = node;
+                        sv[l] = nv;
+                        carry = false;
+                    }
+                }
+            }
+        }
+        // the last group (b = 2^H - 1) carried through every level: the root
+        result[j] = node;
     }
 }
 
@@ -193,7 +271,8 @@ ecc_status_t ecc_reduce_threshold(int32_t P, int32_t root, int64_t m, double the
                                   const double *const *d_src, double *d_result,
                                   int64_t *h_elements, int32_t *h_processes, void *hip_stream) {
     clear_error();
-    ECC_ARG(P >= 1 && P <= (1 << kThrMaxStages), "P = %d must lie in [1, 64]", P);
+    ECC_ARG(P >= 1 && P <= (1 << kThrMaxStagesBig), "P = %d must lie in [1, %d]", P,
+            1 << kThrMaxStagesBig);
     ECC_ARG(root >= 0 && root < P, "root %d outside [0, P)", root);
     ECC_ARG(m >= 0, "m must be >= 0");
     ECC_ARG(mode == ECC_THRESHOLD_DATA || mode == ECC_THRESHOLD_PROCS, "unknown mode %d", mode);
@@ -223,7 +302,13 @@ ecc_status_t ecc_reduce_threshold(int32_t P, int32_t root, int64_t m, double the
         case 3: hipLaunchKernelGGL(k_reduce_bst<3>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
         case 4: hipLaunchKernelGGL(k_reduce_bst<4>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
         case 5: hipLaunchKernelGGL(k_reduce_bst<5>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
-        default: hipLaunchKernelGGL(k_reduce_bst<6>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        case 6: hipLaunchKernelGGL(k_reduce_bst<6>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        case 7: hipLaunchKernelGGL(k_reduce_bst_big<7>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        case 8: hipLaunchKernelGGL(k_reduce_bst_big<8>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        case 9: hipLaunchKernelGGL(k_reduce_bst_big<9>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        case 10: hipLaunchKernelGGL(k_reduce_bst_big<10>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        case 11: hipLaunchKernelGGL(k_reduce_bst_big<11>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        default: hipLaunchKernelGGL(k_reduce_bst_big<12>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
     }
     ECC_LAUNCH_CHECK();
     return ECC_OK;

@@ -77,6 +77,31 @@ def test_reduce(P, root, mode, theta):
     assert np.array_equal(got, res_h), np.abs(got - res_h).max()
 
 
+@pytest.mark.parametrize("P,root", [(65, 0), (100, 99), (128, 5), (257, 100), (1000, 1),
+                                    (4096, 4095)])
+@pytest.mark.parametrize("mode,theta", [(TH.DATA, 1.0), (TH.DATA, 0.4), (TH.PROCS, 0.3),
+                                        (TH.PROCS, 0.6)])
+def test_reduce_many_processes(P, root, mode, theta):
+    """More than 64 processes: the tree's pairwise form, relative ranks
+    missing from the top of the tree (P and the involved count not powers
+    of two) and processes of the first stages only."""
+    E = _E()
+    m = 2053
+    announce("reduce many", P, root, mode, theta, m)
+    rng = np.random.default_rng(P + 7 * root)
+    scale = 10.0 ** rng.integers(-6, 6, size=P)
+    xs_h = [rng.standard_normal(m) * scale[p] for p in range(P)]
+    res_h = np.full(m, -3.25)
+    k_ref, n_ref = TH.reduce(P, root, theta, mode, xs_h, res_h)
+    xs = [torch.from_numpy(x).cuda() for x in xs_h]
+    res = torch.full((m,), -3.25, dtype=torch.float64, device="cuda")
+    k, n = E.ecc_reduce_threshold(P, root, m, theta, mode, _ptrs(xs), res, _stream())
+    torch.cuda.synchronize()
+    assert (k, n) == (k_ref, n_ref)
+    got = res.cpu().numpy()
+    assert np.array_equal(got, res_h), np.abs(got - res_h).max()
+
+
 @pytest.mark.parametrize("m", [0, 1, 7, 300007])
 def test_reduce_lengths(m):
     E = _E()
@@ -120,7 +145,7 @@ def test_threshold_errors():
     announce("threshold errors")
     x = torch.zeros(4, dtype=torch.float64, device="cuda")
     p = _ptrs([x] * 65)
-    for args in [(65, 0, 4, 1.0, TH.DATA), (4, 4, 4, 1.0, TH.DATA), (4, 0, 4, 1.5, TH.DATA),
+    for args in [(4097, 0, 4, 1.0, TH.DATA), (0, 0, 4, 1.0, TH.DATA), (4, 4, 4, 1.0, TH.DATA), (4, 0, 4, 1.5, TH.DATA),
                  (4, 0, 4, 0.0, TH.PROCS), (4, 0, 4, 0.5, 7), (4, 0, -1, 0.5, TH.DATA)]:
         with pytest.raises(E.EccError) as ei:
             E.ecc_reduce_threshold(*args, p, x, _stream())
