@@ -77,7 +77,10 @@ struct TinyArgs {
 // p's steps for a chunk of iterations at once, into LDS, and the
 // iterations then only read them.  The loop thus issues no global load: no
 // wait on the memory counter (which also counts the history stores) stalls
-// an iteration.
+// an iteration.  Two barriers per iteration: between the assembly and the
+// gathers, and between the gathers and the new iterate; the norm's waves
+// sums are kept per step and finished once per chunk, so only a tolerance
+// needs a third barrier (every thread then compares the norm).
 constexpr int kTinyMaskBytes = 1024;  // arrival flags staged per chunk
 constexpr int kTinyChunkMax = 256;    // iterations per chunk at most
 
@@ -98,7 +101,7 @@ __global__ __launch_bounds__(kTinyThreads) void k_solve_tiny(TinyArgs a) {
     __shared__ uint8_t s_mask[kTinyMaskBytes];   // arrival flags of a chunk, [u][p]
     __shared__ uint8_t s_eff[kTinyMaskBytes];    // its decisions: bit 0 taken, bit 1 forced
     __shared__ int32_t s_nv[kTinyMaskBytes];     // the versions after each of its steps
-    __shared__ double s_red[kNormThreads / 64];
+    __shared__ double s_sum[kTinyChunkMax][kNormThreads / 64];  // waves' norm sums per step
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int jn = tid & (kNormThreads - 1), qn = tid / kNormThreads;
@@ -185,11 +188,17 @@ __global__ __launch_bounds__(kTinyThreads) void k_solve_tiny(TinyArgs a) {
     unsigned forced = 0;
     const int32_t chunk = min(kTinyChunkMax, max(1, kTinyMaskBytes / max(P, 1)));
 
+    // The norm of step u of the chunk from its waves' sums.
+    auto norm_of = [&](int32_t u) -> double {
+        double sum = s_sum[u][0];
+        for (int w = 1; w < kNormThreads / 64; ++w) sum += s_sum[u][w];
+        return (a.norm == ECC_NORM_L2) ? sqrt(sum) : sum;
+    };
+
     // One iteration: the assembly of the taken ranks' rows, the sweep, the
     // new iterate over the old one, the norm.  Returns whether the tolerance
     // stops the loop.
-    auto iteration = [&](int32_t tc, int32_t u) -> bool {
-        const int32_t t = tc + u;
+    auto iteration = [&](int32_t u) -> bool {
         const uint8_t *ef = s_eff + u * P;
 #pragma unroll
         for (int m = 0; m < RPT; ++m) {
@@ -252,18 +261,16 @@ __global__ __launch_bounds__(kTinyThreads) void k_solve_tiny(TinyArgs a) {
             }
             for (; k <= n; k += kNormThreads) acc += k < n ? s_c[k] : 0.0;
             acc = wave_sum_lane63(acc);
-            if (lane == 63) s_red[wave] = acc;
+            if (lane == 63) s_sum[u][wave] = acc;
         }
-        lds_barrier();
-        bool stop = false;
-        if (tid == 0 || a.tol > 0.0) {  // uniform unless only thread 0's rho is needed
-            double sum = s_red[0];
-            for (int w = 1; w < kNormThreads / 64; ++w) sum += s_red[w];
-            const double v = (a.norm == ECC_NORM_L2) ? sqrt(sum) : sum;
-            if (tid == 0) a.rho[t] = v;
-            stop = a.tol > 0.0 && v < a.tol;
+        // Without a tolerance nothing here needs the norm: the next step's
+        // first barrier orders these reads of s_h and s_c before their next
+        // writes, and the norms of the chunk are finished after it.
+        if (a.tol > 0.0) {
+            lds_barrier();
+            return norm_of(u) < a.tol;
         }
-        return stop;
+        return false;
     };
 
     for (int32_t tc = 0; tc < a.T && !stopped; tc += chunk) {
@@ -296,9 +303,11 @@ __global__ __launch_bounds__(kTinyThreads) void k_solve_tiny(TinyArgs a) {
         int32_t u = 0;
         bool stop = false;
         while (!stop && u < cn) {
-            stop = iteration(tc, u);
+            stop = iteration(u);
             ++u;
         }
+        __syncthreads();  // the chunk's norm sums are in
+        for (int32_t k = tid; k < u; k += kTinyThreads) a.rho[tc + k] = norm_of(k);
         // the histories and forced arrivals of the iterations run
         if (tid < P) {
             for (int32_t k = 0; k < u; ++k) {
