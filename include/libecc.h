@@ -444,8 +444,9 @@ ecc_status_t ecc_solve(ecc_plan_t plan, ecc_matrix_t A, const double *d_b, doubl
  * d - 3 launches (the decisions, the first five steps in sub-cubes of 32
  * processes, then one launch per further step, partials kept in the result),
  * with the same results bit for bit.  ECC_ERR_ARG for a bad P, m or slack; ECC_ERR_RANGE when the
- * slots would exceed 2^40 elements or m exceeds 256 (2^31 - 1) (one thread
- * per element); ECC_ERR_ALLOC when allocation fails. */
+ * slots would exceed 2^40 elements or m exceeds 64 (2^31 - 1) (one thread
+ * per element, 64 elements per workgroup); ECC_ERR_ALLOC when allocation
+ * fails. */
 ecc_status_t ecc_hypercube_create(int32_t P, int64_t m, int32_t slack, void *hip_stream,
                                   ecc_hypercube_t *out);
 ecc_status_t ecc_hypercube_destroy(ecc_hypercube_t h);

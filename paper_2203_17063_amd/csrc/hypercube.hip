@@ -2,17 +2,19 @@
 // Algorithm 1): P = 2^d virtual processes on one GPU, each with d dedicated
 // receive slots (data and clock of the last message that landed there).
 //
-// One call is one iteration of every process, as one kernel launch:
+// One call is one iteration of every process, as one kernel launch (up to
+// 32 processes; beyond, see k_hc_decide_big):
 //  (1) every workgroup replays the scalar part of the call in LDS -- which
 //      slot of which process takes this call's message from its partner
 //      (process XOR 2^k) and which reuses its last message -- from the slot
 //      clocks of the previous call (read-only in this launch; workgroup 0
 //      writes the new ones into the other half of a double buffer);
 //  (2) the data part is elementwise: element j of every result depends only
-//      on element j of the contributions and slots, so one thread (or a few
-//      lanes) carries element j of all P partial reductions through the d
-//      steps, storing each arriving message into its slot and reading each
-//      reused slot, and no workgroup waits for another.
+//      on element j of the contributions and slots, so one thread (up to 4
+//      processes) or one lane of each of four waves (8 to 32) carries element
+//      j of all P partial reductions through the d steps, storing each
+//      arriving message into its slot and reading each reused slot, and no
+//      workgroup waits for another.
 // A partial reduction is updated as partial + received, in that order, in
 // fp64 without contraction: the same operations as the sequential
 // definition, so results are bitwise reproducible.
@@ -93,20 +95,14 @@ __device__ __forceinline__ unsigned long long uniform64(unsigned long long v) {
     return ((unsigned long long)hi << 32) | lo;
 }
 
-// Column layout: a thread carries element j of all P = 2^D partial
-// reductions in registers (P <= 32), so every load and store of a wave
+// Column layout, for up to 4 processes: a thread carries element j of all
+// P = 2^D partial reductions in registers, so every load and store of a wave
 // covers contiguous bytes of one row.  At step k the two processes of each
 // pair (r, r XOR 2^k) sit in the same thread and are updated together from
 // their old partials.  A scheduling barrier between steps keeps the loads of
 // a step from being hoisted above the stores of the previous one (register
-// pressure).  The grid has one thread per element and no loop: a loop over
-// elements kept every row address live across it, and the 224 addresses of
-// P = 32 then spilled 620 SGPRs (942 against 933 us per call).  Measured on
-// MI355X (slack 2, 80 % delivery): P = 32 x 16 MB, 166 VGPRs, 4.03 TB/s.
-// Sixty-four processes take the multi-launch path below: 1,202 us per call
-// of 8 MB vectors, against 1,530 us with all 64 partials of an element in
-// one thread (255 VGPRs, one wave per SIMD), and slower still with two lanes
-// per element, whose per-lane delivery bits make every slot access divergent.
+// pressure).  The grid has one thread per element and no loop (a loop over
+// elements kept every row address live across it).
 template <int D>
 __global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp(HcArgs a) {
     constexpr int Pt = 1 << D;
@@ -146,15 +142,104 @@ __global__ __launch_bounds__(kHcThreads) void k_allreduce_ssp(HcArgs a) {
     }
 }
 
+// Split layout, for 8 to 32 processes and for the 32-process sub-cubes of
+// larger calls: the 2^D partials of element j are held by the W = 2^LW
+// waves of a workgroup, 2^D / W each (wave w holds processes w 2^D / W + i),
+// so that every decision stays uniform in a wave and a thread holds few
+// partials.  Steps 0 .. D-LW-1 pair processes within a wave; each of the
+// last LW steps pairs process w 2^D / W + i with the same i of wave
+// w XOR 2^(k-D+LW), whose old partials the waves exchange through LDS.  The
+// additions are those of k_allreduce_ssp, in the same order.  With CUBE,
+// blockIdx.y selects the sub-cube of processes 2^D y .. 2^D (y + 1) - 1,
+// whose fresh flags for steps 0 .. D-1 come from fresh_in, and the partials
+// go to the result for the remaining steps.  Measured on MI355X (32
+// processes x 16 MB, slack 2, 80 % delivery): 789 us per call with four
+// waves (50 VGPRs, 8 waves per SIMD), 885 us with two (90 VGPRs), 827 us
+// with eight, against 937 us with the 32 partials in one thread.
+template <int D, int LW, bool CUBE>
+__global__ __launch_bounds__(64 << LW) void k_allreduce_ssp_split(HcArgs a,
+                                                                  const uint8_t *__restrict__ fresh_in) {
+    constexpr int Pt = 1 << D, W = 1 << LW, H = Pt / W;
+    static_assert(LW >= 1 && LW < D && D <= kHcMaxDims, "a split of at most 32 processes");
+    __shared__ unsigned long long s_fresh[kHcMaxDims];
+    __shared__ double s_x[W][H][64];
+    const int32_t pc = CUBE ? (int32_t)blockIdx.y * Pt : 0;  // the sub-cube's first process
+    if constexpr (CUBE) {
+        if (threadIdx.x < 64) {
+            const int lane = threadIdx.x;
+            for (int k = 0; k < D; ++k) {
+                const bool f = lane < Pt && fresh_in[(int64_t)(pc + lane) * a.D + k] != 0;
+                const unsigned long long mask = __ballot(f);
+                if (lane == 0) s_fresh[k] = mask;
+            }
+        }
+    } else {
+        hc_decide(a, s_fresh);
+    }
+    __syncthreads();
+    unsigned long long fresh[D];
+#pragma unroll
+    for (int k = 0; k < D; ++k) fresh[k] = uniform64(s_fresh[k]);
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t m = a.m;
+    const int64_t sd = CUBE ? (int64_t)a.D : D;  // slots per process
+    const int64_t j = (int64_t)blockIdx.x * 64 + lane;
+    const bool live = j < m;
+    const int p0 = wv * H;  // this wave's first process in the (sub-)cube
+    auto slot = [&](int i, int k) { return a.slots + ((int64_t)(pc + p0 + i) * sd + k) * m + j; };
+    double part[H];
+#pragma unroll
+    for (int i = 0; i < H; ++i)
+        part[i] = live ? hc_ld(a.contrib + (int64_t)(pc + p0 + i) * m + j) : 0.0;
+#pragma unroll
+    for (int k = 0; k < D - LW; ++k) {
+        const int bit = 1 << k;
+#pragma unroll
+        for (int i = 0; i < H; ++i) {
+            if (i & bit) continue;
+            const int q = i | bit;
+            const bool fr = (fresh[k] >> (p0 + i)) & 1ull, fq = (fresh[k] >> (p0 + q)) & 1ull;
+            double *sr = slot(i, k), *sq = slot(q, k);
+            const double gr = fr ? part[q] : (live ? hc_ld(sr) : 0.0);
+            const double gq = fq ? part[i] : (live ? hc_ld(sq) : 0.0);
+            if (fr && live) hc_st(sr, gr);
+            if (fq && live) hc_st(sq, gq);
+            part[i] = part[i] + gr;
+            part[q] = part[q] + gq;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int k = D - LW; k < D; ++k) {
+        const int pw = wv ^ (1 << (k - (D - LW)));  // the partner wave
+#pragma unroll
+        for (int i = 0; i < H; ++i) s_x[wv][i][lane] = part[i];
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < H; ++i) {
+            const bool fr = (fresh[k] >> (p0 + i)) & 1ull;
+            double *sr = slot(i, k);
+            const double gr = fr ? s_x[pw][i][lane] : (live ? hc_ld(sr) : 0.0);
+            if (fr && live) hc_st(sr, gr);
+            part[i] = part[i] + gr;
+        }
+        if (k + 1 < D) __syncthreads();  // every partner read before the next writes
+    }
+    if (live) {
+#pragma unroll
+        for (int i = 0; i < H; ++i) hc_st(a.result + (int64_t)(pc + p0 + i) * m + j, part[i]);
+    }
+}
+
 // More than 32 processes.  One call is then three kinds of launch:
 //  (1) k_hc_decide_big, one workgroup: process r's thread replays its d
 //      steps in order (its partner's partial clock read from LDS after every
 //      step), writes the (process, step) fresh flags for the data kernels
 //      and the same bookkeeping as hc_decide;
-//  (2) k_hc_cube: the first five steps inside every sub-cube of 32
-//      processes (partners r XOR 2^k, k < 5, share the sub-cube), a thread
-//      carrying element j of the sub-cube's 32 partials in registers as
-//      k_allreduce_ssp<5> does, the partials then stored in the result;
+//  (2) k_allreduce_ssp_split<5, 2, true>: the first five steps inside every
+//      sub-cube of 32 processes (partners r XOR 2^k, k < 5, share the
+//      sub-cube) in the split layout, the partials then stored in the result;
 //  (3) k_hc_pair_step for every further step k: a thread takes element j of
 //      one pair (r, r XOR 2^k) of partials from the result, receives for
 //      each from the partner's partial or its slot, and stores both
@@ -191,54 +276,6 @@ __global__ __launch_bounds__(kHcDecideThreads) void k_hc_decide_big(HcArgs a,
     if (a.result_clock)
         for (int32_t r = threadIdx.x; r < a.P; r += kHcDecideThreads)
             a.result_clock[r] = s_pc[a.D & 1][r];
-}
-
-// Steps 0 .. kHcCubeDims-1 of sub-cube blockIdx.y (processes 32 y .. 32 y +
-// 31); element blockIdx.x * kHcThreads + threadIdx.x.
-__global__ __launch_bounds__(kHcThreads) void k_hc_cube(HcArgs a,
-                                                        const uint8_t *__restrict__ fresh_in) {
-    constexpr int DL = kHcCubeDims, Pt = 1 << DL;
-    __shared__ unsigned long long s_fresh[DL];
-    const int32_t p0 = (int32_t)blockIdx.y * Pt;
-    if (threadIdx.x < 64) {
-        const int lane = threadIdx.x;
-        for (int k = 0; k < DL; ++k) {
-            const bool f = lane < Pt && fresh_in[(int64_t)(p0 + lane) * a.D + k] != 0;
-            const unsigned long long mask = __ballot(f);
-            if (lane == 0) s_fresh[k] = mask;
-        }
-    }
-    __syncthreads();
-    unsigned long long fresh[DL];
-#pragma unroll
-    for (int k = 0; k < DL; ++k) fresh[k] = uniform64(s_fresh[k]);
-    const int64_t m = a.m;
-    const int64_t j = (int64_t)blockIdx.x * kHcThreads + threadIdx.x;
-    if (j >= m) return;
-    double part[Pt];
-#pragma unroll
-    for (int i = 0; i < Pt; ++i) part[i] = hc_ld(a.contrib + (int64_t)(p0 + i) * m + j);
-#pragma unroll
-    for (int k = 0; k < DL; ++k) {
-        double *srow = a.slots + ((int64_t)p0 * a.D + k) * m + j;  // + i * D * m
-        const int bit = 1 << k;
-#pragma unroll
-        for (int i = 0; i < Pt; ++i) {
-            if (i & bit) continue;
-            const int q = i | bit;
-            const bool fr = (fresh[k] >> i) & 1ull, fq = (fresh[k] >> q) & 1ull;
-            double *sr = srow + (int64_t)i * a.D * m, *sq = srow + (int64_t)q * a.D * m;
-            const double gr = fr ? part[q] : hc_ld(sr);
-            const double gq = fq ? part[i] : hc_ld(sq);
-            if (fr) hc_st(sr, gr);
-            if (fq) hc_st(sq, gq);
-            part[i] = part[i] + gr;
-            part[q] = part[q] + gq;
-        }
-        __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int i = 0; i < Pt; ++i) hc_st(a.result + (int64_t)(p0 + i) * m + j, part[i]);
 }
 
 // Step k >= kHcCubeDims for pair blockIdx.y of the partials in the result.
@@ -278,7 +315,7 @@ struct ecc_hypercube_s {
     double *d_slots = nullptr;               // [P][D][m]
     int32_t *d_clk = nullptr;                // [2][P][D]
     unsigned long long *d_waits = nullptr;   // [P][D]
-    uint8_t *d_fresh = nullptr;              // P > 64: [P][D] this call's fresh slots
+    uint8_t *d_fresh = nullptr;              // P > 32: [P][D] this call's fresh slots
 };
 
 namespace {
@@ -306,6 +343,15 @@ void hc_launch(dim3 grid, hipStream_t st, const HcArgs &a) {
     hipLaunchKernelGGL((k_allreduce_ssp<D>), grid, dim3(kHcThreads), 0, st, a);
 }
 
+constexpr int kHcSplitLW = 2;  // four waves per 64 elements
+
+template <int D>
+void hc_launch_split(int64_t m, hipStream_t st, const HcArgs &a) {
+    const int64_t g = std::max<int64_t>(1, (m + 63) / 64);
+    hipLaunchKernelGGL((k_allreduce_ssp_split<D, kHcSplitLW, false>), dim3((unsigned)g),
+                       dim3(64 << kHcSplitLW), 0, st, a, nullptr);
+}
+
 }  // namespace
 
 extern "C" {
@@ -326,8 +372,9 @@ ecc_status_t ecc_hypercube_create(int32_t P, int64_t m, int32_t slack, void *hip
         set_error("P * d * m too large");
         return ECC_ERR_RANGE;
     }
-    // one thread per element: the grid's x extent holds at most 2^31 - 1 workgroups
-    if (m > (int64_t)0x7fffffff * kHcThreads) {
+    // one thread per element and at most 64 elements per workgroup: the
+    // grid's x extent holds at most 2^31 - 1 workgroups
+    if (m > (int64_t)0x7fffffff * 64) {
         set_error("m too large");
         return ECC_ERR_RANGE;
     }
@@ -426,7 +473,9 @@ ecc_status_t ecc_allreduce_ssp(ecc_hypercube_t h, const double *d_contrib,
         hipLaunchKernelGGL(k_hc_decide_big, dim3(1), dim3(kHcDecideThreads), 0, h->stream, a,
                            h->d_fresh);
         ECC_LAUNCH_CHECK();
-        hipLaunchKernelGGL(k_hc_cube, dim3(h->grid, h->P >> kHcCubeDims), dim3(kHcThreads), 0,
+        const int64_t g = std::max<int64_t>(1, (h->m + 63) / 64);
+        hipLaunchKernelGGL((k_allreduce_ssp_split<kHcCubeDims, kHcSplitLW, true>),
+                           dim3((unsigned)g, h->P >> kHcCubeDims), dim3(64 << kHcSplitLW), 0,
                            h->stream, a, h->d_fresh);
         ECC_LAUNCH_CHECK();
         for (int32_t k = kHcCubeDims; k < h->D; ++k) {
@@ -441,9 +490,9 @@ ecc_status_t ecc_allreduce_ssp(ecc_hypercube_t h, const double *d_contrib,
         case 0: hc_launch<0>(grid, h->stream, a); break;
         case 1: hc_launch<1>(grid, h->stream, a); break;
         case 2: hc_launch<2>(grid, h->stream, a); break;
-        case 3: hc_launch<3>(grid, h->stream, a); break;
-        case 4: hc_launch<4>(grid, h->stream, a); break;
-        default: hc_launch<5>(grid, h->stream, a); break;
+        case 3: hc_launch_split<3>(h->m, h->stream, a); break;
+        case 4: hc_launch_split<4>(h->m, h->stream, a); break;
+        default: hc_launch_split<5>(h->m, h->stream, a); break;
     }
     ECC_LAUNCH_CHECK();
     h->clock += 1;

@@ -109,7 +109,7 @@ def test_product_path_does_not_touch_oracle():
     (4, -1, 0, E.ECC_ERR_ARG),                        # negative length
     (4, 16, -1, E.ECC_ERR_ARG),                       # negative slack
     (4, (1 << 40) // 8 + 1, 0, E.ECC_ERR_RANGE),      # slots beyond 2^40 elements
-    (1, 0x7fffffff * 256 + 1, 0, E.ECC_ERR_RANGE),    # beyond one thread per element
+    (1, 0x7fffffff * 64 + 1, 0, E.ECC_ERR_RANGE),     # beyond the grid's 64 elements per workgroup
 ])
 def test_hypercube_create_checks_without_device(P, m, slack, expect):
     """Argument and range checks return before any device call."""
