@@ -237,6 +237,18 @@ def test_allreduce_hand_example(golden):
         assert [s[0] for s in slots] == e["slots"]
 
 
+def test_allreduce_rank_order_hand_example(golden):
+    """Values whose rounding depends on the order of the additions: the
+    result is the rank-order sum of the held contributions, a stale rank's
+    taken from its slot (the second step keeps rank 0's first value)."""
+    g = golden("hand_examples.json")["allreduce_rank_order"]
+    slots = [np.zeros(2) for _ in range(3)]
+    for st in g["steps"]:
+        fresh = [np.array(f, dtype=np.float64) for f in st["fresh"]]
+        out = oracle.allreduce(np.array(st["eff"], dtype=np.uint8), fresh, slots)
+        assert out.tolist() == st["expect"]
+
+
 @pytest.mark.parametrize("S", [0, 2, UNB])
 def test_allreduce_equals_sum_of_last_versions(S):
     """After every step each slot holds the contribution of the rank's last
