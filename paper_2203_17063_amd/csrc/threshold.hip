@@ -14,7 +14,7 @@
 //    (at least ceil(theta * P) of them).  The order is the tree's: a parent
 //    adds its children's partial sums leaves first, which is, stage by stage
 //    from the last one, q += partial(q + 2^s) for every q < 2^s.  A thread
-//    carries one element of every involved process in registers; beyond 64
+//    carries one element of every involved process in registers; beyond 32
 //    processes it sums them in the same tree as a pairwise sum (below).
 //  - The dropping allreduce sums, in rank order from +0.0, the contributions
 //    of the ranks that arrived in this step.
@@ -28,8 +28,8 @@
 namespace ecc {
 
 constexpr int kThrThreads = 256;
-constexpr int kThrMaxStages = 6;  // Reduce: at most 64 processes in registers
-constexpr int kThrMaxStagesBig = 12;  // Reduce beyond 64 processes: up to 4096
+constexpr int kThrMaxStages = 5;  // Reduce: at most 32 processes in registers
+constexpr int kThrMaxStagesBig = 12;  // Reduce beyond 32 processes: up to 4096
 constexpr int kBcastTile = 4096;  // elements one workgroup copies
 
 // One workgroup per tile of kBcastTile elements of the prefix: the tile is
@@ -105,11 +105,13 @@ __global__ __launch_bounds__(kThrThreads) void k_reduce_bst(int32_t P, int32_t r
     }
 }
 
-// More than 64 processes.  Stage by stage from the last, q += partial(q +
-// 2^s) builds a binary tree whose leaves, read left to right, are the
-// relative ranks in the bit-reversed order of D = ceil(log2 n) bits: the
-// two children of a node combined at stage s are its halves, the lower
-// rank on the left and added first.  A rank at or beyond n is absent; as
+// More than 32 processes (measured on MI355X, 64 x 32 MB: 362 against 369
+// us with all 64 in registers, 169 VGPRs; 32 x 64 MB: 377 against 360 us,
+// so the register fold stays up to 32).  Stage by stage from the last,
+// q += partial(q + 2^s) builds a binary tree whose leaves, read left to
+// right, are the relative ranks in the bit-reversed order of D =
+// ceil(log2 n) bits: the two children of a node combined at stage s are
+// its halves, the lower rank on the left and added first.  A rank at or beyond n is absent; as
 // absence grows with the rank, a node whose left child is absent has an
 // absent right child too, and a node with an absent right child is its
 // left child.  So the reduction is a pairwise sum over that order, and a
@@ -124,7 +126,7 @@ __global__ __launch_bounds__(kThrThreads) void k_reduce_bst_big(
     int32_t P, int32_t root, int32_t n, int64_t k, const double *const *__restrict__ src,
     double *__restrict__ result) {
     constexpr int H = D - 3;  // levels above a group of 8 leaves
-    static_assert(H >= 1 && D <= kThrMaxStagesBig, "more than 64 processes");
+    static_assert(H >= 1 && D <= kThrMaxStagesBig, "more than 8 processes");
     const int64_t stride = (int64_t)gridDim.x * kThrThreads;
     for (int64_t j = (int64_t)blockIdx.x * kThrThreads + threadIdx.x; j < k; j += stride) {
         double st[H];
@@ -302,7 +304,7 @@ ecc_status_t ecc_reduce_threshold(int32_t P, int32_t root, int64_t m, double the
         case 3: hipLaunchKernelGGL(k_reduce_bst<3>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
         case 4: hipLaunchKernelGGL(k_reduce_bst<4>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
         case 5: hipLaunchKernelGGL(k_reduce_bst<5>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
-        case 6: hipLaunchKernelGGL(k_reduce_bst<6>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
+        case 6: hipLaunchKernelGGL(k_reduce_bst_big<6>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
         case 7: hipLaunchKernelGGL(k_reduce_bst_big<7>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
         case 8: hipLaunchKernelGGL(k_reduce_bst_big<8>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
         case 9: hipLaunchKernelGGL(k_reduce_bst_big<9>, grid, block, 0, st, P, root, n, k, d_src, d_result); break;
