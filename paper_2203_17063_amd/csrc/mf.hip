@@ -26,8 +26,10 @@
 // minibatch): the ratings of each row in storage order (other factor's row
 // index and rating value, stored in that order), and every entity's row in
 // order of its number of ratings, longest first.  The gradient kernel's
-// grid is two-dimensional: blockIdx.y is the worker, whose workgroups walk
-// the rows of its minibatch's list.
+// grid holds g workgroups per worker, which walk the rows of its
+// minibatch's list; with a multiple of 8 workers every worker's workgroups
+// run on one XCD (workgroups are dealt to the 8 XCDs round-robin), so that
+// the factor rows its list gathers most stay in that XCD's L2.
 //  - A row of more than kMfHeavy ratings takes a whole workgroup: chunks of
 //    its ratings are spread over the workgroup, whose lane groups compute
 //    the errors and products into LDS, and then `rank` lanes add the
@@ -94,7 +96,9 @@ struct MfGradArgs {
     const int32_t *n_rated;       // [P K] rows with ratings, per list (the rows without follow)
     const int32_t *batch;         // [P] this iteration's minibatch of each worker
     double *const *grads;         // [P] -> m doubles
-    double *partials;             // [gridDim.y][gridDim.x] sums of e^2 over user rows
+    double *partials;             // [P][g] sums of e^2 over user rows
+    int32_t g;                    // workgroups per worker
+    int32_t pin;                  // P a multiple of 8: a worker's workgroups on one XCD
 };
 
 // own . other over a lane group: lane l holds columns l*C .. l*C + C-1 of
@@ -234,7 +238,21 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfGradArgs a) {
     static_assert(MfShape<R>::CHUNK * R == kMfStage, "a heavy chunk fills the stage");
     const int lane = threadIdx.x % LPR, grp = threadIdx.x / LPR;
     // worker p's list for its minibatch of this iteration
-    const int32_t p = blockIdx.y;
+    // this workgroup's worker p and its index wgx among the worker's g:
+    // workgroup b runs on XCD b mod 8, and with pinning the workers
+    // x, x + 8, ... take XCD x's workgroups in turn (measured on MI355X, 25M
+    // ratings, 32 workers: 742 against 774 us per iteration, bitwise the same)
+    const int64_t g = a.g;
+    int32_t p;
+    int64_t wgx;
+    if (a.pin) {
+        const int64_t xb = blockIdx.x & 7, kb = blockIdx.x >> 3;
+        p = (int32_t)(xb + 8 * (kb / g));
+        wgx = kb % g;
+    } else {
+        p = (int32_t)(blockIdx.x / g);
+        wgx = blockIdx.x % g;
+    }
     const int32_t bp = min(max(a.batch[p], 0), a.K - 1);  // (values outside [0, K) clamped)
     const int64_t list = (int64_t)p * a.K + bp;
     const int32_t *row_of = a.row_of + list * a.E;
@@ -242,7 +260,6 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfGradArgs a) {
     const int32_t *len_of = a.len_of + list * a.E;
     const int64_t n_rows = a.E, n_heavy = a.n_heavy[list], n_rated = a.n_rated[list];
     const int64_t n_work = n_heavy + (n_rated - n_heavy + G - 1) / G;
-    const int64_t g = gridDim.x;
     double sq = 0.0;
     // Rows without ratings (list positions n_rated .. E-1, in entity order):
     // this workgroup's contiguous share is written as zeros first,
@@ -252,8 +269,8 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfGradArgs a) {
     // of the list; writing them last, or first in every other workgroup,
     // 815 and 810 us).
     const int64_t n_zero = n_rows - n_rated;
-    const int64_t z_lo = n_rated + n_zero * (int64_t)blockIdx.x / g;
-    const int64_t z_hi = n_rated + n_zero * ((int64_t)blockIdx.x + 1) / g;
+    const int64_t z_lo = n_rated + n_zero * wgx / g;
+    const int64_t z_hi = n_rated + n_zero * (wgx + 1) / g;
     {
         double *const grad = a.grads[p];
         const int zl = threadIdx.x % Z::LPR, zr = threadIdx.x / Z::LPR;
@@ -277,7 +294,7 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfGradArgs a) {
     // this lane group's row in a light item w (descriptors one item ahead)
     auto light_q = [&](int64_t w) { return n_heavy + (w - n_heavy) * G + grp; };
     int32_t nrow = 0, nx0 = 0, nlen = -1;
-    int64_t w = blockIdx.x;
+    int64_t w = wgx;
     if (w < n_work && w >= n_heavy && light_q(w) < n_rated) {
         const int64_t q = light_q(w);
         nrow = row_of[q];
@@ -309,7 +326,7 @@ __global__ __launch_bounds__(kMfThreads) void k_mf_grad(MfGradArgs a) {
         if (len >= 0) sq += mf_light_row<R>(a, p, row, x0, len, lane);
     }
     const double tot = block_sum<kMfThreads>(sq, s_red);
-    if (threadIdx.x == 0) a.partials[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = tot;
+    if (threadIdx.x == 0) a.partials[(int64_t)p * g + wgx] = tot;
 }
 
 // The minibatch error of an iteration: sqrt(sum / count) of the gradient
@@ -666,7 +683,9 @@ ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam,
     ga.partials = h->d_partials;
     {
         TimedLaunch timed(plan, ECC_TIMING_MF_GRAD);
-        const dim3 grid(h->grad_grid, h->P);
+        ga.g = h->grad_grid;
+        ga.pin = (h->P % 8) == 0;
+        const dim3 grid((unsigned)((int64_t)h->grad_grid * h->P));
         ECC_MF_RANKS(k_mf_grad, grid, ga)
         ECC_LAUNCH_CHECK();
     }
