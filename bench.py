@@ -552,14 +552,16 @@ def run_threshold_gpu(prob, steps, warmup):
             "dominant_bytes": bytes_r, "footprint": footprint, "unit_per_step": prob.reps}
 
 
-def mf_bytes(prob, arrivals):
+def mf_bytes(prob):
     """Algorithmic bytes of one factorisation iteration, per kernel."""
     N, m, P = prob.N, prob.m, prob.P
     rows = prob.n_users + prob.n_items
     return {"MF_GRAD": 24.0 * N / prob.K + 12.0 * P * rows + 8.0 * m + 8.0 * m * P,
             # 2 x (other row, rating) per rating of the minibatches, (row,
             # start, length) per (worker, row), the model, P gradients written
-            "ALLREDUCE": 8.0 * m * (P + arrivals + 1),
+            # the P slots read (the gradients of the workers taken this
+            # iteration were written into their slots), the result written
+            "ALLREDUCE": 8.0 * m * (P + 1),
             "MF_STEP": 24.0 * m + 8.0 * rows}
 
 
@@ -605,7 +607,7 @@ def run_mf_gpu(prob, steps, warmup):
     times = {name: E.ecc_plan_timing(ph, k) for name, k in kinds.items()}
     E.ecc_plan_set_timing(ph, False)
     run.close()
-    per = mf_bytes(prob, float(arrivals.mean()))
+    per = mf_bytes(prob)
     # slack study, 3 x T iterations each, arrivals Bernoulli(q) per (iteration,
     # worker), the same minibatch schedule; the full training error before
     # every iteration (err[t] = error of W^t) and after the last
@@ -625,8 +627,7 @@ def run_mf_gpu(prob, steps, warmup):
             target = float(err[prob.T])
         hit = np.nonzero(err[1:] <= target)[0]
         # time to the target: the iterations it takes, run again without the
-        # error evaluations (a fresh slot costs a write where a reused one
-        # costs a read, so the time per iteration depends on the slack)
+        # error evaluations
         ms_to_target = None
         if hit.size:
             n_it = int(hit[0]) + 1
@@ -648,6 +649,7 @@ def run_mf_gpu(prob, steps, warmup):
             "bytes_per_step": sum(per.values()) * prob.T, "dominant": "mf_grad",
             "dominant_bytes": per["MF_GRAD"], "footprint": footprint, "unit_per_step": prob.T,
             "extra": {"minibatch_rmse_at_T": round(rmse_T, 6), "target_error": round(target, 6),
+                      "workers_taken_per_iteration": round(float(arrivals.mean()), 3),
                       "minibatches_per_worker": prob.K, "eta": prob.eta,
                       "slack_study": study,
                       "kernel_bytes": {k: round(v) for k, v in per.items()}}}

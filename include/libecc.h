@@ -189,7 +189,11 @@ ecc_status_t ecc_allgatherv_assemble_packed(ecc_plan_t plan, const double *d_sen
  *   d_slots    device array of P device pointers to the caller-owned receive
  *              memory of each rank (m doubles each); read every call, written
  *              where eff[p].  At the plan's first call every rank is eff, so
- *              the slots need no initialisation.
+ *              the slots need no initialisation.  d_fresh[p] may equal
+ *              d_slots[p]: the contribution was then written into the slot
+ *              by its producer, which must do so only where eff[p] (the
+ *              slot keeps the newest taken contribution), and the slot is
+ *              read without being written.
  *   d_result   device vector of m doubles; must not alias any slot or fresh.
  *   d_arrived, d_eff_out as for the assembly. */
 ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *const *d_fresh,
@@ -570,13 +574,16 @@ ecc_status_t ecc_mf_destroy(ecc_mf_t h);
  *     for the ratings of every worker's minibatch;
  *   *d_rmse = sqrt(sum e_k^2 / (ratings of those minibatches))  (the error
  *     at the model on entry);
- *   d_grads[p] := worker p's gradient of the sum over its minibatch of e_k^2:
+ *   g_p := worker p's gradient of the sum over its minibatch of e_k^2:
  *     row U[u] accumulates (-2 e_k) V[i_k] and row V[i] accumulates
  *     (-2 e_k) U[u_k] over the minibatch's ratings in storage order (0 for
- *     rows without);
- *   d_G := ecc_allreduce_partial(plan, m, d_grads, d_slots, ..., d_arrived,
+ *     rows without), written into d_slots[p] when the allreduce takes
+ *     worker p at this clock (eff[p] of Algorithm 1's rule, from the plan's
+ *     versions and d_arrived), else into d_grads[p];
+ *   d_G := ecc_allreduce_partial(plan, m, g, d_slots, ..., d_arrived,
  *     d_eff_out) with m = (n_users + n_items) * rank (stale gradients
- *     substituted from the slots; the plan's clock advances);
+ *     substituted from the slots; the plan's clock advances), the taken
+ *     gradients read in place from their slots;
  *   W := W - eta * (G * c_row + 2 lam W), c_row = K / max(1, ratings of
  *     the row).
  * d_grads, d_slots: device arrays of P device pointers to m doubles each. */

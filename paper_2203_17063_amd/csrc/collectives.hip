@@ -80,7 +80,9 @@ __global__ __launch_bounds__(kAssembleThreads) void k_assemble(
 // Partial allreduce: workgroup 0 records the step; every other workgroup owns
 // kReduceThreads * kReduceElems consecutive elements and, for p = 0..P-1 in
 // order, takes the fresh contribution of eff ranks (writing it to the rank's
-// slot) or the slot of the others, summing in rank order.
+// slot) or the slot of the others, summing in rank order.  A contribution
+// that its producer wrote into the slot itself (fresh[p] == slots[p]) is
+// read there and not written back.
 __global__ __launch_bounds__(kReduceThreads) void k_allreduce(
     int32_t P, int32_t S, int64_t t, const uint8_t *__restrict__ arrived,
     const int32_t *__restrict__ ver_in, int32_t *__restrict__ ver_out,
@@ -117,14 +119,15 @@ __global__ __launch_bounds__(kReduceThreads) void k_allreduce(
         }
         for (int32_t p0 = 0; p0 < P; p0 += U) {
             double2 v[U][VP];
-            bool e[U];
+            bool e[U], wr[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int32_t p = p0 + u;
                 if (p < P) {
                     e[u] = stale_select(ver_in[p], arrived[p], t, S);
-                    const double2 *src =
-                        reinterpret_cast<const double2 *>(e[u] ? fresh[p] : slots[p]);
+                    const double *fp = fresh[p], *sp = slots[p];
+                    wr[u] = e[u] && fp != sp;
+                    const double2 *src = reinterpret_cast<const double2 *>(e[u] ? fp : sp);
 #pragma unroll
                     for (int j = 0; j < VP; ++j)
                         if (in[j]) v[u][j] = src[q[j]];
@@ -134,7 +137,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_allreduce(
             for (int u = 0; u < U; ++u) {
                 const int32_t p = p0 + u;
                 if (p < P) {
-                    if (e[u]) {
+                    if (wr[u]) {
                         double2 *dst = reinterpret_cast<double2 *>(slots[p]);
 #pragma unroll
                         for (int j = 0; j < VP; ++j) {
@@ -167,7 +170,10 @@ __global__ __launch_bounds__(kReduceThreads) void k_allreduce(
         }
         for (int32_t p = 0; p < P; ++p) {
             const bool e = stale_select(ver_in[p], arrived[p], t, S);
-            const double *src = e ? fresh[p] : slots[p];
+            const double *fp = fresh[p];
+            double *sp = slots[p];
+            const bool wr = e && fp != sp;
+            const double *src = e ? fp : sp;
             double v[kReduceElems];
 #pragma unroll
             for (int j = 0; j < kReduceElems; ++j)
@@ -175,7 +181,7 @@ __global__ __launch_bounds__(kReduceThreads) void k_allreduce(
 #pragma unroll
             for (int j = 0; j < kReduceElems; ++j) {
                 if (idx[j] < m) {
-                    if (e) slots[p][idx[j]] = v[j];
+                    if (wr) sp[idx[j]] = v[j];
                     acc[j] = (p == 0) ? v[j] : acc[j] + v[j];
                 }
             }

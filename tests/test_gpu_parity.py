@@ -207,6 +207,54 @@ def test_allreduce_parity(P, m, S, aligned):
     plan.close()
 
 
+@pytest.mark.parametrize("P,m,S,aligned", [
+    (6, 1023, 1, True),
+    (17, 4097, UNB, False),
+    (64, 3000, 0, True),
+])
+def test_allreduce_in_place(P, m, S, aligned):
+    """Contributions that their producer wrote into the slot itself
+    (fresh[p] == slots[p] for every third rank, written only where the rank
+    is taken, as the matrix factorisation does) next to ordinary ones: the
+    same results and slots as copying them."""
+    E, R = _capi(), _runner()
+    rng = np.random.default_rng(2000 + P + m)
+    R_ = 10
+    mask = (rng.random((R_, P)) < 0.5).astype(np.uint8)
+    announce("allreduce in place", P, m, S, aligned)
+    off = 0 if aligned else 1
+    inplace = [p % 3 == 0 for p in range(P)]
+    fresh_store = [torch.empty(m + 2, dtype=torch.float64, device="cuda") for _ in range(P)]
+    slot_store = [torch.full((m + 2,), np.nan, dtype=torch.float64, device="cuda")
+                  for _ in range(P)]
+    slots = [s_[off:off + m] for s_ in slot_store]
+    fresh = [slots[p] if inplace[p] else fresh_store[p][off:off + m] for p in range(P)]
+    result = torch.empty(m + 1, dtype=torch.float64, device="cuda")[off:off + m]
+    d_fresh, d_slots = R.ptr_array(fresh), R.ptr_array(slots)
+    d_mask = torch.from_numpy(mask).cuda()
+    eff_d = torch.empty(P, dtype=torch.uint8, device="cuda")
+    clk_d = torch.empty(1, dtype=torch.int32, device="cuda")
+    plan = R.Plan(P, None, None, S)
+    version = np.full(P, -1, dtype=np.int32)
+    ref_slots = [np.zeros(m) for _ in range(P)]
+    for r in range(R_):
+        host_fresh = [rng.uniform(-1, 1, m) for _ in range(P)]
+        eff, _, _ = oracle.select(S, r, mask[r], version)
+        for p in range(P):
+            if not inplace[p] or eff[p]:
+                fresh[p].copy_(torch.from_numpy(host_fresh[p]))
+        E.ecc_allreduce_partial(plan.handle, m, d_fresh, d_slots, result, d_mask[r].data_ptr(),
+                                eff_d, clk_d)
+        ref = oracle.allreduce(eff, host_fresh, ref_slots)
+        torch.cuda.synchronize()
+        assert np.array_equal(eff_d.cpu().numpy(), eff)
+        assert np.array_equal(result.cpu().numpy(), ref), r
+        assert int(clk_d.item()) == oracle.result_clock(version)
+        for p in range(P):
+            assert np.array_equal(slots[p].cpu().numpy(), ref_slots[p]), (r, p)
+    plan.close()
+
+
 def test_partial_allreduce_full_sampled():
     """The benchmark's partial allreduce shape (256 ranks x 4M, 70% arrival, no staleness bound) for a
     few repetitions, checked at sampled indices against the last-arrival sum."""
