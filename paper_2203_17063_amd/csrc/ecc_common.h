@@ -96,6 +96,7 @@ enum { kLayStream = 0, kLaySorted = 1, kLayShort = 2, kLayRanges = 3 };
 constexpr int kMaxRanges = 16;              // column ranges of the range layout at most
 constexpr int64_t kRangeBytes = 8 << 20;    // bytes of the vector per column range
 constexpr int64_t kRangeBytesColumns = 16 << 20;  // the same for a column-value matrix
+constexpr int32_t kHotCols = 1024;  // column values, range layout: columns held in LDS
 // Plane tiling of the short-row layout: applied when one plane of rows
 // streams more than kTileMinBytes (the rows one plane apart no longer meet
 // in an XCD's 4 MB L2); tiles of kTileNearFactor times the largest in-plane
@@ -426,6 +427,12 @@ struct ecc_matrix_s {
     double *d_cscale = nullptr;     // [n] the value of each column (0 for empty ones)
     double *d_zown = nullptr;       // [n] c * x_own of the current sweep
     double *d_zhat = nullptr;       // [n] c * x_hat of the current sweep
+    // column values in the range layout: the most gathered columns, whose
+    // gathers from outside their own rank block read an LDS copy instead
+    int32_t n_hot = 0;              // such columns (at most kHotCols)
+    int32_t *d_hot_col = nullptr;   // [n_hot] the columns, ascending
+    int32_t *d_hot_rank = nullptr;  // [n_hot] the rank whose block holds each
+    double *d_hot = nullptr;        // [n_hot] c * x_hat at those columns, this sweep
 };
 
 namespace ecc {

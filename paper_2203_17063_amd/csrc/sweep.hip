@@ -77,6 +77,10 @@ struct SweepArgs {
     // matrix the scaled views c * x_own and c * x_hat
     const double *g_own;
     const double *g_hat;
+    // column values, range layout: g_hat at the most gathered columns, which
+    // the entries name as -1 - slot (copied to LDS by every workgroup)
+    const double *hot;
+    int32_t n_hot;
     double *partials;
     double2 *pieces;
     const int32_t *order;    // sorted layout: the row at each sorted position
@@ -157,12 +161,17 @@ __device__ __forceinline__ bool col_arrives(const StepView &v, int32_t c, RankCa
     return e;
 }
 
-// A gather of the assembled vector.
-template <bool STEP>
+// A gather of the assembled vector.  HOT: a negative column -1 - k names
+// slot k of the LDS copy s_hot of the most gathered columns.
+template <bool STEP, bool HOT = false>
 __device__ __forceinline__ double view_load(int32_t c, int32_t lo, int32_t hi,
                                             const double *__restrict__ x_own,
                                             const double *__restrict__ x_hat,
-                                            const StepView &sv, RankCache &rc) {
+                                            const StepView &sv, RankCache &rc,
+                                            const double *s_hot = nullptr) {
+    if constexpr (HOT) {
+        if (c < 0) return s_hot[-1 - c];
+    }
     bool own = (c >= lo && c < hi);
     if constexpr (STEP) {
         if (!own) own = col_arrives(sv, c, rc);
@@ -187,11 +196,11 @@ __device__ __forceinline__ int lanes_per_row(int32_t nnz, int32_t nr) {
 // order.  Jacobi skips (and records) the diagonal entry.  CS: the gathers
 // come from the scaled views and the entries' values are all 1 (the product
 // v * y is then y itself).
-template <int KIND, bool STEP, int W, bool CS>
+template <int KIND, bool STEP, int W, bool CS, bool HOT = false>
 __device__ __forceinline__ void seg_accumulate(int32_t i, int32_t k0, int32_t k1, int32_t stride,
                                                const SweepArgs &a, int32_t lo, int32_t hi,
                                                const StepView &sv, RankCache &rc, double &s,
-                                               double &dg) {
+                                               double &dg, const double *s_hot = nullptr) {
     if (k0 >= k1) return;
     int32_t c[W];
     double v[W];
@@ -205,8 +214,9 @@ __device__ __forceinline__ void seg_accumulate(int32_t i, int32_t k0, int32_t k1
         double y[W];
 #pragma unroll
         for (int u = 0; u < W; ++u)
-            y[u] = (k + u * stride < k1) ? view_load<STEP>(c[u], lo, hi, a.g_own, a.g_hat, sv, rc)
-                                          : 0.0;
+            y[u] = (k + u * stride < k1)
+                       ? view_load<STEP, HOT>(c[u], lo, hi, a.g_own, a.g_hat, sv, rc, s_hot)
+                       : 0.0;
         const int32_t kn = k + W * stride;
         int32_t cn[W];
         double vn[W];
@@ -312,8 +322,9 @@ __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0
                                                  int32_t i, int32_t lo, int32_t hi, double bi,
                                                  double xo, const SweepArgs &a,
                                                  const int32_t *s_col, const double *s_val,
-                                                 const StepView &sv, RankCache &rc,
-                                                 bool own_arrives) {
+                                                 const double *s_hot, const StepView &sv,
+                                                 RankCache &rc, bool own_arrives) {
+    constexpr bool HOT = LAY == kLayRanges && CS;
     const int tid = threadIdx.x;
     const int32_t nnz = it.k1 - it.k0;
     const int tpr = lanes_per_row(nnz, it.nrows);
@@ -335,8 +346,9 @@ __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0
         }
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-            y8[j] = (j < len) ? view_load<STEP>(c8[j], lo, hi, a.g_own, a.g_hat, sv, rc)
-                              : 0.0;
+            y8[j] = (j < len)
+                        ? view_load<STEP, HOT>(c8[j], lo, hi, a.g_own, a.g_hat, sv, rc, s_hot)
+                        : 0.0;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             if (j < len) {
@@ -351,7 +363,7 @@ __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0
                 dg = v;
                 continue;
             }
-            s = s + v * view_load<STEP>(c, lo, hi, a.g_own, a.g_hat, sv, rc);
+            s = s + v * view_load<STEP, HOT>(c, lo, hi, a.g_own, a.g_hat, sv, rc, s_hot);
         }
     } else {
         for (int32_t k = rs + lane; k < re; k += tpr) {
@@ -361,7 +373,7 @@ __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0
                 dg = v;
                 continue;
             }
-            s = s + v * view_load<STEP>(c, lo, hi, a.g_own, a.g_hat, sv, rc);
+            s = s + v * view_load<STEP, HOT>(c, lo, hi, a.g_own, a.g_hat, sv, rc, s_hot);
         }
         s = group_sum_dyn(s, tpr);
         if (KIND == ECC_KIND_JACOBI) dg = group_sum_dyn(dg, tpr);
@@ -381,11 +393,14 @@ __device__ __forceinline__ double stream_compute(const WorkItem &it, int32_t rp0
 template <int KIND, bool STEP, int LAY, bool CS>
 __device__ __forceinline__ double long_compute(const WorkItem &it, const SweepArgs &a,
                                                const StepView &sv, RankCache &rc,
-                                               bool own_arrives, double *s_red) {
+                                               bool own_arrives, double *s_red,
+                                               const double *s_hot) {
+    constexpr bool HOT = LAY == kLayRanges && CS;
     const int tid = threadIdx.x;
     const int32_t i = it.row0, lo = it.lo, hi = it.hi;
     double s = 0.0, dg = 0.0;
-    seg_accumulate<KIND, STEP, 4, CS>(i, it.k0 + tid, it.k1, kSweepThreads, a, lo, hi, sv, rc, s, dg);
+    seg_accumulate<KIND, STEP, 4, CS, HOT>(i, it.k0 + tid, it.k1, kSweepThreads, a, lo, hi, sv,
+                                           rc, s, dg, s_hot);
     s = block_sum<kSweepThreads>(s, s_red);
     if (KIND == ECC_KIND_JACOBI) dg = block_sum<kSweepThreads>(dg, s_red);
     if (tid != 0) return 0.0;
@@ -476,6 +491,13 @@ __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
     __shared__ double s_red[kSweepThreads / 64];
     __shared__ uint8_t s_eff[STEP ? kFusedMaxP : 1];
     __shared__ int32_t s_bs[STEP ? kFusedMaxP + 1 : 1];
+    // column values, range layout: the most gathered columns' values.
+    // Measured on MI355X (PageRank on a scale-22 R-MAT graph, 64 ranks): 1,024
+    // columns (13 % of the gathers) 439 against 453 us per iteration; 2,048
+    // the same; 4,096 or 8,192 (25 or 34 %) 539 or 671 us, their LDS leaving
+    // fewer workgroups per CU to hide the other gathers.
+    constexpr bool HOT = LAY == kLayRanges && CS;
+    __shared__ double s_hot[HOT ? kHotCols : 1];
     if (a.done && *a.done) return;
     const int tid = threadIdx.x;
     int64_t i_end;
@@ -495,6 +517,10 @@ __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
 
     StepView sv{s_eff, s_bs, a.P};
     sweep_prologue<STEP>(a, s_eff, s_bs, s_red);
+    if constexpr (HOT) {
+        for (int32_t k = tid; k < a.n_hot; k += kSweepThreads) s_hot[k] = a.hot[k];
+        __syncthreads();
+    }
 
     // Software pipeline over this workgroup's items: while an item is computed
     // from LDS, the loads of the next one (and the descriptor of the one
@@ -517,11 +543,11 @@ __device__ __forceinline__ void sweep_body(const SweepArgs &a) {
             if (next_stream) stream_load<KIND, LAY, CS>(nxt, a, pf);
             if (have_nn) nn = a.items[w + 2 * w_step];
             contrib += stream_compute<KIND, STEP, LAY, CS>(cur, rp0, rp1, ri, lo, hi, bi, xo, a, s_col,
-                                                       s_val, sv, rc, own_arrives);
+                                                           s_val, s_hot, sv, rc, own_arrives);
             __syncthreads();  // LDS is reused by the next item
         } else {
             if (have_nn) nn = a.items[w + 2 * w_step];
-            contrib += long_compute<KIND, STEP, LAY, CS>(cur, a, sv, rc, own_arrives, s_red);
+            contrib += long_compute<KIND, STEP, LAY, CS>(cur, a, sv, rc, own_arrives, s_red, s_hot);
             if (next_stream) stream_load<KIND, LAY, CS>(nxt, a, pf);
         }
         w += w_step;
@@ -569,13 +595,19 @@ __global__ void k_col_check(int64_t nnz, const int32_t *__restrict__ col,
 constexpr int kScaleThreads = 256;
 constexpr int kScaleElems = 4;  // elements per thread, all loads in flight together
 
-// The scaled views of a plain sweep: z_own = c * x_own, z_hat = c * x_hat.
+// The scaled views of a plain sweep: z_own = c * x_own, z_hat = c * x_hat;
+// and hot[k] = z_hat at column hot_col[k] for the range layout's LDS copy.
 __global__ __launch_bounds__(kScaleThreads) void k_col_scale(
     int64_t n, const double *__restrict__ c, const double *__restrict__ x_own,
     const double *__restrict__ x_hat, double *__restrict__ z_own, double *__restrict__ z_hat,
+    int32_t n_hot, const int32_t *__restrict__ hot_col, double *__restrict__ hot,
     const int32_t *__restrict__ done) {
     if (done && *done) return;
     const int64_t stride = (int64_t)gridDim.x * kScaleThreads;
+    for (int64_t k = (int64_t)blockIdx.x * kScaleThreads + threadIdx.x; k < n_hot; k += stride) {
+        const int32_t j = hot_col[k];
+        hot[k] = c[j] * x_hat[j];
+    }
     for (int64_t j0 = (int64_t)blockIdx.x * kScaleThreads + threadIdx.x; j0 < n;
          j0 += stride * kScaleElems) {
         double cj[kScaleElems], xo[kScaleElems], xh[kScaleElems];
@@ -601,7 +633,9 @@ __global__ __launch_bounds__(kScaleThreads) void k_col_scale(
 // the same tiles) fused with the scaled views: for every element j of a tile
 // of rank p, z_own[j] = c_j * x_own[j]; if p's block is taken at this step,
 // x_hat[j] = x_own[j] and z_hat[j] = z_own[j] (= c_j * x_hat[j] after the
-// copy), else z_hat[j] = c_j * x_hat[j].  Workgroup 0 records the step.
+// copy), else z_hat[j] = c_j * x_hat[j].  Workgroup 0 records the step;
+// the workgroups after the n_tiles tiles write the same z_hat at the hot
+// columns (kAssembleTile of them each) for the range layout's LDS copy.
 __global__ __launch_bounds__(kAssembleThreads) void k_assemble_scaled(
     int32_t P, int32_t S, int64_t t, const uint8_t *__restrict__ arrived,
     const int32_t *__restrict__ ver_in, int32_t *__restrict__ ver_out,
@@ -610,11 +644,28 @@ __global__ __launch_bounds__(kAssembleThreads) void k_assemble_scaled(
     int32_t *__restrict__ age_user, const Tile *__restrict__ tiles,
     const int64_t *__restrict__ displs, const double *__restrict__ c,
     const double *__restrict__ x_own, double *__restrict__ x_hat, double *__restrict__ z_own,
-    double *__restrict__ z_hat, const int32_t *__restrict__ done) {
+    double *__restrict__ z_hat, int64_t n_tiles, int32_t n_hot,
+    const int32_t *__restrict__ hot_col, const int32_t *__restrict__ hot_rank,
+    double *__restrict__ hot, const int32_t *__restrict__ done) {
     if (done && *done) return;
     if (blockIdx.x == 0) {
         record_step(P, S, t, arrived, ver_in, ver_out, age_state, eff_state, forced, eff_user,
                     age_user, nullptr);
+        return;
+    }
+    if ((int64_t)blockIdx.x > n_tiles) {
+        // x_hat[j] is read only where j's block is not taken, which no tile
+        // of this launch writes
+        const int64_t h0 = ((int64_t)blockIdx.x - 1 - n_tiles) * kAssembleTile;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int64_t k = h0 + threadIdx.x + u * kAssembleThreads;
+            if (k < n_hot) {
+                const int32_t j = hot_col[k], p = hot_rank[k];
+                hot[k] = stale_select(ver_in[p], arrived[p], t, S) ? c[j] * x_own[j]
+                                                                   : c[j] * x_hat[j];
+            }
+        }
         return;
     }
     const Tile tile = tiles[blockIdx.x - 1];
@@ -1415,6 +1466,8 @@ struct RangeBuild {
     std::vector<uint16_t> rmask;  // [n] ranges in which a row has entries
     std::vector<double> diag;     // [n] Jacobi diagonal
     std::vector<Fixup> rfix;      // split sub-rows
+    std::vector<int32_t> hot_col;   // the most gathered columns, ascending
+    std::vector<int32_t> hot_rank;  // the rank whose block holds each
 };
 
 // Range layout: every row cut into sub-rows by column range (its entries of
@@ -1427,14 +1480,43 @@ struct RangeBuild {
 // or piece = its row's rank block (stream items carry theirs per sub-row).
 static void build_ranges(const std::vector<int32_t> &rp, const std::vector<int32_t> &col,
                          const std::vector<double> &val, const std::vector<int64_t> &counts,
-                         int32_t NR, bool jacobi, RangeBuild &B, std::vector<WorkItem> &items,
-                         int64_t &n_pieces) {
+                         int32_t NR, bool jacobi, int32_t hot_cap, RangeBuild &B,
+                         std::vector<WorkItem> &items, int64_t &n_pieces) {
     const int64_t n = (int64_t)rp.size() - 1;
     std::vector<int64_t> bs(counts.size() + 1, 0);
     for (size_t p = 0; p < counts.size(); ++p) bs[p + 1] = bs[p] + counts[p];
     std::vector<int32_t> rank_of(n);
     for (size_t p = 0; p < counts.size(); ++p)
         for (int64_t i = bs[p]; i < bs[p + 1]; ++i) rank_of[i] = (int32_t)p;
+    // With hot_cap > 0: the hot_cap columns gathered most often from outside
+    // their own rank block (at least twice, ties to the lower column), whose
+    // entries outside the row's block then name slot k as -1 - k; the sweep
+    // reads them from a copy in LDS (the same values: the sums do not change).
+    std::vector<int32_t> hot_slot;
+    if (hot_cap > 0 && n > 0) {
+        std::vector<int64_t> g(n, 0);
+        for (int64_t i = 0; i < n; ++i) {
+            const int64_t lo = bs[rank_of[i]], hi = bs[rank_of[i] + 1];
+            for (int32_t k = rp[i]; k < rp[i + 1]; ++k)
+                if (col[k] < lo || col[k] >= hi) ++g[col[k]];
+        }
+        std::vector<int32_t> cand;
+        for (int64_t c = 0; c < n; ++c)
+            if (g[c] >= 2) cand.push_back((int32_t)c);
+        if ((int64_t)cand.size() > hot_cap) {
+            std::nth_element(cand.begin(), cand.begin() + hot_cap, cand.end(),
+                             [&](int32_t u, int32_t v) { return g[u] > g[v] || (g[u] == g[v] && u < v); });
+            cand.resize(hot_cap);
+        }
+        std::sort(cand.begin(), cand.end());
+        hot_slot.assign(n, -1);
+        B.hot_col = cand;
+        B.hot_rank.resize(cand.size());
+        for (size_t k = 0; k < cand.size(); ++k) {
+            hot_slot[cand[k]] = (int32_t)k;
+            B.hot_rank[k] = rank_of[cand[k]];
+        }
+    }
     // sub-rows of each range in row order: (row, length)
     std::vector<std::vector<int32_t>> srow(NR), slen(NR);
     std::vector<int32_t> cnt(NR);
@@ -1487,9 +1569,12 @@ static void build_ranges(const std::vector<int32_t> &rp, const std::vector<int32
     for (int64_t i = 0; i < n; ++i) {
         for (int32_t x = 0; x < NR; ++x)
             if ((B.rmask[i] >> x) & 1u) cur[x] = B.srp[base[x] + inv[x][seen[x]++]];
+        const int64_t lo = bs[rank_of[i]], hi = bs[rank_of[i] + 1];
         for (int32_t k = rp[i]; k < rp[i + 1]; ++k) {
-            const int64_t d = cur[range_of(col[k], n, NR)]++;
-            B.scol[d] = col[k];
+            const int32_t c = col[k];
+            const int64_t d = cur[range_of(c, n, NR)]++;
+            const bool hot = !hot_slot.empty() && hot_slot[c] >= 0 && (c < lo || c >= hi);
+            B.scol[d] = hot ? -1 - hot_slot[c] : c;
             B.sval[d] = val[k];
         }
     }
@@ -1696,6 +1781,8 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
     a.x_next = L.x_next;
     a.g_own = M->colscale ? M->d_zown : L.x_own;
     a.g_hat = M->colscale ? M->d_zhat : L.x_hat;
+    a.hot = M->d_hot;
+    a.n_hot = M->n_hot;
     a.partials = L.partials;
     a.pieces = M->d_pieces;
     a.order = M->d_order;
@@ -1751,7 +1838,8 @@ ecc_status_t launch_sweep(ecc_matrix_t M, const SweepLaunch &L) {
         const int64_t per = (int64_t)kScaleThreads * kScaleElems;
         const int sg = (int)std::min<int64_t>(8192, (n + per - 1) / per);
         hipLaunchKernelGGL(k_col_scale, dim3(sg), dim3(kScaleThreads), 0, st, n, M->d_cscale,
-                           L.x_own, L.x_hat, M->d_zown, M->d_zhat, L.done);
+                           L.x_own, L.x_hat, M->d_zown, M->d_zhat, M->n_hot, M->d_hot_col,
+                           M->d_hot, L.done);
         ECC_LAUNCH_CHECK();
     }
     if (M->kind == ECC_KIND_JACOBI) {
@@ -1805,7 +1893,8 @@ ecc_status_t launch_assemble_scaled(ecc_matrix_t M, const double *x_own, double 
     const int64_t t = plan->clock;
     const int32_t *ver_in = plan->d_version + (t & 1) * plan->P;
     int32_t *ver_out = plan->d_version + ((t + 1) & 1) * plan->P;
-    const int64_t grid = 1 + plan->n_tiles;
+    // the tiles, then the hot columns' copy (kAssembleTile per workgroup)
+    const int64_t grid = 1 + plan->n_tiles + (M->n_hot + kAssembleTile - 1) / kAssembleTile;
     if (grid > 0x7fffffff) {
         set_error("too many assembly tiles");
         return ECC_ERR_RANGE;
@@ -1814,7 +1903,8 @@ ecc_status_t launch_assemble_scaled(ecc_matrix_t M, const double *x_own, double 
     hipLaunchKernelGGL(k_assemble_scaled, dim3((unsigned)grid), dim3(kAssembleThreads), 0,
                        plan->stream, plan->P, plan->S, t, d_arrived, ver_in, ver_out, plan->d_age,
                        plan->d_eff, plan->d_forced, d_eff_out, d_age_out, plan->d_tiles,
-                       plan->d_displs, M->d_cscale, x_own, x_hat, M->d_zown, M->d_zhat, d_done);
+                       plan->d_displs, M->d_cscale, x_own, x_hat, M->d_zown, M->d_zhat,
+                       plan->n_tiles, M->n_hot, M->d_hot_col, M->d_hot_rank, M->d_hot, d_done);
     ECC_LAUNCH_CHECK();
     plan->clock = t + 1;
     return ECC_OK;
@@ -2032,7 +2122,8 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
         std::vector<double> hval(A->nnz);
         ECC_HIP(hipMemcpy(hcol.data(), A->d_col, sizeof(int32_t) * A->nnz, hipMemcpyDeviceToHost));
         ECC_HIP(hipMemcpy(hval.data(), A->d_val, sizeof(double) * A->nnz, hipMemcpyDeviceToHost));
-        build_ranges(rp, hcol, hval, plan->counts, n_ranges, kind == ECC_KIND_JACOBI, RB, items,
+        build_ranges(rp, hcol, hval, plan->counts, n_ranges, kind == ECC_KIND_JACOBI,
+                     colscale ? kHotCols : 0, RB, items,
                      n_pieces);
     } else if (irregular) {
         sort_rows(rp, plan->counts, order, srp);
@@ -2232,6 +2323,13 @@ static ecc_status_t ecc_matrix_create_impl(ecc_plan_t plan, const ecc_csr_t *A, 
             !up((void **)&M->d_diag, RB.diag.data(), sizeof(double) * RB.diag.size()) ||
             !up((void **)&M->d_rfix, RB.rfix.data(), sizeof(Fixup) * RB.rfix.size()))
             return fail("building the range layout failed");
+        M->n_hot = (int32_t)RB.hot_col.size();
+        if (M->n_hot > 0 &&
+            (!up((void **)&M->d_hot_col, RB.hot_col.data(), sizeof(int32_t) * RB.hot_col.size()) ||
+             !up((void **)&M->d_hot_rank, RB.hot_rank.data(),
+                 sizeof(int32_t) * RB.hot_rank.size()) ||
+             hipMalloc((void **)&M->d_hot, sizeof(double) * RB.hot_col.size()) != hipSuccess))
+            return fail("building the hot-column copy failed");
         if (hipMalloc((void **)&M->d_rpart, sizeof(double) * (size_t)n_ranges * (size_t)n) !=
             hipSuccess)
             return fail("hipMalloc of the range sums failed");
@@ -2313,6 +2411,9 @@ ecc_status_t ecc_matrix_destroy(ecc_matrix_t M) {
     (void)hipFree(M->d_cscale);
     (void)hipFree(M->d_zown);
     (void)hipFree(M->d_zhat);
+    (void)hipFree(M->d_hot_col);
+    (void)hipFree(M->d_hot_rank);
+    (void)hipFree(M->d_hot);
     delete M;
     return ECC_OK;
 }
