@@ -693,7 +693,7 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
                 oracle.run_iterative(prob, T=sample_iters, threads=threads)
                 done_iters += sample_iters
                 k += 1
-                if time.perf_counter() - t0 >= budget or k >= 50:
+                if time.perf_counter() - t0 >= budget:
                     break
             dt = time.perf_counter() - t0
             return per_iter_bytes * done_iters / dt / 1e9, done_iters, k, dt
@@ -724,16 +724,18 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
                 "sample": "%d of %d repetitions, 1 thread (the oracle has no threaded loop here), %.1f s"
                                             % (reps, prob.reps, dt)}
     if cfg == "mf":
-        # workers' shares of iteration 0, one after another: the errors and
-        # gradient of each worker's minibatch, until the time is used
+        # workers' shares of the iterations in order (iteration t's minibatch
+        # of worker p, at the initial model), one after another: the errors
+        # and gradient of each worker's minibatch, until the time is used
         from oracle import mf as MFO
         e = np.zeros(prob.N)
         t0 = time.perf_counter()
         done = 0
-        while done < prob.P and (done == 0 or time.perf_counter() - t0 < budget_s):
-            lo, hi = prob.batch_range(done, int(prob.batch[0][done]))
+        while done < prob.P * prob.T and (done == 0 or time.perf_counter() - t0 < budget_s):
+            t, p = divmod(done, prob.P)
+            lo, hi = prob.batch_range(p, int(prob.batch[t][p]))
             e[lo:hi] = MFO.errors(prob, prob.W0, lo, hi)
-            MFO.worker_gradient(prob, prob.W0, e, done, lo, hi)
+            MFO.worker_gradient(prob, prob.W0, e, p, lo, hi)
             done += 1
         dt = time.perf_counter() - t0
         # per worker: its share of the index and ratings, the model read,
@@ -742,8 +744,9 @@ def cpu_baseline(cfg, prob, res, budget_s=12.0):
         per_worker = (24.0 * prob.N / prob.K + 12.0 * prob.P * rows) / prob.P + 16.0 * prob.m
         return {"value": round(per_worker * done / dt / 1e9, 4), "unit": "GB/s", "cores": cores,
                 "kind": "oracle", "cpu_model": model,
-                "sample": "the errors and gradients of %d of the %d workers' minibatches at "
-                          "iteration 0 (1/%d of the ratings each), 1 thread, %.1f s"
+                "sample": "the errors and gradients of %d worker minibatches of the first "
+                          "iterations' schedule (%d per iteration, 1/%d of the ratings each) at "
+                          "the initial model, 1 thread, %.1f s"
                           % (done, prob.P, prob.P * prob.K, dt)}
     if cfg == "threshold":
         from oracle import threshold as THO
