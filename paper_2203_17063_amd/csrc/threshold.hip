@@ -84,6 +84,7 @@ __global__ __launch_bounds__(kThrThreads) void k_reduce_bst(int32_t P, int32_t r
                                                             int64_t k,
                                                             const double *const *__restrict__ src,
                                                             double *__restrict__ result) {
+    static_assert(S >= 0 && S <= kThrMaxStages, "the register fold holds at most 32 processes");
     constexpr int N = 1 << S;
     const int64_t stride = (int64_t)gridDim.x * kThrThreads;
     for (int64_t j = (int64_t)blockIdx.x * kThrThreads + threadIdx.x; j < k; j += stride) {
@@ -126,7 +127,7 @@ __global__ __launch_bounds__(kThrThreads) void k_reduce_bst_big(
     int32_t P, int32_t root, int32_t n, int64_t k, const double *const *__restrict__ src,
     double *__restrict__ result) {
     constexpr int H = D - 3;  // levels above a group of 8 leaves
-    static_assert(H >= 1 && D <= kThrMaxStagesBig, "more than 8 processes");
+    static_assert(H >= 1 && D <= kThrMaxStagesBig, "between 9 and 4,096 processes");
     const int64_t stride = (int64_t)gridDim.x * kThrThreads;
     for (int64_t j = (int64_t)blockIdx.x * kThrThreads + threadIdx.x; j < k; j += stride) {
         double st[H];
