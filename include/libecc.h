@@ -586,7 +586,8 @@ ecc_status_t ecc_mf_destroy(ecc_mf_t h);
  *     gradients read in place from their slots;
  *   W := W - eta * (G * c_row + 2 lam W), c_row = K / max(1, ratings of
  *     the row).
- * d_grads, d_slots: device arrays of P device pointers to m doubles each. */
+ * d_grads, d_slots: device arrays of P device pointers to m doubles each;
+ * no gradient buffer may alias a slot, and d_G aliases neither. */
 ecc_status_t ecc_mf_iterate(ecc_mf_t h, ecc_plan_t plan, double eta, double lam, double *d_W,
                             double *const *d_grads, double *const *d_slots, double *d_G,
                             const uint8_t *d_arrived, const int32_t *d_batch, double *d_rmse,
