@@ -271,7 +271,11 @@ ecc_status_t ecc_allreduce_partial(ecc_plan_t plan, int64_t m, const double *con
  * product of the same two operands, so the iterates are bit for bit those
  * of the general form (the residual norm agrees to rounding: the kernel
  * stages no values, more of its workgroups fit on the device, and the
- * per-workgroup partial sums group the rows differently). */
+ * per-workgroup partial sums group the rows differently).  In
+ * ECC_LAYOUT_RANGES the 1,024 columns gathered most often from outside
+ * their own rank block also get a copy of their z_hat values (16 bytes per
+ * column in the handle, 8 bytes more formed with the views) that every
+ * sweep workgroup reads into LDS; the values gathered are the same. */
 #define ECC_LAYOUT_STREAM 0
 #define ECC_LAYOUT_SORTED 1
 #define ECC_LAYOUT_SHORT 2
