@@ -664,6 +664,30 @@ def test_solve_pagerank_rmat_ranges(scale):
                        range_bytes=4096)
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_irregular_random(seed):
+    """R-MAT PageRank of random scale (8-16), rank count (1-128), staleness
+    bound (0-4), arrival rate (0.3-1) and range size (unsplit or 2 KB-64 KB
+    ranges): the sorted or range layout in the column-value form (with its
+    copy of the most gathered columns) against the oracle at every
+    iteration, and bit for bit against the general form of the same layout."""
+    import dataclasses
+    E = _capi()
+    rng = np.random.default_rng(5000 + seed)
+    scale = int(rng.integers(8, 17))
+    base = W.pagerank_rmat(scale=scale, T=20,
+                           P=max(1, min(int(rng.integers(1, 129)), (1 << scale) // 4)))
+    mask = (rng.random((base.T, base.P)) < rng.uniform(0.3, 1.0)).astype(np.uint8)
+    mask[0] = 1
+    prob = dataclasses.replace(base, S=int(rng.integers(0, 5)), mask=mask, tol=0.0)
+    rb = int(rng.choice([0, 2048, 4096, 16384, 65536]))
+    _solve_and_compare(prob, bitwise=False, range_bytes=rb)
+    it1, x1, xh1, _, f1 = _solve_x_rho(prob, range_bytes=rb)
+    it2, x2, xh2, _, f2 = _solve_x_rho(prob, range_bytes=rb, compact=E.ECC_COMPACT_NONE)
+    assert (f1, f2) == (E.ECC_FORM_COLUMN_VALUES, E.ECC_FORM_GENERAL)
+    assert it1 == it2 and np.array_equal(x1, x2) and np.array_equal(xh1, xh2)
+
+
 def test_solve_arrow_ranges():
     _solve_and_compare(_arrow_problem(), bitwise=False, layout="RANGES", range_bytes=8192)
 
