@@ -115,6 +115,22 @@ def test_mf_empty_minibatches():
     _compare(prob)
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_mf_random(seed):
+    """Random worker counts (1-64, multiples of 8 and not, so with and
+    without the XCD pinning), ranks, minibatch counts, sizes, staleness
+    bounds and arrival rates."""
+    rng = np.random.default_rng(7000 + seed)
+    P = int(rng.choice([1, 2, 3, 8, 16, 24, 32, 40, 64]))
+    rank = int(rng.choice([1, 2, 4, 8, 16, 32, 64]))
+    K = int(rng.integers(1, 9))
+    nu, ni = int(rng.integers(20, 3000)), int(rng.integers(10, 800))
+    nr = int(rng.integers(P * 2, 60000))
+    _compare(W.mf_problem(n_users=nu, n_items=ni, n_ratings=nr, rank=rank, P=P,
+                          S=int(rng.integers(0, 6)), q=float(rng.uniform(0.2, 1.0)), T=8,
+                          eta=0.3, seed=100 + seed, K=K))
+
+
 def test_mf_errors():
     from paper_2203_17063_amd import capi as E
     announce("mf errors")
