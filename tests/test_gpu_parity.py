@@ -1015,6 +1015,31 @@ def test_solve_queue_schedule(case):
                        solves=3)
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_short_layout_random(seed):
+    """3-D stencils of random size (6-47 per side; random rank counts and
+    plane tiles) and 2-D ones (8-199), random staleness bounds and arrival
+    rates, the static or the queue schedule: the diagonal-form short layout
+    bitwise against the oracle over two solves of one handle."""
+    import dataclasses
+    E = _capi()
+    rng = np.random.default_rng(9000 + seed)
+    if seed % 3 != 0:
+        N = int(rng.integers(6, 48))
+        base = W.jacobi_3d(N=N, T=12, P=int(rng.integers(1, 80)))
+        tile = int(rng.choice([0, 256, 512, 768, 1024]))
+        tile = tile if tile < N * N else 0
+    else:
+        base = W.jacobi_2d(N=int(rng.integers(8, 200)), T=12)
+        tile = 0
+    S = int(rng.integers(0, 6))
+    mask = (rng.random((base.T, base.P)) < rng.uniform(0.3, 1.0)).astype(np.uint8)
+    mask[0] = 1
+    sch = int(rng.choice([E.ECC_SCHEDULE_STATIC, E.ECC_SCHEDULE_QUEUE]))
+    _solve_and_compare(dataclasses.replace(base, S=S, mask=mask), bitwise=True, layout="SHORT",
+                       tile_rows=tile, schedule=sch, expect_schedule=sch, solves=2)
+
+
 def test_step_api_matches_solve_queue():
     E = _capi()
     _step_api_matches_solve((W.jacobi_2d(N=40, T=25), W.jacobi_3d(N=20, T=15, P=6)),
