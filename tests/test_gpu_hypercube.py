@@ -95,6 +95,20 @@ def test_parity_many_processes(P, m, slack, q, in_place):
     _run_and_compare(P, m, slack, q, T=6, seed=P + m, in_place=in_place)
 
 
+@pytest.mark.parametrize("seed", range(4))
+def test_parity_random(seed):
+    """Random process counts (1-4,096), lengths, slacks, delivery rates,
+    call counts and in-place calls (a one-off run of 30 such cases passed as
+    well)."""
+    rng = np.random.default_rng(11000 + seed)
+    P = int(2 ** rng.integers(0, 13))
+    m = int(rng.integers(0, 5000)) if P <= 256 else int(rng.integers(0, 300))
+    slack = int(rng.choice([0, 1, 2, 3, -1]))
+    slack = H.UNBOUNDED if slack < 0 else slack
+    _run_and_compare(P, m, slack, float(rng.uniform(0.1, 1.0)), int(rng.integers(1, 8)),
+                     11000 + seed, in_place=bool(rng.integers(0, 2)))
+
+
 def test_too_many_processes_refused():
     E = _E()
     for P in (8192, 96):

@@ -140,6 +140,31 @@ def test_allreduce_drop(P, q):
     assert int(cnt.item()) == int(arrived_h.sum())
 
 
+@pytest.mark.parametrize("seed", range(4))
+def test_reduce_random(seed):
+    """Random process counts (up to 64, or up to 4,096), roots, modes,
+    fractions and lengths (a one-off run of 30 such cases passed as well)."""
+    E = _E()
+    rng = np.random.default_rng(12000 + seed)
+    P = int(rng.integers(1, 4097)) if seed % 2 else int(rng.integers(1, 65))
+    root = int(rng.integers(0, P))
+    mode = int(rng.choice([TH.DATA, TH.PROCS]))
+    theta = float(rng.choice([0.0, 0.1, 0.37, 0.5, 0.75, 1.0]))
+    if mode == TH.PROCS and theta == 0.0:
+        theta = 0.05
+    m = int(rng.integers(0, 20000)) if P <= 256 else int(rng.integers(0, 1500))
+    announce("reduce random", P, root, mode, theta, m)
+    xs_h = [rng.standard_normal(m) * 10.0 ** rng.integers(-6, 6) for _ in range(P)]
+    res_h = np.full(m, -3.25)
+    k_ref, n_ref = TH.reduce(P, root, theta, mode, xs_h, res_h)
+    xs = [torch.from_numpy(x).cuda() for x in xs_h]
+    res = torch.full((m,), -3.25, dtype=torch.float64, device="cuda")
+    k, n = E.ecc_reduce_threshold(P, root, m, theta, mode, _ptrs(xs), res, _stream())
+    torch.cuda.synchronize()
+    assert (k, n) == (k_ref, n_ref)
+    assert np.array_equal(res.cpu().numpy(), res_h)
+
+
 def test_threshold_errors():
     E = _E()
     announce("threshold errors")
